@@ -1,0 +1,122 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check a pin catches each.
+
+A pin set that passes a wrong oracle proves nothing; each mutation below is a
+mistake one could make writing the definition (a wrong KV-head map, a dropped
+scale, a dropped root segment, swapped operands, a wrong start offset, a
+missing LSE weight) and must make at least one pin fail.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from oracle import cascade as C
+from oracle import metadata as M
+from tests import oracle_pins as P
+
+
+def _attend_factory(kind):
+    def attend(q, K, V, scale):
+        hq, hkv = q.shape[0], K.shape[1]
+        group = hq // hkv
+        out = np.empty((hq, V.shape[2]))
+        lse = np.empty(hq)
+        for h in range(hq):
+            g = (h % hkv) if kind == "interleaved_heads" else h // group
+            sc = 1.0 if kind == "no_scale" else scale
+            s = sc * (K[:, g, :] @ q[h])
+            m = s.max()
+            e = np.exp(s - m)
+            z = e.sum()
+            vals = K if kind == "k_as_v" else V
+            out[h] = (e @ vals[:, g, :]) / (len(e) if kind == "mean_norm" else z)
+            lse[h] = (np.log(z) if kind == "lse_no_max" else m + np.log(z))
+        return out, lse
+    return attend
+
+
+def _materialize_drop_root(model, node_kv, x, cache=None):
+    ks, vs = [], []
+    for n in model.chain(x)[1:] or model.chain(x):
+        ln = model.nodes[n]["len"]
+        kb, vb = node_kv(n)
+        ks.append(A.bf16_bits_to_f64(kb[:ln])); vs.append(A.bf16_bits_to_f64(vb[:ln]))
+    return np.concatenate(ks), np.concatenate(vs)
+
+
+def _materialize_off_by_one(model, node_kv, x, cache=None):
+    ks, vs = [], []
+    for n in model.chain(x):
+        ln = model.nodes[n]["len"]
+        kb, vb = node_kv(n)
+        lo = 1 if ln > 1 else 0
+        ks.append(A.bf16_bits_to_f64(kb[lo:ln])); vs.append(A.bf16_bits_to_f64(vb[lo:ln]))
+    return np.concatenate(ks), np.concatenate(vs)
+
+
+def _make_factory(kind):
+    orig = M.TreeModel._make
+
+    def _make(self, parent, depth, start, cap, tree_id):
+        if kind == "start_ignores_len" and parent >= 0:
+            start = self.nodes[parent]["start"]
+        if kind == "depth_not_incremented" and parent >= 0:
+            depth = self.nodes[parent]["depth"]
+        nid = orig(self, parent, depth, start, cap, tree_id)
+        if kind == "blocks_off_by_one" and nid > 0:
+            self.nodes[nid]["block_begin"] += 1
+        return nid
+    return _make
+
+
+def _combine_factory(kind):
+    def combine(parts):
+        ms = np.array([p[1] for p in parts])
+        m_star = ms.max()
+        w = np.exp(ms - m_star)
+        if kind == "unweighted_l":
+            L = sum(p[2] for p in parts)
+        else:
+            L = sum(wi * p[2] for wi, p in zip(w, parts))
+        if kind == "unweighted_o":
+            O = sum(p[0] for p in parts)
+        else:
+            O = sum(wi * p[0] for wi, p in zip(w, parts))
+        return O / L, m_star + np.log(L)
+    return combine
+
+
+MUTATIONS = {
+    "interleaved_heads": (A, "attend", _attend_factory("interleaved_heads")),
+    "no_scale": (A, "attend", _attend_factory("no_scale")),
+    "k_as_v": (A, "attend", _attend_factory("k_as_v")),
+    "mean_norm": (A, "attend", _attend_factory("mean_norm")),
+    "lse_no_max": (A, "attend", _attend_factory("lse_no_max")),
+    "drop_root": (A, "materialize", _materialize_drop_root),
+    "skip_first_row": (A, "materialize", _materialize_off_by_one),
+    "start_ignores_len": (M.TreeModel, "_make", _make_factory("start_ignores_len")),
+    "depth_not_incremented": (M.TreeModel, "_make", _make_factory("depth_not_incremented")),
+    "blocks_off_by_one": (M.TreeModel, "_make", _make_factory("blocks_off_by_one")),
+    "unweighted_l": (C, "combine", _combine_factory("unweighted_l")),
+    "unweighted_o": (C, "combine", _combine_factory("unweighted_o")),
+}
+
+FAST_PINS = [p for p in P.ALL_PINS if p is not P.pin_long_context_counts]
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(name, monkeypatch):
+    obj, attr, repl = MUTATIONS[name]
+    monkeypatch.setattr(obj, attr, repl)
+    failed = []
+    for pin in FAST_PINS:
+        try:
+            if pin is P.pin_bruteforce:
+                pin(seeds=(1, 2))
+            elif pin is P.pin_structure_invariants:
+                pin(cfgs=(1, 2, 4))
+            else:
+                pin()
+        except (AssertionError, IndexError, ValueError):
+            failed.append(pin.__name__)
+    assert failed, f"mutation {name} passed every pin"
