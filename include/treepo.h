@@ -1,0 +1,226 @@
+/*
+ * treepo.h -- C-ABI of the segment-tree decode-attention library (gfx950).
+ *
+ * The operation (TreePO, arXiv 2508.17445):
+ *   - a rollout forest: every query is a root node at depth 0; before each
+ *     segment step a path is forked into children that share its prefix
+ *     (Alg. 1; Sec. 2.2 "Segment-level Tree Sampling", "Branching and
+ *     Fallback"); each step appends one generated segment of at most l tokens
+ *     to a path (Alg. 1, the concatenation p_last + s_k);
+ *   - a leaf's trajectory is the concatenation of its chain's segments
+ *     (Sec. 2.3, segment decomposition), and shared prefixes are stored once
+ *     (Sec. 2.1);
+ *   - a decode step: every active leaf's new query, all Hq heads, attends with
+ *     softmax over the K/V of its whole root-to-leaf chain (Sec. 2.2,
+ *     segment-level decoding).  KV head g = h / (Hq / Hkv) serves query head h.
+ *
+ * Conventions
+ *   - Every function returns an int32_t status: TREEPO_OK or a negative code.
+ *     A failing call changes no state (arguments are validated before anything
+ *     is mutated).  No C++ exception crosses this boundary.
+ *   - "host" pointers are ordinary CPU memory read during the call; "device"
+ *     pointers are HIP device memory owned by the caller (the library never
+ *     allocates device memory; it allocates pinned host staging for uploads).
+ *   - Device work is enqueued on the caller's stream and is asynchronous; the
+ *     node table is host state updated synchronously at call time.  A context
+ *     is single-threaded, and its device work must be issued on one stream at a
+ *     time (or the caller orders the streams).
+ *   - bf16 is IEEE bfloat16 (1-8-7 bits), little-endian, 2 bytes.
+ */
+#ifndef TREEPO_H
+#define TREEPO_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+#define TREEPO_OK 0
+#define TREEPO_EINVAL (-1)       /* bad id, shape, count or null pointer         */
+#define TREEPO_ENOMEM (-2)       /* pool blocks or node slots exhausted          */
+#define TREEPO_EFULL (-3)        /* append would exceed the node's capacity      */
+#define TREEPO_EFROZEN (-4)      /* append to a node that has children           */
+#define TREEPO_EEMPTY (-5)       /* decode of a chain holding zero tokens        */
+#define TREEPO_EWORKSPACE (-6)   /* workspace missing or too small               */
+#define TREEPO_EHIP (-7)         /* HIP runtime error; see treepo_last_error     */
+#define TREEPO_EUNSUPPORTED (-8) /* shape outside what the kernels implement     */
+
+/* decode modes for treepo_decode_workspace_size / treepo_export_plan */
+#define TREEPO_MODE_TREE 0  /* cascade: each node's KV read once for all its leaves */
+#define TREEPO_MODE_NAIVE 1 /* baseline: each leaf reads its whole chain            */
+
+typedef struct treepo_ctx treepo_ctx;
+
+/*
+ * Pool shape.  K pool, device bf16, layout [Hkv][num_blocks][B][D]: token row
+ * r = block * B + offset of KV head g starts at element ((g*num_blocks*B)+r)*D.
+ * V pool, device bf16, layout [Hkv][num_blocks][D][B]: every block is stored
+ * transposed, so element (g, r, d) is at ((g*num_blocks + r/B)*D + d)*B + r%B.
+ * head_dim D must be 64 or 128, block_tokens B must be 64 (one block is one
+ * kernel tile), Hq % Hkv == 0 and Hq / Hkv <= 8.  Pools are caller-owned and
+ * must stay valid until treepo_destroy; their contents need no initialisation.
+ */
+typedef struct treepo_config {
+  int32_t num_q_heads;  /* Hq  */
+  int32_t num_kv_heads; /* Hkv */
+  int32_t head_dim;     /* D   */
+  int32_t block_tokens; /* B   */
+  int64_t num_blocks;   /* pool capacity in blocks                     */
+  int32_t max_nodes;    /* node-table capacity                          */
+  int32_t reserved;     /* must be 0                                    */
+  void* k_pool;         /* device, see above                            */
+  void* v_pool;         /* device, see above                            */
+} treepo_config;
+
+/* Node record exported by treepo_export_nodes: 8 int32 per node. */
+#define TREEPO_NODE_FIELDS 8 /* parent, depth, start, len, cap, block_begin, n_blocks, tree_id */
+
+/* Creates a context for one pool.  No device call is made.  *out receives the
+ * handle; EINVAL / EUNSUPPORTED on a bad config. */
+int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out);
+/* Releases host state and pinned staging (waits for this context's pending
+ * uploads).  Null is accepted. */
+int32_t treepo_destroy(treepo_ctx* ctx);
+
+/* New tree: a root node (the query/prompt segment, depth 0, Sec. 2.2 item 1)
+ * able to hold cap_tokens tokens.  Reserves ceil(cap/B) contiguous blocks,
+ * starting at the running total of all blocks reserved so far.  Node ids are
+ * 0,1,2,... in creation order.  EINVAL if cap < 1; ENOMEM if out of nodes or
+ * blocks. */
+int32_t treepo_new_root(treepo_ctx* ctx, int32_t cap_tokens, int32_t* node_out);
+
+/* Branching (Alg. 1 Branching; Sec. 2.2): spawns n_children nodes that all
+ * continue the parent's sequence (start = parent.start + parent.len, depth =
+ * parent.depth + 1) with no KV copy; each reserves ceil(child_cap/B) blocks.
+ * Ids are consecutive and written to children_out (host, n_children entries).
+ * The parent becomes frozen (no further appends).  A node may be forked
+ * again later (fallback re-forks, partially filled parents).  EINVAL on a bad
+ * parent, n_children < 1 or child_cap < 1; ENOMEM when out of nodes/blocks. */
+int32_t treepo_fork(treepo_ctx* ctx, int32_t parent, int32_t n_children,
+                    int32_t child_cap, int32_t* children_out);
+
+/* Appends generated tokens (Alg. 1: the segment s_k joins its path).  nodes and
+ * ntok are host arrays of n entries; node i gets ntok[i] >= 0 tokens whose
+ * K and V rows are rows [sum(ntok[0..i)), +ntok[i]) of k and v (device bf16,
+ * [sum ntok][Hkv][D], packed in call order).  A node may appear more than
+ * once (its rows are appended in call order).  The whole call is validated
+ * first: EINVAL (bad id, ntok < 0, null k/v with tokens), EFROZEN (node has
+ * children), EFULL (len would exceed cap).  The scatter into the pools is
+ * enqueued on stream; lengths are updated at call time. */
+int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes,
+                         const int32_t* ntok, const void* k, const void* v,
+                         hipStream_t stream);
+
+/* Pool token rows (block * B + offset) that the next treepo_kv_append /
+ * treepo_kv_commit with the same arguments would fill, in call order
+ * (rows_out: host, sum(ntok) entries).  For callers that write K/V into the
+ * pools with their own kernels.  Same validation as treepo_kv_append; no state
+ * change. */
+int32_t treepo_kv_slots(treepo_ctx* ctx, int32_t n, const int32_t* nodes,
+                        const int32_t* ntok, int64_t* rows_out);
+
+/* Advances lengths exactly like treepo_kv_append but writes no K/V: the
+ * caller has already written the rows given by treepo_kv_slots. */
+int32_t treepo_kv_commit(treepo_ctx* ctx, int32_t n, const int32_t* nodes,
+                         const int32_t* ntok);
+
+/* Workspace bytes that a decode of these leaves needs (mode TREEPO_MODE_TREE
+ * or TREEPO_MODE_NAIVE).  Builds and caches the decode plan. */
+int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
+                                     const int32_t* leaves, int32_t mode,
+                                     size_t* bytes);
+
+/* One decode step of attention for n_leaves leaves (Sec. 2.2 segment-level
+ * decoding; Sec. 2.3 chains).  leaves: host node ids (any node, duplicates
+ * allowed), call position i.
+ *   q     device bf16 [n_leaves][Hq][D]   the step's queries
+ *   out   device fp32 [n_leaves][Hq][D]   softmax(scale q K^T) V over the chain
+ *   lse   device fp32 [n_leaves][Hq] or null: natural-log sum exp(scale q.k)
+ *   workspace  device, >= treepo_decode_workspace_size(..., TREEPO_MODE_TREE)
+ * Cascade schedule: every node's K/V is read once and scored against all of
+ * its descendant leaves' query rows (the nested sub-groups G_j of Sec. 2.3);
+ * per-node partials are merged with a log-sum-exp combine.  The library keeps
+ * the plan it uploaded into the workspace and reuses it while the tree and
+ * the leaf list are unchanged: do not modify the workspace between calls.
+ * EINVAL (bad id, null pointer, n_leaves < 1), EEMPTY (a chain holds no
+ * tokens), EWORKSPACE, EHIP. */
+int32_t treepo_tree_decode(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                           const void* q, float scale, float* out, float* lse,
+                           void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* The per-leaf paged-decode baseline: same contract and results as
+ * treepo_tree_decode, but every leaf streams its whole chain's blocks on its
+ * own, so shared prefixes are read once per descendant leaf (the separate
+ * per-path KV that Sec. 1 contrasts with sharing).  Workspace from mode
+ * TREEPO_MODE_NAIVE. */
+int32_t treepo_paged_decode_naive(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                                  const void* q, float scale, float* out, float* lse,
+                                  void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* ---- metadata export (host arrays) -------------------------------------- */
+
+/* Number of nodes created so far. */
+int32_t treepo_num_nodes(treepo_ctx* ctx, int32_t* n_nodes);
+
+/* Node records, TREEPO_NODE_FIELDS int32 per node in id order, for the first
+ * min(capacity, n_nodes) nodes; *n_nodes receives the node count. */
+int32_t treepo_export_nodes(treepo_ctx* ctx, int32_t* records, int32_t capacity,
+                            int32_t* n_nodes);
+
+/* Per-leaf chains (root first) and leaf block tables (each chain node's first
+ * ceil(len/B) blocks, in chain order) as CSR arrays:
+ *   chain_off[n_leaves+1], chain_nodes[*total_chain],
+ *   block_off[n_leaves+1], blocks[*total_blocks].
+ * Pass null arrays to query the totals only. */
+int32_t treepo_export_chains(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                             int32_t* chain_off, int32_t* chain_nodes,
+                             int32_t* block_off, int32_t* blocks,
+                             int32_t* total_chain, int32_t* total_blocks);
+
+/* Node -> descendant-leaf sets of one decode call (Sec. 2.3, Eq. groups):
+ * every node on some chain, ascending id (nodes[*n_nodes]), with the ascending
+ * call positions whose chain contains it (desc_off[*n_nodes+1], desc[*total]).
+ * Pass null arrays to query the sizes only. */
+int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                           int32_t* nodes, int32_t* desc_off, int32_t* desc,
+                           int32_t* n_nodes, int32_t* total);
+
+/* The decode schedule for inspection.  Work items, 8 int32 each:
+ *   {kind (0 VALU, 1 MFMA), rowset_begin, n_leaves, tile_begin, tile_end,
+ *    partial_base, rows, run}
+ * rowsets[]: call positions; tiles[] 4 int32 each {block, node, tile_in_node,
+ * valid_tokens}.  Pass null arrays to query the counts only. */
+int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                           int32_t mode, int32_t* items, int32_t* rowsets, int32_t* tiles,
+                           int32_t* n_items, int32_t* n_rowsets, int32_t* n_tiles);
+
+/* ---- kernel timing ------------------------------------------------------ */
+
+/* Kernel kinds for treepo_profile_read. */
+#define TREEPO_KERNEL_APPEND 0
+#define TREEPO_KERNEL_PARTIAL_VALU 1
+#define TREEPO_KERNEL_PARTIAL_MFMA 2
+#define TREEPO_KERNEL_COMBINE 3
+#define TREEPO_KERNEL_KINDS 4
+
+/* When enabled, every kernel launch of this context is bracketed by HIP events
+ * on the launch stream.  Enabling or disabling clears the totals. */
+int32_t treepo_set_profiling(treepo_ctx* ctx, int32_t enable);
+/* Total milliseconds and launch count per kernel kind since profiling was
+ * enabled; waits for the recorded events to complete. */
+int32_t treepo_profile_read(treepo_ctx* ctx, int32_t kind, double* total_ms,
+                            int64_t* launches);
+
+/* ---- errors ------------------------------------------------------------- */
+const char* treepo_strerror(int32_t code);
+/* Message of the last failing call on ctx (empty if none). */
+const char* treepo_last_error(treepo_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TREEPO_H */

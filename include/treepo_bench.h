@@ -1,0 +1,33 @@
+/*
+ * treepo_bench.h -- measurement probes shipped with the library.
+ *
+ * These are not part of the decode path.  They give the bandwidth figures
+ * that the decode kernels are judged against: a plain device copy of known
+ * size (to calibrate hardware byte counters) and a streaming read (the
+ * attainable HBM read bandwidth on this device).
+ */
+#ifndef TREEPO_BENCH_H
+#define TREEPO_BENCH_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* dst[0:bytes) = src[0:bytes) on stream.  bytes must be a multiple of 16 and
+ * both pointers 16-byte aligned (device memory).  Returns 0 or TREEPO_EINVAL /
+ * TREEPO_EHIP. */
+int32_t treepo_bench_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
+
+/* Reads src[0:bytes) once with 16-byte loads and writes one fp32 per
+ * workgroup into sink (device, >= 4096 floats) so the reads cannot be elided.
+ * Same alignment rules as treepo_bench_copy. */
+int32_t treepo_bench_read(const void* src, size_t bytes, float* sink, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TREEPO_BENCH_H */

@@ -1,0 +1,49 @@
+// Launch interface between the C-ABI host code and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace treepo {
+
+constexpr int kTile = 64;  // tokens per KV tile == tokens per pool block
+
+// Device views of the decode plan and buffers (see tree_core.h for layouts).
+struct DecodeArgs {
+  const uint16_t* k_pool;  // bf16 [Hkv][num_blocks][64][D]
+  const uint16_t* v_pool;  // bf16 [Hkv][num_blocks][D][64]
+  int64_t num_blocks;
+  int32_t hq, hkv, group, d;
+  const uint16_t* q;       // bf16 [n_leaves][Hq][D]
+  float scale_log2;        // softmax scale * log2(e)
+  const int32_t* items;    // Item, 8 int32 each
+  const int32_t* rowsets;
+  const int32_t* tiles;    // Tile, 4 int32 each
+  float* part_o;           // fp32 [partial_rows][D], unnormalised
+  float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
+  const int32_t* leaf_off; // [n_leaves + 1]
+  const int32_t* entries;  // Entry, 2 int32 each
+  int32_t n_leaves;
+  float* out;              // fp32 [n_leaves][Hq][D]
+  float* lse;              // fp32 [n_leaves][Hq] or null
+};
+
+hipError_t launch_partial_valu(const DecodeArgs& a, int32_t first_item, int32_t n_items,
+                               hipStream_t s);
+hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
+
+// One block-aligned run of appended tokens: source rows [src_row, +count) go
+// to token offsets [off, off + count) of pool block `block` (off + count <= 64).
+struct AppendPiece {
+  int32_t src_row;
+  int32_t block;
+  int32_t off;
+  int32_t count;
+};
+
+hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool,
+                            uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
+                            const AppendPiece* pieces, int32_t n_pieces, hipStream_t s);
+
+}  // namespace treepo

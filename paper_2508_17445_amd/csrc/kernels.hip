@@ -1,0 +1,502 @@
+// gfx950 kernels of the segment-tree decode path: KV append (scatter into the
+// pools), the VALU node-partial kernel, and the log-sum-exp combine.
+//
+// Node-partial attention (cascade schedule): for a work item -- a chunk of one
+// node run's KV tiles and the query rows of a group of its descendant leaves
+// (the nested sub-groups of TreePO Sec. 2.3) -- one 256-thread workgroup
+// streams every KV tile once from HBM into LDS with 128-bit global->LDS loads,
+// scores all query rows of the group against it, and writes per-row partials
+// (O unnormalised, running max, sum) in fp32.  The combine merges, per leaf
+// and query head, the partials of its chain (exact log-sum-exp algebra).
+//
+// Layouts: K pool [Hkv][blocks][64][D] (token rows), V pool [Hkv][blocks][D][64]
+// (each block transposed, so a d-row holds 64 consecutive tokens).  One pool
+// block is one 64-token tile.
+#include "kernels.h"
+
+#include <math.h>
+
+namespace treepo {
+namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr float kLn2 = 0.69314718055994530942f;
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
+                                         __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+// Sum over the four lanes of a quad (DPP quad permutations xor 1, xor 2).
+__device__ __forceinline__ float quad_sum(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, true));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, true));
+  return x;
+}
+
+__device__ __forceinline__ uint32_t f2bf_bits(float x) {
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(x)));
+}
+__device__ __forceinline__ float bf_bits2f(uint32_t b) { return __builtin_bit_cast(float, b << 16); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---- KV tile staging ----------------------------------------------------------
+//
+// LDS tile = K rows [64][D] then V^T rows [D][64], both in 16-byte chunks with
+// an XOR swizzle so that the compute reads below are bank-conflict free:
+//   K: chunk c of token row r sits at chunk position c ^ ((r & 1) << 2)
+//   V: chunk c of d-row d sits at chunk position c ^ (d & 7)
+// Every wave moves whole 1 KiB LDS slots; the swizzle is applied on the global
+// side (each lane picks which chunk of the same row it fetches), so the global
+// reads of a slot stay fully coalesced.
+template <int D>
+struct TileSmem {
+  static constexpr int kElems = kTile * D;
+  uint16_t kv[2][2 * kElems];
+  uint32_t pbuf[kWaves][8][8];  // per wave: token pair x query row, packed bf16 P
+};
+
+__device__ __forceinline__ int k_swz(int r) { return (r & 1) << 2; }
+
+// One 16-byte global->LDS load per lane into the 1 KiB LDS slot at byte
+// address `lds` (wave-uniform).  Issued as inline asm so that the compiler does
+// not treat the in-flight LDS writes as aliasing every later LDS access (which
+// would drain the prefetch of the next tile); completion is tracked by hand
+// with vmcnt waits before the barrier that publishes a tile.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(lds) : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)p));
+}
+
+// Stages tile `block` of KV head g into the LDS buffer at byte address `dst`.
+// D/16 loads per lane.
+template <int D>
+__device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
+                                         const uint16_t* __restrict__ vpool, int64_t num_blocks,
+                                         int g, int block, uint32_t dst, int wave, int lane) {
+  constexpr int kKChunks = D / 8;   // 16-byte chunks per K row
+  constexpr int kPerWave = D / 32;  // 1 KiB slots per wave for each of K and V
+  const int64_t base = (static_cast<int64_t>(g) * num_blocks + block) * (kTile * D);
+  const char* kg = reinterpret_cast<const char*>(kpool + base);
+  const char* vg = reinterpret_cast<const char*>(vpool + base);
+  const uint32_t vd = dst + kTile * D * 2;
+#pragma unroll
+  for (int j = 0; j < kPerWave; ++j) {
+    const int slot = wave * kPerWave + j;
+    const int c = slot * 64 + lane;
+    const int row = c / kKChunks;
+    const int col = (c % kKChunks) ^ k_swz(row);
+    dma16(kg + row * (D * 2) + col * 16, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
+  }
+#pragma unroll
+  for (int j = 0; j < kPerWave; ++j) {
+    const int slot = wave * kPerWave + j;
+    const int c = slot * 64 + lane;
+    const int row = c >> 3;
+    const int col = (c & 7) ^ (row & 7);
+    dma16(vg + row * 128 + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
+  }
+}
+
+// Barrier after which this workgroup's loads, except the newest N per lane,
+// have landed in LDS.
+template <int N>
+__device__ __forceinline__ void barrier_tile_landed() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" :: "n"(N) : "memory");
+}
+// Barrier after which no wave still reads the LDS it read before it.
+__device__ __forceinline__ void barrier_lds_reads_done() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// ---- VALU node-partial ----------------------------------------------------------
+//
+// M query rows (M <= 8) per workgroup.  Wave w takes tokens [16w, 16w+16) of
+// every tile and keeps its own online-softmax state; the four states are
+// merged at the end.
+//   QK: lane (t = lane/4, j = lane%4) owns token 16w+t and the K chunks j, j+4,
+//       ... of its row; q rows sit in registers in the same chunk order.  The
+//       partial dot products (v_dot2 bf16 -> fp32) are summed across the quad
+//       with DPP.
+//   P : rounded to bf16; the sum l is accumulated from the rounded values so
+//       the output stays a convex combination of V rows.  Token pairs are
+//       packed into one 32-bit word and staged in a per-wave LDS slot.
+//   PV: lane i owns d = i (+64); V^T words hold two consecutive tokens of one
+//       d, matching the packed P pairs, so each v_dot2 does two tokens.
+// Kernel arguments: the pointers are passed as separate __restrict__ kernel
+// parameters so that uniform metadata reads become scalar loads.
+struct Scalars {
+  int64_t num_blocks;
+  int32_t hq, hkv, group;
+  float scale_log2;
+};
+
+#define TREEPO_PARTIAL_PARAMS                                                         \
+  const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,            \
+      const uint16_t *__restrict__ q, const int32_t *__restrict__ items,             \
+      const int32_t *__restrict__ rowsets, const int32_t *__restrict__ tiles,        \
+      float *__restrict__ part_o, float *__restrict__ part_ml, Scalars sc
+#define TREEPO_PARTIAL_ARGS kpool, vpool, q, items, rowsets, tiles, part_o, part_ml, sc
+
+template <int D, int M>
+__device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g,
+                                          TileSmem<D>& sm) {
+  constexpr int kKW = D / 8;   // K words per lane in QK
+  constexpr int kKC = D / 32;  // K chunks per lane in QK
+  constexpr int kDD = D / 64;  // d values per lane in PV
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t = lane >> 2;
+  const int j = lane & 3;
+  const int rowset = it[1], tb = it[3], te = it[4], pbase = it[5], rows = it[6];
+  const int G = sc.group;
+
+  float m_run[M], l_run[M], acc[M][kDD];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    m_run[m] = -INFINITY;
+    l_run[m] = 0.f;
+#pragma unroll
+    for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = 0.f;
+  }
+
+  const int nt = te - tb;
+  const uint32_t buf0 = lds_addr(sm.kv[0]);
+  constexpr uint32_t kBufBytes = 2 * kTile * D * 2;
+  dma_tile<D>(kpool, vpool, sc.num_blocks, g, tiles[4 * tb], buf0, wave, lane);
+
+  uint32_t qr[M][kKW];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    const int leaf = rowsets[rowset + m / G];
+    const int head = g * G + m % G;
+    const uint4* qp = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(leaf) * sc.hq + head) * D);
+#pragma unroll
+    for (int i = 0; i < kKC; ++i) {
+      const uint4 v = qp[j + 4 * i];
+      qr[m][4 * i + 0] = v.x;
+      qr[m][4 * i + 1] = v.y;
+      qr[m][4 * i + 2] = v.z;
+      qr[m][4 * i + 3] = v.w;
+    }
+  }
+
+  // Make the query loads complete here, outside the tile loop: the compiler
+  // does not see the asm tile loads, and a wait for q inside the loop would
+  // also drain the prefetch of the next tile.
+#pragma unroll
+  for (int m = 0; m < M; ++m)
+#pragma unroll
+    for (int w = 0; w < kKW; ++w) asm volatile("" ::"v"(qr[m][w]));
+
+  for (int k = 0; k < nt; ++k) {
+    const int valid = tiles[4 * (tb + k) + 3];
+    if (k + 1 < nt) {
+      dma_tile<D>(kpool, vpool, sc.num_blocks, g, tiles[4 * (tb + k + 1)],
+                  buf0 + ((k + 1) & 1) * kBufBytes, wave, lane);
+      barrier_tile_landed<D / 16>();
+    } else {
+      barrier_tile_landed<0>();
+    }
+    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 1]);
+    const char* vt = kt + kTile * D * 2;
+
+    // ---- scores
+    const int row = wave * 16 + t;
+    uint32_t kr[kKW];
+#pragma unroll
+    for (int i = 0; i < kKC; ++i) {
+      const int c = j + 4 * i;
+      const uint4 v = *reinterpret_cast<const uint4*>(kt + row * (D * 2) + ((c ^ k_swz(row)) << 4));
+      kr[4 * i + 0] = v.x;
+      kr[4 * i + 1] = v.y;
+      kr[4 * i + 2] = v.z;
+      kr[4 * i + 3] = v.w;
+    }
+    float s[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      float x = 0.f;
+#pragma unroll
+      for (int w = 0; w < kKW; ++w) x = dot2(qr[m][w], kr[w], x);
+      x = quad_sum(x);
+      s[m] = row < valid ? x * sc.scale_log2 : -INFINITY;
+    }
+
+    // ---- online softmax over this wave's 16 tokens
+    uint32_t pk[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      float mx = s[m];
+      mx = fmaxf(mx, __shfl_xor(mx, 4));
+      mx = fmaxf(mx, __shfl_xor(mx, 8));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m_run[m], mx);
+      const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[m] - mn);
+      const float p = s[m] == -INFINITY ? 0.f : fast_exp2(s[m] - mn);
+      const uint32_t pb = f2bf_bits(p);
+      l_run[m] = l_run[m] * alpha + bf_bits2f(pb);
+#pragma unroll
+      for (int dd = 0; dd < kDD; ++dd) acc[m][dd] *= alpha;
+      m_run[m] = mn;
+      const uint32_t partner = static_cast<uint32_t>(__shfl_xor(static_cast<int>(pb), 4));
+      pk[m] = pb | (partner << 16);
+    }
+    if ((t & 1) == 0 && j == 0) {
+#pragma unroll
+      for (int m = 0; m < M; ++m) sm.pbuf[wave][t >> 1][m] = pk[m];
+    }
+
+    // ---- P V
+    uint32_t vw[kDD][8];
+#pragma unroll
+    for (int dd = 0; dd < kDD; ++dd) {
+      const int d = lane + 64 * dd;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint4 v = *reinterpret_cast<const uint4*>(vt + d * 128 + ((((2 * wave + h) ^ (d & 7))) << 4));
+        vw[dd][4 * h + 0] = v.x;
+        vw[dd][4 * h + 1] = v.y;
+        vw[dd][4 * h + 2] = v.z;
+        vw[dd][4 * h + 3] = v.w;
+      }
+    }
+    if (valid < kTile) {
+      // tokens past the node's length may hold anything; P is 0 there, and the
+      // V halves are cleared so that 0 * garbage cannot produce NaN
+#pragma unroll
+      for (int tp = 0; tp < 8; ++tp) {
+        const int tk = wave * 16 + 2 * tp;
+        const uint32_t msk = tk >= valid ? 0u : (tk + 1 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
+#pragma unroll
+        for (int dd = 0; dd < kDD; ++dd) vw[dd][tp] &= msk;
+      }
+    }
+#pragma unroll
+    for (int tp = 0; tp < 8; ++tp) {
+      const uint4 p0 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][0]);
+      const uint4 p1 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][4]);
+      const uint32_t pw[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+      for (int m = 0; m < M; ++m)
+#pragma unroll
+        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = dot2(pw[m], vw[dd][tp], acc[m][dd]);
+    }
+    barrier_lds_reads_done();
+  }
+
+  // ---- merge the four waves' states and write the partial rows
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    float l = l_run[m];
+    l += __shfl_xor(l, 4);
+    l += __shfl_xor(l, 8);
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    l_run[m] = l;
+  }
+  float* oacc = reinterpret_cast<float*>(sm.kv);  // [waves][M][D]
+  float* mlb = oacc + kWaves * M * D;             // [waves][M][2]
+#pragma unroll
+  for (int m = 0; m < M; ++m)
+#pragma unroll
+    for (int dd = 0; dd < kDD; ++dd) oacc[(wave * M + m) * D + lane + 64 * dd] = acc[m][dd];
+  if (lane == 0) {
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      mlb[(wave * M + m) * 2 + 0] = m_run[m];
+      mlb[(wave * M + m) * 2 + 1] = l_run[m];
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < M * D; idx += kThreads) {
+    const int m = idx / D;
+    const int d = idx % D;
+    float mstar = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) mstar = fmaxf(mstar, mlb[(w * M + m) * 2]);
+    float o = 0.f, l = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float mw = mlb[(w * M + m) * 2];
+      if (mw != -INFINITY) {
+        const float f = fast_exp2(mw - mstar);
+        o += f * oacc[(w * M + m) * D + d];
+        l += f * mlb[(w * M + m) * 2 + 1];
+      }
+    }
+    const int64_t slot = static_cast<int64_t>(pbase) + static_cast<int64_t>(g) * rows + m;
+    part_o[slot * D + d] = o;
+    if (d == 0) {
+      part_ml[slot * 2 + 0] = mstar;
+      part_ml[slot * 2 + 1] = l;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void partial_valu_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
+  __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;
+  const int item = first_item + static_cast<int>(blockIdx.x) / sc.hkv;
+  const int g = static_cast<int>(blockIdx.x) % sc.hkv;
+  const int32_t* it = items + 8 * item;
+  switch (it[6]) {
+    case 1: valu_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 2: valu_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 3: valu_item<D, 3>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 4: valu_item<D, 4>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 5: valu_item<D, 5>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 6: valu_item<D, 6>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 7: valu_item<D, 7>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 8: valu_item<D, 8>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    default: break;
+  }
+}
+
+// ---- combine ------------------------------------------------------------------
+//
+// One wave per (leaf, query head): m* = max m_i, L = sum l_i 2^(m_i - m*),
+// out = sum 2^(m_i - m*) O_i / L, lse = (m* + log2 L) ln 2.  Partials of empty
+// pieces (m = -inf) contribute nothing.  Entries are visited in chain order.
+template <int D>
+__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
+  constexpr int kPL = D / 64;
+  const int lane = threadIdx.x & 63;
+  const int gw = static_cast<int>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+  if (gw >= a.n_leaves * a.hq) return;
+  const int x = gw / a.hq;
+  const int h = gw % a.hq;
+  const int g = h / a.group;
+  const int hp = h % a.group;
+  const int e0 = a.leaf_off[x], e1 = a.leaf_off[x + 1];
+  float mstar = -INFINITY;
+  for (int e = e0 + lane; e < e1; e += 64) {
+    const int slot = a.entries[2 * e] + g * a.entries[2 * e + 1] + hp;
+    mstar = fmaxf(mstar, a.part_ml[2 * static_cast<int64_t>(slot)]);
+  }
+  mstar = fmaxf(mstar, __shfl_xor(mstar, 1));
+  mstar = fmaxf(mstar, __shfl_xor(mstar, 2));
+  mstar = fmaxf(mstar, __shfl_xor(mstar, 4));
+  mstar = fmaxf(mstar, __shfl_xor(mstar, 8));
+  mstar = fmaxf(mstar, __shfl_xor(mstar, 16));
+  mstar = fmaxf(mstar, __shfl_xor(mstar, 32));
+  float o[kPL];
+#pragma unroll
+  for (int i = 0; i < kPL; ++i) o[i] = 0.f;
+  float l = 0.f;
+  for (int e = e0; e < e1; ++e) {
+    const int64_t slot = a.entries[2 * e] + static_cast<int64_t>(g) * a.entries[2 * e + 1] + hp;
+    const float mi = a.part_ml[2 * slot];
+    if (mi == -INFINITY) continue;
+    const float f = fast_exp2(mi - mstar);
+    l += f * a.part_ml[2 * slot + 1];
+    const float* po = a.part_o + slot * D + lane * kPL;
+#pragma unroll
+    for (int i = 0; i < kPL; ++i) o[i] += f * po[i];
+  }
+  const float inv = 1.f / l;
+  float* op = a.out + (static_cast<int64_t>(x) * a.hq + h) * D + lane * kPL;
+#pragma unroll
+  for (int i = 0; i < kPL; ++i) op[i] = o[i] * inv;
+  if (a.lse != nullptr && lane == 0) a.lse[static_cast<int64_t>(x) * a.hq + h] = (mstar + __log2f(l)) * kLn2;
+}
+
+// ---- KV append --------------------------------------------------------------
+//
+// One workgroup per (piece, KV head).  K rows are copied with 16-byte moves;
+// V rows are transposed through LDS (padded rows, no bank conflicts) and
+// written as runs of consecutive tokens of each d-row of the transposed block.
+constexpr int kMaxPieces = 128;
+struct AppendBatch {
+  int32_t n;
+  int32_t pad;
+  AppendPiece p[kMaxPieces];
+};
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __restrict__ ksrc,
+                                                             const uint16_t* __restrict__ vsrc,
+                                                             uint16_t* __restrict__ kpool,
+                                                             uint16_t* __restrict__ vpool,
+                                                             int64_t num_blocks, int32_t hkv,
+                                                             AppendBatch b) {
+  constexpr int kPad = D + 2;
+  __shared__ uint16_t vt[kTile * kPad];
+  const AppendPiece pc = b.p[blockIdx.x];
+  const int g = blockIdx.y;
+  const int64_t blk = static_cast<int64_t>(g) * num_blocks + pc.block;
+  constexpr int kCh = D / 8;
+  for (int idx = threadIdx.x; idx < pc.count * kCh; idx += kThreads) {
+    const int i = idx / kCh, c = idx % kCh;
+    const int64_t src = (static_cast<int64_t>(pc.src_row + i) * hkv + g) * D + c * 8;
+    const uint4 kvv = *reinterpret_cast<const uint4*>(ksrc + src);
+    *reinterpret_cast<uint4*>(kpool + (blk * kTile + pc.off + i) * D + c * 8) = kvv;
+    const uint4 vv = *reinterpret_cast<const uint4*>(vsrc + src);
+    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      vt[i * kPad + c * 8 + 2 * e] = static_cast<uint16_t>(w[e] & 0xFFFFu);
+      vt[i * kPad + c * 8 + 2 * e + 1] = static_cast<uint16_t>(w[e] >> 16);
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < D * pc.count; idx += kThreads) {
+    const int d = idx / pc.count, i = idx % pc.count;
+    vpool[(blk * D + d) * kTile + pc.off + i] = vt[i * kPad + d];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_partial_valu(const DecodeArgs& a, int32_t first_item, int32_t n_items,
+                               hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(n_items) * a.hkv);
+  const Scalars sc{a.num_blocks, a.hq, a.hkv, a.group, a.scale_log2};
+  if (a.d == 128)
+    partial_valu_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
+                                                       a.part_o, a.part_ml, sc, first_item);
+  else
+    partial_valu_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
+                                                      a.part_o, a.part_ml, sc, first_item);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
+  const int64_t waves = static_cast<int64_t>(a.n_leaves) * a.hq;
+  const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
+  if (a.d == 128)
+    combine_kernel<128><<<grid, kThreads, 0, s>>>(a);
+  else
+    combine_kernel<64><<<grid, kThreads, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool,
+                            uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
+                            const AppendPiece* pieces, int32_t n_pieces, hipStream_t s) {
+  for (int32_t p0 = 0; p0 < n_pieces; p0 += kMaxPieces) {
+    AppendBatch b{};
+    b.n = n_pieces - p0 < kMaxPieces ? n_pieces - p0 : kMaxPieces;
+    for (int32_t i = 0; i < b.n; ++i) b.p[i] = pieces[p0 + i];
+    const dim3 grid(static_cast<unsigned>(b.n), static_cast<unsigned>(hkv));
+    if (d == 128)
+      kv_append_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, b);
+    else
+      kv_append_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, b);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace treepo

@@ -1,0 +1,580 @@
+// C-ABI of the segment-tree decode-attention library: argument validation,
+// plan caching, pinned-staging uploads into the caller's workspace, kernel
+// launches on the caller's stream, metadata export and kernel timing.
+#include "treepo.h"
+
+#include <algorithm>
+#include <array>
+#include <cstring>
+#include <new>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "kernels.h"
+#include "tree_core.h"
+
+using treepo::Plan;
+using treepo::PlanMode;
+using treepo::PlanParams;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kPlanCache = 4;
+constexpr int kRing = 4;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct CachedPlan {
+  uint64_t version = 0;
+  int32_t mode = 0;
+  std::vector<int32_t> leaves;
+  Plan plan;
+  std::vector<char> blob;  // host image of the plan region
+  size_t off_items = 0, off_rowsets = 0, off_tiles = 0, off_leaf_off = 0, off_entries = 0;
+  size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;
+  uint64_t uid = 0;
+  uint64_t last_use = 0;
+};
+
+struct PinnedSlot {
+  void* p = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+
+struct TimedLaunch {
+  int kind;
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct treepo_ctx {
+  treepo_config cfg;
+  treepo::Tree tree;
+  PlanParams params;
+  std::string last_error;
+  std::vector<CachedPlan> plans;
+  uint64_t next_uid = 1;
+  uint64_t clock = 0;
+  std::vector<std::pair<void*, uint64_t>> uploaded;  // workspace -> plan uid
+  std::array<PinnedSlot, kRing> ring;
+  int ring_next = 0;
+  bool profiling = false;
+  std::vector<TimedLaunch> timed;
+  std::vector<hipEvent_t> spare_events;
+  double prof_ms[TREEPO_KERNEL_KINDS] = {0, 0, 0, 0};
+  int64_t prof_n[TREEPO_KERNEL_KINDS] = {0, 0, 0, 0};
+
+  treepo_ctx(const treepo_config& c)
+      : cfg(c), tree(c.block_tokens, c.num_blocks, c.max_nodes) {}
+};
+
+namespace {
+
+int32_t fail(treepo_ctx* ctx, int32_t code, const std::string& msg) {
+  if (ctx) ctx->last_error = msg;
+  return code;
+}
+
+int32_t hip_fail(treepo_ctx* ctx, hipError_t e, const char* what) {
+  return fail(ctx, TREEPO_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+hipError_t get_event(treepo_ctx* ctx, hipEvent_t* ev) {
+  if (!ctx->spare_events.empty()) {
+    *ev = ctx->spare_events.back();
+    ctx->spare_events.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(ev);
+}
+
+hipError_t drain_timings(treepo_ctx* ctx) {
+  for (const TimedLaunch& t : ctx->timed) {
+    hipError_t e = hipEventSynchronize(t.stop);
+    if (e != hipSuccess) return e;
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, t.start, t.stop);
+    if (e != hipSuccess) return e;
+    ctx->prof_ms[t.kind] += ms;
+    ctx->prof_n[t.kind] += 1;
+    ctx->spare_events.push_back(t.start);
+    ctx->spare_events.push_back(t.stop);
+  }
+  ctx->timed.clear();
+  return hipSuccess;
+}
+
+// Runs `launch` bracketed by events when profiling is on.
+template <class F>
+hipError_t timed_launch(treepo_ctx* ctx, int kind, hipStream_t s, F launch) {
+  if (!ctx->profiling) return launch();
+  if (ctx->timed.size() > 8192) {
+    hipError_t e = drain_timings(ctx);
+    if (e != hipSuccess) return e;
+  }
+  TimedLaunch t{kind, nullptr, nullptr};
+  hipError_t e = get_event(ctx, &t.start);
+  if (e == hipSuccess) e = get_event(ctx, &t.stop);
+  if (e == hipSuccess) e = hipEventRecord(t.start, s);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(t.stop, s);
+  if (e != hipSuccess) return e;
+  ctx->timed.push_back(t);
+  return hipSuccess;
+}
+
+// Copies `bytes` of host data to device `dst` on `s` through a pinned slot.
+hipError_t upload(treepo_ctx* ctx, void* dst, const void* src, size_t bytes, hipStream_t s) {
+  PinnedSlot& sl = ctx->ring[ctx->ring_next];
+  ctx->ring_next = (ctx->ring_next + 1) % kRing;
+  hipError_t e;
+  if (sl.pending) {
+    e = hipEventSynchronize(sl.ev);
+    if (e != hipSuccess) return e;
+    sl.pending = false;
+  }
+  if (!sl.ev) {
+    e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+  }
+  if (sl.cap < bytes) {
+    if (sl.p) {
+      e = hipHostFree(sl.p);
+      if (e != hipSuccess) return e;
+      sl.p = nullptr;
+      sl.cap = 0;
+    }
+    const size_t cap = std::max<size_t>(bytes, 1 << 20);
+    e = hipHostMalloc(&sl.p, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return e;
+    sl.cap = cap;
+  }
+  std::memcpy(sl.p, src, bytes);
+  e = hipMemcpyAsync(dst, sl.p, bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(sl.ev, s);
+  if (e != hipSuccess) return e;
+  sl.pending = true;
+  return hipSuccess;
+}
+
+template <class T>
+void put(std::vector<char>& blob, size_t off, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
+}
+
+int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode, CachedPlan** out) {
+  ++ctx->clock;
+  for (CachedPlan& cp : ctx->plans) {
+    if (cp.version == ctx->tree.version() && cp.mode == mode &&
+        cp.leaves.size() == static_cast<size_t>(n) &&
+        std::equal(cp.leaves.begin(), cp.leaves.end(), leaves)) {
+      cp.last_use = ctx->clock;
+      *out = &cp;
+      return TREEPO_OK;
+    }
+  }
+  CachedPlan cp;
+  std::string err;
+  int32_t st = treepo::build_plan(ctx->tree, n, leaves, static_cast<PlanMode>(mode), ctx->params,
+                                  &cp.plan, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  const Plan& p = cp.plan;
+  size_t off = 0;
+  cp.off_items = off;
+  off = align_up(off + p.items.size() * sizeof(treepo::Item));
+  cp.off_rowsets = off;
+  off = align_up(off + p.rowsets.size() * sizeof(int32_t));
+  cp.off_tiles = off;
+  off = align_up(off + p.tiles.size() * sizeof(treepo::Tile));
+  cp.off_leaf_off = off;
+  off = align_up(off + p.leaf_off.size() * sizeof(int32_t));
+  cp.off_entries = off;
+  off = align_up(off + p.entries.size() * sizeof(treepo::Entry));
+  cp.blob.assign(off, 0);
+  put(cp.blob, cp.off_items, p.items);
+  put(cp.blob, cp.off_rowsets, p.rowsets);
+  put(cp.blob, cp.off_tiles, p.tiles);
+  put(cp.blob, cp.off_leaf_off, p.leaf_off);
+  put(cp.blob, cp.off_entries, p.entries);
+  cp.off_part_o = off;
+  off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
+  cp.off_part_ml = off;
+  off = align_up(off + static_cast<size_t>(p.partial_rows) * 2 * sizeof(float));
+  cp.ws_bytes = off;
+  cp.version = ctx->tree.version();
+  cp.mode = mode;
+  cp.leaves.assign(leaves, leaves + n);
+  cp.uid = ctx->next_uid++;
+  cp.last_use = ctx->clock;
+  if (static_cast<int>(ctx->plans.size()) >= kPlanCache) {
+    auto lru = std::min_element(ctx->plans.begin(), ctx->plans.end(),
+                                [](const CachedPlan& a, const CachedPlan& b) { return a.last_use < b.last_use; });
+    *lru = std::move(cp);
+    *out = &*lru;
+  } else {
+    ctx->plans.push_back(std::move(cp));
+    *out = &ctx->plans.back();
+  }
+  return TREEPO_OK;
+}
+
+int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q, float scale,
+               float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream, int32_t mode) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (!q || !out) return fail(ctx, TREEPO_EINVAL, "null q or out");
+  std::string err;
+  int32_t st = ctx->tree.check_leaves(n, leaves, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  CachedPlan* cp = nullptr;
+  st = get_plan(ctx, n, leaves, mode, &cp);
+  if (st != TREEPO_OK) return st;
+  if (!ws || ws_bytes < cp->ws_bytes)
+    return fail(ctx, TREEPO_EWORKSPACE, "workspace missing or smaller than treepo_decode_workspace_size");
+  char* wsb = static_cast<char*>(ws);
+  auto up = std::find_if(ctx->uploaded.begin(), ctx->uploaded.end(),
+                         [&](const std::pair<void*, uint64_t>& u) { return u.first == ws; });
+  if (up == ctx->uploaded.end() || up->second != cp->uid) {
+    hipError_t e = upload(ctx, wsb, cp->blob.data(), cp->blob.size(), stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "plan upload");
+    if (up == ctx->uploaded.end())
+      ctx->uploaded.emplace_back(ws, cp->uid);
+    else
+      up->second = cp->uid;
+  }
+  const Plan& p = cp->plan;
+  treepo::DecodeArgs a;
+  a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
+  a.v_pool = static_cast<const uint16_t*>(ctx->cfg.v_pool);
+  a.num_blocks = ctx->cfg.num_blocks;
+  a.hq = ctx->cfg.num_q_heads;
+  a.hkv = ctx->cfg.num_kv_heads;
+  a.group = a.hq / a.hkv;
+  a.d = ctx->cfg.head_dim;
+  a.q = static_cast<const uint16_t*>(q);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.items = reinterpret_cast<const int32_t*>(wsb + cp->off_items);
+  a.rowsets = reinterpret_cast<const int32_t*>(wsb + cp->off_rowsets);
+  a.tiles = reinterpret_cast<const int32_t*>(wsb + cp->off_tiles);
+  a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
+  a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
+  a.leaf_off = reinterpret_cast<const int32_t*>(wsb + cp->off_leaf_off);
+  a.entries = reinterpret_cast<const int32_t*>(wsb + cp->off_entries);
+  a.n_leaves = n;
+  a.out = out;
+  a.lse = lse;
+  hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL_VALU, stream, [&] {
+    return treepo::launch_partial_valu(a, 0, p.n_valu_items, stream);
+  });
+  if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
+  e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
+  if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
+  return TREEPO_OK;
+}
+
+// Splits a validated append into block-aligned pieces (source rows in call order).
+void append_pieces(const treepo::Tree& t, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                   std::vector<treepo::AppendPiece>* out) {
+  const int32_t B = t.block_tokens();
+  std::vector<std::pair<int32_t, int32_t>> pending;  // node -> len so far in this call
+  out->clear();
+  int32_t src = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const treepo::Node& nd = t.nodes()[nodes[i]];
+    auto it = std::find_if(pending.begin(), pending.end(),
+                           [&](const std::pair<int32_t, int32_t>& pr) { return pr.first == nodes[i]; });
+    int32_t cur = it == pending.end() ? nd.len : it->second;
+    int32_t left = ntok[i];
+    while (left > 0) {
+      const int32_t off = cur % B;
+      const int32_t cnt = std::min(left, B - off);
+      out->push_back(treepo::AppendPiece{src, nd.block_begin + cur / B, off, cnt});
+      src += cnt;
+      cur += cnt;
+      left -= cnt;
+    }
+    if (it == pending.end())
+      pending.emplace_back(nodes[i], cur);
+    else
+      it->second = cur;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
+  if (!cfg || !out) return TREEPO_EINVAL;
+  const treepo_config& c = *cfg;
+  if (c.num_q_heads < 1 || c.num_kv_heads < 1 || c.num_q_heads % c.num_kv_heads != 0 ||
+      c.num_blocks < 0 || c.num_blocks > INT32_MAX || c.max_nodes < 0 || c.reserved != 0 ||
+      !c.k_pool || !c.v_pool)
+    return TREEPO_EINVAL;
+  if ((c.head_dim != 64 && c.head_dim != 128) || c.block_tokens != treepo::kTile ||
+      c.num_q_heads / c.num_kv_heads > 8)
+    return TREEPO_EUNSUPPORTED;
+  treepo_ctx* ctx = new (std::nothrow) treepo_ctx(c);
+  if (!ctx) return TREEPO_ENOMEM;
+  ctx->params.group = c.num_q_heads / c.num_kv_heads;
+  ctx->params.num_kv_heads = c.num_kv_heads;
+  ctx->params.valu_max_rows = 8;
+  ctx->params.mfma_max_rows = 256;
+  ctx->params.concurrent_wgs = 512;
+  ctx->params.max_chunk_tiles = 64;
+  ctx->params.mfma_enabled = 0;
+  *out = ctx;
+  return TREEPO_OK;
+}
+
+int32_t treepo_destroy(treepo_ctx* ctx) {
+  if (!ctx) return TREEPO_OK;
+  for (PinnedSlot& s : ctx->ring) {
+    if (s.pending) (void)hipEventSynchronize(s.ev);
+    if (s.p) (void)hipHostFree(s.p);
+    if (s.ev) (void)hipEventDestroy(s.ev);
+  }
+  for (const TimedLaunch& t : ctx->timed) {
+    (void)hipEventSynchronize(t.stop);
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  for (hipEvent_t e : ctx->spare_events) (void)hipEventDestroy(e);
+  delete ctx;
+  return TREEPO_OK;
+}
+
+int32_t treepo_new_root(treepo_ctx* ctx, int32_t cap_tokens, int32_t* node_out) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  const int32_t st = ctx->tree.new_root(cap_tokens, node_out, &err);
+  return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
+}
+
+int32_t treepo_fork(treepo_ctx* ctx, int32_t parent, int32_t n_children, int32_t child_cap,
+                    int32_t* children_out) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  const int32_t st = ctx->tree.fork(parent, n_children, child_cap, children_out, &err);
+  return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
+}
+
+int32_t treepo_kv_slots(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                        int64_t* rows_out) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  std::vector<int64_t> rows;
+  const int32_t st = ctx->tree.check_append(n, nodes, ntok, &rows, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  if (!rows.empty()) {
+    if (!rows_out) return fail(ctx, TREEPO_EINVAL, "null rows_out");
+    std::copy(rows.begin(), rows.end(), rows_out);
+  }
+  return TREEPO_OK;
+}
+
+int32_t treepo_kv_commit(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  const int32_t st = ctx->tree.check_append(n, nodes, ntok, nullptr, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  ctx->tree.apply_append(n, nodes, ntok);
+  return TREEPO_OK;
+}
+
+int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                         const void* k, const void* v, hipStream_t stream) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  int32_t st = ctx->tree.check_append(n, nodes, ntok, nullptr, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  int64_t total = 0;
+  for (int32_t i = 0; i < n; ++i) total += ntok[i];
+  if (total > 0) {
+    if (!k || !v) return fail(ctx, TREEPO_EINVAL, "null k or v with tokens to append");
+    std::vector<treepo::AppendPiece> pieces;
+    append_pieces(ctx->tree, n, nodes, ntok, &pieces);
+    const hipError_t e = timed_launch(ctx, TREEPO_KERNEL_APPEND, stream, [&] {
+      return treepo::launch_kv_append(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                                      static_cast<uint16_t*>(ctx->cfg.k_pool),
+                                      static_cast<uint16_t*>(ctx->cfg.v_pool), ctx->cfg.num_blocks,
+                                      ctx->cfg.num_kv_heads, ctx->cfg.head_dim, pieces.data(),
+                                      static_cast<int32_t>(pieces.size()), stream);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "append kernel launch");
+  }
+  ctx->tree.apply_append(n, nodes, ntok);
+  return TREEPO_OK;
+}
+
+int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                                     int32_t mode, size_t* bytes) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (!bytes || (mode != TREEPO_MODE_TREE && mode != TREEPO_MODE_NAIVE))
+    return fail(ctx, TREEPO_EINVAL, "null bytes or bad mode");
+  std::string err;
+  int32_t st = ctx->tree.check_leaves(n_leaves, leaves, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  CachedPlan* cp = nullptr;
+  st = get_plan(ctx, n_leaves, leaves, mode, &cp);
+  if (st != TREEPO_OK) return st;
+  *bytes = cp->ws_bytes;
+  return TREEPO_OK;
+}
+
+int32_t treepo_tree_decode(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, const void* q,
+                           float scale, float* out, float* lse, void* workspace, size_t ws_bytes,
+                           hipStream_t stream) {
+  return decode(ctx, n_leaves, leaves, q, scale, out, lse, workspace, ws_bytes, stream, TREEPO_MODE_TREE);
+}
+
+int32_t treepo_paged_decode_naive(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                                  const void* q, float scale, float* out, float* lse, void* workspace,
+                                  size_t ws_bytes, hipStream_t stream) {
+  return decode(ctx, n_leaves, leaves, q, scale, out, lse, workspace, ws_bytes, stream, TREEPO_MODE_NAIVE);
+}
+
+int32_t treepo_num_nodes(treepo_ctx* ctx, int32_t* n_nodes) {
+  if (!ctx || !n_nodes) return TREEPO_EINVAL;
+  *n_nodes = static_cast<int32_t>(ctx->tree.nodes().size());
+  return TREEPO_OK;
+}
+
+int32_t treepo_export_nodes(treepo_ctx* ctx, int32_t* records, int32_t capacity, int32_t* n_nodes) {
+  if (!ctx || !n_nodes || capacity < 0 || (capacity > 0 && !records)) return TREEPO_EINVAL;
+  const auto& nd = ctx->tree.nodes();
+  *n_nodes = static_cast<int32_t>(nd.size());
+  const int32_t m = std::min<int32_t>(capacity, static_cast<int32_t>(nd.size()));
+  for (int32_t i = 0; i < m; ++i) {
+    const treepo::Node& x = nd[i];
+    const int32_t r[TREEPO_NODE_FIELDS] = {x.parent, x.depth, x.start, x.len,
+                                           x.cap, x.block_begin, x.n_blocks, x.tree_id};
+    std::copy(r, r + TREEPO_NODE_FIELDS, records + static_cast<size_t>(i) * TREEPO_NODE_FIELDS);
+  }
+  return TREEPO_OK;
+}
+
+int32_t treepo_export_chains(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                             int32_t* chain_off, int32_t* chain_nodes, int32_t* block_off,
+                             int32_t* blocks, int32_t* total_chain, int32_t* total_blocks) {
+  if (!ctx || n_leaves < 0 || (n_leaves > 0 && !leaves) || !total_chain || !total_blocks)
+    return TREEPO_EINVAL;
+  const auto& nd = ctx->tree.nodes();
+  for (int32_t i = 0; i < n_leaves; ++i)
+    if (leaves[i] < 0 || leaves[i] >= static_cast<int32_t>(nd.size()))
+      return fail(ctx, TREEPO_EINVAL, "unknown leaf id");
+  const int32_t B = ctx->tree.block_tokens();
+  std::vector<int32_t> ch;
+  int32_t tc = 0, tb = 0;
+  const bool fill = chain_off && chain_nodes && block_off && blocks;
+  if (fill) {
+    chain_off[0] = 0;
+    block_off[0] = 0;
+  }
+  for (int32_t i = 0; i < n_leaves; ++i) {
+    ctx->tree.chain(leaves[i], &ch);
+    for (int32_t n : ch) {
+      if (fill) chain_nodes[tc] = n;
+      ++tc;
+      const int32_t nb = (nd[n].len + B - 1) / B;
+      for (int32_t k = 0; k < nb; ++k) {
+        if (fill) blocks[tb] = nd[n].block_begin + k;
+        ++tb;
+      }
+    }
+    if (fill) {
+      chain_off[i + 1] = tc;
+      block_off[i + 1] = tb;
+    }
+  }
+  *total_chain = tc;
+  *total_blocks = tb;
+  return TREEPO_OK;
+}
+
+int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t* nodes,
+                           int32_t* desc_off, int32_t* desc, int32_t* n_nodes, int32_t* total) {
+  if (!ctx || n_leaves < 0 || (n_leaves > 0 && !leaves) || !n_nodes || !total) return TREEPO_EINVAL;
+  const auto& nd = ctx->tree.nodes();
+  for (int32_t i = 0; i < n_leaves; ++i)
+    if (leaves[i] < 0 || leaves[i] >= static_cast<int32_t>(nd.size()))
+      return fail(ctx, TREEPO_EINVAL, "unknown leaf id");
+  std::vector<int32_t> nv, off, dv;
+  treepo::desc_sets(ctx->tree, n_leaves, leaves, &nv, &off, &dv);
+  *n_nodes = static_cast<int32_t>(nv.size());
+  *total = static_cast<int32_t>(dv.size());
+  if (nodes && desc_off && desc) {
+    std::copy(nv.begin(), nv.end(), nodes);
+    std::copy(off.begin(), off.end(), desc_off);
+    std::copy(dv.begin(), dv.end(), desc);
+  }
+  return TREEPO_OK;
+}
+
+int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t mode,
+                           int32_t* items, int32_t* rowsets, int32_t* tiles, int32_t* n_items,
+                           int32_t* n_rowsets, int32_t* n_tiles) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (!n_items || !n_rowsets || !n_tiles || (mode != TREEPO_MODE_TREE && mode != TREEPO_MODE_NAIVE))
+    return fail(ctx, TREEPO_EINVAL, "null count pointer or bad mode");
+  std::string err;
+  int32_t st = ctx->tree.check_leaves(n_leaves, leaves, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  CachedPlan* cp = nullptr;
+  st = get_plan(ctx, n_leaves, leaves, mode, &cp);
+  if (st != TREEPO_OK) return st;
+  const Plan& p = cp->plan;
+  *n_items = static_cast<int32_t>(p.items.size());
+  *n_rowsets = static_cast<int32_t>(p.rowsets.size());
+  *n_tiles = static_cast<int32_t>(p.tiles.size());
+  if (items && rowsets && tiles) {
+    std::memcpy(items, p.items.data(), p.items.size() * sizeof(treepo::Item));
+    std::memcpy(rowsets, p.rowsets.data(), p.rowsets.size() * sizeof(int32_t));
+    std::memcpy(tiles, p.tiles.data(), p.tiles.size() * sizeof(treepo::Tile));
+  }
+  return TREEPO_OK;
+}
+
+int32_t treepo_set_profiling(treepo_ctx* ctx, int32_t enable) {
+  if (!ctx) return TREEPO_EINVAL;
+  const hipError_t e = drain_timings(ctx);
+  ctx->profiling = enable != 0;
+  std::fill(ctx->prof_ms, ctx->prof_ms + TREEPO_KERNEL_KINDS, 0.0);
+  std::fill(ctx->prof_n, ctx->prof_n + TREEPO_KERNEL_KINDS, 0);
+  return e == hipSuccess ? TREEPO_OK : hip_fail(ctx, e, "profiling events");
+}
+
+int32_t treepo_profile_read(treepo_ctx* ctx, int32_t kind, double* total_ms, int64_t* launches) {
+  if (!ctx || kind < 0 || kind >= TREEPO_KERNEL_KINDS || !total_ms || !launches) return TREEPO_EINVAL;
+  const hipError_t e = drain_timings(ctx);
+  if (e != hipSuccess) return hip_fail(ctx, e, "profiling events");
+  *total_ms = ctx->prof_ms[kind];
+  *launches = ctx->prof_n[kind];
+  return TREEPO_OK;
+}
+
+const char* treepo_strerror(int32_t code) {
+  switch (code) {
+    case TREEPO_OK: return "ok";
+    case TREEPO_EINVAL: return "invalid argument";
+    case TREEPO_ENOMEM: return "pool blocks or node slots exhausted";
+    case TREEPO_EFULL: return "append past node capacity";
+    case TREEPO_EFROZEN: return "append to a node that has children";
+    case TREEPO_EEMPTY: return "decode of an empty chain";
+    case TREEPO_EWORKSPACE: return "workspace missing or too small";
+    case TREEPO_EHIP: return "HIP runtime error";
+    case TREEPO_EUNSUPPORTED: return "unsupported shape";
+    default: return "unknown status";
+  }
+}
+
+const char* treepo_last_error(treepo_ctx* ctx) { return ctx ? ctx->last_error.c_str() : ""; }
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+"""Every status code forced from the host; a failing call changes no state.
+The library's codes agree with the oracle model's on random op sequences."""
+
+import numpy as np
+import pytest
+
+from oracle import metadata as M
+from paper_2508_17445_amd import TreePOError
+from paper_2508_17445_amd import treepo as T
+from tests.lib_helpers import FAKE_POOL, ensure_lib, host_ctx
+
+
+def _code(fn, *a):
+    try:
+        fn(*a)
+    except TreePOError as e:
+        return e.code
+    return 0
+
+
+def test_create_rejects_bad_configs():
+    ensure_lib()
+    from paper_2508_17445_amd import Context
+    bad = [
+        (dict(hq=6, hkv=4, d=64), T.EINVAL),
+        (dict(hq=4, hkv=1, d=96), T.EUNSUPPORTED),
+        (dict(hq=32, hkv=2, d=128), T.EUNSUPPORTED),
+        (dict(hq=4, hkv=1, d=64, block_tokens=16), T.EUNSUPPORTED),
+    ]
+    for kw, code in bad:
+        bt = kw.pop("block_tokens", 64)
+        with pytest.raises(TreePOError) as e:
+            Context(kw["hq"], kw["hkv"], kw["d"], 10, 10, FAKE_POOL, FAKE_POOL, bt)
+        assert e.value.code == code
+    with pytest.raises(TreePOError) as e:
+        Context(4, 1, 64, 10, 10, 0, FAKE_POOL)
+    assert e.value.code == T.EINVAL
+
+
+def test_each_code_and_no_state_change():
+    ctx = host_ctx(num_blocks=10, max_nodes=6)
+    r = ctx.new_root(128)                                  # 2 blocks
+    snap = ctx.export_nodes().copy()
+    assert _code(ctx.new_root, 0) == T.EINVAL
+    assert _code(ctx.fork, 7, 1, 64) == T.EINVAL
+    assert _code(ctx.fork, r, 0, 64) == T.EINVAL
+    assert _code(ctx.fork, r, 1, 0) == T.EINVAL
+    assert _code(ctx.fork, r, 5, 64 * 2) == T.ENOMEM       # 10 blocks > 8 left
+    assert _code(ctx.fork, r, 6, 1) == T.ENOMEM            # node table
+    assert _code(ctx.kv_commit, [r], [129]) == T.EFULL
+    assert _code(ctx.kv_commit, [r, r], [100, 29]) == T.EFULL
+    assert _code(ctx.kv_commit, [r], [-1]) == T.EINVAL
+    assert _code(ctx.kv_commit, [9], [1]) == T.EINVAL
+    assert _code(ctx.workspace_size, [r]) == T.EEMPTY
+    assert np.array_equal(ctx.export_nodes(), snap)
+    ctx.kv_commit([r], [5])
+    a, = ctx.fork(r, 1, 64)
+    assert _code(ctx.kv_commit, [r], [1]) == T.EFROZEN
+    assert _code(ctx.kv_commit, [a, r], [1, 1]) == T.EFROZEN   # whole call rejected
+    assert ctx.export_nodes()[a][3] == 0
+    assert _code(ctx.workspace_size, [a, 17]) == T.EINVAL
+    assert _code(ctx.workspace_size, []) == T.EINVAL
+    # decode: workspace is checked before any device work
+    assert _code(ctx.tree_decode, [a], FAKE_POOL, 0.1, FAKE_POOL, None, None, 0) == T.EWORKSPACE
+    assert _code(ctx.tree_decode, [a], None, 0.1, FAKE_POOL, None, FAKE_POOL, 1 << 30) == T.EINVAL
+    # append with tokens but no K/V buffers
+    assert _code(ctx.kv_append, [a], [1], None, None, 0) == T.EINVAL
+    assert ctx.export_nodes()[a][3] == 0
+    assert ctx.lib.treepo_last_error(ctx.h).decode() != ""
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_codes_match_oracle_on_random_ops(seed):
+    rng = np.random.default_rng(seed)
+    ctx = host_ctx(num_blocks=40, max_nodes=25)
+    model = M.TreeModel(64, 40, 25)
+    for _ in range(60):
+        n = len(model.nodes)
+        kind = rng.integers(4)
+        if kind == 0 or n == 0:
+            cap = int(rng.integers(-1, 300))
+            args = (cap,)
+            f_lib, f_ref = ctx.new_root, model.new_root
+        elif kind == 1:
+            args = (int(rng.integers(-1, n + 1)), int(rng.integers(0, 4)), int(rng.integers(0, 200)))
+            f_lib, f_ref = ctx.fork, model.fork
+        else:
+            k = int(rng.integers(1, 4))
+            nodes = [int(x) for x in rng.integers(-1, n + 1, size=k)]
+            ntok = [int(x) for x in rng.integers(-1, 80, size=k)]
+            args = (nodes, ntok)
+            f_lib, f_ref = ctx.kv_commit, model.append
+        try:
+            r_ref = f_ref(*args)
+            c_ref = 0
+        except M.TreeError as e:
+            c_ref, r_ref = e.code, None
+        try:
+            r_lib = f_lib(*args)
+            c_lib = 0
+        except TreePOError as e:
+            c_lib, r_lib = e.code, None
+        assert c_lib == c_ref, (args, c_lib, c_ref)
+        if c_ref == 0 and r_ref is not None:
+            assert r_lib == r_ref
+        ref = np.array([model.record(i) for i in range(len(model.nodes))], dtype=np.int32).reshape(-1, 8)
+        assert np.array_equal(ctx.export_nodes().reshape(-1, 8), ref)
