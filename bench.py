@@ -1,0 +1,223 @@
+"""Decode-step throughput of segment-tree attention on one MI355X.
+
+A step is one ``treepo_tree_decode`` call: every active leaf's query (all Hq
+heads) attends over its root-to-leaf chain of segments, with inputs already
+resident in HBM.  The default workload is the single 7B-style tree (1 prompt
+of 512 tokens, segment length 512, binary forks at the first 4 boundaries, 16
+leaves of 7680 tokens, Hq=28 Hkv=4 D=128, bf16 N(0,1) data).
+
+Timing protocol: ``--replicas`` copies of the pools are built and the steps
+rotate over them, so that no step finds its KV in the 256 MB Infinity Cache
+(the whole working set of this tree is ~200 MB).  W untimed warm-up steps,
+then exactly K timed steps between two device synchronisations.  The library
+brackets every kernel launch with HIP events on the launch stream during the
+timed region, which gives the dominant kernel's average duration.  The same
+protocol times the per-leaf paged-decode baseline, and a streaming-read probe
+gives the attainable HBM read bandwidth.  The fp64 oracle is timed on the
+host cores on the same workload.
+
+Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "tree-decode leaf-token-steps/sec + achieved HBM GB/s on unique KV (1 MI355X)"
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--replicas", type=int, default=0, help="pool copies rotated over (0: auto)")
+    ap.add_argument("--no-naive", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def _ensure_built():
+    from paper_2508_17445_amd.treepo import LIB_PATH
+    if not os.path.exists(LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+
+
+def _unique_kv(dt):
+    """Tokens per KV head over the nodes of the leaves' chains, each counted once."""
+    model_len = {}
+    nodes = dt.ctx.export_nodes()
+    used = set()
+    for x in dt.leaves:
+        y = x
+        while y != -1 and y not in used:
+            used.add(y)
+            y = int(nodes[y][0])
+    tok = sum(int(nodes[n][3]) for n in used)
+    logical = 0
+    for x in dt.leaves:
+        y = x
+        while y != -1:
+            logical += int(nodes[y][3])
+            y = int(nodes[y][0])
+    return tok, logical
+
+
+def _time_mode(reps, mode, steps, warmup, kernel_kind):
+    import torch
+    from paper_2508_17445_amd import KERNEL_COMBINE
+    bufs = []
+    for r in reps:
+        out, lse = r.outputs()
+        bufs.append((out, lse, r.workspace(mode)))
+    fn = [(r.ctx.tree_decode if mode == 0 else r.ctx.paged_decode_naive) for r in reps]
+    for i in range(warmup):
+        j = i % len(reps)
+        fn[j](reps[j].leaves, reps[j].q, reps[j].cfg.scale, bufs[j][0], bufs[j][1], bufs[j][2])
+    torch.cuda.synchronize()
+    for r in reps:
+        r.ctx.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        j = i % len(reps)
+        fn[j](reps[j].leaves, reps[j].q, reps[j].cfg.scale, bufs[j][0], bufs[j][1], bufs[j][2])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kms, kn, cms, cn = 0.0, 0, 0.0, 0
+    for r in reps:
+        a, b = r.ctx.profile_read(kernel_kind)
+        c, d = r.ctx.profile_read(KERNEL_COMBINE)
+        kms += a; kn += b; cms += c; cn += d
+        r.ctx.set_profiling(False)
+    return (t1 - t0) * 1e3 / steps, kms / max(kn, 1), cms / max(cn, 1), kn // max(steps, 1)
+
+
+def _probe_read(nbytes=4 << 30, iters=10):
+    import torch
+    from paper_2508_17445_amd import bench_read
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(4096, dtype=torch.float32, device="cuda")
+    bench_read(src, nbytes, sink)
+    torch.cuda.synchronize()
+    st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    st.record()
+    for _ in range(iters):
+        bench_read(src, nbytes, sink)
+    en.record()
+    torch.cuda.synchronize()
+    ms = st.elapsed_time(en) / iters
+    del src
+    return nbytes / (ms * 1e-3) / 1e9
+
+
+def _cpu_baseline(cfg_id, seconds):
+    import numpy as np
+    from oracle import attention as A
+    from oracle import metadata as M
+    from workloads import CONFIGS, build_call_log, query_bits
+    from workloads.device import NodeData
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    cfg, log = CONFIGS[cfg_id], build_call_log(cfg_id)
+    model = M.replay(log, cfg.block_tokens, 1 << 30, 1 << 30)
+    data = NodeData(cfg, log)
+    data.prefetch(sorted({n for x in log.leaves for n in model.chain(x)}))
+    q = query_bits(cfg.seed, 0, len(log.leaves), cfg.hq, cfg.d)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        A.tree_decode(model, data, log.leaves, q, cfg.scale)
+        reps += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    cores = min(len(os.sched_getaffinity(0)), blas_threads)
+    return {"value": len(log.leaves) * reps / dt, "unit": "leaf-token-steps/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{reps} full decode step(s) of the same workload ({len(log.leaves)} leaves, fp64 numpy, "
+                      f"chains materialised per leaf) in {dt:.1f} s; host has "
+                      f"{len(os.sched_getaffinity(0))} cores, BLAS threads {blas_threads}"}
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the decode path has no multi-GPU "
+                                   "mode (see DESIGN.md for how it would shard)", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    _ensure_built()
+    from paper_2508_17445_amd import KERNEL_PARTIAL_VALU
+    from workloads import CONFIGS
+    from workloads.device import DeviceTree
+
+    cfg = CONFIGS[args.config]
+    base = DeviceTree(cfg_id=args.config)
+    uniq_tok, logical_tok = _unique_kv(base)
+    kv_bytes_per_tok = cfg.hkv * cfg.d * 2 * 2
+    uniq_bytes = uniq_tok * kv_bytes_per_tok
+    n_rep = args.replicas or max(1, math.ceil(1.2e9 / uniq_bytes))
+    reps = [base] + [base.clone() for _ in range(n_rep - 1)]
+
+    ms, kern_ms, comb_ms, launches = _time_mode(reps, 0, args.steps, args.warmup, KERNEL_PARTIAL_VALU)
+    n_leaves = len(base.leaves)
+    value = n_leaves / (ms * 1e-3)
+    achieved_step = uniq_bytes / (ms * 1e-3) / 1e9
+    achieved_kern = uniq_bytes / (kern_ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "leaf-token-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/K/V; call-log-built tree)",
+        "config": {
+            "workload": f"config {args.config}: {cfg.name}", "leaves": n_leaves, "hq": cfg.hq, "hkv": cfg.hkv,
+            "head_dim": cfg.d, "unique_kv_tokens": uniq_tok, "logical_kv_tokens": logical_tok,
+            "unique_kv_bytes": uniq_bytes, "share_ratio": round(logical_tok / uniq_tok, 4),
+            "pool_replicas": n_rep,
+        },
+        "achieved_unique_kv_GBps_step": round(achieved_step, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved_kern, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved_kern / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "kernel": "partial_valu_kernel<128>", "kernel_avg_ms": round(kern_ms, 5),
+                     "launches_per_step": launches,
+                     "algorithmic_bytes_per_launch": uniq_bytes},
+        "combine_avg_ms": round(comb_ms, 5),
+    }
+    if not args.no_naive:
+        nms, nk, nc, _ = _time_mode(reps, 1, args.steps, args.warmup, KERNEL_PARTIAL_VALU)
+        line["naive_baseline"] = {"ms_per_step": round(nms, 5), "value": round(n_leaves / (nms * 1e-3), 1),
+                                  "kernel_avg_ms": round(nk, 5), "speedup_tree_vs_naive": round(nms / ms, 4)}
+    line["probe_read_GBps"] = round(_probe_read(), 1)
+    del reps, base
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        line["cpu_baseline"] = _cpu_baseline(args.config, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
