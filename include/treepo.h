@@ -61,7 +61,7 @@ typedef struct treepo_ctx treepo_ctx;
  * V pool, device bf16, layout [Hkv][num_blocks][D][B]: every block is stored
  * transposed, so element (g, r, d) is at ((g*num_blocks + r/B)*D + d)*B + r%B.
  * head_dim D must be 64 or 128, block_tokens B must be 64 (one block is one
- * kernel tile), Hq % Hkv == 0 and Hq / Hkv <= 8.  Pools are caller-owned and
+ * kernel tile), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned and
  * must stay valid until treepo_destroy; their contents need no initialisation.
  */
 typedef struct treepo_config {

@@ -60,7 +60,15 @@ struct TileSmem {
   uint32_t pbuf[kWaves][8][8];  // per wave: token pair x query row, packed bf16 P
 };
 
-__device__ __forceinline__ int k_swz(int r) { return (r & 1) << 2; }
+// K chunk swizzles (the position of chunk c of token row r is c ^ swz(r)):
+// the VALU reader takes, per 8-lane LDS phase, chunks j + 4i of two adjacent
+// rows; the MFMA reader takes one chunk of rows {R+0..3, R+8..11}.
+struct KSwzValu {
+  __device__ static int f(int r) { return (r & 1) << 2; }
+};
+struct KSwzMfma {
+  __device__ static int f(int r) { return (r & 3) | ((r >> 1) & 4); }
+};
 
 // One 16-byte global->LDS load per lane into the 1 KiB LDS slot at byte
 // address `lds` (wave-uniform).  Issued as inline asm so that the compiler does
@@ -78,7 +86,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 
 // Stages tile `block` of KV head g into the LDS buffer at byte address `dst`.
 // D/16 loads per lane.
-template <int D>
+template <int D, class KSwz>
 __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
                                          const uint16_t* __restrict__ vpool, int64_t num_blocks,
                                          int g, int block, uint32_t dst, int wave, int lane) {
@@ -93,7 +101,7 @@ __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
     const int slot = wave * kPerWave + j;
     const int c = slot * 64 + lane;
     const int row = c / kKChunks;
-    const int col = (c % kKChunks) ^ k_swz(row);
+    const int col = (c % kKChunks) ^ KSwz::f(row);
     dma16(kg + row * (D * 2) + col * 16, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
   }
 #pragma unroll
@@ -171,7 +179,7 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   const int nt = te - tb;
   const uint32_t buf0 = lds_addr(sm.kv[0]);
   constexpr uint32_t kBufBytes = 2 * kTile * D * 2;
-  dma_tile<D>(kpool, vpool, sc.num_blocks, g, tiles[4 * tb], buf0, wave, lane);
+  dma_tile<D, KSwzValu>(kpool, vpool, sc.num_blocks, g, tiles[4 * tb], buf0, wave, lane);
 
   uint32_t qr[M][kKW];
 #pragma unroll
@@ -200,8 +208,8 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   for (int k = 0; k < nt; ++k) {
     const int valid = tiles[4 * (tb + k) + 3];
     if (k + 1 < nt) {
-      dma_tile<D>(kpool, vpool, sc.num_blocks, g, tiles[4 * (tb + k + 1)],
-                  buf0 + ((k + 1) & 1) * kBufBytes, wave, lane);
+      dma_tile<D, KSwzValu>(kpool, vpool, sc.num_blocks, g, tiles[4 * (tb + k + 1)],
+                            buf0 + ((k + 1) & 1) * kBufBytes, wave, lane);
       barrier_tile_landed<D / 16>();
     } else {
       barrier_tile_landed<0>();
@@ -215,7 +223,7 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 #pragma unroll
     for (int i = 0; i < kKC; ++i) {
       const int c = j + 4 * i;
-      const uint4 v = *reinterpret_cast<const uint4*>(kt + row * (D * 2) + ((c ^ k_swz(row)) << 4));
+      const uint4 v = *reinterpret_cast<const uint4*>(kt + row * (D * 2) + ((c ^ KSwzValu::f(row)) << 4));
       kr[4 * i + 0] = v.x;
       kr[4 * i + 1] = v.y;
       kr[4 * i + 2] = v.z;
@@ -362,6 +370,212 @@ __global__ __launch_bounds__(kThreads) void partial_valu_kernel(TREEPO_PARTIAL_P
   }
 }
 
+// ---- MFMA node-partial ------------------------------------------------------------
+//
+// For shared nodes whose stacked query rows (descendant leaves x GQA group)
+// form dense tiles.  Rows are cut into 16-row blocks; wave w owns blocks
+// w, w+4, w+8, w+12 (NRB per wave) and keeps their online-softmax state; all
+// four waves read every KV tile from LDS.  Items hold at most 128 rows (two
+// row blocks per wave) so that the K and V operands read from LDS are reused
+// across a wave's row blocks without spilling registers.
+//   QK: S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 K rows, B = Q^T).
+//       The K rows of token block b are read in the order
+//       tau(b, r) = 32(b/2) + 8(r/4) + 4(b%2) + r%4, so that each lane's four
+//       outputs of blocks 2s and 2s+1 are the eight consecutive tokens
+//       32s + 8(lane/16) + 0..7 -- exactly the B operand layout of the PV
+//       product, so P never leaves registers.
+//   P : rounded to bf16 (l summed from the rounded values).
+//   PV: O^T = V^T P^T (A = 16 d-rows of the transposed V tile, B = P^T).
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
+
+__device__ __forceinline__ int tau(int b, int r) { return 32 * (b >> 1) + 8 * (r >> 2) + 4 * (b & 1) + (r & 3); }
+
+template <int D, int NRB>
+__device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g, TileSmem<D>& sm) {
+  constexpr int kKS = D / 32;  // QK k-steps
+  constexpr int kDB = D / 16;  // PV output d-blocks
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int a = lane >> 4;      // lane group
+  const int r16 = lane & 15;    // row within a 16-row block / output column
+  const int rowset = it[1], tb = it[3], te = it[4], pbase = it[5], rows = it[6];
+  const int G = sc.group;
+  const int nt = te - tb;
+  const uint32_t buf0 = lds_addr(sm.kv[0]);
+  constexpr uint32_t kBufBytes = 2 * kTile * D * 2;
+  dma_tile<D, KSwzMfma>(kpool, vpool, sc.num_blocks, g, tiles[4 * tb], buf0, wave, lane);
+
+  // Q^T operands: lane holds row m = 16 rb + r16, d chunk 4 ks + a
+  uint4 qb[NRB][kKS];
+#pragma unroll
+  for (int i = 0; i < NRB; ++i) {
+    const int m = 16 * (wave + 4 * i) + r16;
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) qb[i][ks] = make_uint4(0, 0, 0, 0);
+    if (m < rows) {
+      const int leaf = rowsets[rowset + m / G];
+      const int head = g * G + m % G;
+      const uint4* qp = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(leaf) * sc.hq + head) * D);
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) qb[i][ks] = qp[4 * ks + a];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NRB; ++i)
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) asm volatile("" ::"v"(qb[i][ks].x), "v"(qb[i][ks].y), "v"(qb[i][ks].z), "v"(qb[i][ks].w));
+
+  const int nrb_total = (rows + 15) >> 4;
+  const int my_rb = nrb_total > wave ? (nrb_total - wave + 3) >> 2 : 0;  // row blocks of this wave (<= NRB)
+
+  f32x4 acc[NRB][kDB];
+  float m_run[NRB], l_run[NRB];
+#pragma unroll
+  for (int i = 0; i < NRB; ++i) {
+    m_run[i] = -INFINITY;
+    l_run[i] = 0.f;
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) acc[i][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  for (int k = 0; k < nt; ++k) {
+    const int valid = tiles[4 * (tb + k) + 3];
+    if (k + 1 < nt) {
+      dma_tile<D, KSwzMfma>(kpool, vpool, sc.num_blocks, g, tiles[4 * (tb + k + 1)],
+                            buf0 + ((k + 1) & 1) * kBufBytes, wave, lane);
+      barrier_tile_landed<D / 16>();
+    } else {
+      barrier_tile_landed<0>();
+    }
+    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 1]);
+    const char* vt = kt + kTile * D * 2;
+    if (my_rb > 0) {
+      // ---- S^T = K Q^T for the wave's row blocks
+      f32x4 S[NRB][4];
+#pragma unroll
+      for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) S[i][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int tok = tau(b, r16);
+          const int c = 4 * ks + a;
+          const uint4 ka = *reinterpret_cast<const uint4*>(kt + tok * (D * 2) + ((c ^ KSwzMfma::f(tok)) << 4));
+#pragma unroll
+          for (int i = 0; i < NRB; ++i)
+            if (i < my_rb) S[i][b] = mfma16(ka, qb[i][ks], S[i][b]);
+        }
+      }
+      // ---- online softmax; lane holds row r16, tokens tau(b, 4a + e)
+      uint4 P[NRB][2];
+#pragma unroll
+      for (int i = 0; i < NRB; ++i) {
+        if (i >= my_rb) continue;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int tok = 32 * (b >> 1) + 8 * a + 4 * (b & 1) + e;
+            const float x = tok < valid ? S[i][b][e] * sc.scale_log2 : -INFINITY;
+            S[i][b][e] = x;
+            mx = fmaxf(mx, x);
+          }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mn = fmaxf(m_run[i], mx);
+        const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[i] - mn);
+        m_run[i] = mn;
+        float ls = 0.f;
+        uint32_t pw[8];
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int e = 0; e < 4; e += 2) {
+            const float x0 = S[i][b][e], x1 = S[i][b][e + 1];
+            const uint32_t p0 = f2bf_bits(x0 == -INFINITY ? 0.f : fast_exp2(x0 - mn));
+            const uint32_t p1 = f2bf_bits(x1 == -INFINITY ? 0.f : fast_exp2(x1 - mn));
+            ls += bf_bits2f(p0) + bf_bits2f(p1);
+            // k-step s = b/2 holds block 2s in words 0,1 and block 2s+1 in words 2,3
+            pw[4 * (b >> 1) + 2 * (b & 1) + (e >> 1)] = p0 | (p1 << 16);
+          }
+        P[i][0] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+        P[i][1] = make_uint4(pw[4], pw[5], pw[6], pw[7]);
+        l_run[i] = l_run[i] * alpha + ls;
+#pragma unroll
+        for (int db = 0; db < kDB; ++db) acc[i][db] *= alpha;
+      }
+      // ---- O^T += V^T P^T
+#pragma unroll
+      for (int db = 0; db < kDB; ++db) {
+        const int d = 16 * db + r16;
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+          const int c = 4 * st + a;
+          uint4 va = *reinterpret_cast<const uint4*>(vt + d * 128 + ((c ^ (d & 7)) << 4));
+          if (valid < kTile) {
+            // clear the V halves of tokens past the node's length (P is 0 there)
+            const int t0 = 32 * st + 8 * a;
+            uint32_t w[4] = {va.x, va.y, va.z, va.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int tk = t0 + 2 * e;
+              w[e] &= tk >= valid ? 0u : (tk + 1 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
+            }
+            va = make_uint4(w[0], w[1], w[2], w[3]);
+          }
+#pragma unroll
+          for (int i = 0; i < NRB; ++i)
+            if (i < my_rb) acc[i][db] = mfma16(va, P[i][st], acc[i][db]);
+        }
+      }
+    }
+    barrier_lds_reads_done();
+  }
+
+  // ---- write the partial rows (each wave owns its row blocks)
+#pragma unroll
+  for (int i = 0; i < NRB; ++i) {
+    if (i >= my_rb) continue;
+    float l = l_run[i];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const int m = 16 * (wave + 4 * i) + r16;
+    if (m < rows) {
+      const int64_t slot = static_cast<int64_t>(pbase) + static_cast<int64_t>(g) * rows + m;
+#pragma unroll
+      for (int db = 0; db < kDB; ++db)
+        *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * db + 4 * a) = acc[i][db];
+      if (a == 0) {
+        part_ml[slot * 2 + 0] = m_run[i];
+        part_ml[slot * 2 + 1] = l;
+      }
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void partial_mfma_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
+  __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;
+  const int item = first_item + static_cast<int>(blockIdx.x) / sc.hkv;
+  const int g = static_cast<int>(blockIdx.x) % sc.hkv;
+  const int32_t* it = items + 8 * item;
+  const int nrb = (((it[6] + 15) >> 4) + 3) >> 2;
+  switch (nrb) {
+    case 1: mfma_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    case 2: mfma_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+    default: break;  // the planner keeps items at <= 128 rows
+  }
+}
+
 // ---- combine ------------------------------------------------------------------
 //
 // One wave per (leaf, query head): m* = max m_i, L = sum l_i 2^(m_i - m*),
@@ -467,6 +681,20 @@ hipError_t launch_partial_valu(const DecodeArgs& a, int32_t first_item, int32_t 
                                                        a.part_o, a.part_ml, sc, first_item);
   else
     partial_valu_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
+                                                      a.part_o, a.part_ml, sc, first_item);
+  return hipGetLastError();
+}
+
+hipError_t launch_partial_mfma(const DecodeArgs& a, int32_t first_item, int32_t n_items,
+                               hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(n_items) * a.hkv);
+  const Scalars sc{a.num_blocks, a.hq, a.hkv, a.group, a.scale_log2};
+  if (a.d == 128)
+    partial_mfma_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
+                                                       a.part_o, a.part_ml, sc, first_item);
+  else
+    partial_mfma_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
                                                       a.part_o, a.part_ml, sc, first_item);
   return hipGetLastError();
 }

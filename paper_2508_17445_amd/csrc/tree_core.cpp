@@ -183,8 +183,8 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   const auto& nd = t.nodes();
   const int32_t B = t.block_tokens();
   const int32_t G = p.group;
-  if (G < 1 || G > p.valu_max_rows) {
-    if (err) *err = "GQA group larger than the VALU row limit";
+  if (G < 1 || G > (p.mfma_enabled ? p.mfma_max_rows : p.valu_max_rows)) {
+    if (err) *err = "GQA group larger than the kernels' row limit";
     return kEUnsupported;
   }
   *out = Plan();
@@ -243,10 +243,11 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     const int32_t nl = static_cast<int32_t>(r.leaves.size());
     if (nl * G <= p.valu_max_rows) {
       r.group_leaves = nl;
-    } else if (p.mfma_enabled) {
-      r.group_leaves = std::max(1, p.mfma_max_rows / G);
     } else {
-      r.group_leaves = std::max(1, p.valu_max_rows / G);
+      // split the leaves evenly into the fewest groups that fit the row limit
+      const int32_t lim = std::max(1, (p.mfma_enabled ? p.mfma_max_rows : p.valu_max_rows) / G);
+      const int32_t ng = (nl + lim - 1) / lim;
+      r.group_leaves = (nl + ng - 1) / ng;
     }
   }
 

@@ -274,6 +274,13 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
     return treepo::launch_partial_valu(a, 0, p.n_valu_items, stream);
   });
   if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
+  const int32_t n_mfma = static_cast<int32_t>(p.items.size()) - p.n_valu_items;
+  if (n_mfma > 0) {
+    e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL_MFMA, stream, [&] {
+      return treepo::launch_partial_mfma(a, p.n_valu_items, n_mfma, stream);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "mfma partial kernel launch");
+  }
   e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
   return TREEPO_OK;
@@ -319,17 +326,17 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
       !c.k_pool || !c.v_pool)
     return TREEPO_EINVAL;
   if ((c.head_dim != 64 && c.head_dim != 128) || c.block_tokens != treepo::kTile ||
-      c.num_q_heads / c.num_kv_heads > 8)
+      c.num_q_heads / c.num_kv_heads > 128)
     return TREEPO_EUNSUPPORTED;
   treepo_ctx* ctx = new (std::nothrow) treepo_ctx(c);
   if (!ctx) return TREEPO_ENOMEM;
   ctx->params.group = c.num_q_heads / c.num_kv_heads;
   ctx->params.num_kv_heads = c.num_kv_heads;
   ctx->params.valu_max_rows = 8;
-  ctx->params.mfma_max_rows = 256;
+  ctx->params.mfma_max_rows = 128;
   ctx->params.concurrent_wgs = 512;
   ctx->params.max_chunk_tiles = 64;
-  ctx->params.mfma_enabled = 0;
+  ctx->params.mfma_enabled = 1;
   *out = ctx;
   return TREEPO_OK;
 }

@@ -24,7 +24,7 @@ def test_create_rejects_bad_configs():
     bad = [
         (dict(hq=6, hkv=4, d=64), T.EINVAL),
         (dict(hq=4, hkv=1, d=96), T.EUNSUPPORTED),
-        (dict(hq=32, hkv=2, d=128), T.EUNSUPPORTED),
+        (dict(hq=258, hkv=2, d=128), T.EUNSUPPORTED),
         (dict(hq=4, hkv=1, d=64, block_tokens=16), T.EUNSUPPORTED),
     ]
     for kw, code in bad:

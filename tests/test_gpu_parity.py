@@ -5,8 +5,8 @@ compared element (bf16 inputs, fp32 accumulation).  Small workloads are
 compared in full; the large ones at full size on sampled leaves that the
 oracle computes one by one.  Both the cascade (tree) path and the per-leaf
 baseline are checked, plus determinism and edge cases (ragged tails,
-zero-length nodes, one-token chains, duplicate and interior leaves, every GQA
-group size up to 8, D = 64 and 128).
+zero-length nodes, one-token chains, duplicate and interior leaves, GQA
+group sizes from 1 to 48, D = 64 and 128).
 """
 
 from __future__ import annotations
@@ -86,6 +86,7 @@ def _random_cfg(seed, hq, hkv, d):
 @pytest.mark.parametrize("seed,hq,hkv,d", [
     (1, 4, 1, 64), (2, 7, 1, 128), (3, 8, 8, 128), (4, 6, 3, 64), (5, 28, 4, 128),
     (6, 40, 8, 128), (7, 16, 2, 64), (8, 5, 1, 128), (9, 3, 3, 64), (10, 2, 1, 128),
+    (11, 32, 2, 128), (12, 48, 1, 64), (13, 14, 1, 128), (14, 12, 1, 64),
 ])
 def test_random_trees(seed, hq, hkv, d):
     ops, leaves, rows, _ = random_tiny_tree(seed, max_leaves=10, max_tokens=400)
