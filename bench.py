@@ -163,7 +163,7 @@ def main():
         sys.exit(2)
     import torch
     _ensure_built()
-    from paper_2508_17445_amd import KERNEL_PARTIAL_VALU
+    from paper_2508_17445_amd import KERNEL_PARTIAL
     from workloads import CONFIGS
     from workloads.device import DeviceTree
 
@@ -175,7 +175,7 @@ def main():
     n_rep = args.replicas or max(1, math.ceil(1.2e9 / uniq_bytes))
     reps = [base] + [base.clone() for _ in range(n_rep - 1)]
 
-    ms, kern_ms, comb_ms, launches = _time_mode(reps, 0, args.steps, args.warmup, KERNEL_PARTIAL_VALU)
+    ms, kern_ms, comb_ms, launches = _time_mode(reps, 0, args.steps, args.warmup, KERNEL_PARTIAL)
     n_leaves = len(base.leaves)
     value = n_leaves / (ms * 1e-3)
     achieved_step = uniq_bytes / (ms * 1e-3) / 1e9
@@ -202,13 +202,13 @@ def main():
         "achieved_unique_kv_GBps_step": round(achieved_step, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved_kern, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved_kern / PEAK_HBM_GBPS, 4), "traffic": None,
-                     "kernel": "partial_valu_kernel<128>", "kernel_avg_ms": round(kern_ms, 5),
+                     "kernel": "partial_kernel<128>", "kernel_avg_ms": round(kern_ms, 5),
                      "launches_per_step": launches,
                      "algorithmic_bytes_per_launch": uniq_bytes},
         "combine_avg_ms": round(comb_ms, 5),
     }
     if not args.no_naive:
-        nms, nk, nc, _ = _time_mode(reps, 1, args.steps, args.warmup, KERNEL_PARTIAL_VALU)
+        nms, nk, nc, _ = _time_mode(reps, 1, args.steps, args.warmup, KERNEL_PARTIAL)
         line["naive_baseline"] = {"ms_per_step": round(nms, 5), "value": round(n_leaves / (nms * 1e-3), 1),
                                   "kernel_avg_ms": round(nk, 5), "speedup_tree_vs_naive": round(nms / ms, 4)}
     line["probe_read_GBps"] = round(_probe_read(), 1)

@@ -201,11 +201,10 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
 /* ---- kernel timing ------------------------------------------------------ */
 
 /* Kernel kinds for treepo_profile_read. */
-#define TREEPO_KERNEL_APPEND 0
-#define TREEPO_KERNEL_PARTIAL_VALU 1
-#define TREEPO_KERNEL_PARTIAL_MFMA 2
-#define TREEPO_KERNEL_COMBINE 3
-#define TREEPO_KERNEL_KINDS 4
+#define TREEPO_KERNEL_APPEND 0  /* KV scatter into the pools                      */
+#define TREEPO_KERNEL_PARTIAL 1 /* node partials, VALU and MFMA work items        */
+#define TREEPO_KERNEL_COMBINE 2 /* log-sum-exp merge of each leaf's partials      */
+#define TREEPO_KERNEL_KINDS 3
 
 /* When enabled, every kernel launch of this context is bracketed by HIP events
  * on the launch stream.  Enabling or disabling clears the totals. */

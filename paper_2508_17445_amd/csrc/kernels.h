@@ -29,10 +29,8 @@ struct DecodeArgs {
   float* lse;              // fp32 [n_leaves][Hq] or null
 };
 
-hipError_t launch_partial_valu(const DecodeArgs& a, int32_t first_item, int32_t n_items,
-                               hipStream_t s);
-hipError_t launch_partial_mfma(const DecodeArgs& a, int32_t first_item, int32_t n_items,
-                               hipStream_t s);
+// Node partials of items [first_item, first_item + n_items), VALU or MFMA by kind.
+hipError_t launch_partial(const DecodeArgs& a, int32_t first_item, int32_t n_items, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 
 // One block-aligned run of appended tokens: source rows [src_row, +count) go

@@ -57,7 +57,7 @@ template <int D>
 struct TileSmem {
   static constexpr int kElems = kTile * D;
   uint16_t kv[2][2 * kElems];
-  uint32_t pbuf[kWaves][8][8];  // per wave: token pair x query row, packed bf16 P
+  uint32_t pbuf[kWaves][8][16];  // per wave: token pair x (8 hi words, 8 lo words) of packed P
 };
 
 // K chunk swizzles (the position of chunk c of token row r is c ^ swz(r)):
@@ -134,11 +134,13 @@ __device__ __forceinline__ void barrier_lds_reads_done() {
 //       ... of its row; q rows sit in registers in the same chunk order.  The
 //       partial dot products (v_dot2 bf16 -> fp32) are summed across the quad
 //       with DPP.
-//   P : rounded to bf16; the sum l is accumulated from the rounded values so
-//       the output stays a convex combination of V rows.  Token pairs are
-//       packed into one 32-bit word and staged in a per-wave LDS slot.
+//   P : split into two bf16 terms, hi = bf16(p) and lo = bf16(p - hi), so the
+//       weights keep about 16 significant bits (a single bf16 P can be off by
+//       2^-8 relative, too much for short, peaked chains).  Token pairs are
+//       packed into 32-bit words and staged in a per-wave LDS slot.
 //   PV: lane i owns d = i (+64); V^T words hold two consecutive tokens of one
-//       d, matching the packed P pairs, so each v_dot2 does two tokens.
+//       d, matching the packed P pairs, so each v_dot2 does two tokens (one
+//       v_dot2 for hi and one for lo).
 // Kernel arguments: the pointers are passed as separate __restrict__ kernel
 // parameters so that uniform metadata reads become scalar loads.
 struct Scalars {
@@ -240,7 +242,7 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
     }
 
     // ---- online softmax over this wave's 16 tokens
-    uint32_t pk[M];
+    uint32_t pk[M], pkl[M];
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       float mx = s[m];
@@ -252,16 +254,22 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
       const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[m] - mn);
       const float p = s[m] == -INFINITY ? 0.f : fast_exp2(s[m] - mn);
       const uint32_t pb = f2bf_bits(p);
-      l_run[m] = l_run[m] * alpha + bf_bits2f(pb);
+      const uint32_t pl = f2bf_bits(p - bf_bits2f(pb));
+      l_run[m] = l_run[m] * alpha + (bf_bits2f(pb) + bf_bits2f(pl));
 #pragma unroll
       for (int dd = 0; dd < kDD; ++dd) acc[m][dd] *= alpha;
       m_run[m] = mn;
-      const uint32_t partner = static_cast<uint32_t>(__shfl_xor(static_cast<int>(pb), 4));
-      pk[m] = pb | (partner << 16);
+      const uint32_t both = pb | (pl << 16);
+      const uint32_t partner = static_cast<uint32_t>(__shfl_xor(static_cast<int>(both), 4));
+      pk[m] = (both & 0xFFFFu) | (partner << 16);
+      pkl[m] = (both >> 16) | (partner & 0xFFFF0000u);
     }
     if ((t & 1) == 0 && j == 0) {
 #pragma unroll
-      for (int m = 0; m < M; ++m) sm.pbuf[wave][t >> 1][m] = pk[m];
+      for (int m = 0; m < M; ++m) {
+        sm.pbuf[wave][t >> 1][m] = pk[m];
+        sm.pbuf[wave][t >> 1][8 + m] = pkl[m];
+      }
     }
 
     // ---- P V
@@ -293,11 +301,14 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
     for (int tp = 0; tp < 8; ++tp) {
       const uint4 p0 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][0]);
       const uint4 p1 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][4]);
+      const uint4 p2 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][8]);
+      const uint4 p3 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][12]);
       const uint32_t pw[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+      const uint32_t pl[8] = {p2.x, p2.y, p2.z, p2.w, p3.x, p3.y, p3.z, p3.w};
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = dot2(pw[m], vw[dd][tp], acc[m][dd]);
+        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = dot2(pl[m], vw[dd][tp], dot2(pw[m], vw[dd][tp], acc[m][dd]));
     }
     barrier_lds_reads_done();
   }
@@ -351,25 +362,6 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void partial_valu_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
-  __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;
-  const int item = first_item + static_cast<int>(blockIdx.x) / sc.hkv;
-  const int g = static_cast<int>(blockIdx.x) % sc.hkv;
-  const int32_t* it = items + 8 * item;
-  switch (it[6]) {
-    case 1: valu_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 2: valu_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 3: valu_item<D, 3>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 4: valu_item<D, 4>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 5: valu_item<D, 5>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 6: valu_item<D, 6>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 7: valu_item<D, 7>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 8: valu_item<D, 8>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    default: break;
-  }
-}
-
 // ---- MFMA node-partial ------------------------------------------------------------
 //
 // For shared nodes whose stacked query rows (descendant leaves x GQA group)
@@ -384,8 +376,10 @@ __global__ __launch_bounds__(kThreads) void partial_valu_kernel(TREEPO_PARTIAL_P
 //       outputs of blocks 2s and 2s+1 are the eight consecutive tokens
 //       32s + 8(lane/16) + 0..7 -- exactly the B operand layout of the PV
 //       product, so P never leaves registers.
-//   P : rounded to bf16 (l summed from the rounded values).
-//   PV: O^T = V^T P^T (A = 16 d-rows of the transposed V tile, B = P^T).
+//   P : split into hi = bf16(p) and lo = bf16(p - hi) (about 16 significant
+//       bits for the weights).
+//   PV: O^T = V^T P_hi^T + V^T P_lo^T (A = 16 d-rows of the transposed V
+//       tile, B = P^T).
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -475,7 +469,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
         }
       }
       // ---- online softmax; lane holds row r16, tokens tau(b, 4a + e)
-      uint4 P[NRB][2];
+      uint4 P[NRB][2], PL[NRB][2];
 #pragma unroll
       for (int i = 0; i < NRB; ++i) {
         if (i >= my_rb) continue;
@@ -495,20 +489,25 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
         const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[i] - mn);
         m_run[i] = mn;
         float ls = 0.f;
-        uint32_t pw[8];
+        uint32_t pw[8], pwl[8];
 #pragma unroll
         for (int b = 0; b < 4; ++b)
 #pragma unroll
           for (int e = 0; e < 4; e += 2) {
             const float x0 = S[i][b][e], x1 = S[i][b][e + 1];
-            const uint32_t p0 = f2bf_bits(x0 == -INFINITY ? 0.f : fast_exp2(x0 - mn));
-            const uint32_t p1 = f2bf_bits(x1 == -INFINITY ? 0.f : fast_exp2(x1 - mn));
-            ls += bf_bits2f(p0) + bf_bits2f(p1);
+            const float f0 = x0 == -INFINITY ? 0.f : fast_exp2(x0 - mn);
+            const float f1 = x1 == -INFINITY ? 0.f : fast_exp2(x1 - mn);
+            const uint32_t p0 = f2bf_bits(f0), p1 = f2bf_bits(f1);
+            const uint32_t q0 = f2bf_bits(f0 - bf_bits2f(p0)), q1 = f2bf_bits(f1 - bf_bits2f(p1));
+            ls += (bf_bits2f(p0) + bf_bits2f(q0)) + (bf_bits2f(p1) + bf_bits2f(q1));
             // k-step s = b/2 holds block 2s in words 0,1 and block 2s+1 in words 2,3
             pw[4 * (b >> 1) + 2 * (b & 1) + (e >> 1)] = p0 | (p1 << 16);
+            pwl[4 * (b >> 1) + 2 * (b & 1) + (e >> 1)] = q0 | (q1 << 16);
           }
         P[i][0] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
         P[i][1] = make_uint4(pw[4], pw[5], pw[6], pw[7]);
+        PL[i][0] = make_uint4(pwl[0], pwl[1], pwl[2], pwl[3]);
+        PL[i][1] = make_uint4(pwl[4], pwl[5], pwl[6], pwl[7]);
         l_run[i] = l_run[i] * alpha + ls;
 #pragma unroll
         for (int db = 0; db < kDB; ++db) acc[i][db] *= alpha;
@@ -534,7 +533,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
           }
 #pragma unroll
           for (int i = 0; i < NRB; ++i)
-            if (i < my_rb) acc[i][db] = mfma16(va, P[i][st], acc[i][db]);
+            if (i < my_rb) acc[i][db] = mfma16(va, PL[i][st], mfma16(va, P[i][st], acc[i][db]));
         }
       }
     }
@@ -562,17 +561,36 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   }
 }
 
+// ---- the node-partial kernel ----------------------------------------------------
+//
+// One launch covers every work item of a decode step; each workgroup runs one
+// (item, KV head) on the VALU or the MFMA path according to the item's kind.
+// Two workgroups fit per CU (<= 256 registers per lane, 68 KB of LDS each).
 template <int D>
-__global__ __launch_bounds__(kThreads) void partial_mfma_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
+__global__ __launch_bounds__(kThreads, 2) void partial_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
   __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;
   const int item = first_item + static_cast<int>(blockIdx.x) / sc.hkv;
   const int g = static_cast<int>(blockIdx.x) % sc.hkv;
   const int32_t* it = items + 8 * item;
-  const int nrb = (((it[6] + 15) >> 4) + 3) >> 2;
-  switch (nrb) {
-    case 1: mfma_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    case 2: mfma_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-    default: break;  // the planner keeps items at <= 128 rows
+  if (it[0] == 0) {
+    switch (it[6]) {
+      case 1: valu_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 2: valu_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 3: valu_item<D, 3>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 4: valu_item<D, 4>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 5: valu_item<D, 5>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 6: valu_item<D, 6>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 7: valu_item<D, 7>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 8: valu_item<D, 8>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      default: break;
+    }
+  } else {
+    const int nrb = (((it[6] + 15) >> 4) + 3) >> 2;
+    if (nrb == 1)
+      mfma_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm);
+    else if (nrb == 2)
+      mfma_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm);
+    // the planner keeps MFMA items at <= 128 rows
   }
 }
 
@@ -580,48 +598,65 @@ __global__ __launch_bounds__(kThreads) void partial_mfma_kernel(TREEPO_PARTIAL_P
 //
 // One wave per (leaf, query head): m* = max m_i, L = sum l_i 2^(m_i - m*),
 // out = sum 2^(m_i - m*) O_i / L, lse = (m* + log2 L) ln 2.  Partials of empty
-// pieces (m = -inf) contribute nothing.  Entries are visited in chain order.
+// pieces (m = -inf) contribute nothing.  Entries are taken 64 at a time: the
+// lanes load their (m, l) pairs in parallel, then the weights are broadcast
+// with readlane while every lane accumulates its d-slice of the O rows (the
+// row loads are independent, so they overlap).  The order of the sum is fixed
+// (chain order), so results are deterministic.
 template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __restrict__ leaf_off,
+                                                           const int32_t* __restrict__ entries,
+                                                           const float* __restrict__ part_o,
+                                                           const float* __restrict__ part_ml,
+                                                           float* __restrict__ out, float* __restrict__ lse,
+                                                           int32_t n_leaves, int32_t hq, int32_t group) {
   constexpr int kPL = D / 64;
   const int lane = threadIdx.x & 63;
   const int gw = static_cast<int>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
-  if (gw >= a.n_leaves * a.hq) return;
-  const int x = gw / a.hq;
-  const int h = gw % a.hq;
-  const int g = h / a.group;
-  const int hp = h % a.group;
-  const int e0 = a.leaf_off[x], e1 = a.leaf_off[x + 1];
-  float mstar = -INFINITY;
-  for (int e = e0 + lane; e < e1; e += 64) {
-    const int slot = a.entries[2 * e] + g * a.entries[2 * e + 1] + hp;
-    mstar = fmaxf(mstar, a.part_ml[2 * static_cast<int64_t>(slot)]);
-  }
-  mstar = fmaxf(mstar, __shfl_xor(mstar, 1));
-  mstar = fmaxf(mstar, __shfl_xor(mstar, 2));
-  mstar = fmaxf(mstar, __shfl_xor(mstar, 4));
-  mstar = fmaxf(mstar, __shfl_xor(mstar, 8));
-  mstar = fmaxf(mstar, __shfl_xor(mstar, 16));
-  mstar = fmaxf(mstar, __shfl_xor(mstar, 32));
+  if (gw >= n_leaves * hq) return;
+  const int x = gw / hq;
+  const int h = gw % hq;
+  const int g = h / group;
+  const int hp = h % group;
+  const int e0 = leaf_off[x], e1 = leaf_off[x + 1];
+  float run_m = -INFINITY, run_l = 0.f;
   float o[kPL];
 #pragma unroll
   for (int i = 0; i < kPL; ++i) o[i] = 0.f;
-  float l = 0.f;
-  for (int e = e0; e < e1; ++e) {
-    const int64_t slot = a.entries[2 * e] + static_cast<int64_t>(g) * a.entries[2 * e + 1] + hp;
-    const float mi = a.part_ml[2 * slot];
-    if (mi == -INFINITY) continue;
-    const float f = fast_exp2(mi - mstar);
-    l += f * a.part_ml[2 * slot + 1];
-    const float* po = a.part_o + slot * D + lane * kPL;
+  for (int base = e0; base < e1; base += 64) {
+    const int cnt = e1 - base < 64 ? e1 - base : 64;
+    const bool mine = lane < cnt;
+    const int e = base + (mine ? lane : 0);
+    const int slot = entries[2 * e] + g * entries[2 * e + 1] + hp;
+    const float mi = mine ? part_ml[2 * static_cast<int64_t>(slot)] : -INFINITY;
+    const float li = mine ? part_ml[2 * static_cast<int64_t>(slot) + 1] : 0.f;
+    float cm = mi;
 #pragma unroll
-    for (int i = 0; i < kPL; ++i) o[i] += f * po[i];
+    for (int sh = 1; sh < 64; sh <<= 1) cm = fmaxf(cm, __shfl_xor(cm, sh));
+    const float nm = fmaxf(run_m, cm);
+    const float keep = run_m == -INFINITY ? 0.f : fast_exp2(run_m - nm);
+    const float w = mi == -INFINITY ? 0.f : fast_exp2(mi - nm);
+    float wl = w * li;
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) wl += __shfl_xor(wl, sh);
+    run_l = run_l * keep + wl;
+#pragma unroll
+    for (int i = 0; i < kPL; ++i) o[i] *= keep;
+    run_m = nm;
+#pragma unroll 4
+    for (int k = 0; k < cnt; ++k) {
+      const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), k));
+      const int sk = __builtin_amdgcn_readlane(slot, k);
+      const float* po = part_o + static_cast<int64_t>(sk) * D + lane * kPL;
+#pragma unroll
+      for (int i = 0; i < kPL; ++i) o[i] += wk * po[i];
+    }
   }
-  const float inv = 1.f / l;
-  float* op = a.out + (static_cast<int64_t>(x) * a.hq + h) * D + lane * kPL;
+  const float inv = 1.f / run_l;
+  float* op = out + (static_cast<int64_t>(x) * hq + h) * D + lane * kPL;
 #pragma unroll
   for (int i = 0; i < kPL; ++i) op[i] = o[i] * inv;
-  if (a.lse != nullptr && lane == 0) a.lse[static_cast<int64_t>(x) * a.hq + h] = (mstar + __log2f(l)) * kLn2;
+  if (lse != nullptr && lane == 0) lse[static_cast<int64_t>(x) * hq + h] = (run_m + __log2f(run_l)) * kLn2;
 }
 
 // ---- KV append --------------------------------------------------------------
@@ -671,31 +706,16 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
 
 }  // namespace
 
-hipError_t launch_partial_valu(const DecodeArgs& a, int32_t first_item, int32_t n_items,
-                               hipStream_t s) {
+hipError_t launch_partial(const DecodeArgs& a, int32_t first_item, int32_t n_items, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(n_items) * a.hkv);
   const Scalars sc{a.num_blocks, a.hq, a.hkv, a.group, a.scale_log2};
   if (a.d == 128)
-    partial_valu_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
-                                                       a.part_o, a.part_ml, sc, first_item);
+    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
+                                                  a.part_o, a.part_ml, sc, first_item);
   else
-    partial_valu_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
-                                                      a.part_o, a.part_ml, sc, first_item);
-  return hipGetLastError();
-}
-
-hipError_t launch_partial_mfma(const DecodeArgs& a, int32_t first_item, int32_t n_items,
-                               hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>(n_items) * a.hkv);
-  const Scalars sc{a.num_blocks, a.hq, a.hkv, a.group, a.scale_log2};
-  if (a.d == 128)
-    partial_mfma_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
-                                                       a.part_o, a.part_ml, sc, first_item);
-  else
-    partial_mfma_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
-                                                      a.part_o, a.part_ml, sc, first_item);
+    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
+                                                 a.part_o, a.part_ml, sc, first_item);
   return hipGetLastError();
 }
 
@@ -703,9 +723,11 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   const int64_t waves = static_cast<int64_t>(a.n_leaves) * a.hq;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
   if (a.d == 128)
-    combine_kernel<128><<<grid, kThreads, 0, s>>>(a);
+    combine_kernel<128><<<grid, kThreads, 0, s>>>(a.leaf_off, a.entries, a.part_o, a.part_ml, a.out, a.lse,
+                                                  a.n_leaves, a.hq, a.group);
   else
-    combine_kernel<64><<<grid, kThreads, 0, s>>>(a);
+    combine_kernel<64><<<grid, kThreads, 0, s>>>(a.leaf_off, a.entries, a.part_o, a.part_ml, a.out, a.lse,
+                                                 a.n_leaves, a.hq, a.group);
   return hipGetLastError();
 }
 

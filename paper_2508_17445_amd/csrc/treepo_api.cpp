@@ -66,8 +66,8 @@ struct treepo_ctx {
   bool profiling = false;
   std::vector<TimedLaunch> timed;
   std::vector<hipEvent_t> spare_events;
-  double prof_ms[TREEPO_KERNEL_KINDS] = {0, 0, 0, 0};
-  int64_t prof_n[TREEPO_KERNEL_KINDS] = {0, 0, 0, 0};
+  double prof_ms[TREEPO_KERNEL_KINDS] = {0, 0, 0};
+  int64_t prof_n[TREEPO_KERNEL_KINDS] = {0, 0, 0};
 
   treepo_ctx(const treepo_config& c)
       : cfg(c), tree(c.block_tokens, c.num_blocks, c.max_nodes) {}
@@ -270,17 +270,10 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;
-  hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL_VALU, stream, [&] {
-    return treepo::launch_partial_valu(a, 0, p.n_valu_items, stream);
+  hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL, stream, [&] {
+    return treepo::launch_partial(a, 0, static_cast<int32_t>(p.items.size()), stream);
   });
   if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
-  const int32_t n_mfma = static_cast<int32_t>(p.items.size()) - p.n_valu_items;
-  if (n_mfma > 0) {
-    e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL_MFMA, stream, [&] {
-      return treepo::launch_partial_mfma(a, p.n_valu_items, n_mfma, stream);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "mfma partial kernel launch");
-  }
   e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
   return TREEPO_OK;

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libtreepo.so")
 
 OK, EINVAL, ENOMEM, EFULL, EFROZEN, EEMPTY, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 MODE_TREE, MODE_NAIVE = 0, 1
-KERNEL_APPEND, KERNEL_PARTIAL_VALU, KERNEL_PARTIAL_MFMA, KERNEL_COMBINE = 0, 1, 2, 3
+KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE = 0, 1, 2
 NODE_FIELDS = ("parent", "depth", "start", "len", "cap", "block_begin", "n_blocks", "tree_id")
 BLOCK_TOKENS = 64
 
