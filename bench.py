@@ -46,6 +46,9 @@ def _parse():
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="short run for hardware counters: a few decode steps of the workload, then one "
+                         "1 GiB device copy whose byte counters calibrate the kernels'")
     return ap.parse_args()
 
 
@@ -77,6 +80,13 @@ def _unique_kv(dt):
 
 
 def _time_mode(reps, mode, steps, warmup, kernel_kind):
+    """Times `steps` decode steps rotating over the replicas.
+
+    Two timed passes of the same length: the first without instrumentation
+    gives the step time; the second brackets every kernel launch with HIP
+    events on the launch stream (library profiling) and gives the average
+    duration of each kernel.
+    """
     import torch
     from paper_2508_17445_amd import KERNEL_COMBINE
     bufs = []
@@ -84,26 +94,33 @@ def _time_mode(reps, mode, steps, warmup, kernel_kind):
         out, lse = r.outputs()
         bufs.append((out, lse, r.workspace(mode)))
     fn = [(r.ctx.tree_decode if mode == 0 else r.ctx.paged_decode_naive) for r in reps]
-    for i in range(warmup):
-        j = i % len(reps)
-        fn[j](reps[j].leaves, reps[j].q, reps[j].cfg.scale, bufs[j][0], bufs[j][1], bufs[j][2])
+
+    def run(n):
+        for i in range(n):
+            j = i % len(reps)
+            fn[j](reps[j].leaves, reps[j].q, reps[j].cfg.scale, bufs[j][0], bufs[j][1], bufs[j][2])
+
+    run(warmup)
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(steps)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
     for r in reps:
         r.ctx.set_profiling(True)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        j = i % len(reps)
-        fn[j](reps[j].leaves, reps[j].q, reps[j].cfg.scale, bufs[j][0], bufs[j][1], bufs[j][2])
+    t2 = time.perf_counter()
+    run(steps)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    t3 = time.perf_counter()
     kms, kn, cms, cn = 0.0, 0, 0.0, 0
     for r in reps:
         a, b = r.ctx.profile_read(kernel_kind)
         c, d = r.ctx.profile_read(KERNEL_COMBINE)
         kms += a; kn += b; cms += c; cn += d
         r.ctx.set_profiling(False)
-    return (t1 - t0) * 1e3 / steps, kms / max(kn, 1), cms / max(cn, 1), kn // max(steps, 1)
+    return {"ms": (t1 - t0) * 1e3 / steps, "ms_instrumented": (t3 - t2) * 1e3 / steps,
+            "kernel_ms": kms / max(kn, 1), "combine_ms": cms / max(cn, 1), "launches": kn // max(steps, 1)}
 
 
 def _probe_read(nbytes=4 << 30, iters=10):
@@ -155,6 +172,25 @@ def _cpu_baseline(cfg_id, seconds):
                       f"{len(os.sched_getaffinity(0))} cores, BLAS threads {blas_threads}"}
 
 
+def _profile_pass(dt, args):
+    """A few decode steps (tree, then naive) and a 1 GiB copy, nothing else on the GPU."""
+    import torch
+    from paper_2508_17445_amd import bench_copy
+    for mode in (0, 1):
+        out, lse = dt.outputs()
+        ws = dt.workspace(mode)
+        fn = dt.ctx.tree_decode if mode == 0 else dt.ctx.paged_decode_naive
+        for _ in range(args.steps):
+            fn(dt.leaves, dt.q, dt.cfg.scale, out, lse, ws)
+        torch.cuda.synchronize()
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    bench_copy(dst, src, nbytes)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_pass": True, "steps_per_mode": args.steps, "copy_bytes": nbytes}), flush=True)
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -169,13 +205,17 @@ def main():
 
     cfg = CONFIGS[args.config]
     base = DeviceTree(cfg_id=args.config)
+    if args.profile_pass:
+        _profile_pass(base, args)
+        return
     uniq_tok, logical_tok = _unique_kv(base)
     kv_bytes_per_tok = cfg.hkv * cfg.d * 2 * 2
     uniq_bytes = uniq_tok * kv_bytes_per_tok
     n_rep = args.replicas or max(1, math.ceil(1.2e9 / uniq_bytes))
     reps = [base] + [base.clone() for _ in range(n_rep - 1)]
 
-    ms, kern_ms, comb_ms, launches = _time_mode(reps, 0, args.steps, args.warmup, KERNEL_PARTIAL)
+    tm = _time_mode(reps, 0, args.steps, args.warmup, KERNEL_PARTIAL)
+    ms, kern_ms, comb_ms, launches = tm["ms"], tm["kernel_ms"], tm["combine_ms"], tm["launches"]
     n_leaves = len(base.leaves)
     value = n_leaves / (ms * 1e-3)
     achieved_step = uniq_bytes / (ms * 1e-3) / 1e9
@@ -188,6 +228,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 5),
+        "ms_per_step_with_kernel_events": round(tm["ms_instrumented"], 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -208,9 +249,12 @@ def main():
         "combine_avg_ms": round(comb_ms, 5),
     }
     if not args.no_naive:
-        nms, nk, nc, _ = _time_mode(reps, 1, args.steps, args.warmup, KERNEL_PARTIAL)
+        tn = _time_mode(reps, 1, args.steps, args.warmup, KERNEL_PARTIAL)
+        nms = tn["ms"]
         line["naive_baseline"] = {"ms_per_step": round(nms, 5), "value": round(n_leaves / (nms * 1e-3), 1),
-                                  "kernel_avg_ms": round(nk, 5), "speedup_tree_vs_naive": round(nms / ms, 4)}
+                                  "kernel_avg_ms": round(tn["kernel_ms"], 5),
+                                  "combine_avg_ms": round(tn["combine_ms"], 5),
+                                  "speedup_tree_vs_naive": round(nms / ms, 4)}
     line["probe_read_GBps"] = round(_probe_read(), 1)
     del reps, base
     torch.cuda.empty_cache()

@@ -60,8 +60,8 @@ typedef struct treepo_ctx treepo_ctx;
  * r = block * B + offset of KV head g starts at element ((g*num_blocks*B)+r)*D.
  * V pool, device bf16, layout [Hkv][num_blocks][D][B]: every block is stored
  * transposed, so element (g, r, d) is at ((g*num_blocks + r/B)*D + d)*B + r%B.
- * head_dim D must be 64 or 128, block_tokens B must be 64 (one block is one
- * kernel tile), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned and
+ * head_dim D must be 64 or 128, block_tokens B must be 64 (the decode kernels
+ * stream 32-token half blocks), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned and
  * must stay valid until treepo_destroy; their contents need no initialisation.
  */
 typedef struct treepo_config {
@@ -193,7 +193,8 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  *   {kind (0 VALU, 1 MFMA), rowset_begin, n_leaves, tile_begin, tile_end,
  *    partial_base, rows, run}
  * rowsets[]: call positions; tiles[] 4 int32 each {block, node, tile_in_node,
- * valid_tokens}.  Pass null arrays to query the counts only. */
+ * valid_tokens}: tile k of a node holds its tokens [32k, 32k+32) and lives in
+ * pool block block_begin + k/2.  Pass null arrays to query the counts only. */
 int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
                            int32_t mode, int32_t* items, int32_t* rowsets, int32_t* tiles,
                            int32_t* n_items, int32_t* n_rowsets, int32_t* n_tiles);

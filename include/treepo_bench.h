@@ -27,6 +27,20 @@ int32_t treepo_bench_copy(void* dst, const void* src, size_t bytes, hipStream_t 
  * Same alignment rules as treepo_bench_copy. */
 int32_t treepo_bench_read(const void* src, size_t bytes, float* sink, hipStream_t stream);
 
+/* Streams src[0:bytes) with `workgroups` workgroups of 256 threads and the
+ * staging pattern of the decode kernels, writing one fp32 per workgroup into
+ * sink (device, >= workgroups floats):
+ *   mode 0: each workgroup reads one contiguous share in 16 KiB chunks through
+ *           16-byte global->LDS loads, three chunks in flight, a workgroup
+ *           barrier per chunk (the decode pipeline);
+ *   mode 1: the same staging with chunks assigned grid-stride;
+ *   mode 2: each workgroup reads one contiguous share with 16-byte register
+ *           loads.
+ * bytes must be a multiple of 16 KiB * workgroups, 1 <= workgroups <= 4096,
+ * src 16-byte aligned.  Returns 0, TREEPO_EINVAL or TREEPO_EHIP. */
+int32_t treepo_bench_stream(const void* src, size_t bytes, float* sink, int32_t mode,
+                            int32_t workgroups, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -4,5 +4,5 @@ The compute lives in ``libtreepo.so`` (HIP kernels behind the C-ABI of
 ``include/treepo.h``); ``treepo`` is its ctypes binding.
 """
 
-from .treepo import (Context, TreePOError, load_library, bench_copy, bench_read,  # noqa: F401
+from .treepo import (Context, TreePOError, load_library, bench_copy, bench_read, bench_stream,  # noqa: F401
                      MODE_TREE, MODE_NAIVE, KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE, NODE_FIELDS, BLOCK_TOKENS, LIB_PATH)

@@ -34,7 +34,90 @@ __global__ __launch_bounds__(kThreads) void read_kernel(const uint4* __restrict_
   if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(red[0] & 0xFFFF);
 }
 
+// Streaming reads with the staging pattern of the decode kernels: 16 KiB
+// chunks moved with 16-byte global->LDS loads into a ring of four LDS buffers,
+// three chunks in flight, one workgroup barrier per chunk.  `blocked` selects
+// whether each workgroup streams one contiguous share (as a decode work item
+// does) or takes chunks grid-stride.
+constexpr int kChunk = 16384;
+
+__device__ __forceinline__ void lds_load16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(lds) : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void landed_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(N) : "memory");
+}
+
+__global__ __launch_bounds__(kThreads) void stream_lds_kernel(const char* __restrict__ src, int64_t nchunks,
+                                                              int32_t blocked, float* __restrict__ sink) {
+  __shared__ __attribute__((aligned(1024))) char buf[4][kChunk];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t G = gridDim.x;
+  const int64_t per = nchunks / G;
+  const int64_t first = blocked ? blockIdx.x * per : blockIdx.x;
+  const int64_t step = blocked ? 1 : G;
+  const int64_t count = blocked ? per : (nchunks - blockIdx.x + G - 1) / G;
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+      (const __attribute__((address_space(3))) char*)&buf[0][0]));
+  auto issue = [&](int64_t i) {
+    const char* g = src + (first + i * step) * kChunk;
+    const uint32_t b = base + static_cast<uint32_t>(i & 3) * kChunk;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int slot = wave * 4 + j;
+      lds_load16(g + slot * 1024 + lane * 16, __builtin_amdgcn_readfirstlane(b + slot * 1024));
+    }
+  };
+  for (int64_t p = 0; p < 3 && p < count; ++p) issue(p);
+  uint32_t acc = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    const int64_t ahead = count - 1 - i;
+    if (ahead >= 2)
+      landed_barrier<8>();
+    else if (ahead == 1)
+      landed_barrier<4>();
+    else
+      landed_barrier<0>();
+    if (i + 3 < count) issue(i + 3);
+    acc ^= reinterpret_cast<const uint32_t*>(buf[i & 3])[threadIdx.x];
+  }
+  if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(acc & 0xFFFF);
+}
+
+// Each workgroup streams one contiguous share with 16-byte register loads.
+__global__ __launch_bounds__(kThreads) void stream_reg_kernel(const uint4* __restrict__ src, int64_t n16_per_wg,
+                                                              float* __restrict__ sink) {
+  const uint4* p = src + blockIdx.x * n16_per_wg;
+  uint32_t acc = 0;
+#pragma unroll 4
+  for (int64_t i = threadIdx.x; i < n16_per_wg; i += kThreads) {
+    const uint4 v = p[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(acc & 0xFFFF);
+}
+
 }  // namespace
+
+extern "C" int32_t treepo_bench_stream(const void* src, size_t bytes, float* sink, int32_t mode,
+                                       int32_t workgroups, hipStream_t stream) {
+  if (!src || !sink || workgroups < 1 || workgroups > 4096 || reinterpret_cast<uintptr_t>(src) % 16 ||
+      mode < 0 || mode > 2)
+    return TREEPO_EINVAL;
+  if (bytes % (static_cast<size_t>(kChunk) * workgroups) != 0) return TREEPO_EINVAL;
+  const int64_t nchunks = static_cast<int64_t>(bytes / kChunk);
+  if (mode == 2)
+    stream_reg_kernel<<<workgroups, kThreads, 0, stream>>>(static_cast<const uint4*>(src),
+                                                           static_cast<int64_t>(bytes / 16 / workgroups), sink);
+  else
+    stream_lds_kernel<<<workgroups, kThreads, 0, stream>>>(static_cast<const char*>(src), nchunks, mode == 0 ? 1 : 0,
+                                                           sink);
+  return hipGetLastError() == hipSuccess ? TREEPO_OK : TREEPO_EHIP;
+}
 
 extern "C" int32_t treepo_bench_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
   if (!dst || !src || bytes % 16 != 0 || (reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) % 16)

@@ -1,0 +1,16 @@
+// Host-only stand-ins for the kernel launchers, for the sanitizer build of the
+// host core (node table, planner, C-ABI bookkeeping).  Every launch reports
+// that no device is present; the metadata, validation and error paths under
+// test never launch.
+#include "kernels.h"
+
+namespace treepo {
+
+hipError_t launch_partial(const DecodeArgs&, int32_t, int32_t, hipStream_t) { return hipErrorNoDevice; }
+hipError_t launch_combine(const DecodeArgs&, hipStream_t) { return hipErrorNoDevice; }
+hipError_t launch_kv_append(const uint16_t*, const uint16_t*, uint16_t*, uint16_t*, int64_t, int32_t, int32_t,
+                            const AppendPiece*, int32_t, hipStream_t) {
+  return hipErrorNoDevice;
+}
+
+}  // namespace treepo

@@ -7,7 +7,7 @@
 
 namespace treepo {
 
-constexpr int kTile = 64;  // tokens per KV tile == tokens per pool block
+constexpr int kTile = 64;  // tokens per pool block
 
 // Device views of the decode plan and buffers (see tree_core.h for layouts).
 struct DecodeArgs {

@@ -10,8 +10,8 @@
 // and query head, the partials of its chain (exact log-sum-exp algebra).
 //
 // Layouts: K pool [Hkv][blocks][64][D] (token rows), V pool [Hkv][blocks][D][64]
-// (each block transposed, so a d-row holds 64 consecutive tokens).  One pool
-// block is one 64-token tile.
+// (each block transposed, so a d-row holds 64 consecutive tokens).  The decode
+// kernels stream half blocks (32-token tiles).
 #include "kernels.h"
 
 #include <math.h>
@@ -46,35 +46,36 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 // ---- KV tile staging ----------------------------------------------------------
 //
-// LDS tile = K rows [64][D] then V^T rows [D][64], both in 16-byte chunks with
-// an XOR swizzle so that the compute reads below are bank-conflict free:
-//   K: chunk c of token row r sits at chunk position c ^ ((r & 1) << 2)
-//   V: chunk c of d-row d sits at chunk position c ^ (d & 7)
-// Every wave moves whole 1 KiB LDS slots; the swizzle is applied on the global
-// side (each lane picks which chunk of the same row it fetches), so the global
-// reads of a slot stay fully coalesced.
+// A tile is 32 tokens: one half of a 64-token pool block.  LDS tile = K rows
+// [32][D] then V^T rows [D][32], in 16-byte chunks with XOR swizzles that make
+// the compute reads conflict free (per 8-lane LDS phase):
+//   K: chunk c of token row r sits at position c ^ ((r & 3) | ((r >> 1) & 4));
+//      the VALU reader takes 8 chunks of one row, the MFMA reader one chunk of
+//      rows {R+0..3, R+8..11} -- both hit 8 distinct bank groups.
+//   V: chunk c of d-row d sits at position c ^ ((d >> 1) & 3); both readers
+//      take one chunk of 8 consecutive d-rows.
+// Each wave moves whole 1 KiB LDS slots; the swizzle is applied on the global
+// side (a lane picks which chunk of the same row it fetches), so each slot is
+// still read from HBM in whole row segments.  Four tile buffers per workgroup
+// keep three tiles in flight while one is consumed.
+constexpr int kSub = 32;   // tokens per tile
+constexpr int kNBuf = 4;   // LDS tile buffers per workgroup
+
 template <int D>
 struct TileSmem {
-  static constexpr int kElems = kTile * D;
-  uint16_t kv[2][2 * kElems];
-  uint32_t pbuf[kWaves][8][16];  // per wave: token pair x (8 hi words, 8 lo words) of packed P
+  static constexpr int kElems = kSub * D;   // K (or V^T) elements per tile
+  uint16_t kv[kNBuf][2 * kElems];
+  uint32_t pbuf[kWaves][4][16];  // per wave: token pair x (8 hi, 8 lo) packed P words
 };
 
-// K chunk swizzles (the position of chunk c of token row r is c ^ swz(r)):
-// the VALU reader takes, per 8-lane LDS phase, chunks j + 4i of two adjacent
-// rows; the MFMA reader takes one chunk of rows {R+0..3, R+8..11}.
-struct KSwzValu {
-  __device__ static int f(int r) { return (r & 1) << 2; }
-};
-struct KSwzMfma {
-  __device__ static int f(int r) { return (r & 3) | ((r >> 1) & 4); }
-};
+__device__ __forceinline__ int k_swz(int r) { return (r & 3) | ((r >> 1) & 4); }
+__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
 
 // One 16-byte global->LDS load per lane into the 1 KiB LDS slot at byte
 // address `lds` (wave-uniform).  Issued as inline asm so that the compiler does
 // not treat the in-flight LDS writes as aliasing every later LDS access (which
-// would drain the prefetch of the next tile); completion is tracked by hand
-// with vmcnt waits before the barrier that publishes a tile.
+// would drain the prefetch); completion is tracked by hand with vmcnt waits
+// before the barrier that publishes a tile.
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(g), "s"(lds) : "memory", "m0");
@@ -84,63 +85,66 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)p));
 }
 
-// Stages tile `block` of KV head g into the LDS buffer at byte address `dst`.
-// D/16 loads per lane.
-template <int D, class KSwz>
+// Loads per lane per tile.
+template <int D>
+constexpr int dma_per_tile() { return D / 32; }
+
+// Stages tile (block, half) of KV head g into the LDS buffer at byte address `dst`.
+template <int D>
 __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
                                          const uint16_t* __restrict__ vpool, int64_t num_blocks,
-                                         int g, int block, uint32_t dst, int wave, int lane) {
+                                         int g, int block, int half, uint32_t dst, int wave, int lane) {
   constexpr int kKChunks = D / 8;   // 16-byte chunks per K row
-  constexpr int kPerWave = D / 32;  // 1 KiB slots per wave for each of K and V
-  const int64_t base = (static_cast<int64_t>(g) * num_blocks + block) * (kTile * D);
-  const char* kg = reinterpret_cast<const char*>(kpool + base);
-  const char* vg = reinterpret_cast<const char*>(vpool + base);
-  const uint32_t vd = dst + kTile * D * 2;
+  constexpr int kPerWave = D / 64;  // 1 KiB slots per wave for each of K and V
+  const int64_t blk = static_cast<int64_t>(g) * num_blocks + block;
+  const char* kg = reinterpret_cast<const char*>(kpool + (blk * kTile + half * kSub) * D);
+  const char* vg = reinterpret_cast<const char*>(vpool + blk * kTile * D) + half * (kSub * 2);
+  const uint32_t vd = dst + kSub * D * 2;
 #pragma unroll
   for (int j = 0; j < kPerWave; ++j) {
     const int slot = wave * kPerWave + j;
     const int c = slot * 64 + lane;
     const int row = c / kKChunks;
-    const int col = (c % kKChunks) ^ KSwz::f(row);
+    const int col = (c % kKChunks) ^ k_swz(row);
     dma16(kg + row * (D * 2) + col * 16, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
   }
 #pragma unroll
   for (int j = 0; j < kPerWave; ++j) {
     const int slot = wave * kPerWave + j;
     const int c = slot * 64 + lane;
-    const int row = c >> 3;
-    const int col = (c & 7) ^ (row & 7);
-    dma16(vg + row * 128 + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
+    const int row = c >> 2;
+    const int col = (c & 3) ^ v_swz(row);
+    dma16(vg + row * (kTile * 2) + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
   }
 }
 
-// Barrier after which this workgroup's loads, except the newest N per lane,
-// have landed in LDS.
+// Barrier after which this workgroup's global->LDS loads, except the newest N
+// per lane, have landed; it also orders each wave's earlier LDS reads before
+// any later overwrite (every wave waits for its own LDS reads before it).
 template <int N>
 __device__ __forceinline__ void barrier_tile_landed() {
-  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" :: "n"(N) : "memory");
-}
-// Barrier after which no wave still reads the LDS it read before it.
-__device__ __forceinline__ void barrier_lds_reads_done() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(N) : "memory");
 }
 
-// ---- VALU node-partial ----------------------------------------------------------
-//
-// M query rows (M <= 8) per workgroup.  Wave w takes tokens [16w, 16w+16) of
-// every tile and keeps its own online-softmax state; the four states are
-// merged at the end.
-//   QK: lane (t = lane/4, j = lane%4) owns token 16w+t and the K chunks j, j+4,
-//       ... of its row; q rows sit in registers in the same chunk order.  The
-//       partial dot products (v_dot2 bf16 -> fp32) are summed across the quad
-//       with DPP.
-//   P : split into two bf16 terms, hi = bf16(p) and lo = bf16(p - hi), so the
-//       weights keep about 16 significant bits (a single bf16 P can be off by
-//       2^-8 relative, too much for short, peaked chains).  Token pairs are
-//       packed into 32-bit words and staged in a per-wave LDS slot.
-//   PV: lane i owns d = i (+64); V^T words hold two consecutive tokens of one
-//       d, matching the packed P pairs, so each v_dot2 does two tokens (one
-//       v_dot2 for hi and one for lo).
+// Waits for tile k (tiles up to k+2 may have been issued) and publishes it.
+template <int D>
+__device__ __forceinline__ void wait_tile(int k, int nt) {
+  constexpr int kD = dma_per_tile<D>();
+  const int ahead = nt - 1 - k;
+  if (ahead >= 2)
+    barrier_tile_landed<2 * kD>();
+  else if (ahead == 1)
+    barrier_tile_landed<kD>();
+  else
+    barrier_tile_landed<0>();
+}
+
+// Tile t of an item: (pool block, half) from the plan's tile record.
+__device__ __forceinline__ void tile_src(const int32_t* __restrict__ tiles, int t, int* block, int* half) {
+  *block = tiles[4 * t];
+  *half = tiles[4 * t + 2] & 1;
+}
+
 // Kernel arguments: the pointers are passed as separate __restrict__ kernel
 // parameters so that uniform metadata reads become scalar loads.
 struct Scalars {
@@ -156,18 +160,87 @@ struct Scalars {
       float *__restrict__ part_o, float *__restrict__ part_ml, Scalars sc
 #define TREEPO_PARTIAL_ARGS kpool, vpool, q, items, rowsets, tiles, part_o, part_ml, sc
 
+// Issues the first min(3, nt) tiles of an item.
+template <int D>
+__device__ __forceinline__ void dma_prologue(TREEPO_PARTIAL_PARAMS, int tb, int nt, int g, uint32_t buf0,
+                                             int wave, int lane) {
+  constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
+#pragma unroll
+  for (int p = 0; p < 3; ++p) {
+    if (p < nt) {
+      int block, half;
+      tile_src(tiles, tb + p, &block, &half);
+      dma_tile<D>(kpool, vpool, sc.num_blocks, g, block, half, buf0 + p * kBufBytes, wave, lane);
+    }
+  }
+}
+
+// After tile k is published: prefetch tile k+3 into the buffer tile k-1 used.
+template <int D>
+__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int tb, int nt, int k, int g, uint32_t buf0,
+                                          int wave, int lane) {
+  constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
+  if (k + 3 < nt) {
+    int block, half;
+    tile_src(tiles, tb + k + 3, &block, &half);
+    dma_tile<D>(kpool, vpool, sc.num_blocks, g, block, half, buf0 + ((k + 3) & 3) * kBufBytes, wave, lane);
+  }
+}
+
+// ---- VALU node-partial ----------------------------------------------------------
+//
+// M query rows (M <= 8) per workgroup.  Wave w takes tokens [8w, 8w+8) of
+// every tile and keeps its own online-softmax state; the four states are
+// merged at the end.
+//   QK: lane (t = lane/8, j = lane%8) owns token 8w+t and the K chunks j, j+8
+//       of its row; q rows sit in registers in the same chunk order.  The
+//       partial dot products (v_dot2 bf16 -> fp32) are summed across the 8
+//       lanes with DPP (quad permutes, then a half-row mirror).
+//   P : split into two bf16 terms, hi = bf16(p) and lo = bf16(p - hi), so the
+//       weights keep about 16 significant bits (a single bf16 P can be off by
+//       2^-8 relative, too much for short, peaked chains).  Token pairs are
+//       packed into 32-bit words and staged in a per-wave LDS slot.
+//   PV: lane i owns d = i (+64); V^T words hold two consecutive tokens of one
+//       d, matching the packed P pairs, so each v_dot2 does two tokens (one
+//       v_dot2 for hi and one for lo).
 template <int D, int M>
 __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g,
                                           TileSmem<D>& sm) {
-  constexpr int kKW = D / 8;   // K words per lane in QK
-  constexpr int kKC = D / 32;  // K chunks per lane in QK
+  constexpr int kKC = D / 64;  // K chunks per lane in QK
+  constexpr int kKW = 4 * kKC; // K words per lane in QK
   constexpr int kDD = D / 64;  // d values per lane in PV
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int t = lane >> 2;
-  const int j = lane & 3;
+  const int t = lane >> 3;
+  const int j = lane & 7;
   const int rowset = it[1], tb = it[3], te = it[4], pbase = it[5], rows = it[6];
   const int G = sc.group;
+  const int nt = te - tb;
+  const uint32_t buf0 = lds_addr(sm.kv[0]);
+  dma_prologue<D>(TREEPO_PARTIAL_ARGS, tb, nt, g, buf0, wave, lane);
+
+  uint32_t qr[M][kKW];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    const int leaf = rowsets[rowset + m / G];
+    const int head = g * G + m % G;
+    const uint4* qp = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(leaf) * sc.hq + head) * D);
+#pragma unroll
+    for (int i = 0; i < kKC; ++i) {
+      const uint4 v = qp[j + 8 * i];
+      qr[m][4 * i + 0] = v.x;
+      qr[m][4 * i + 1] = v.y;
+      qr[m][4 * i + 2] = v.z;
+      qr[m][4 * i + 3] = v.w;
+    }
+  }
+  // Make the query loads complete here, outside the tile loop: the compiler
+  // does not see the asm tile loads, and a wait for q inside the loop would
+  // also drain the prefetch.
+#pragma unroll
+  for (int m = 0; m < M; ++m)
+#pragma unroll
+    for (int w = 0; w < kKW; ++w) asm volatile("" ::"v"(qr[m][w]));
 
   float m_run[M], l_run[M], acc[M][kDD];
 #pragma unroll
@@ -178,54 +251,20 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
     for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = 0.f;
   }
 
-  const int nt = te - tb;
-  const uint32_t buf0 = lds_addr(sm.kv[0]);
-  constexpr uint32_t kBufBytes = 2 * kTile * D * 2;
-  dma_tile<D, KSwzValu>(kpool, vpool, sc.num_blocks, g, tiles[4 * tb], buf0, wave, lane);
-
-  uint32_t qr[M][kKW];
-#pragma unroll
-  for (int m = 0; m < M; ++m) {
-    const int leaf = rowsets[rowset + m / G];
-    const int head = g * G + m % G;
-    const uint4* qp = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(leaf) * sc.hq + head) * D);
-#pragma unroll
-    for (int i = 0; i < kKC; ++i) {
-      const uint4 v = qp[j + 4 * i];
-      qr[m][4 * i + 0] = v.x;
-      qr[m][4 * i + 1] = v.y;
-      qr[m][4 * i + 2] = v.z;
-      qr[m][4 * i + 3] = v.w;
-    }
-  }
-
-  // Make the query loads complete here, outside the tile loop: the compiler
-  // does not see the asm tile loads, and a wait for q inside the loop would
-  // also drain the prefetch of the next tile.
-#pragma unroll
-  for (int m = 0; m < M; ++m)
-#pragma unroll
-    for (int w = 0; w < kKW; ++w) asm volatile("" ::"v"(qr[m][w]));
-
   for (int k = 0; k < nt; ++k) {
     const int valid = tiles[4 * (tb + k) + 3];
-    if (k + 1 < nt) {
-      dma_tile<D, KSwzValu>(kpool, vpool, sc.num_blocks, g, tiles[4 * (tb + k + 1)],
-                            buf0 + ((k + 1) & 1) * kBufBytes, wave, lane);
-      barrier_tile_landed<D / 16>();
-    } else {
-      barrier_tile_landed<0>();
-    }
-    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 1]);
-    const char* vt = kt + kTile * D * 2;
+    wait_tile<D>(k, nt);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, tb, nt, k, g, buf0, wave, lane);
+    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 3]);
+    const char* vt = kt + kSub * D * 2;
 
     // ---- scores
-    const int row = wave * 16 + t;
+    const int row = wave * 8 + t;
     uint32_t kr[kKW];
 #pragma unroll
     for (int i = 0; i < kKC; ++i) {
-      const int c = j + 4 * i;
-      const uint4 v = *reinterpret_cast<const uint4*>(kt + row * (D * 2) + ((c ^ KSwzValu::f(row)) << 4));
+      const int c = j + 8 * i;
+      const uint4 v = *reinterpret_cast<const uint4*>(kt + row * (D * 2) + ((c ^ k_swz(row)) << 4));
       kr[4 * i + 0] = v.x;
       kr[4 * i + 1] = v.y;
       kr[4 * i + 2] = v.z;
@@ -238,33 +277,48 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 #pragma unroll
       for (int w = 0; w < kKW; ++w) x = dot2(qr[m][w], kr[w], x);
       x = quad_sum(x);
+      x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141, 0xF, 0xF, true));
       s[m] = row < valid ? x * sc.scale_log2 : -INFINITY;
     }
 
-    // ---- online softmax over this wave's 16 tokens
+    // ---- online softmax over this wave's 8 tokens.  m_run is a per-row
+    // reference, not necessarily the exact running max: the weights are
+    // 2^(s - m_run) and the result does not depend on the reference.  Only
+    // when a score exceeds it by more than 2^8 (always on the first tile) are
+    // the exact tile maxima reduced across the wave and the state rescaled.
+    bool over = false;
+#pragma unroll
+    for (int m = 0; m < M; ++m) over |= s[m] > m_run[m] + 8.f;
+    if (__builtin_amdgcn_ballot_w64(over) != 0) {
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        float mx = s[m];
+        mx = fmaxf(mx, __shfl_xor(mx, 8));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mn = fmaxf(m_run[m], mx);
+        const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[m] - mn);
+        l_run[m] *= alpha;
+#pragma unroll
+        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] *= alpha;
+        m_run[m] = mn;
+      }
+    }
     uint32_t pk[M], pkl[M];
 #pragma unroll
     for (int m = 0; m < M; ++m) {
-      float mx = s[m];
-      mx = fmaxf(mx, __shfl_xor(mx, 4));
-      mx = fmaxf(mx, __shfl_xor(mx, 8));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m_run[m], mx);
-      const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[m] - mn);
-      const float p = s[m] == -INFINITY ? 0.f : fast_exp2(s[m] - mn);
+      const float p = s[m] == -INFINITY ? 0.f : fast_exp2(s[m] - m_run[m]);
       const uint32_t pb = f2bf_bits(p);
       const uint32_t pl = f2bf_bits(p - bf_bits2f(pb));
-      l_run[m] = l_run[m] * alpha + (bf_bits2f(pb) + bf_bits2f(pl));
-#pragma unroll
-      for (int dd = 0; dd < kDD; ++dd) acc[m][dd] *= alpha;
-      m_run[m] = mn;
+      l_run[m] += bf_bits2f(pb) + bf_bits2f(pl);
+      // token t-1 sits 8 lanes down in the same row of 16 lanes
       const uint32_t both = pb | (pl << 16);
-      const uint32_t partner = static_cast<uint32_t>(__shfl_xor(static_cast<int>(both), 4));
-      pk[m] = (both & 0xFFFFu) | (partner << 16);
-      pkl[m] = (both >> 16) | (partner & 0xFFFF0000u);
+      const uint32_t prev = static_cast<uint32_t>(
+          __builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x118, 0xF, 0xF, false));
+      pk[m] = (prev & 0xFFFFu) | (both << 16);
+      pkl[m] = (prev >> 16) | (both & 0xFFFF0000u);
     }
-    if ((t & 1) == 0 && j == 0) {
+    if ((t & 1) == 1 && j == 0) {
 #pragma unroll
       for (int m = 0; m < M; ++m) {
         sm.pbuf[wave][t >> 1][m] = pk[m];
@@ -273,32 +327,29 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
     }
 
     // ---- P V
-    uint32_t vw[kDD][8];
+    uint32_t vw[kDD][4];
 #pragma unroll
     for (int dd = 0; dd < kDD; ++dd) {
       const int d = lane + 64 * dd;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint4 v = *reinterpret_cast<const uint4*>(vt + d * 128 + ((((2 * wave + h) ^ (d & 7))) << 4));
-        vw[dd][4 * h + 0] = v.x;
-        vw[dd][4 * h + 1] = v.y;
-        vw[dd][4 * h + 2] = v.z;
-        vw[dd][4 * h + 3] = v.w;
-      }
+      const uint4 v = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((wave ^ v_swz(d)) << 4));
+      vw[dd][0] = v.x;
+      vw[dd][1] = v.y;
+      vw[dd][2] = v.z;
+      vw[dd][3] = v.w;
     }
-    if (valid < kTile) {
+    if (valid < kSub) {
       // tokens past the node's length may hold anything; P is 0 there, and the
       // V halves are cleared so that 0 * garbage cannot produce NaN
 #pragma unroll
-      for (int tp = 0; tp < 8; ++tp) {
-        const int tk = wave * 16 + 2 * tp;
+      for (int tp = 0; tp < 4; ++tp) {
+        const int tk = wave * 8 + 2 * tp;
         const uint32_t msk = tk >= valid ? 0u : (tk + 1 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
 #pragma unroll
         for (int dd = 0; dd < kDD; ++dd) vw[dd][tp] &= msk;
       }
     }
 #pragma unroll
-    for (int tp = 0; tp < 8; ++tp) {
+    for (int tp = 0; tp < 4; ++tp) {
       const uint4 p0 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][0]);
       const uint4 p1 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][4]);
       const uint4 p2 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][8]);
@@ -310,14 +361,13 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 #pragma unroll
         for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = dot2(pl[m], vw[dd][tp], dot2(pw[m], vw[dd][tp], acc[m][dd]));
     }
-    barrier_lds_reads_done();
   }
+  __syncthreads();
 
   // ---- merge the four waves' states and write the partial rows
 #pragma unroll
   for (int m = 0; m < M; ++m) {
     float l = l_run[m];
-    l += __shfl_xor(l, 4);
     l += __shfl_xor(l, 8);
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
@@ -366,16 +416,16 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 //
 // For shared nodes whose stacked query rows (descendant leaves x GQA group)
 // form dense tiles.  Rows are cut into 16-row blocks; wave w owns blocks
-// w, w+4, w+8, w+12 (NRB per wave) and keeps their online-softmax state; all
-// four waves read every KV tile from LDS.  Items hold at most 128 rows (two
-// row blocks per wave) so that the K and V operands read from LDS are reused
-// across a wave's row blocks without spilling registers.
+// w, w+4 (NRB per wave) and keeps their online-softmax state; all four waves
+// read every KV tile from LDS.  Items hold at most 128 rows (two row blocks
+// per wave) so that the K and V operands read from LDS are reused across a
+// wave's row blocks without spilling registers.
 //   QK: S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 K rows, B = Q^T).
-//       The K rows of token block b are read in the order
-//       tau(b, r) = 32(b/2) + 8(r/4) + 4(b%2) + r%4, so that each lane's four
-//       outputs of blocks 2s and 2s+1 are the eight consecutive tokens
-//       32s + 8(lane/16) + 0..7 -- exactly the B operand layout of the PV
-//       product, so P never leaves registers.
+//       The K rows of token block b (0, 1) are read in the order
+//       tau(b, r) = 8(r/4) + 4b + r%4, so that each lane's four outputs of the
+//       two blocks are the eight consecutive tokens 8(lane/16) + 0..7 --
+//       exactly the B operand layout of the PV product, so P never leaves
+//       registers.
 //   P : split into hi = bf16(p) and lo = bf16(p - hi) (about 16 significant
 //       bits for the weights).
 //   PV: O^T = V^T P_hi^T + V^T P_lo^T (A = 16 d-rows of the transposed V
@@ -388,7 +438,7 @@ __device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c)
                                                  0, 0, 0);
 }
 
-__device__ __forceinline__ int tau(int b, int r) { return 32 * (b >> 1) + 8 * (r >> 2) + 4 * (b & 1) + (r & 3); }
+__device__ __forceinline__ int tau(int b, int r) { return 8 * (r >> 2) + 4 * b + (r & 3); }
 
 template <int D, int NRB>
 __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g, TileSmem<D>& sm) {
@@ -402,8 +452,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   const int G = sc.group;
   const int nt = te - tb;
   const uint32_t buf0 = lds_addr(sm.kv[0]);
-  constexpr uint32_t kBufBytes = 2 * kTile * D * 2;
-  dma_tile<D, KSwzMfma>(kpool, vpool, sc.num_blocks, g, tiles[4 * tb], buf0, wave, lane);
+  dma_prologue<D>(TREEPO_PARTIAL_ARGS, tb, nt, g, buf0, wave, lane);
 
   // Q^T operands: lane holds row m = 16 rb + r16, d chunk 4 ks + a
   uint4 qb[NRB][kKS];
@@ -440,45 +489,40 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 
   for (int k = 0; k < nt; ++k) {
     const int valid = tiles[4 * (tb + k) + 3];
-    if (k + 1 < nt) {
-      dma_tile<D, KSwzMfma>(kpool, vpool, sc.num_blocks, g, tiles[4 * (tb + k + 1)],
-                            buf0 + ((k + 1) & 1) * kBufBytes, wave, lane);
-      barrier_tile_landed<D / 16>();
-    } else {
-      barrier_tile_landed<0>();
-    }
-    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 1]);
-    const char* vt = kt + kTile * D * 2;
+    wait_tile<D>(k, nt);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, tb, nt, k, g, buf0, wave, lane);
+    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 3]);
+    const char* vt = kt + kSub * D * 2;
     if (my_rb > 0) {
       // ---- S^T = K Q^T for the wave's row blocks
-      f32x4 S[NRB][4];
+      f32x4 S[NRB][2];
 #pragma unroll
       for (int i = 0; i < NRB; ++i)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) S[i][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int b = 0; b < 2; ++b) S[i][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < kKS; ++ks) {
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < 2; ++b) {
           const int tok = tau(b, r16);
           const int c = 4 * ks + a;
-          const uint4 ka = *reinterpret_cast<const uint4*>(kt + tok * (D * 2) + ((c ^ KSwzMfma::f(tok)) << 4));
+          const uint4 ka = *reinterpret_cast<const uint4*>(kt + tok * (D * 2) + ((c ^ k_swz(tok)) << 4));
 #pragma unroll
           for (int i = 0; i < NRB; ++i)
             if (i < my_rb) S[i][b] = mfma16(ka, qb[i][ks], S[i][b]);
         }
       }
-      // ---- online softmax; lane holds row r16, tokens tau(b, 4a + e)
-      uint4 P[NRB][2], PL[NRB][2];
+      // ---- online softmax; lane holds row r16, tokens 8a + 4b + e
+      uint4 P[NRB], PL[NRB];
 #pragma unroll
       for (int i = 0; i < NRB; ++i) {
         if (i >= my_rb) continue;
         float mx = -INFINITY;
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int tok = 32 * (b >> 1) + 8 * a + 4 * (b & 1) + e;
+            const int tok = 8 * a + 4 * b + e;
             const float x = tok < valid ? S[i][b][e] * sc.scale_log2 : -INFINITY;
             S[i][b][e] = x;
             mx = fmaxf(mx, x);
@@ -489,9 +533,9 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
         const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[i] - mn);
         m_run[i] = mn;
         float ls = 0.f;
-        uint32_t pw[8], pwl[8];
+        uint32_t pw[4], pwl[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int e = 0; e < 4; e += 2) {
             const float x0 = S[i][b][e], x1 = S[i][b][e + 1];
@@ -500,14 +544,11 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
             const uint32_t p0 = f2bf_bits(f0), p1 = f2bf_bits(f1);
             const uint32_t q0 = f2bf_bits(f0 - bf_bits2f(p0)), q1 = f2bf_bits(f1 - bf_bits2f(p1));
             ls += (bf_bits2f(p0) + bf_bits2f(q0)) + (bf_bits2f(p1) + bf_bits2f(q1));
-            // k-step s = b/2 holds block 2s in words 0,1 and block 2s+1 in words 2,3
-            pw[4 * (b >> 1) + 2 * (b & 1) + (e >> 1)] = p0 | (p1 << 16);
-            pwl[4 * (b >> 1) + 2 * (b & 1) + (e >> 1)] = q0 | (q1 << 16);
+            pw[2 * b + (e >> 1)] = p0 | (p1 << 16);
+            pwl[2 * b + (e >> 1)] = q0 | (q1 << 16);
           }
-        P[i][0] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
-        P[i][1] = make_uint4(pw[4], pw[5], pw[6], pw[7]);
-        PL[i][0] = make_uint4(pwl[0], pwl[1], pwl[2], pwl[3]);
-        PL[i][1] = make_uint4(pwl[4], pwl[5], pwl[6], pwl[7]);
+        P[i] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+        PL[i] = make_uint4(pwl[0], pwl[1], pwl[2], pwl[3]);
         l_run[i] = l_run[i] * alpha + ls;
 #pragma unroll
         for (int db = 0; db < kDB; ++db) acc[i][db] *= alpha;
@@ -516,28 +557,22 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 #pragma unroll
       for (int db = 0; db < kDB; ++db) {
         const int d = 16 * db + r16;
+        uint4 va = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
+        if (valid < kSub) {
+          // clear the V halves of tokens past the node's length (P is 0 there)
+          uint32_t w[4] = {va.x, va.y, va.z, va.w};
 #pragma unroll
-        for (int st = 0; st < 2; ++st) {
-          const int c = 4 * st + a;
-          uint4 va = *reinterpret_cast<const uint4*>(vt + d * 128 + ((c ^ (d & 7)) << 4));
-          if (valid < kTile) {
-            // clear the V halves of tokens past the node's length (P is 0 there)
-            const int t0 = 32 * st + 8 * a;
-            uint32_t w[4] = {va.x, va.y, va.z, va.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int tk = t0 + 2 * e;
-              w[e] &= tk >= valid ? 0u : (tk + 1 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
-            }
-            va = make_uint4(w[0], w[1], w[2], w[3]);
+          for (int e = 0; e < 4; ++e) {
+            const int tk = 8 * a + 2 * e;
+            w[e] &= tk >= valid ? 0u : (tk + 1 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
           }
-#pragma unroll
-          for (int i = 0; i < NRB; ++i)
-            if (i < my_rb) acc[i][db] = mfma16(va, PL[i][st], mfma16(va, P[i][st], acc[i][db]));
+          va = make_uint4(w[0], w[1], w[2], w[3]);
         }
+#pragma unroll
+        for (int i = 0; i < NRB; ++i)
+          if (i < my_rb) acc[i][db] = mfma16(va, PL[i], mfma16(va, P[i], acc[i][db]));
       }
     }
-    barrier_lds_reads_done();
   }
 
   // ---- write the partial rows (each wave owns its row blocks)
@@ -565,7 +600,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 //
 // One launch covers every work item of a decode step; each workgroup runs one
 // (item, KV head) on the VALU or the MFMA path according to the item's kind.
-// Two workgroups fit per CU (<= 256 registers per lane, 68 KB of LDS each).
+// Two workgroups fit per CU (<= 256 registers per lane, 65 KB of LDS each).
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void partial_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
   __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;

@@ -229,12 +229,14 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     r.tile_begin = static_cast<int32_t>(out->tiles.size());
     for (int32_t n : r.nodes) {
       const int32_t ln = nd[n].len;
-      for (int32_t k = 0; k * B < ln; ++k) {
+      constexpr int32_t T = kPlanTileTokens;
+      const int32_t per_block = B / T;
+      for (int32_t k = 0; k * T < ln; ++k) {
         Tile tl;
-        tl.block = nd[n].block_begin + k;
+        tl.block = nd[n].block_begin + k / per_block;
         tl.node = n;
         tl.tile_in_node = k;
-        tl.valid = std::min(B, ln - k * B);
+        tl.valid = std::min(T, ln - k * T);
         out->tiles.push_back(tl);
         out->unique_kv_tokens += tl.valid;
       }

@@ -76,6 +76,9 @@ class Tree {
 // ---- decode plan -----------------------------------------------------------
 
 enum PlanMode : int32_t { kModeTree = 0, kModeNaive = 1 };
+
+// Tokens per decode tile (half of a 64-token pool block).
+constexpr int32_t kPlanTileTokens = 32;
 enum ItemKind : int32_t { kKindValu = 0, kKindMfma = 1 };
 
 // One work item: a chunk of consecutive KV tiles of one run (a maximal chain
@@ -94,12 +97,14 @@ struct Item {
   int32_t run;
 };
 
-// A KV tile: up to B tokens of one block of one node.
+// A KV tile: up to kPlanTileTokens tokens of one node, tokens
+// [32 k, 32 k + 32) of the node for tile_in_node = k, inside pool block
+// block_begin + k / 2.
 struct Tile {
   int32_t block;
   int32_t node;
   int32_t tile_in_node;
-  int32_t valid;  // tokens of the tile holding data (1..B)
+  int32_t valid;  // tokens of the tile holding data (1..32)
 };
 
 // Per leaf, the partials to merge: slot(g, h') = a + g * b + h'.

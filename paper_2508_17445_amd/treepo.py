@@ -15,7 +15,9 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtreepo.so")
+# TREEPO_LIBRARY selects another build of the same C-ABI (the host-sanitizer
+# build in the CPU tests); by default the in-tree libtreepo.so is loaded.
+LIB_PATH = os.environ.get("TREEPO_LIBRARY") or os.path.join(HERE, "libtreepo.so")
 
 OK, EINVAL, ENOMEM, EFULL, EFROZEN, EEMPTY, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 MODE_TREE, MODE_NAIVE = 0, 1
@@ -75,8 +77,11 @@ def load_library(path: str = LIB_PATH):
         "treepo_last_error": (ctypes.c_char_p, [_p]),
         "treepo_bench_copy": (_i32, [_p, _p, ctypes.c_size_t, _p]),
         "treepo_bench_read": (_i32, [_p, ctypes.c_size_t, _p, _p]),
+        "treepo_bench_stream": (_i32, [_p, ctypes.c_size_t, _p, _i32, _i32, _p]),
     }
     for name, (res, args) in sig.items():
+        if name.startswith("treepo_bench_") and not hasattr(lib, name):
+            continue  # measurement probes are absent from host-only builds
         f = getattr(lib, name)
         f.restype = res
         f.argtypes = args
@@ -270,3 +275,10 @@ def bench_read(src, nbytes: int, sink, stream=None):
     st = lib.treepo_bench_read(_dev(src), nbytes, _dev(sink), _stream(stream))
     if st != OK:
         raise TreePOError(st, "treepo_bench_read")
+
+
+def bench_stream(src, nbytes: int, sink, mode: int, workgroups: int, stream=None):
+    lib = load_library()
+    st = lib.treepo_bench_stream(_dev(src), nbytes, _dev(sink), mode, workgroups, _stream(stream))
+    if st != OK:
+        raise TreePOError(st, "treepo_bench_stream")

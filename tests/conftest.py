@@ -14,6 +14,8 @@ def pytest_configure(config):
 
 
 def _gpu_available() -> bool:
+    if os.environ.get("TREEPO_NO_GPU_PROBE"):
+        return False
     try:
         import torch
         return torch.cuda.is_available()

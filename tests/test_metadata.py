@@ -74,8 +74,8 @@ def _plan_checks(ctx, model, leaves, mode):
         want = []
         for n in model.chain(x):
             ln = model.nodes[n]["len"]
-            for k in range((ln + 63) // 64):
-                want.append((model.nodes[n]["block_begin"] + k, n, k, min(64, ln - 64 * k)))
+            for k in range((ln + 31) // 32):     # 32-token tiles, two per 64-token block
+                want.append((model.nodes[n]["block_begin"] + k // 2, n, k, min(32, ln - 32 * k)))
         assert got == sorted(want), (mode, pos)
     # partial rows are laid out back to back without overlap
     bases = sorted((it[5], it[6] * ctx.cfg.num_kv_heads) for it in items)
