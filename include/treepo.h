@@ -58,8 +58,9 @@ typedef struct treepo_ctx treepo_ctx;
 /*
  * Pool shape.  K pool, device bf16, layout [Hkv][num_blocks][B][D]: token row
  * r = block * B + offset of KV head g starts at element ((g*num_blocks*B)+r)*D.
- * V pool, device bf16, layout [Hkv][num_blocks][D][B]: every block is stored
- * transposed, so element (g, r, d) is at ((g*num_blocks + r/B)*D + d)*B + r%B.
+ * V pool, device bf16, layout [Hkv][num_blocks][2][D][B/2]: every half block
+ * of 32 tokens is stored transposed, so element (g, r, d) is at
+ * (g*num_blocks*B + (r/32)*32)*D + d*32 + r%32.
  * head_dim D must be 64 or 128, block_tokens B must be 64 (the decode kernels
  * stream 32-token half blocks), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned and
  * must stay valid until treepo_destroy; their contents need no initialisation.
@@ -75,6 +76,9 @@ typedef struct treepo_config {
   void* k_pool;         /* device, see above                            */
   void* v_pool;         /* device, see above                            */
 } treepo_config;
+
+/* Work-item record exported by treepo_export_plan. */
+#define TREEPO_ITEM_FIELDS 12
 
 /* Node record exported by treepo_export_nodes: 8 int32 per node. */
 #define TREEPO_NODE_FIELDS 8 /* parent, depth, start, len, cap, block_begin, n_blocks, tree_id */
@@ -189,9 +193,10 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
                            int32_t* nodes, int32_t* desc_off, int32_t* desc,
                            int32_t* n_nodes, int32_t* total);
 
-/* The decode schedule for inspection.  Work items, 8 int32 each:
+/* The decode schedule for inspection.  Work items, TREEPO_ITEM_FIELDS int32 each:
  *   {kind (0 VALU, 1 MFMA), rowset_begin, n_leaves, tile_begin, tile_end,
- *    partial_base, rows, run}
+ *    partial_base, rows, run, src0, src1, src2, 0}
+ * where src_i = 2 * block + half of the item's i-th tile (-1 past its end)
  * rowsets[]: call positions; tiles[] 4 int32 each {block, node, tile_in_node,
  * valid_tokens}: tile k of a node holds its tokens [32k, 32k+32) and lives in
  * pool block block_begin + k/2.  Pass null arrays to query the counts only. */

@@ -12,12 +12,12 @@ constexpr int kTile = 64;  // tokens per pool block
 // Device views of the decode plan and buffers (see tree_core.h for layouts).
 struct DecodeArgs {
   const uint16_t* k_pool;  // bf16 [Hkv][num_blocks][64][D]
-  const uint16_t* v_pool;  // bf16 [Hkv][num_blocks][D][64]
+  const uint16_t* v_pool;  // bf16 [Hkv][num_blocks][2][D][32] (V^T per 32-token half block)
   int64_t num_blocks;
   int32_t hq, hkv, group, d;
   const uint16_t* q;       // bf16 [n_leaves][Hq][D]
   float scale_log2;        // softmax scale * log2(e)
-  const int32_t* items;    // Item, 8 int32 each
+  const int32_t* items;    // Item, 12 int32 each
   const int32_t* rowsets;
   const int32_t* tiles;    // Tile, 4 int32 each
   float* part_o;           // fp32 [partial_rows][D], unnormalised
@@ -32,6 +32,10 @@ struct DecodeArgs {
 // Node partials of items [first_item, first_item + n_items), VALU or MFMA by kind.
 hipError_t launch_partial(const DecodeArgs& a, int32_t first_item, int32_t n_items, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
+// Node-partial workgroups resident per compute unit (set by the kernel's
+// register and LDS budget); the planner sizes item chunks against it.
+int32_t partial_workgroups_per_cu();
+constexpr int32_t kComputeUnits = 256;  // MI355X
 
 // One block-aligned run of appended tokens: source rows [src_row, +count) go
 // to token offsets [off, off + count) of pool block `block` (off + count <= 64).

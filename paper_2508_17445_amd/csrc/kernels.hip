@@ -9,9 +9,10 @@
 // (O unnormalised, running max, sum) in fp32.  The combine merges, per leaf
 // and query head, the partials of its chain (exact log-sum-exp algebra).
 //
-// Layouts: K pool [Hkv][blocks][64][D] (token rows), V pool [Hkv][blocks][D][64]
-// (each block transposed, so a d-row holds 64 consecutive tokens).  The decode
-// kernels stream half blocks (32-token tiles).
+// Layouts: K pool [Hkv][blocks][64][D] (token rows), V pool
+// [Hkv][blocks][2][D][32] (each 32-token half block transposed, so a d-row
+// holds 32 consecutive tokens).  The decode kernels stream half blocks
+// (32-token tiles), each one contiguous 8 KiB (D = 128) range per pool.
 #include "kernels.h"
 
 #include <math.h>
@@ -37,6 +38,34 @@ __device__ __forceinline__ float quad_sum(float x) {
   return x;
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
+}
+
+// Reduce-scatter over the 8 lanes j = lane % 8 of a half row: lane j returns
+// sum over the 8 lanes of x[j].  Butterfly with DPP: half-row mirror (j <-> 7-j),
+// then quad swaps (j <-> j^2, j <-> j^1); each step keeps half of the rows.
+__device__ __forceinline__ float reduce_scatter8(const float (&x)[8], int j) {
+  const bool h4 = (j & 4) != 0, h2 = (j & 2) != 0, h1 = (j & 1) != 0;
+  float k4[4], k2[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float send = h4 ? x[i] : x[4 + i];
+    const float own = h4 ? x[4 + i] : x[i];
+    k4[i] = own + dppf<0x141>(send);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float send = h2 ? k4[i] : k4[2 + i];
+    const float own = h2 ? k4[2 + i] : k4[i];
+    k2[i] = own + dppf<0x4E>(send);
+  }
+  const float send = h1 ? k2[0] : k2[1];
+  const float own = h1 ? k2[1] : k2[0];
+  return own + dppf<0xB1>(send);
+}
+
 __device__ __forceinline__ uint32_t f2bf_bits(float x) {
   return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(x)));
 }
@@ -56,16 +85,28 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 //      take one chunk of 8 consecutive d-rows.
 // Each wave moves whole 1 KiB LDS slots; the swizzle is applied on the global
 // side (a lane picks which chunk of the same row it fetches), so each slot is
-// still read from HBM in whole row segments.  Four tile buffers per workgroup
-// keep three tiles in flight while one is consumed.
-constexpr int kSub = 32;   // tokens per tile
-constexpr int kNBuf = 4;   // LDS tile buffers per workgroup
+// still read from HBM in whole row segments.  kNBuf tile buffers per
+// workgroup keep kDepth tiles in flight while one is consumed.  Depth 3
+// (66.5 KB of LDS at D = 128) lets two workgroups share a CU; depth 2
+// (50 KB) lets three.
+#ifndef TREEPO_PIPE_DEPTH
+#define TREEPO_PIPE_DEPTH 3
+#endif
+constexpr int kSub = 32;                   // tokens per tile
+constexpr int kDepth = TREEPO_PIPE_DEPTH;  // tiles in flight while one is consumed
+constexpr int kNBuf = kDepth + 1;          // LDS tile buffers per workgroup
+constexpr int kWgsPerCu = kDepth == 3 ? 2 : 3;
+static_assert(kDepth == 2 || kDepth == 3, "pipeline depth 2 or 3");
+
+constexpr int kMaxItemTiles = 128;  // the planner keeps items at <= 128 tiles
+constexpr int kItemInts = 12;       // work-item record size (int32)
 
 template <int D>
 struct TileSmem {
   static constexpr int kElems = kSub * D;   // K (or V^T) elements per tile
   uint16_t kv[kNBuf][2 * kElems];
   uint32_t pbuf[kWaves][4][16];  // per wave: token pair x (8 hi, 8 lo) packed P words
+  int2 tile_meta[kMaxItemTiles];  // per tile of the item: (2 * block + half, valid tokens)
 };
 
 __device__ __forceinline__ int k_swz(int r) { return (r & 3) | ((r >> 1) & 4); }
@@ -98,7 +139,7 @@ __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
   constexpr int kPerWave = D / 64;  // 1 KiB slots per wave for each of K and V
   const int64_t blk = static_cast<int64_t>(g) * num_blocks + block;
   const char* kg = reinterpret_cast<const char*>(kpool + (blk * kTile + half * kSub) * D);
-  const char* vg = reinterpret_cast<const char*>(vpool + blk * kTile * D) + half * (kSub * 2);
+  const char* vg = reinterpret_cast<const char*>(vpool + (blk * kTile + half * kSub) * D);
   const uint32_t vd = dst + kSub * D * 2;
 #pragma unroll
   for (int j = 0; j < kPerWave; ++j) {
@@ -114,7 +155,7 @@ __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
     const int c = slot * 64 + lane;
     const int row = c >> 2;
     const int col = (c & 3) ^ v_swz(row);
-    dma16(vg + row * (kTile * 2) + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
+    dma16(vg + row * (kSub * 2) + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
   }
 }
 
@@ -126,23 +167,17 @@ __device__ __forceinline__ void barrier_tile_landed() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(N) : "memory");
 }
 
-// Waits for tile k (tiles up to k+2 may have been issued) and publishes it.
+// Waits for tile k (tiles up to k+kDepth may have been issued) and publishes it.
 template <int D>
 __device__ __forceinline__ void wait_tile(int k, int nt) {
   constexpr int kD = dma_per_tile<D>();
-  const int ahead = nt - 1 - k;
-  if (ahead >= 2)
-    barrier_tile_landed<2 * kD>();
-  else if (ahead == 1)
+  const int ahead = nt - 1 - k;  // tiles issued after tile k (capped at kDepth - 1)
+  if (kDepth == 3 && ahead >= 2)
+    barrier_tile_landed<(kDepth - 1) * kD>();
+  else if (ahead >= 1)
     barrier_tile_landed<kD>();
   else
     barrier_tile_landed<0>();
-}
-
-// Tile t of an item: (pool block, half) from the plan's tile record.
-__device__ __forceinline__ void tile_src(const int32_t* __restrict__ tiles, int t, int* block, int* half) {
-  *block = tiles[4 * t];
-  *half = tiles[4 * t + 2] & 1;
 }
 
 // Kernel arguments: the pointers are passed as separate __restrict__ kernel
@@ -160,30 +195,36 @@ struct Scalars {
       float *__restrict__ part_o, float *__restrict__ part_ml, Scalars sc
 #define TREEPO_PARTIAL_ARGS kpool, vpool, q, items, rowsets, tiles, part_o, part_ml, sc
 
-// Issues the first min(3, nt) tiles of an item.
+// Issues the first min(kDepth, nt) tiles of an item (their sources ride in the
+// item record, so this needs no further metadata load), then stages the
+// item's per-tile (source, valid) pairs into LDS for the loop; the loop reads
+// them from LDS instead of waiting on a scalar load every iteration.
 template <int D>
-__device__ __forceinline__ void dma_prologue(TREEPO_PARTIAL_PARAMS, int tb, int nt, int g, uint32_t buf0,
-                                             int wave, int lane) {
+__device__ __forceinline__ void item_prologue(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g, uint32_t buf0,
+                                              TileSmem<D>& sm, int wave, int lane) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
+  const int tb = it[3], te = it[4];
 #pragma unroll
-  for (int p = 0; p < 3; ++p) {
-    if (p < nt) {
-      int block, half;
-      tile_src(tiles, tb + p, &block, &half);
-      dma_tile<D>(kpool, vpool, sc.num_blocks, g, block, half, buf0 + p * kBufBytes, wave, lane);
-    }
+  for (int p = 0; p < kDepth; ++p) {
+    const int src = it[8 + p];
+    if (src >= 0)
+      dma_tile<D>(kpool, vpool, sc.num_blocks, g, src >> 1, src & 1, buf0 + p * kBufBytes, wave, lane);
+  }
+  for (int t = threadIdx.x; t < te - tb; t += kThreads) {
+    const int4 rec = reinterpret_cast<const int4*>(tiles)[tb + t];
+    sm.tile_meta[t] = make_int2(2 * rec.x + (rec.z & 1), rec.w);
   }
 }
 
-// After tile k is published: prefetch tile k+3 into the buffer tile k-1 used.
+// After tile k is published: prefetch tile k+kDepth into the buffer tile k-1
+// used (buffer index `nb`, i.e. (k + kDepth) mod kNBuf).
 template <int D>
-__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int tb, int nt, int k, int g, uint32_t buf0,
-                                          int wave, int lane) {
+__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int nt, int k, int nb, int g, uint32_t buf0,
+                                          const TileSmem<D>& sm, int wave, int lane) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
-  if (k + 3 < nt) {
-    int block, half;
-    tile_src(tiles, tb + k + 3, &block, &half);
-    dma_tile<D>(kpool, vpool, sc.num_blocks, g, block, half, buf0 + ((k + 3) & 3) * kBufBytes, wave, lane);
+  if (k + kDepth < nt) {
+    const int src = __builtin_amdgcn_readfirstlane(sm.tile_meta[k + kDepth].x);
+    dma_tile<D>(kpool, vpool, sc.num_blocks, g, src >> 1, src & 1, buf0 + nb * kBufBytes, wave, lane);
   }
 }
 
@@ -194,8 +235,9 @@ __device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int tb, int nt,
 // merged at the end.
 //   QK: lane (t = lane/8, j = lane%8) owns token 8w+t and the K chunks j, j+8
 //       of its row; q rows sit in registers in the same chunk order.  The
-//       partial dot products (v_dot2 bf16 -> fp32) are summed across the 8
-//       lanes with DPP (quad permutes, then a half-row mirror).
+//       partial dot products (v_dot2 bf16 -> fp32) of all rows are combined by
+//       a DPP reduce-scatter, after which lane j holds row j's score, so the
+//       softmax work is done once per (token, row).
 //   P : split into two bf16 terms, hi = bf16(p) and lo = bf16(p - hi), so the
 //       weights keep about 16 significant bits (a single bf16 P can be off by
 //       2^-8 relative, too much for short, peaked chains).  Token pairs are
@@ -217,7 +259,7 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   const int G = sc.group;
   const int nt = te - tb;
   const uint32_t buf0 = lds_addr(sm.kv[0]);
-  dma_prologue<D>(TREEPO_PARTIAL_ARGS, tb, nt, g, buf0, wave, lane);
+  item_prologue<D>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
 
   uint32_t qr[M][kKW];
 #pragma unroll
@@ -242,23 +284,24 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 #pragma unroll
     for (int w = 0; w < kKW; ++w) asm volatile("" ::"v"(qr[m][w]));
 
-  float m_run[M], l_run[M], acc[M][kDD];
+  // per lane: reference max and weight sum of row j (lanes with equal j agree
+  // on the reference; each sums the weights of its own token slot)
+  float m_ref = -INFINITY, l_sum = 0.f;
+  float acc[M][kDD];
 #pragma unroll
-  for (int m = 0; m < M; ++m) {
-    m_run[m] = -INFINITY;
-    l_run[m] = 0.f;
+  for (int m = 0; m < M; ++m)
 #pragma unroll
     for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = 0.f;
-  }
 
-  for (int k = 0; k < nt; ++k) {
-    const int valid = tiles[4 * (tb + k) + 3];
-    wait_tile<D>(k, nt);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, tb, nt, k, g, buf0, wave, lane);
-    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 3]);
+  for (int k = 0, cb = 0, nb = kDepth; k < nt; ++k, cb = cb == kNBuf - 1 ? 0 : cb + 1,
+                                             nb = nb == kNBuf - 1 ? 0 : nb + 1) {
+    wait_tile<D>(k, nt);  // also publishes the tile metadata staged in the prologue
+    const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
+    const char* kt = reinterpret_cast<const char*>(sm.kv[cb]);
     const char* vt = kt + kSub * D * 2;
 
-    // ---- scores
+    // ---- scores: lane j ends with row j's score of token 8w+t
     const int row = wave * 8 + t;
     uint32_t kr[kKW];
 #pragma unroll
@@ -270,60 +313,52 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
       kr[4 * i + 2] = v.z;
       kr[4 * i + 3] = v.w;
     }
-    float s[M];
+    float part[8];
 #pragma unroll
-    for (int m = 0; m < M; ++m) {
+    for (int m = 0; m < 8; ++m) {
       float x = 0.f;
+      if (m < M) {
 #pragma unroll
-      for (int w = 0; w < kKW; ++w) x = dot2(qr[m][w], kr[w], x);
-      x = quad_sum(x);
-      x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141, 0xF, 0xF, true));
-      s[m] = row < valid ? x * sc.scale_log2 : -INFINITY;
+        for (int w = 0; w < kKW; ++w) x = dot2(qr[m][w], kr[w], x);
+      }
+      part[m] = x;
     }
+    const float sc_j = reduce_scatter8(part, j);
+    const float s = (row < valid && j < M) ? sc_j * sc.scale_log2 : -INFINITY;
 
-    // ---- online softmax over this wave's 8 tokens.  m_run is a per-row
-    // reference, not necessarily the exact running max: the weights are
-    // 2^(s - m_run) and the result does not depend on the reference.  Only
-    // when a score exceeds it by more than 2^8 (always on the first tile) are
-    // the exact tile maxima reduced across the wave and the state rescaled.
-    bool over = false;
-#pragma unroll
-    for (int m = 0; m < M; ++m) over |= s[m] > m_run[m] + 8.f;
-    if (__builtin_amdgcn_ballot_w64(over) != 0) {
-#pragma unroll
-      for (int m = 0; m < M; ++m) {
-        float mx = s[m];
-        mx = fmaxf(mx, __shfl_xor(mx, 8));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mn = fmaxf(m_run[m], mx);
-        const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_run[m] - mn);
-        l_run[m] *= alpha;
-#pragma unroll
-        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] *= alpha;
-        m_run[m] = mn;
-      }
-    }
-    uint32_t pk[M], pkl[M];
-#pragma unroll
-    for (int m = 0; m < M; ++m) {
-      const float p = s[m] == -INFINITY ? 0.f : fast_exp2(s[m] - m_run[m]);
-      const uint32_t pb = f2bf_bits(p);
-      const uint32_t pl = f2bf_bits(p - bf_bits2f(pb));
-      l_run[m] += bf_bits2f(pb) + bf_bits2f(pl);
-      // token t-1 sits 8 lanes down in the same row of 16 lanes
-      const uint32_t both = pb | (pl << 16);
-      const uint32_t prev = static_cast<uint32_t>(
-          __builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x118, 0xF, 0xF, false));
-      pk[m] = (prev & 0xFFFFu) | (both << 16);
-      pkl[m] = (prev >> 16) | (both & 0xFFFF0000u);
-    }
-    if ((t & 1) == 1 && j == 0) {
+    // ---- online softmax.  m_ref is a per-row reference, not necessarily the
+    // exact running max: the weights are 2^(s - m_ref) and the result does not
+    // depend on the reference.  Only when a score exceeds it by more than 2^8
+    // (always on the first tile) are the exact tile maxima reduced across the
+    // wave and the state rescaled.
+    if (__builtin_amdgcn_ballot_w64(s > m_ref + 8.f) != 0) {
+      float mx = s;
+      mx = fmaxf(mx, __shfl_xor(mx, 8));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m_ref, mx);
+      const float alpha = mn == -INFINITY ? 1.f : fast_exp2(m_ref - mn);
+      m_ref = mn;
+      l_sum *= alpha;
 #pragma unroll
       for (int m = 0; m < M; ++m) {
-        sm.pbuf[wave][t >> 1][m] = pk[m];
-        sm.pbuf[wave][t >> 1][8 + m] = pkl[m];
+        // row m's factor from lane m (token slot 0, j = m)
+        const float am = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), m));
+#pragma unroll
+        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] *= am;
       }
+    }
+    const float p = s == -INFINITY ? 0.f : fast_exp2(s - m_ref);
+    const uint32_t pb = f2bf_bits(p);
+    const uint32_t pl = f2bf_bits(p - bf_bits2f(pb));
+    l_sum += bf_bits2f(pb) + bf_bits2f(pl);
+    // token t-1 sits 8 lanes down in the same row of 16 lanes
+    const uint32_t both = pb | (pl << 16);
+    const uint32_t prev = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(both), 0x118, 0xF, 0xF, false));
+    if ((t & 1) == 1 && j < M) {
+      sm.pbuf[wave][t >> 1][j] = (prev & 0xFFFFu) | (both << 16);
+      sm.pbuf[wave][t >> 1][8 + j] = (prev >> 16) | (both & 0xFFFF0000u);
     }
 
     // ---- P V
@@ -355,36 +390,29 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
       const uint4 p2 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][8]);
       const uint4 p3 = *reinterpret_cast<const uint4*>(&sm.pbuf[wave][tp][12]);
       const uint32_t pw[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-      const uint32_t pl[8] = {p2.x, p2.y, p2.z, p2.w, p3.x, p3.y, p3.z, p3.w};
+      const uint32_t pwl[8] = {p2.x, p2.y, p2.z, p2.w, p3.x, p3.y, p3.z, p3.w};
 #pragma unroll
       for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = dot2(pl[m], vw[dd][tp], dot2(pw[m], vw[dd][tp], acc[m][dd]));
+        for (int dd = 0; dd < kDD; ++dd) acc[m][dd] = dot2(pwl[m], vw[dd][tp], dot2(pw[m], vw[dd][tp], acc[m][dd]));
     }
   }
   __syncthreads();
 
   // ---- merge the four waves' states and write the partial rows
-#pragma unroll
-  for (int m = 0; m < M; ++m) {
-    float l = l_run[m];
-    l += __shfl_xor(l, 8);
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    l_run[m] = l;
-  }
+  float l = l_sum;
+  l += __shfl_xor(l, 8);
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
   float* oacc = reinterpret_cast<float*>(sm.kv);  // [waves][M][D]
   float* mlb = oacc + kWaves * M * D;             // [waves][M][2]
 #pragma unroll
   for (int m = 0; m < M; ++m)
 #pragma unroll
     for (int dd = 0; dd < kDD; ++dd) oacc[(wave * M + m) * D + lane + 64 * dd] = acc[m][dd];
-  if (lane == 0) {
-#pragma unroll
-    for (int m = 0; m < M; ++m) {
-      mlb[(wave * M + m) * 2 + 0] = m_run[m];
-      mlb[(wave * M + m) * 2 + 1] = l_run[m];
-    }
+  if (t == 0 && j < M) {
+    mlb[(wave * M + j) * 2 + 0] = m_ref;
+    mlb[(wave * M + j) * 2 + 1] = l;
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < M * D; idx += kThreads) {
@@ -393,21 +421,21 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
     float mstar = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) mstar = fmaxf(mstar, mlb[(w * M + m) * 2]);
-    float o = 0.f, l = 0.f;
+    float o = 0.f, lt = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       const float mw = mlb[(w * M + m) * 2];
       if (mw != -INFINITY) {
         const float f = fast_exp2(mw - mstar);
         o += f * oacc[(w * M + m) * D + d];
-        l += f * mlb[(w * M + m) * 2 + 1];
+        lt += f * mlb[(w * M + m) * 2 + 1];
       }
     }
     const int64_t slot = static_cast<int64_t>(pbase) + static_cast<int64_t>(g) * rows + m;
     part_o[slot * D + d] = o;
     if (d == 0) {
       part_ml[slot * 2 + 0] = mstar;
-      part_ml[slot * 2 + 1] = l;
+      part_ml[slot * 2 + 1] = lt;
     }
   }
 }
@@ -452,7 +480,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   const int G = sc.group;
   const int nt = te - tb;
   const uint32_t buf0 = lds_addr(sm.kv[0]);
-  dma_prologue<D>(TREEPO_PARTIAL_ARGS, tb, nt, g, buf0, wave, lane);
+  item_prologue<D>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
 
   // Q^T operands: lane holds row m = 16 rb + r16, d chunk 4 ks + a
   uint4 qb[NRB][kKS];
@@ -487,11 +515,12 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
     for (int db = 0; db < kDB; ++db) acc[i][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int k = 0; k < nt; ++k) {
-    const int valid = tiles[4 * (tb + k) + 3];
+  for (int k = 0, cb = 0, nb = kDepth; k < nt; ++k, cb = cb == kNBuf - 1 ? 0 : cb + 1,
+                                             nb = nb == kNBuf - 1 ? 0 : nb + 1) {
     wait_tile<D>(k, nt);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, tb, nt, k, g, buf0, wave, lane);
-    const char* kt = reinterpret_cast<const char*>(sm.kv[k & 3]);
+    const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
+    const char* kt = reinterpret_cast<const char*>(sm.kv[cb]);
     const char* vt = kt + kSub * D * 2;
     if (my_rb > 0) {
       // ---- S^T = K Q^T for the wave's row blocks
@@ -600,13 +629,13 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
 //
 // One launch covers every work item of a decode step; each workgroup runs one
 // (item, KV head) on the VALU or the MFMA path according to the item's kind.
-// Two workgroups fit per CU (<= 256 registers per lane, 65 KB of LDS each).
+// kWgsPerCu workgroups fit per CU (register budget 256 / kWgsPerCu per lane).
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void partial_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
+__global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
   __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;
   const int item = first_item + static_cast<int>(blockIdx.x) / sc.hkv;
   const int g = static_cast<int>(blockIdx.x) % sc.hkv;
-  const int32_t* it = items + 8 * item;
+  const int32_t* it = items + kItemInts * item;
   if (it[0] == 0) {
     switch (it[6]) {
       case 1: valu_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
@@ -698,7 +727,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
 //
 // One workgroup per (piece, KV head).  K rows are copied with 16-byte moves;
 // V rows are transposed through LDS (padded rows, no bank conflicts) and
-// written as runs of consecutive tokens of each d-row of the transposed block.
+// written as runs of consecutive tokens of each d-row of the transposed half
+// blocks.
 constexpr int kMaxPieces = 128;
 struct AppendBatch {
   int32_t n;
@@ -735,11 +765,14 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
   __syncthreads();
   for (int idx = threadIdx.x; idx < D * pc.count; idx += kThreads) {
     const int d = idx / pc.count, i = idx % pc.count;
-    vpool[(blk * D + d) * kTile + pc.off + i] = vt[i * kPad + d];
+    const int p = pc.off + i;  // token within the 64-token block
+    vpool[(blk * kTile + (p / kSub) * kSub) * D + d * kSub + (p % kSub)] = vt[i * kPad + d];
   }
 }
 
 }  // namespace
+
+int32_t partial_workgroups_per_cu() { return kWgsPerCu; }
 
 hipError_t launch_partial(const DecodeArgs& a, int32_t first_item, int32_t n_items, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;

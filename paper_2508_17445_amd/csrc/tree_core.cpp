@@ -300,6 +300,11 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         it.tile_end = r.tile_begin + static_cast<int32_t>(static_cast<int64_t>(nt) * (c + 1) / nchunks);
         it.partial_base = 0;
         it.run = ri;
+        for (int32_t f = 0; f < 3; ++f) {
+          const int32_t ti = it.tile_begin + f;
+          it.first_src[f] = ti < it.tile_end ? 2 * out->tiles[ti].block + (out->tiles[ti].tile_in_node & 1) : -1;
+        }
+        it.pad = 0;
         r.group_items[gi].push_back(static_cast<int32_t>(tmp.size()));
         tmp.push_back(it);
       }

@@ -95,7 +95,10 @@ struct Item {
   int32_t partial_base;  // partial row of (g=0, row 0); (g, r) -> base + g*rows + r
   int32_t rows;          // n_leaves * G
   int32_t run;
+  int32_t first_src[3];  // half-block index (2 * block + half) of the first tiles, -1 past the end
+  int32_t pad;
 };
+constexpr int32_t kItemInts = 12;
 
 // A KV tile: up to kPlanTileTokens tokens of one node, tokens
 // [32 k, 32 k + 32) of the node for tile_in_node = k, inside pool block

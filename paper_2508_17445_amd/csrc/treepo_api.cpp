@@ -327,7 +327,7 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   ctx->params.num_kv_heads = c.num_kv_heads;
   ctx->params.valu_max_rows = 8;
   ctx->params.mfma_max_rows = 128;
-  ctx->params.concurrent_wgs = 512;
+  ctx->params.concurrent_wgs = treepo::kComputeUnits * treepo::partial_workgroups_per_cu();
   ctx->params.max_chunk_tiles = 128;
   ctx->params.mfma_enabled = 1;
   *out = ctx;

@@ -24,6 +24,7 @@ MODE_TREE, MODE_NAIVE = 0, 1
 KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE = 0, 1, 2
 NODE_FIELDS = ("parent", "depth", "start", "len", "cap", "block_begin", "n_blocks", "tree_id")
 BLOCK_TOKENS = 64
+ITEM_FIELDS = 12
 
 _i32 = ctypes.c_int32
 _i64 = ctypes.c_int64
@@ -244,7 +245,7 @@ class Context:
         z = ctypes.POINTER(ctypes.c_int32)()
         self._check(self.lib.treepo_export_plan(self.h, len(lv), _ptr32(lv), mode, z, z, z, ctypes.byref(ni),
                                                 ctypes.byref(nr), ctypes.byref(nt)), "treepo_export_plan")
-        items = np.zeros((max(ni.value, 1), 8), np.int32)
+        items = np.zeros((max(ni.value, 1), ITEM_FIELDS), np.int32)
         rowsets = np.zeros(max(nr.value, 1), np.int32)
         tiles = np.zeros((max(nt.value, 1), 4), np.int32)
         self._check(self.lib.treepo_export_plan(self.h, len(lv), _ptr32(lv), mode, _ptr32(items), _ptr32(rowsets),

@@ -64,8 +64,11 @@ def _plan_checks(ctx, model, leaves, mode):
     G = ctx.cfg.num_q_heads // ctx.cfg.num_kv_heads
     covered = {x: [] for x in range(len(leaves))}
     for it in items:
-        kind, rb, nl, tb, te, pbase, rows, run = it
+        kind, rb, nl, tb, te, pbase, rows, run = it[:8]
         assert rows == nl * G and te > tb and nl >= 1
+        for f in range(3):   # the first tiles' half-block sources ride in the record
+            want_src = 2 * tiles[tb + f][0] + (tiles[tb + f][2] & 1) if tb + f < te else -1
+            assert it[8 + f] == want_src
         for pos in rowsets[rb:rb + nl]:
             for t in tiles[tb:te]:
                 covered[pos].append(tuple(t))
