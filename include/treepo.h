@@ -204,6 +204,19 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
                            int32_t mode, int32_t* items, int32_t* rowsets, int32_t* tiles,
                            int32_t* n_items, int32_t* n_rowsets, int32_t* n_tiles);
 
+/* ---- schedule options --------------------------------------------------- */
+
+/* Work items whose stacked query rows (descendant leaves x GQA group) number at
+ * most this value run the wavefront-shuffle (VALU) partial; the others run on
+ * MFMA.  Range 0..8; 0 (the default) puts every item on MFMA. */
+#define TREEPO_OPT_VALU_MAX_ROWS 0
+
+/* Sets a schedule option; cached plans are dropped and rebuilt on the next
+ * decode (results agree to rounding; the schedule changes).  EINVAL for an
+ * unknown option or a value out of range. */
+int32_t treepo_set_option(treepo_ctx* ctx, int32_t option, int32_t value);
+int32_t treepo_get_option(treepo_ctx* ctx, int32_t option, int32_t* value);
+
 /* ---- kernel timing ------------------------------------------------------ */
 
 /* Kernel kinds for treepo_profile_read. */

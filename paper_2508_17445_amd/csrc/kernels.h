@@ -27,6 +27,7 @@ struct DecodeArgs {
   int32_t n_leaves;
   float* out;              // fp32 [n_leaves][Hq][D]
   float* lse;              // fp32 [n_leaves][Hq] or null
+  bool nontemporal;        // KV tiles are read once per call: stream them past the caches
 };
 
 // Node partials of items [first_item, first_item + n_items), VALU or MFMA by kind.

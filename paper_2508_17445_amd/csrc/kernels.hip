@@ -117,9 +117,16 @@ __device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
 // not treat the in-flight LDS writes as aliasing every later LDS access (which
 // would drain the prefetch); completion is tracked by hand with vmcnt waits
 // before the barrier that publishes a tile.
+// NT marks the load non-temporal: the line is not kept in the caches, which
+// raises the streaming rate when every byte is read once per step.
+template <bool NT>
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(g), "s"(lds) : "memory", "m0");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
+                 :: "v"(g), "s"(lds) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "s"(lds) : "memory", "m0");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
@@ -131,7 +138,7 @@ template <int D>
 constexpr int dma_per_tile() { return D / 32; }
 
 // Stages tile (block, half) of KV head g into the LDS buffer at byte address `dst`.
-template <int D>
+template <int D, bool NT>
 __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
                                          const uint16_t* __restrict__ vpool, int64_t num_blocks,
                                          int g, int block, int half, uint32_t dst, int wave, int lane) {
@@ -147,7 +154,7 @@ __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
     const int c = slot * 64 + lane;
     const int row = c / kKChunks;
     const int col = (c % kKChunks) ^ k_swz(row);
-    dma16(kg + row * (D * 2) + col * 16, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
+    dma16<NT>(kg + row * (D * 2) + col * 16, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
   }
 #pragma unroll
   for (int j = 0; j < kPerWave; ++j) {
@@ -155,7 +162,7 @@ __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool,
     const int c = slot * 64 + lane;
     const int row = c >> 2;
     const int col = (c & 3) ^ v_swz(row);
-    dma16(vg + row * (kSub * 2) + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
+    dma16<NT>(vg + row * (kSub * 2) + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
   }
 }
 
@@ -199,7 +206,7 @@ struct Scalars {
 // item record, so this needs no further metadata load), then stages the
 // item's per-tile (source, valid) pairs into LDS for the loop; the loop reads
 // them from LDS instead of waiting on a scalar load every iteration.
-template <int D>
+template <int D, bool NT>
 __device__ __forceinline__ void item_prologue(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g, uint32_t buf0,
                                               TileSmem<D>& sm, int wave, int lane) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
@@ -208,7 +215,7 @@ __device__ __forceinline__ void item_prologue(TREEPO_PARTIAL_PARAMS, const int32
   for (int p = 0; p < kDepth; ++p) {
     const int src = it[8 + p];
     if (src >= 0)
-      dma_tile<D>(kpool, vpool, sc.num_blocks, g, src >> 1, src & 1, buf0 + p * kBufBytes, wave, lane);
+      dma_tile<D, NT>(kpool, vpool, sc.num_blocks, g, src >> 1, src & 1, buf0 + p * kBufBytes, wave, lane);
   }
   for (int t = threadIdx.x; t < te - tb; t += kThreads) {
     const int4 rec = reinterpret_cast<const int4*>(tiles)[tb + t];
@@ -218,13 +225,13 @@ __device__ __forceinline__ void item_prologue(TREEPO_PARTIAL_PARAMS, const int32
 
 // After tile k is published: prefetch tile k+kDepth into the buffer tile k-1
 // used (buffer index `nb`, i.e. (k + kDepth) mod kNBuf).
-template <int D>
+template <int D, bool NT>
 __device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int nt, int k, int nb, int g, uint32_t buf0,
                                           const TileSmem<D>& sm, int wave, int lane) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
   if (k + kDepth < nt) {
     const int src = __builtin_amdgcn_readfirstlane(sm.tile_meta[k + kDepth].x);
-    dma_tile<D>(kpool, vpool, sc.num_blocks, g, src >> 1, src & 1, buf0 + nb * kBufBytes, wave, lane);
+    dma_tile<D, NT>(kpool, vpool, sc.num_blocks, g, src >> 1, src & 1, buf0 + nb * kBufBytes, wave, lane);
   }
 }
 
@@ -245,7 +252,7 @@ __device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int nt, int k, 
 //   PV: lane i owns d = i (+64); V^T words hold two consecutive tokens of one
 //       d, matching the packed P pairs, so each v_dot2 does two tokens (one
 //       v_dot2 for hi and one for lo).
-template <int D, int M>
+template <int D, int M, bool NT>
 __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g,
                                           TileSmem<D>& sm) {
   constexpr int kKC = D / 64;  // K chunks per lane in QK
@@ -259,7 +266,7 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   const int G = sc.group;
   const int nt = te - tb;
   const uint32_t buf0 = lds_addr(sm.kv[0]);
-  item_prologue<D>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
+  item_prologue<D, NT>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
 
   uint32_t qr[M][kKW];
 #pragma unroll
@@ -297,7 +304,7 @@ __device__ __forceinline__ void valu_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
                                              nb = nb == kNBuf - 1 ? 0 : nb + 1) {
     wait_tile<D>(k, nt);  // also publishes the tile metadata staged in the prologue
     const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
+    dma_ahead<D, NT>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
     const char* kt = reinterpret_cast<const char*>(sm.kv[cb]);
     const char* vt = kt + kSub * D * 2;
 
@@ -468,7 +475,7 @@ __device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c)
 
 __device__ __forceinline__ int tau(int b, int r) { return 8 * (r >> 2) + 4 * b + (r & 3); }
 
-template <int D, int NRB>
+template <int D, int NRB, bool NT>
 __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g, TileSmem<D>& sm) {
   constexpr int kKS = D / 32;  // QK k-steps
   constexpr int kDB = D / 16;  // PV output d-blocks
@@ -480,7 +487,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   const int G = sc.group;
   const int nt = te - tb;
   const uint32_t buf0 = lds_addr(sm.kv[0]);
-  item_prologue<D>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
+  item_prologue<D, NT>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
 
   // Q^T operands: lane holds row m = 16 rb + r16, d chunk 4 ks + a
   uint4 qb[NRB][kKS];
@@ -519,7 +526,7 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
                                              nb = nb == kNBuf - 1 ? 0 : nb + 1) {
     wait_tile<D>(k, nt);
     const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
+    dma_ahead<D, NT>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
     const char* kt = reinterpret_cast<const char*>(sm.kv[cb]);
     const char* vt = kt + kSub * D * 2;
     if (my_rb > 0) {
@@ -625,12 +632,176 @@ __device__ __forceinline__ void mfma_item(TREEPO_PARTIAL_PARAMS, const int32_t* 
   }
 }
 
+// ---- MFMA node-partial, token split ----------------------------------------------
+//
+// Items of at most 32 rows (one or two 16-row blocks: one leaf's GQA group, or
+// a few leaves of a shared node).  Splitting rows over waves would leave most
+// waves idle, so the tile is split by tokens instead: wave w takes row block
+// w/2 and token block b = w%2 of every tile -- the 16 tokens tau(b, 0..15) --
+// and keeps its own online-softmax state; the two waves of a row block merge
+// at the end.
+//   QK: as in mfma_item, for the wave's token block only (four MFMAs per row
+//       block); each lane's four scores are the consecutive tokens
+//       8(lane/16) + 4b + 0..3.
+//   PV: O^T += V^T P^T with v_mfma_f32_16x16x16_bf16: the B operand (four
+//       tokens x row) is exactly the lane's four scores, the A operand four
+//       consecutive tokens of one V^T row (8 bytes).
+//   Max: lazy reference per row: the running sum and O are rescaled only when a
+//       score exceeds the reference by more than 2^8, so in steady state a tile
+//       costs no cross-lane max and no rescale.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16k16(const uint2& a, const uint2& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a), __builtin_bit_cast(s16x4, b), c,
+                                                   0, 0, 0);
+}
+
+constexpr float kLazyMaxSlack = 8.f;  // log2 units: weights stay <= 2^8 before a rescale
+
+template <int D, bool NT>
+__device__ __forceinline__ void mfma_split_item(TREEPO_PARTIAL_PARAMS, const int32_t* it, int g, TileSmem<D>& sm) {
+  constexpr int kKS = D / 32;  // QK k-steps
+  constexpr int kDB = D / 16;  // PV output d-blocks
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int a = lane >> 4;    // lane group
+  const int r16 = lane & 15;  // row within the 16-row block
+  const int rb = wave >> 1;   // row block
+  const int tb = wave & 1;    // token block
+  const int rowset = it[1], tbeg = it[3], tend = it[4], pbase = it[5], rows = it[6];
+  const int G = sc.group;
+  const int nt = tend - tbeg;
+  const uint32_t buf0 = lds_addr(sm.kv[0]);
+  item_prologue<D, NT>(TREEPO_PARTIAL_ARGS, it, g, buf0, sm, wave, lane);
+
+  const bool active = 16 * rb < rows;  // wave-uniform
+  const int m = 16 * rb + r16;         // this lane's query row
+  uint4 qb[kKS];
+#pragma unroll
+  for (int ks = 0; ks < kKS; ++ks) qb[ks] = make_uint4(0, 0, 0, 0);
+  if (m < rows) {
+    const int leaf = rowsets[rowset + m / G];
+    const int head = g * G + m % G;
+    const uint4* qp = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(leaf) * sc.hq + head) * D);
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) qb[ks] = qp[4 * ks + a];
+  }
+#pragma unroll
+  for (int ks = 0; ks < kKS; ++ks) asm volatile("" ::"v"(qb[ks].x), "v"(qb[ks].y), "v"(qb[ks].z), "v"(qb[ks].w));
+
+  f32x4 acc[kDB];
+#pragma unroll
+  for (int db = 0; db < kDB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_ref = -INFINITY;  // per row (equal on the row's four lane groups)
+  float l_sum = 0.f;        // per lane: this lane's tokens only
+  const int tok0 = 8 * a + 4 * tb;  // first of the lane's four tokens
+
+  for (int k = 0, cb = 0, nb = kDepth; k < nt; ++k, cb = cb == kNBuf - 1 ? 0 : cb + 1,
+                                             nb = nb == kNBuf - 1 ? 0 : nb + 1) {
+    wait_tile<D>(k, nt);
+    const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
+    dma_ahead<D, NT>(TREEPO_PARTIAL_ARGS, nt, k, nb, g, buf0, sm, wave, lane);
+    if (!active) continue;
+    const char* kt = reinterpret_cast<const char*>(sm.kv[cb]);
+    const char* vt = kt + kSub * D * 2;
+    // ---- S^T = K Q^T for the wave's 16 tokens
+    f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
+    {
+      const int tok = tau(tb, r16);
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) {
+        const int c = 4 * ks + a;
+        const uint4 ka = *reinterpret_cast<const uint4*>(kt + tok * (D * 2) + ((c ^ k_swz(tok)) << 4));
+        S = mfma16(ka, qb[ks], S);
+      }
+    }
+    // ---- scores (log2 units), masked past the node's length
+    float x[4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = tok0 + e < valid ? S[e] * sc.scale_log2 : -INFINITY;
+      mx = fmaxf(mx, x[e]);
+    }
+    if (__builtin_amdgcn_ballot_w64(mx > m_ref + kLazyMaxSlack) != 0) {
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m_ref, mx);
+      const float alpha = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - mn);
+      m_ref = mn;
+      l_sum *= alpha;
+#pragma unroll
+      for (int db = 0; db < kDB; ++db) acc[db] *= alpha;
+    }
+    // ---- P = 2^(x - m_ref) as hi + lo bf16 terms
+    uint32_t ph[2], pl[2];
+#pragma unroll
+    for (int e = 0; e < 4; e += 2) {
+      const float f0 = x[e] == -INFINITY ? 0.f : fast_exp2(x[e] - m_ref);
+      const float f1 = x[e + 1] == -INFINITY ? 0.f : fast_exp2(x[e + 1] - m_ref);
+      const uint32_t h0 = f2bf_bits(f0), h1 = f2bf_bits(f1);
+      const uint32_t q0 = f2bf_bits(f0 - bf_bits2f(h0)), q1 = f2bf_bits(f1 - bf_bits2f(h1));
+      l_sum += (bf_bits2f(h0) + bf_bits2f(q0)) + (bf_bits2f(h1) + bf_bits2f(q1));
+      ph[e >> 1] = h0 | (h1 << 16);
+      pl[e >> 1] = q0 | (q1 << 16);
+    }
+    const uint2 P = make_uint2(ph[0], ph[1]), PL = make_uint2(pl[0], pl[1]);
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+      const int d = 16 * db + r16;
+      uint2 va = *reinterpret_cast<const uint2*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4) + tb * 8);
+      if (valid < kSub) {
+        // clear the V entries of tokens past the node's length (P is 0 there)
+        va.x &= tok0 >= valid ? 0u : (tok0 + 1 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
+        va.y &= tok0 + 2 >= valid ? 0u : (tok0 + 3 >= valid ? 0xFFFFu : 0xFFFFFFFFu);
+      }
+      acc[db] = mfma16k16(va, PL, mfma16k16(va, P, acc[db]));
+    }
+  }
+
+  // ---- merge the two token blocks of each row block, write the partial rows
+  l_sum += __shfl_xor(l_sum, 16);
+  l_sum += __shfl_xor(l_sum, 32);
+  float* xs = reinterpret_cast<float*>(sm.kv[0]);  // [row block][2 + 4 kDB][64] floats
+  constexpr int kFields = 2 + 4 * kDB;
+  float* mine = xs + (rb * kFields) * 64 + lane;
+  barrier_tile_landed<0>();  // every wave is done with the tile buffers
+  if (active && tb == 1) {
+    mine[0] = m_ref;
+    mine[64] = l_sum;
+#pragma unroll
+    for (int db = 0; db < kDB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mine[(2 + 4 * db + i) * 64] = acc[db][i];
+  }
+  barrier_tile_landed<0>();
+  if (active && tb == 0 && m < rows) {
+    const float m1 = mine[0], l1 = mine[64];
+    const float mn = fmaxf(m_ref, m1);
+    const float a0 = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - mn);
+    const float a1 = m1 == -INFINITY ? 0.f : fast_exp2(m1 - mn);
+    const int64_t slot = static_cast<int64_t>(pbase) + static_cast<int64_t>(g) * rows + m;
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+      f32x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = a0 * acc[db][i] + a1 * mine[(2 + 4 * db + i) * 64];
+      *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * db + 4 * a) = o;
+    }
+    if (a == 0) {
+      part_ml[slot * 2 + 0] = mn;
+      part_ml[slot * 2 + 1] = a0 * l_sum + a1 * l1;
+    }
+  }
+}
+
 // ---- the node-partial kernel ----------------------------------------------------
 //
 // One launch covers every work item of a decode step; each workgroup runs one
 // (item, KV head) on the VALU or the MFMA path according to the item's kind.
 // kWgsPerCu workgroups fit per CU (register budget 256 / kWgsPerCu per lane).
-template <int D>
+template <int D, bool NT>
 __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(TREEPO_PARTIAL_PARAMS, int32_t first_item) {
   __shared__ __attribute__((aligned(1024))) TileSmem<D> sm;
   const int item = first_item + static_cast<int>(blockIdx.x) / sc.hkv;
@@ -638,22 +809,24 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(TREEPO_PAR
   const int32_t* it = items + kItemInts * item;
   if (it[0] == 0) {
     switch (it[6]) {
-      case 1: valu_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 2: valu_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 3: valu_item<D, 3>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 4: valu_item<D, 4>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 5: valu_item<D, 5>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 6: valu_item<D, 6>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 7: valu_item<D, 7>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
-      case 8: valu_item<D, 8>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 1: valu_item<D, 1, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 2: valu_item<D, 2, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 3: valu_item<D, 3, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 4: valu_item<D, 4, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 5: valu_item<D, 5, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 6: valu_item<D, 6, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 7: valu_item<D, 7, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
+      case 8: valu_item<D, 8, NT>(TREEPO_PARTIAL_ARGS, it, g, sm); break;
       default: break;
     }
+  } else if (it[6] <= 32) {
+    mfma_split_item<D, NT>(TREEPO_PARTIAL_ARGS, it, g, sm);
   } else {
     const int nrb = (((it[6] + 15) >> 4) + 3) >> 2;
     if (nrb == 1)
-      mfma_item<D, 1>(TREEPO_PARTIAL_ARGS, it, g, sm);
+      mfma_item<D, 1, NT>(TREEPO_PARTIAL_ARGS, it, g, sm);
     else if (nrb == 2)
-      mfma_item<D, 2>(TREEPO_PARTIAL_ARGS, it, g, sm);
+      mfma_item<D, 2, NT>(TREEPO_PARTIAL_ARGS, it, g, sm);
     // the planner keeps MFMA items at <= 128 rows
   }
 }
@@ -778,12 +951,14 @@ hipError_t launch_partial(const DecodeArgs& a, int32_t first_item, int32_t n_ite
   if (n_items <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(n_items) * a.hkv);
   const Scalars sc{a.num_blocks, a.hq, a.hkv, a.group, a.scale_log2};
+  auto go = [&](auto kernel) {
+    kernel<<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles, a.part_o, a.part_ml, sc,
+                                     first_item);
+  };
   if (a.d == 128)
-    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
-                                                  a.part_o, a.part_ml, sc, first_item);
+    a.nontemporal ? go(partial_kernel<128, true>) : go(partial_kernel<128, false>);
   else
-    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.items, a.rowsets, a.tiles,
-                                                 a.part_o, a.part_ml, sc, first_item);
+    a.nontemporal ? go(partial_kernel<64, true>) : go(partial_kernel<64, false>);
   return hipGetLastError();
 }
 

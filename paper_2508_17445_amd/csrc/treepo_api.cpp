@@ -270,6 +270,9 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;
+  // The cascade schedule reads each KV tile once per call; the per-leaf
+  // baseline re-reads shared prefixes and keeps them cacheable.
+  a.nontemporal = p.mode == treepo::kModeTree;
   hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL, stream, [&] {
     return treepo::launch_partial(a, 0, static_cast<int32_t>(p.items.size()), stream);
   });
@@ -325,7 +328,7 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   if (!ctx) return TREEPO_ENOMEM;
   ctx->params.group = c.num_q_heads / c.num_kv_heads;
   ctx->params.num_kv_heads = c.num_kv_heads;
-  ctx->params.valu_max_rows = 8;
+  ctx->params.valu_max_rows = 0;
   ctx->params.mfma_max_rows = 128;
   ctx->params.concurrent_wgs = treepo::kComputeUnits * treepo::partial_workgroups_per_cu();
   ctx->params.max_chunk_tiles = 128;
@@ -540,6 +543,29 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
     std::memcpy(tiles, p.tiles.data(), p.tiles.size() * sizeof(treepo::Tile));
   }
   return TREEPO_OK;
+}
+
+int32_t treepo_set_option(treepo_ctx* ctx, int32_t option, int32_t value) {
+  if (!ctx) return TREEPO_EINVAL;
+  switch (option) {
+    case TREEPO_OPT_VALU_MAX_ROWS:
+      if (value < 0 || value > 8) return fail(ctx, TREEPO_EINVAL, "VALU row limit must be in 0..8");
+      if (ctx->params.valu_max_rows != value) {
+        ctx->params.valu_max_rows = value;
+        ctx->plans.clear();
+      }
+      return TREEPO_OK;
+    default:
+      return fail(ctx, TREEPO_EINVAL, "unknown option");
+  }
+}
+
+int32_t treepo_get_option(treepo_ctx* ctx, int32_t option, int32_t* value) {
+  if (!ctx || !value) return TREEPO_EINVAL;
+  switch (option) {
+    case TREEPO_OPT_VALU_MAX_ROWS: *value = ctx->params.valu_max_rows; return TREEPO_OK;
+    default: return fail(ctx, TREEPO_EINVAL, "unknown option");
+  }
 }
 
 int32_t treepo_set_profiling(treepo_ctx* ctx, int32_t enable) {

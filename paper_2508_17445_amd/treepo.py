@@ -22,6 +22,7 @@ LIB_PATH = os.environ.get("TREEPO_LIBRARY") or os.path.join(HERE, "libtreepo.so"
 OK, EINVAL, ENOMEM, EFULL, EFROZEN, EEMPTY, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 MODE_TREE, MODE_NAIVE = 0, 1
 KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE = 0, 1, 2
+OPT_VALU_MAX_ROWS = 0
 NODE_FIELDS = ("parent", "depth", "start", "len", "cap", "block_begin", "n_blocks", "tree_id")
 BLOCK_TOKENS = 64
 ITEM_FIELDS = 12
@@ -72,6 +73,8 @@ def load_library(path: str = LIB_PATH):
         "treepo_export_chains": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
         "treepo_export_desc": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
         "treepo_export_plan": (_i32, [_p, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
+        "treepo_set_option": (_i32, [_p, _i32, _i32]),
+        "treepo_get_option": (_i32, [_p, _i32, _pi32]),
         "treepo_set_profiling": (_i32, [_p, _i32]),
         "treepo_profile_read": (_i32, [_p, _i32, ctypes.POINTER(ctypes.c_double), _pi64]),
         "treepo_strerror": (ctypes.c_char_p, [_i32]),
@@ -252,6 +255,15 @@ class Context:
                                                 _ptr32(tiles), ctypes.byref(ni), ctypes.byref(nr), ctypes.byref(nt)),
                     "treepo_export_plan")
         return items[:ni.value], rowsets[:nr.value], tiles[:nt.value]
+
+    # ---- schedule options ----------------------------------------------------
+    def set_option(self, option: int, value: int):
+        self._check(self.lib.treepo_set_option(self.h, option, value), "treepo_set_option")
+
+    def get_option(self, option: int) -> int:
+        v = _i32()
+        self._check(self.lib.treepo_get_option(self.h, option, ctypes.byref(v)), "treepo_get_option")
+        return v.value
 
     # ---- timing ------------------------------------------------------------
     def set_profiling(self, enable: bool):

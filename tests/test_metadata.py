@@ -115,3 +115,33 @@ def test_duplicate_and_interior_leaves():
     model = oracle_model(log)
     _compare(ctx, model, leaves)
     _plan_checks(ctx, model, leaves, 0)
+
+
+def test_schedule_option_sets_item_kinds():
+    """VALU_MAX_ROWS moves items between the shuffle and MFMA partials; the
+    plan's coverage is unchanged and out-of-range values are rejected."""
+    from paper_2508_17445_amd import OPT_VALU_MAX_ROWS, TreePOError
+    from workloads import CONFIGS
+    log = build_call_log(2)
+    c = CONFIGS[2]
+    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    replay_host(ctx, log)
+    model = oracle_model(log)
+    kinds = {}
+    for v in (0, 8):
+        ctx.set_option(OPT_VALU_MAX_ROWS, v)
+        assert ctx.get_option(OPT_VALU_MAX_ROWS) == v
+        items, _ = _plan_checks(ctx, model, log.leaves, 0)
+        kinds[v] = items[:, 0]
+        if v == 0:
+            assert (items[:, 0] == 1).all()
+        else:
+            # VALU items are exactly those of at most 8 rows, and come first
+            assert ((items[:, 0] == 0) == (items[:, 6] <= 8)).all()
+            assert (np.diff(items[:, 0]) >= 0).all()
+    assert (kinds[8] == 0).any()
+    for bad in (-1, 9):
+        with pytest.raises(TreePOError):
+            ctx.set_option(OPT_VALU_MAX_ROWS, bad)
+    with pytest.raises(TreePOError):
+        ctx.set_option(12345, 0)
