@@ -62,8 +62,9 @@ typedef struct treepo_ctx treepo_ctx;
  * of 32 tokens is stored transposed, so element (g, r, d) is at
  * (g*num_blocks*B + (r/32)*32)*D + d*32 + r%32.
  * head_dim D must be 64 or 128, block_tokens B must be 64 (the decode kernels
- * stream 32-token half blocks), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned and
- * must stay valid until treepo_destroy; their contents need no initialisation.
+ * stream 32-token half blocks), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned,
+ * 16-byte aligned, and must stay valid until treepo_destroy; their contents
+ * need no initialisation.
  */
 typedef struct treepo_config {
   int32_t num_q_heads;  /* Hq  */
@@ -77,8 +78,9 @@ typedef struct treepo_config {
   void* v_pool;         /* device, see above                            */
 } treepo_config;
 
-/* Work-item record exported by treepo_export_plan. */
-#define TREEPO_ITEM_FIELDS 12
+/* Records exported by treepo_export_plan. */
+#define TREEPO_PIECE_FIELDS 16
+#define TREEPO_TILE_FIELDS 4
 
 /* Node record exported by treepo_export_nodes: 8 int32 per node. */
 #define TREEPO_NODE_FIELDS 8 /* parent, depth, start, len, cap, block_begin, n_blocks, tree_id */
@@ -141,17 +143,18 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
 /* One decode step of attention for n_leaves leaves (Sec. 2.2 segment-level
  * decoding; Sec. 2.3 chains).  leaves: host node ids (any node, duplicates
  * allowed), call position i.
- *   q     device bf16 [n_leaves][Hq][D]   the step's queries
+ *   q     device bf16 [n_leaves][Hq][D]   the step's queries (16-byte aligned)
  *   out   device fp32 [n_leaves][Hq][D]   softmax(scale q K^T) V over the chain
  *   lse   device fp32 [n_leaves][Hq] or null: natural-log sum exp(scale q.k)
- *   workspace  device, >= treepo_decode_workspace_size(..., TREEPO_MODE_TREE)
+ *   workspace  device, 256-byte aligned, >= treepo_decode_workspace_size(..., TREEPO_MODE_TREE)
  * Cascade schedule: every node's K/V is read once and scored against all of
  * its descendant leaves' query rows (the nested sub-groups G_j of Sec. 2.3);
  * per-node partials are merged with a log-sum-exp combine.  The library keeps
  * the plan it uploaded into the workspace and reuses it while the tree and
  * the leaf list are unchanged: do not modify the workspace between calls.
- * EINVAL (bad id, null pointer, n_leaves < 1), EEMPTY (a chain holds no
- * tokens), EWORKSPACE, EHIP. */
+ * EINVAL (bad id, null pointer, n_leaves < 1, q not 16-byte aligned),
+ * EEMPTY (a chain holds no tokens), EWORKSPACE (missing, too small or not
+ * 256-byte aligned), EHIP. */
 int32_t treepo_tree_decode(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
                            const void* q, float scale, float* out, float* lse,
                            void* workspace, size_t ws_bytes, hipStream_t stream);
@@ -193,29 +196,24 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
                            int32_t* nodes, int32_t* desc_off, int32_t* desc,
                            int32_t* n_nodes, int32_t* total);
 
-/* The decode schedule for inspection.  Work items, TREEPO_ITEM_FIELDS int32 each:
- *   {kind (0 VALU, 1 MFMA), rowset_begin, n_leaves, tile_begin, tile_end,
- *    partial_base, rows, run, src0, src1, src2, 0}
- * where src_i = 2 * block + half of the item's i-th tile (-1 past its end)
- * rowsets[]: call positions; tiles[] 4 int32 each {block, node, tile_in_node,
- * valid_tokens}: tile k of a node holds its tokens [32k, 32k+32) and lives in
- * pool block block_begin + k/2.  Pass null arrays to query the counts only. */
+/* The decode schedule for inspection.  The chain nodes are cut into runs
+ * (maximal chain segments whose nodes have the same descendant leaves); each
+ * (run, leaf group, KV head) is a sequence of 32-token tiles; the sequences
+ * are cut into streams of equal estimated cost, one workgroup each, and a
+ * piece is the part of one sequence inside one stream.  Pieces,
+ * TREEPO_PIECE_FIELDS int32 each, in stream order:
+ *   {rowset_begin, n_leaves, rows, kv_head, stream_tile, n_tiles,
+ *    partial_base, q_row, run, stream, plan_tile, 0, 0, 0, 0, 0}
+ * rows = n_leaves * (Hq / Hkv); the piece's leaves are rowsets[rowset_begin ..
+ * + n_leaves) (call positions); its tiles are tiles[plan_tile .. + n_tiles),
+ * TREEPO_TILE_FIELDS int32 each {block, node, tile_in_node, valid_tokens}:
+ * tile k of a node holds its tokens [32k, 32k+32) and lives in pool block
+ * block_begin + k/2.  *n_streams receives the stream count.  Pass null arrays
+ * to query the counts only. */
 int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
-                           int32_t mode, int32_t* items, int32_t* rowsets, int32_t* tiles,
-                           int32_t* n_items, int32_t* n_rowsets, int32_t* n_tiles);
-
-/* ---- schedule options --------------------------------------------------- */
-
-/* Work items whose stacked query rows (descendant leaves x GQA group) number at
- * most this value run the wavefront-shuffle (VALU) partial; the others run on
- * MFMA.  Range 0..8; 0 (the default) puts every item on MFMA. */
-#define TREEPO_OPT_VALU_MAX_ROWS 0
-
-/* Sets a schedule option; cached plans are dropped and rebuilt on the next
- * decode (results agree to rounding; the schedule changes).  EINVAL for an
- * unknown option or a value out of range. */
-int32_t treepo_set_option(treepo_ctx* ctx, int32_t option, int32_t value);
-int32_t treepo_get_option(treepo_ctx* ctx, int32_t option, int32_t* value);
+                           int32_t mode, int32_t* pieces, int32_t* rowsets, int32_t* tiles,
+                           int32_t* n_pieces, int32_t* n_rowsets, int32_t* n_tiles,
+                           int32_t* n_streams);
 
 /* ---- kernel timing ------------------------------------------------------ */
 

@@ -9,7 +9,7 @@ namespace treepo {
 
 constexpr int kTile = 64;  // tokens per pool block
 
-// Device views of the decode plan and buffers (see tree_core.h for layouts).
+// Device views of the decode plan and buffers (record layouts in tree_core.h).
 struct DecodeArgs {
   const uint16_t* k_pool;  // bf16 [Hkv][num_blocks][64][D]
   const uint16_t* v_pool;  // bf16 [Hkv][num_blocks][2][D][32] (V^T per 32-token half block)
@@ -17,24 +17,26 @@ struct DecodeArgs {
   int32_t hq, hkv, group, d;
   const uint16_t* q;       // bf16 [n_leaves][Hq][D]
   float scale_log2;        // softmax scale * log2(e)
-  const int32_t* items;    // Item, 12 int32 each
+  const int32_t* streams;  // Stream records
+  int32_t n_streams;
+  const int32_t* pieces;   // Piece records
   const int32_t* rowsets;
-  const int32_t* tiles;    // Tile, 4 int32 each
+  const int32_t* stiles;   // StreamTile records
+  const int32_t* segs;     // query segment offsets
   float* part_o;           // fp32 [partial_rows][D], unnormalised
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
-  const int32_t* leaf_off; // [n_leaves + 1]
-  const int32_t* entries;  // Entry, 2 int32 each
+  const int32_t* leaf_off; // [n_leaves * Hkv + 1]
+  const int32_t* entries;
   int32_t n_leaves;
   float* out;              // fp32 [n_leaves][Hq][D]
   float* lse;              // fp32 [n_leaves][Hq] or null
-  bool nontemporal;        // KV tiles are read once per call: stream them past the caches
 };
 
-// Node partials of items [first_item, first_item + n_items), VALU or MFMA by kind.
-hipError_t launch_partial(const DecodeArgs& a, int32_t first_item, int32_t n_items, hipStream_t s);
+// One workgroup per stream: every piece's node partials.
+hipError_t launch_partial(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // Node-partial workgroups resident per compute unit (set by the kernel's
-// register and LDS budget); the planner sizes item chunks against it.
+// register and LDS budget); the planner makes one stream per resident slot.
 int32_t partial_workgroups_per_cu();
 constexpr int32_t kComputeUnits = 256;  // MI355X
 

@@ -169,12 +169,20 @@ void desc_sets(const Tree& t, int32_t n_leaves, const int32_t* leaves, std::vect
 namespace {
 
 struct Run {
-  std::vector<int32_t> nodes;  // root-first
-  std::vector<int32_t> leaves; // ascending call positions
-  int32_t tile_begin = 0, tile_end = 0;
-  int32_t group_leaves = 1;    // leaves per item group
-  std::vector<std::vector<int32_t>> group_items;  // per group: item ids (pre-sort)
+  std::vector<int32_t> nodes;   // root-first
+  std::vector<int32_t> leaves;  // ascending call positions
+  std::vector<Tile> tiles;
+  int32_t group_leaves = 1;     // leaves per group
 };
+
+// A piece's query tiles cost little next to its KV tiles (a few rows each).
+constexpr double kQTileCost = 0.25;
+
+// Estimated cost of one KV tile for a piece of `rows` query rows, in units of
+// one tile's load time at full load (measured): the token-split path (up to
+// 32 rows) hides its compute under the loads; the row-split path takes about
+// 1.4 (one 16-row block per wave) and 2 (two per wave) times as long.
+double tile_cost(int32_t rows) { return rows <= 32 ? 1.0 : rows <= 64 ? 1.4 : 2.0; }
 
 }  // namespace
 
@@ -183,8 +191,14 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   const auto& nd = t.nodes();
   const int32_t B = t.block_tokens();
   const int32_t G = p.group;
-  if (G < 1 || G > (p.mfma_enabled ? p.mfma_max_rows : p.valu_max_rows)) {
+  const int32_t Hkv = p.num_kv_heads;
+  if (G < 1 || G > p.max_rows) {
     if (err) *err = "GQA group larger than the kernels' row limit";
+    return kEUnsupported;
+  }
+  if (2 * static_cast<int64_t>(Hkv) * p.num_blocks > INT32_MAX ||
+      static_cast<int64_t>(n_leaves) * p.num_q_heads * p.head_dim > INT32_MAX) {
+    if (err) *err = "pool or query tensor too large for 32-bit tile and row offsets";
     return kEUnsupported;
   }
   *out = Plan();
@@ -224,9 +238,8 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     }
   }
 
-  // ---- tiles -----------------------------------------------------------------
+  // ---- tiles and leaf groups ---------------------------------------------------
   for (Run& r : runs) {
-    r.tile_begin = static_cast<int32_t>(out->tiles.size());
     for (int32_t n : r.nodes) {
       const int32_t ln = nd[n].len;
       constexpr int32_t T = kPlanTileTokens;
@@ -237,124 +250,156 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         tl.node = n;
         tl.tile_in_node = k;
         tl.valid = std::min(T, ln - k * T);
-        out->tiles.push_back(tl);
+        r.tiles.push_back(tl);
         out->unique_kv_tokens += tl.valid;
       }
     }
-    r.tile_end = static_cast<int32_t>(out->tiles.size());
     const int32_t nl = static_cast<int32_t>(r.leaves.size());
-    if (nl * G <= p.valu_max_rows) {
-      r.group_leaves = nl;
-    } else {
-      // split the leaves evenly into the fewest groups that fit the row limit
-      const int32_t lim = std::max(1, (p.mfma_enabled ? p.mfma_max_rows : p.valu_max_rows) / G);
-      const int32_t ng = (nl + lim - 1) / lim;
-      r.group_leaves = (nl + ng - 1) / ng;
-    }
+    // split the leaves evenly into the fewest groups that fit the row limit
+    const int32_t lim = std::max(1, p.max_rows / G);
+    const int32_t ng = (nl + lim - 1) / lim;
+    r.group_leaves = (nl + ng - 1) / ng;
   }
 
-  // ---- chunk size: minimise rounds x (tiles per item + one tile of overhead) --
-  auto groups_of = [](const Run& r) {
-    return (static_cast<int32_t>(r.leaves.size()) + r.group_leaves - 1) / r.group_leaves;
+  // ---- sequences: (run, leaf group, KV head) -------------------------------------
+  struct Seq {
+    int32_t run, rowset_begin, n_leaves, g;
   };
-  const int64_t S = std::max(1, p.concurrent_wgs);
-  int32_t best_c = 1;
-  double best_cost = 1e300;
-  for (int32_t c = 1; c <= std::max(1, p.max_chunk_tiles); ++c) {
-    int64_t w = 0;
-    for (const Run& r : runs) {
-      const int32_t nt = r.tile_end - r.tile_begin;
-      if (nt == 0) continue;
-      w += static_cast<int64_t>(groups_of(r)) * ((nt + c - 1) / c);
-    }
-    w *= p.num_kv_heads;
-    const double cost = static_cast<double>((w + S - 1) / S) * (c + 1.0);
-    if (cost <= best_cost) {
-      best_cost = cost;
-      best_c = c;
-    }
-  }
-  out->chunk_tiles = best_c;
-
-  // ---- items -----------------------------------------------------------------
-  std::vector<Item> tmp;
+  std::vector<Seq> seqs;
+  double total_cost = 0.0;
+  int64_t total_tiles = 0;
   for (int32_t ri = 0; ri < static_cast<int32_t>(runs.size()); ++ri) {
-    Run& r = runs[ri];
-    const int32_t nt = r.tile_end - r.tile_begin;
-    const int32_t ng = groups_of(r);
-    r.group_items.assign(ng, {});
-    if (nt == 0) continue;
-    const int32_t nchunks = (nt + best_c - 1) / best_c;
-    for (int32_t gi = 0; gi < ng; ++gi) {
-      const int32_t l0 = gi * r.group_leaves;
-      const int32_t l1 = std::min<int32_t>(static_cast<int32_t>(r.leaves.size()), l0 + r.group_leaves);
+    const Run& r = runs[ri];
+    if (r.tiles.empty()) continue;
+    const int32_t nl = static_cast<int32_t>(r.leaves.size());
+    for (int32_t l0 = 0; l0 < nl; l0 += r.group_leaves) {
+      const int32_t l1 = std::min(nl, l0 + r.group_leaves);
       const int32_t rs = static_cast<int32_t>(out->rowsets.size());
       for (int32_t l = l0; l < l1; ++l) out->rowsets.push_back(r.leaves[l]);
-      for (int32_t c = 0; c < nchunks; ++c) {
-        Item it;
-        it.rowset_begin = rs;
-        it.n_leaves = l1 - l0;
-        it.rows = it.n_leaves * G;
-        it.kind = it.rows <= p.valu_max_rows ? kKindValu : kKindMfma;
-        it.tile_begin = r.tile_begin + static_cast<int32_t>(static_cast<int64_t>(nt) * c / nchunks);
-        it.tile_end = r.tile_begin + static_cast<int32_t>(static_cast<int64_t>(nt) * (c + 1) / nchunks);
-        it.partial_base = 0;
-        it.run = ri;
-        for (int32_t f = 0; f < 3; ++f) {
-          const int32_t ti = it.tile_begin + f;
-          it.first_src[f] = ti < it.tile_end ? 2 * out->tiles[ti].block + (out->tiles[ti].tile_in_node & 1) : -1;
-        }
-        it.pad = 0;
-        r.group_items[gi].push_back(static_cast<int32_t>(tmp.size()));
-        tmp.push_back(it);
+      int64_t tok = 0;
+      for (const Tile& tl : r.tiles) tok += tl.valid;
+      out->kv_token_visits += tok;
+      for (int32_t g = 0; g < Hkv; ++g) {
+        seqs.push_back(Seq{ri, rs, l1 - l0, g});
+        total_cost += tile_cost((l1 - l0) * G) * static_cast<double>(r.tiles.size()) +
+                      kQTileCost * ((l1 - l0) * G + kQTileRows - 1) / kQTileRows;
+        total_tiles += static_cast<int64_t>(r.tiles.size());
       }
     }
   }
-  // VALU items first, stable
-  std::vector<int32_t> order(tmp.size()), newid(tmp.size());
-  for (size_t i = 0; i < tmp.size(); ++i) order[i] = static_cast<int32_t>(i);
-  std::stable_sort(order.begin(), order.end(),
-                   [&](int32_t a, int32_t b) { return tmp[a].kind < tmp[b].kind; });
-  int64_t base = 0;
-  for (size_t k = 0; k < order.size(); ++k) {
-    Item it = tmp[order[k]];
-    if (base > INT32_MAX - static_cast<int64_t>(it.rows) * p.num_kv_heads) {
-      if (err) *err = "too many partial rows";
-      return kEUnsupported;
-    }
-    it.partial_base = static_cast<int32_t>(base);
-    base += static_cast<int64_t>(it.rows) * p.num_kv_heads;
-    newid[order[k]] = static_cast<int32_t>(k);
-    if (it.kind == kKindValu) ++out->n_valu_items;
-    for (int32_t ti = it.tile_begin; ti < it.tile_end; ++ti) out->kv_token_visits += out->tiles[ti].valid;
-    out->items.push_back(it);
+  if (total_tiles == 0) {
+    if (err) *err = "no KV tokens on the leaves' chains";
+    return kEEmpty;
   }
-  out->partial_rows = base;
 
-  // ---- per-leaf combine entries, chain order -----------------------------------
-  out->leaf_off.assign(n_leaves + 1, 0);
-  std::vector<int32_t> ch;
-  for (int32_t x = 0; x < n_leaves; ++x) {
-    std::vector<int32_t> leaf_runs;
-    if (mode == kModeTree) {
-      t.chain(leaves[x], &ch);
-      for (int32_t n : ch)
-        if (leaf_runs.empty() || leaf_runs.back() != run_of[n]) leaf_runs.push_back(run_of[n]);
-    } else {
-      leaf_runs.push_back(x);
+  // ---- streams: cut the concatenated sequences at equal cumulative cost --------
+  const int64_t S0 = std::max(1, p.concurrent_wgs);
+  const int64_t per_round = S0 * (3 * kMaxStreamTiles / 4);
+  const int64_t rounds = std::max<int64_t>(1, (total_tiles + per_round - 1) / per_round);
+  const int64_t planned = std::min<int64_t>(total_tiles, S0 * rounds);
+  // every stream may start with a cut piece's query tiles; the slack keeps the
+  // last stream from collecting the rounding remainder
+  const double target = total_cost / static_cast<double>(planned) + 2 * kQTileCost;
+  double acc = 0.0;
+  int64_t partial = 0;
+  auto pad_to = [](auto* v, size_t m, auto fill) {
+    while (v->size() % m) v->push_back(fill);
+  };
+  auto open_stream = [&]() {
+    pad_to(&out->stream_tiles, 2, StreamTile{0, 0});
+    pad_to(&out->segs, 4, 0);
+    Stream st{};
+    st.piece_begin = st.piece_end = static_cast<int32_t>(out->pieces.size());
+    st.tile_off = static_cast<int32_t>(out->stream_tiles.size());
+    st.seg_off = static_cast<int32_t>(out->segs.size());
+    out->streams.push_back(st);
+  };
+  open_stream();
+  for (int32_t si = 0; si < static_cast<int32_t>(seqs.size()); ++si) {
+    const Seq& sq = seqs[si];
+    const Run& r = runs[sq.run];
+    const int32_t rows = sq.n_leaves * G;
+    const int32_t nq = (rows + kQTileRows - 1) / kQTileRows;
+    const double c = tile_cost(rows);
+    bool new_piece = true;
+    for (const Tile& tl : r.tiles) {
+      Stream* st = &out->streams.back();
+      const int64_t s = static_cast<int64_t>(out->streams.size()) - 1;
+      const bool quota = acc >= target * static_cast<double>(s + 1) && s + 1 < planned;
+      const bool room = st->n_tiles + (new_piece ? nq + 1 : 1) <= kMaxStreamTiles &&
+                        st->n_segs + (new_piece ? sq.n_leaves : 0) <= kMaxStreamSegs;
+      if (st->n_tiles > 0 && (quota || !room)) {
+        open_stream();
+        st = &out->streams.back();
+        new_piece = true;
+      }
+      if (new_piece) {
+        Piece pc{};
+        pc.rowset_begin = sq.rowset_begin;
+        pc.n_leaves = sq.n_leaves;
+        pc.rows = rows;
+        pc.g = sq.g;
+        pc.tile_begin = st->n_tiles;
+        pc.n_tiles = 0;
+        pc.seg_begin = st->n_segs;
+        pc.run = sq.run;
+        pc.stream = static_cast<int32_t>(out->streams.size()) - 1;
+        pc.plan_tile = static_cast<int32_t>(out->tiles.size());
+        pc.n_qtiles = nq;
+        for (int32_t j = 0; j < sq.n_leaves; ++j) {
+          const int32_t x = out->rowsets[sq.rowset_begin + j];
+          out->segs.push_back((x * p.num_q_heads + sq.g * G) * p.head_dim);
+        }
+        st->n_segs += sq.n_leaves;
+        for (int32_t t = 0; t < nq; ++t) {
+          const int32_t row0 = t * kQTileRows;
+          const int32_t n = std::min(kQTileRows, rows - row0);
+          out->stream_tiles.push_back(StreamTile{-1 - pc.seg_begin, row0 | (n << 16)});
+        }
+        st->n_tiles += nq;
+        acc += kQTileCost * nq;
+        const int64_t prow = rows <= kSplitMaxRows ? 2 * static_cast<int64_t>(rows) : rows;
+        if (partial + prow > INT32_MAX) {
+          if (err) *err = "too many partial rows";
+          return kEUnsupported;
+        }
+        pc.partial_base = static_cast<int32_t>(partial);
+        partial += prow;
+        out->pieces.push_back(pc);
+        st->piece_end = static_cast<int32_t>(out->pieces.size());
+        new_piece = false;
+      }
+      const int32_t half = tl.tile_in_node & 1;
+      out->stream_tiles.push_back(
+          StreamTile{static_cast<int32_t>(2 * (static_cast<int64_t>(sq.g) * p.num_blocks + tl.block) + half),
+                     tl.valid});
+      out->tiles.push_back(tl);
+      ++st->n_tiles;
+      ++out->pieces.back().n_tiles;
+      acc += c;
     }
-    for (int32_t ri : leaf_runs) {
-      const Run& r = runs[ri];
-      const auto pos = std::lower_bound(r.leaves.begin(), r.leaves.end(), x) - r.leaves.begin();
-      const int32_t gi = static_cast<int32_t>(pos) / r.group_leaves;
-      const int32_t j = static_cast<int32_t>(pos) - gi * r.group_leaves;
-      for (int32_t old : r.group_items[gi]) {
-        const Item& it = out->items[newid[old]];
-        out->entries.push_back(Entry{it.partial_base + j * G, it.rows});
+  }
+  pad_to(&out->stream_tiles, 2, StreamTile{0, 0});
+  pad_to(&out->segs, 4, 0);
+  out->partial_rows = partial;
+
+  // ---- per (leaf, KV head) merge entries -----------------------------------------
+  const int64_t nkeys = static_cast<int64_t>(n_leaves) * Hkv;
+  out->leaf_off.assign(nkeys + 1, 0);
+  auto for_each_entry = [&](auto&& f) {
+    for (const Piece& pc : out->pieces) {
+      for (int32_t j = 0; j < pc.n_leaves; ++j) {
+        const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
+        f(key, pc.partial_base + j * G);
+        if (pc.rows <= kSplitMaxRows) f(key, pc.partial_base + pc.rows + j * G);
       }
     }
-    out->leaf_off[x + 1] = static_cast<int32_t>(out->entries.size());
-  }
+  };
+  for_each_entry([&](int64_t key, int32_t) { ++out->leaf_off[key + 1]; });
+  for (int64_t k = 0; k < nkeys; ++k) out->leaf_off[k + 1] += out->leaf_off[k];
+  out->entries.assign(out->leaf_off.back(), 0);
+  std::vector<int32_t> cursor(out->leaf_off.begin(), out->leaf_off.end() - 1);
+  for_each_entry([&](int64_t key, int32_t row) { out->entries[cursor[key]++] = row; });
   return kOk;
 }
 

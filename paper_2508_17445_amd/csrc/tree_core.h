@@ -74,70 +74,117 @@ class Tree {
 };
 
 // ---- decode plan -----------------------------------------------------------
+//
+// Cascade schedule (the nested descendant sub-groups of TreePO Sec. 2.3 as the
+// unit of shared attention work): the chain nodes of the decoded leaves are
+// cut into runs (maximal chain segments whose nodes have the same descendant
+// leaves), every run is streamed once per KV head for the query rows of its
+// descendant leaves, and the per-leaf results are merged by log-sum-exp.
+//
+// Work distribution: every (run, leaf group, KV head) contributes a sequence
+// of 32-token KV tiles.  The sequences are concatenated and cut into streams
+// of equal estimated cost, one stream per resident workgroup, so every
+// workgroup streams the same amount of KV and its load pipeline runs across
+// the pieces of its stream without draining.
 
 enum PlanMode : int32_t { kModeTree = 0, kModeNaive = 1 };
 
 // Tokens per decode tile (half of a 64-token pool block).
 constexpr int32_t kPlanTileTokens = 32;
-enum ItemKind : int32_t { kKindValu = 0, kKindMfma = 1 };
+// Upper bounds on the tiles and query segments of one stream (sized for the
+// kernel's LDS tables).
+constexpr int32_t kMaxStreamTiles = 256;
+constexpr int32_t kMaxStreamSegs = 256;
+// Query rows carried by one query tile (a tile buffer holds 64 rows of D).
+constexpr int32_t kQTileRows = 64;
+// Query rows of a piece that the token-split kernel path handles (two 16-row
+// blocks); larger row groups use the row-split path.
+constexpr int32_t kSplitMaxRows = 32;
 
-// One work item: a chunk of consecutive KV tiles of one run (a maximal chain
-// segment whose nodes share the same descendant-leaf set), scored against the
-// query rows of a group of those leaves.  A workgroup processes one item for
-// one KV head.  Rows are (leaf j of the group, head h' of the GQA group):
-// row = j * G + h'.
-struct Item {
-  int32_t kind;
-  int32_t rowset_begin;  // index into Plan::rowsets
-  int32_t n_leaves;      // leaves in the group
-  int32_t tile_begin;    // index into Plan::tiles
-  int32_t tile_end;
-  int32_t partial_base;  // partial row of (g=0, row 0); (g, r) -> base + g*rows + r
+// A piece: consecutive tiles of one (run, leaf group, KV head) sequence, all
+// in one stream.  Rows are (leaf j of the group, head h' of the GQA group):
+// row = j * G + h'.  In its stream's tile list a piece is n_qtiles query tiles
+// (its query rows, 64 per tile) followed by n_tiles KV tiles.  A token-split
+// piece (rows <= 32) writes two partial rows per query row (one per token half
+// of each tile): rows [base, base + rows) and [base + rows, base + 2 rows); a
+// row-split piece writes rows partial rows.
+struct Piece {
+  int32_t rowset_begin;  // index into Plan::rowsets (the group's call positions)
+  int32_t n_leaves;
   int32_t rows;          // n_leaves * G
+  int32_t g;             // KV head
+  int32_t tile_begin;    // its first query tile, index into the stream's tile list
+  int32_t n_tiles;       // KV tiles
+  int32_t partial_base;
+  int32_t seg_begin;     // its first query segment, index into the stream's segment list
   int32_t run;
-  int32_t first_src[3];  // half-block index (2 * block + half) of the first tiles, -1 past the end
-  int32_t pad;
+  int32_t stream;
+  int32_t plan_tile;     // index of its first KV tile in Plan::tiles
+  int32_t n_qtiles;
+  int32_t pad[4];
 };
-constexpr int32_t kItemInts = 12;
+constexpr int32_t kPieceInts = 16;
+static_assert(sizeof(Piece) == kPieceInts * sizeof(int32_t), "piece record size");
 
-// A KV tile: up to kPlanTileTokens tokens of one node, tokens
-// [32 k, 32 k + 32) of the node for tile_in_node = k, inside pool block
-// block_begin + k / 2.
+// A stream: pieces [piece_begin, piece_end) processed in order by one
+// workgroup; its tiles are Plan::stream_tiles[tile_off, tile_off + n_tiles)
+// and its query segments Plan::segs[seg_off, seg_off + n_segs).  tile_off is
+// even and seg_off a multiple of 4; both arrays are padded so that a stream's
+// lists can be read in 16-byte pieces.
+struct Stream {
+  int32_t piece_begin, piece_end;
+  int32_t tile_off, n_tiles;
+  int32_t seg_off, n_segs;
+  int32_t pad[2];
+};
+constexpr int32_t kStreamInts = 8;
+static_assert(sizeof(Stream) == kStreamInts * sizeof(int32_t), "stream record size");
+
+// Device record of a tile.  KV tile: hb = 2 * (g * num_blocks + block) + half
+// >= 0 locates its K and V data, valid = tokens holding data (1..32).  Query
+// tile: hb = -1 - (the piece's first segment, stream-local), valid =
+// row0 | (n_rows << 16): rows [row0, row0 + n_rows) of the piece.
+struct StreamTile {
+  int32_t hb;
+  int32_t valid;
+};
+
+// Host record of a KV tile, for inspection: tokens [32 k, 32 k + 32) of node
+// `node` (k = tile_in_node) in pool block `block` (= block_begin + k / 2).
 struct Tile {
   int32_t block;
   int32_t node;
   int32_t tile_in_node;
-  int32_t valid;  // tokens of the tile holding data (1..32)
-};
-
-// Per leaf, the partials to merge: slot(g, h') = a + g * b + h'.
-struct Entry {
-  int32_t a;
-  int32_t b;
+  int32_t valid;
 };
 
 struct PlanParams {
   int32_t group;            // G = Hq / Hkv
   int32_t num_kv_heads;     // Hkv
-  int32_t valu_max_rows;    // rows <= this use the VALU kernel
-  int32_t mfma_max_rows;    // rows per MFMA item at most
-  int32_t concurrent_wgs;   // workgroups resident at once (chunking target)
-  int32_t max_chunk_tiles;  // upper bound on tiles per item
-  int32_t mfma_enabled;     // 0: every item is split to the VALU row limit
+  int32_t num_q_heads;      // Hq
+  int32_t head_dim;         // D
+  int64_t num_blocks;       // pool blocks per KV head
+  int32_t max_rows;         // query rows of a piece at most (leaf groups are split to fit)
+  int32_t concurrent_wgs;   // workgroups resident at once (streams per round)
 };
 
 struct Plan {
   PlanMode mode = kModeTree;
-  std::vector<Item> items;  // VALU items first, then MFMA items
-  int32_t n_valu_items = 0;
+  std::vector<Stream> streams;
+  std::vector<Piece> pieces;          // stream order
   std::vector<int32_t> rowsets;
-  std::vector<Tile> tiles;
-  std::vector<int32_t> leaf_off;  // n_leaves + 1
-  std::vector<Entry> entries;
-  int64_t partial_rows = 0;       // total partial rows over items and KV heads
-  int32_t chunk_tiles = 0;
+  std::vector<StreamTile> stream_tiles;
+  std::vector<Tile> tiles;            // host view of the KV tiles, piece order
+  // Query segments: element offset in the query tensor of the G rows of one
+  // leaf for one KV head (contiguous there), one per (piece, leaf).
+  std::vector<int32_t> segs;
+  // Per (leaf x, KV head g): partial rows to merge for query head g * G + h'
+  // are entries[e] + h' for e in [leaf_off[x * Hkv + g], leaf_off[x * Hkv + g + 1]).
+  std::vector<int32_t> leaf_off;
+  std::vector<int32_t> entries;
+  int64_t partial_rows = 0;
   int64_t unique_kv_tokens = 0;   // tokens streamed per KV head (tree: unique)
-  int64_t kv_token_visits = 0;    // tiles' tokens x item groups (reads per head)
+  int64_t kv_token_visits = 0;    // tokens streamed, summed over leaf groups (per KV head)
 };
 
 // Builds the decode schedule for `leaves` (validated by the caller).

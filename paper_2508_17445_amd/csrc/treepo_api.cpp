@@ -32,7 +32,8 @@ struct CachedPlan {
   std::vector<int32_t> leaves;
   Plan plan;
   std::vector<char> blob;  // host image of the plan region
-  size_t off_items = 0, off_rowsets = 0, off_tiles = 0, off_leaf_off = 0, off_entries = 0;
+  size_t off_streams = 0, off_pieces = 0, off_rowsets = 0, off_stiles = 0, off_segs = 0;
+  size_t off_leaf_off = 0, off_entries = 0;
   size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;
   uint64_t uid = 0;
   uint64_t last_use = 0;
@@ -188,20 +189,23 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   if (st != treepo::kOk) return fail(ctx, st, err);
   const Plan& p = cp.plan;
   size_t off = 0;
-  cp.off_items = off;
-  off = align_up(off + p.items.size() * sizeof(treepo::Item));
-  cp.off_rowsets = off;
-  off = align_up(off + p.rowsets.size() * sizeof(int32_t));
-  cp.off_tiles = off;
-  off = align_up(off + p.tiles.size() * sizeof(treepo::Tile));
-  cp.off_leaf_off = off;
-  off = align_up(off + p.leaf_off.size() * sizeof(int32_t));
-  cp.off_entries = off;
-  off = align_up(off + p.entries.size() * sizeof(treepo::Entry));
+  auto place = [&](size_t* at, size_t bytes) {
+    *at = off;
+    off = align_up(off + bytes);
+  };
+  place(&cp.off_streams, p.streams.size() * sizeof(treepo::Stream));
+  place(&cp.off_pieces, p.pieces.size() * sizeof(treepo::Piece));
+  place(&cp.off_rowsets, p.rowsets.size() * sizeof(int32_t));
+  place(&cp.off_stiles, p.stream_tiles.size() * sizeof(treepo::StreamTile));
+  place(&cp.off_segs, p.segs.size() * sizeof(int32_t));
+  place(&cp.off_leaf_off, p.leaf_off.size() * sizeof(int32_t));
+  place(&cp.off_entries, p.entries.size() * sizeof(int32_t));
   cp.blob.assign(off, 0);
-  put(cp.blob, cp.off_items, p.items);
+  put(cp.blob, cp.off_streams, p.streams);
+  put(cp.blob, cp.off_pieces, p.pieces);
   put(cp.blob, cp.off_rowsets, p.rowsets);
-  put(cp.blob, cp.off_tiles, p.tiles);
+  put(cp.blob, cp.off_stiles, p.stream_tiles);
+  put(cp.blob, cp.off_segs, p.segs);
   put(cp.blob, cp.off_leaf_off, p.leaf_off);
   put(cp.blob, cp.off_entries, p.entries);
   cp.off_part_o = off;
@@ -230,14 +234,16 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
                float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream, int32_t mode) {
   if (!ctx) return TREEPO_EINVAL;
   if (!q || !out) return fail(ctx, TREEPO_EINVAL, "null q or out");
+  if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return fail(ctx, TREEPO_EINVAL, "q must be 16-byte aligned");
   std::string err;
   int32_t st = ctx->tree.check_leaves(n, leaves, &err);
   if (st != treepo::kOk) return fail(ctx, st, err);
   CachedPlan* cp = nullptr;
   st = get_plan(ctx, n, leaves, mode, &cp);
   if (st != TREEPO_OK) return st;
-  if (!ws || ws_bytes < cp->ws_bytes)
-    return fail(ctx, TREEPO_EWORKSPACE, "workspace missing or smaller than treepo_decode_workspace_size");
+  if (!ws || ws_bytes < cp->ws_bytes || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return fail(ctx, TREEPO_EWORKSPACE,
+                "workspace missing, smaller than treepo_decode_workspace_size or not 256-byte aligned");
   char* wsb = static_cast<char*>(ws);
   auto up = std::find_if(ctx->uploaded.begin(), ctx->uploaded.end(),
                          [&](const std::pair<void*, uint64_t>& u) { return u.first == ws; });
@@ -260,9 +266,12 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.d = ctx->cfg.head_dim;
   a.q = static_cast<const uint16_t*>(q);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.items = reinterpret_cast<const int32_t*>(wsb + cp->off_items);
+  a.streams = reinterpret_cast<const int32_t*>(wsb + cp->off_streams);
+  a.n_streams = static_cast<int32_t>(p.streams.size());
+  a.pieces = reinterpret_cast<const int32_t*>(wsb + cp->off_pieces);
   a.rowsets = reinterpret_cast<const int32_t*>(wsb + cp->off_rowsets);
-  a.tiles = reinterpret_cast<const int32_t*>(wsb + cp->off_tiles);
+  a.stiles = reinterpret_cast<const int32_t*>(wsb + cp->off_stiles);
+  a.segs = reinterpret_cast<const int32_t*>(wsb + cp->off_segs);
   a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
   a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
   a.leaf_off = reinterpret_cast<const int32_t*>(wsb + cp->off_leaf_off);
@@ -270,12 +279,7 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;
-  // The cascade schedule reads each KV tile once per call; the per-leaf
-  // baseline re-reads shared prefixes and keeps them cacheable.
-  a.nontemporal = p.mode == treepo::kModeTree;
-  hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL, stream, [&] {
-    return treepo::launch_partial(a, 0, static_cast<int32_t>(p.items.size()), stream);
-  });
+  hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL, stream, [&] { return treepo::launch_partial(a, stream); });
   if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
   e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
@@ -319,7 +323,8 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   const treepo_config& c = *cfg;
   if (c.num_q_heads < 1 || c.num_kv_heads < 1 || c.num_q_heads % c.num_kv_heads != 0 ||
       c.num_blocks < 0 || c.num_blocks > INT32_MAX || c.max_nodes < 0 || c.reserved != 0 ||
-      !c.k_pool || !c.v_pool)
+      !c.k_pool || !c.v_pool || reinterpret_cast<uintptr_t>(c.k_pool) % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(c.v_pool) % 16 != 0)
     return TREEPO_EINVAL;
   if ((c.head_dim != 64 && c.head_dim != 128) || c.block_tokens != treepo::kTile ||
       c.num_q_heads / c.num_kv_heads > 128)
@@ -328,11 +333,11 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   if (!ctx) return TREEPO_ENOMEM;
   ctx->params.group = c.num_q_heads / c.num_kv_heads;
   ctx->params.num_kv_heads = c.num_kv_heads;
-  ctx->params.valu_max_rows = 0;
-  ctx->params.mfma_max_rows = 128;
+  ctx->params.num_q_heads = c.num_q_heads;
+  ctx->params.head_dim = c.head_dim;
+  ctx->params.num_blocks = c.num_blocks;
+  ctx->params.max_rows = 128;
   ctx->params.concurrent_wgs = treepo::kComputeUnits * treepo::partial_workgroups_per_cu();
-  ctx->params.max_chunk_tiles = 128;
-  ctx->params.mfma_enabled = 1;
   *out = ctx;
   return TREEPO_OK;
 }
@@ -522,10 +527,10 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
 }
 
 int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t mode,
-                           int32_t* items, int32_t* rowsets, int32_t* tiles, int32_t* n_items,
-                           int32_t* n_rowsets, int32_t* n_tiles) {
+                           int32_t* pieces, int32_t* rowsets, int32_t* tiles, int32_t* n_pieces,
+                           int32_t* n_rowsets, int32_t* n_tiles, int32_t* n_streams) {
   if (!ctx) return TREEPO_EINVAL;
-  if (!n_items || !n_rowsets || !n_tiles || (mode != TREEPO_MODE_TREE && mode != TREEPO_MODE_NAIVE))
+  if (!n_pieces || !n_rowsets || !n_tiles || !n_streams || (mode != TREEPO_MODE_TREE && mode != TREEPO_MODE_NAIVE))
     return fail(ctx, TREEPO_EINVAL, "null count pointer or bad mode");
   std::string err;
   int32_t st = ctx->tree.check_leaves(n_leaves, leaves, &err);
@@ -534,38 +539,16 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
   st = get_plan(ctx, n_leaves, leaves, mode, &cp);
   if (st != TREEPO_OK) return st;
   const Plan& p = cp->plan;
-  *n_items = static_cast<int32_t>(p.items.size());
+  *n_pieces = static_cast<int32_t>(p.pieces.size());
   *n_rowsets = static_cast<int32_t>(p.rowsets.size());
   *n_tiles = static_cast<int32_t>(p.tiles.size());
-  if (items && rowsets && tiles) {
-    std::memcpy(items, p.items.data(), p.items.size() * sizeof(treepo::Item));
+  *n_streams = static_cast<int32_t>(p.streams.size());
+  if (pieces && rowsets && tiles) {
+    std::memcpy(pieces, p.pieces.data(), p.pieces.size() * sizeof(treepo::Piece));
     std::memcpy(rowsets, p.rowsets.data(), p.rowsets.size() * sizeof(int32_t));
     std::memcpy(tiles, p.tiles.data(), p.tiles.size() * sizeof(treepo::Tile));
   }
   return TREEPO_OK;
-}
-
-int32_t treepo_set_option(treepo_ctx* ctx, int32_t option, int32_t value) {
-  if (!ctx) return TREEPO_EINVAL;
-  switch (option) {
-    case TREEPO_OPT_VALU_MAX_ROWS:
-      if (value < 0 || value > 8) return fail(ctx, TREEPO_EINVAL, "VALU row limit must be in 0..8");
-      if (ctx->params.valu_max_rows != value) {
-        ctx->params.valu_max_rows = value;
-        ctx->plans.clear();
-      }
-      return TREEPO_OK;
-    default:
-      return fail(ctx, TREEPO_EINVAL, "unknown option");
-  }
-}
-
-int32_t treepo_get_option(treepo_ctx* ctx, int32_t option, int32_t* value) {
-  if (!ctx || !value) return TREEPO_EINVAL;
-  switch (option) {
-    case TREEPO_OPT_VALU_MAX_ROWS: *value = ctx->params.valu_max_rows; return TREEPO_OK;
-    default: return fail(ctx, TREEPO_EINVAL, "unknown option");
-  }
 }
 
 int32_t treepo_set_profiling(treepo_ctx* ctx, int32_t enable) {

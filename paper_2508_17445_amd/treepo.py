@@ -22,10 +22,10 @@ LIB_PATH = os.environ.get("TREEPO_LIBRARY") or os.path.join(HERE, "libtreepo.so"
 OK, EINVAL, ENOMEM, EFULL, EFROZEN, EEMPTY, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 MODE_TREE, MODE_NAIVE = 0, 1
 KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE = 0, 1, 2
-OPT_VALU_MAX_ROWS = 0
 NODE_FIELDS = ("parent", "depth", "start", "len", "cap", "block_begin", "n_blocks", "tree_id")
 BLOCK_TOKENS = 64
-ITEM_FIELDS = 12
+PIECE_FIELDS = 16
+TILE_FIELDS = 4
 
 _i32 = ctypes.c_int32
 _i64 = ctypes.c_int64
@@ -72,9 +72,7 @@ def load_library(path: str = LIB_PATH):
         "treepo_export_nodes": (_i32, [_p, _pi32, _i32, _pi32]),
         "treepo_export_chains": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
         "treepo_export_desc": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
-        "treepo_export_plan": (_i32, [_p, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
-        "treepo_set_option": (_i32, [_p, _i32, _i32]),
-        "treepo_get_option": (_i32, [_p, _i32, _pi32]),
+        "treepo_export_plan": (_i32, [_p, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
         "treepo_set_profiling": (_i32, [_p, _i32]),
         "treepo_profile_read": (_i32, [_p, _i32, ctypes.POINTER(ctypes.c_double), _pi64]),
         "treepo_strerror": (ctypes.c_char_p, [_i32]),
@@ -243,27 +241,21 @@ class Context:
         return nodes[:nn.value], off, desc[:tot.value]
 
     def export_plan(self, leaves, mode: int = MODE_TREE):
+        """(pieces [n, PIECE_FIELDS], rowsets, tiles [m, TILE_FIELDS], n_streams)."""
         lv = _arr32(leaves)
-        ni, nr, nt = _i32(), _i32(), _i32()
-        z = ctypes.POINTER(ctypes.c_int32)()
+        ni, nr, nt, ns = _i32(), _i32(), _i32(), _i32()
+        z = ctypes.cast(None, _pi32)
         self._check(self.lib.treepo_export_plan(self.h, len(lv), _ptr32(lv), mode, z, z, z, ctypes.byref(ni),
-                                                ctypes.byref(nr), ctypes.byref(nt)), "treepo_export_plan")
-        items = np.zeros((max(ni.value, 1), ITEM_FIELDS), np.int32)
-        rowsets = np.zeros(max(nr.value, 1), np.int32)
-        tiles = np.zeros((max(nt.value, 1), 4), np.int32)
-        self._check(self.lib.treepo_export_plan(self.h, len(lv), _ptr32(lv), mode, _ptr32(items), _ptr32(rowsets),
-                                                _ptr32(tiles), ctypes.byref(ni), ctypes.byref(nr), ctypes.byref(nt)),
+                                                ctypes.byref(nr), ctypes.byref(nt), ctypes.byref(ns)),
                     "treepo_export_plan")
-        return items[:ni.value], rowsets[:nr.value], tiles[:nt.value]
-
-    # ---- schedule options ----------------------------------------------------
-    def set_option(self, option: int, value: int):
-        self._check(self.lib.treepo_set_option(self.h, option, value), "treepo_set_option")
-
-    def get_option(self, option: int) -> int:
-        v = _i32()
-        self._check(self.lib.treepo_get_option(self.h, option, ctypes.byref(v)), "treepo_get_option")
-        return v.value
+        pieces = np.zeros((max(ni.value, 1), PIECE_FIELDS), np.int32)
+        rowsets = np.zeros(max(nr.value, 1), np.int32)
+        tiles = np.zeros((max(nt.value, 1), TILE_FIELDS), np.int32)
+        self._check(self.lib.treepo_export_plan(self.h, len(lv), _ptr32(lv), mode, _ptr32(pieces), _ptr32(rowsets),
+                                                _ptr32(tiles), ctypes.byref(ni), ctypes.byref(nr), ctypes.byref(nt),
+                                                ctypes.byref(ns)),
+                    "treepo_export_plan")
+        return pieces[:ni.value], rowsets[:nr.value], tiles[:nt.value], ns.value
 
     # ---- timing ------------------------------------------------------------
     def set_profiling(self, enable: bool):

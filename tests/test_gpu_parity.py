@@ -6,9 +6,7 @@ compared in full; the large ones at full size on sampled leaves that the
 oracle computes one by one.  Both the cascade (tree) path and the per-leaf
 baseline are checked, plus determinism and edge cases (ragged tails,
 zero-length nodes, one-token chains, duplicate and interior leaves, GQA
-group sizes from 1 to 48, D = 64 and 128).  The small cases run under both
-partial-kernel schedules: every item on MFMA, and items of up to 8 query rows
-on the wavefront-shuffle (VALU) path.
+group sizes from 1 to 48, D = 64 and 128).
 """
 
 from __future__ import annotations
@@ -51,24 +49,15 @@ def _check(dt, mode, positions=None, tag=""):
     return out
 
 
-def _dt(cfg_id=None, cfg=None, log=None, valu_rows=None, **kw):
-    from paper_2508_17445_amd import OPT_VALU_MAX_ROWS
+def _dt(cfg_id=None, cfg=None, log=None, **kw):
     from workloads.device import DeviceTree
-    print(f"[build cfg={cfg_id or (cfg and cfg.name)} valu_rows={valu_rows}]", flush=True)
-    dt = DeviceTree(cfg_id=cfg_id, cfg=cfg, log=log, keep_host_data=True, **kw)
-    if valu_rows is not None:
-        dt.ctx.set_option(OPT_VALU_MAX_ROWS, valu_rows)
-        assert dt.ctx.get_option(OPT_VALU_MAX_ROWS) == valu_rows
-    return dt
+    print(f"[build cfg={cfg_id or (cfg and cfg.name)}]", flush=True)
+    return DeviceTree(cfg_id=cfg_id, cfg=cfg, log=log, keep_host_data=True, **kw)
 
 
-SCHEDULES = pytest.mark.parametrize("valu_rows", [0, 8], ids=["mfma", "valu8"])
-
-
-@SCHEDULES
 @pytest.mark.parametrize("cfg_id", [1, 2])
-def test_small_configs_full(cfg_id, valu_rows):
-    dt = _dt(cfg_id, valu_rows=valu_rows)
+def test_small_configs_full(cfg_id):
+    dt = _dt(cfg_id)
     for mode in (0, 1):
         _check(dt, mode, tag=f"cfg{cfg_id}")
 
@@ -99,19 +88,17 @@ def _random_cfg(seed, hq, hkv, d):
     (6, 40, 8, 128), (7, 16, 2, 64), (8, 5, 1, 128), (9, 3, 3, 64), (10, 2, 1, 128),
     (11, 32, 2, 128), (12, 48, 1, 64), (13, 14, 1, 128), (14, 12, 1, 64),
 ])
-@SCHEDULES
-def test_random_trees(seed, hq, hkv, d, valu_rows):
+def test_random_trees(seed, hq, hkv, d):
     ops, leaves, rows, _ = random_tiny_tree(seed, max_leaves=10, max_tokens=400)
     log = _Log(ops, leaves or [0], rows)
     log.n_nodes = len(rows)
     cfg = _random_cfg(seed, hq, hkv, d)
-    dt = _dt(cfg=cfg, log=log, valu_rows=valu_rows)
+    dt = _dt(cfg=cfg, log=log)
     for mode in (0, 1):
         _check(dt, mode, tag=f"rand{seed}")
 
 
-@SCHEDULES
-def test_ragged_and_degenerate_shapes(valu_rows):
+def test_ragged_and_degenerate_shapes():
     """One-token chains, a leaf whose own node is empty, tails of 1 and 63
     tokens, a chain crossing many partial tiles, an interior node decoded as a
     leaf, and a 64-token-aligned chain."""
@@ -125,7 +112,7 @@ def test_ragged_and_degenerate_shapes(valu_rows):
     log = _Log(ops, leaves, rows)
     log.n_nodes = 8
     for (hq, hkv, d) in ((28, 4, 128), (4, 1, 64)):
-        dt = _dt(cfg=_random_cfg(77, hq, hkv, d), log=log, valu_rows=valu_rows)
+        dt = _dt(cfg=_random_cfg(77, hq, hkv, d), log=log)
         for mode in (0, 1):
             _check(dt, mode, tag=f"ragged-d{d}")
 

@@ -59,32 +59,61 @@ def test_kv_slots_follow_block_reservation():
     assert list(ctx.kv_slots([a], [2])) == [138, 139]
 
 
+SPLIT_MAX_ROWS = 32      # pieces up to this many rows write two partial rows per query row
+MAX_STREAM_TILES = 256
+
+
+def _tile_cost(rows):
+    return 1.0 if rows <= 32 else 1.4 if rows <= 64 else 2.0
+
+
 def _plan_checks(ctx, model, leaves, mode):
-    items, rowsets, tiles = ctx.export_plan(leaves, mode)
-    G = ctx.cfg.num_q_heads // ctx.cfg.num_kv_heads
-    covered = {x: [] for x in range(len(leaves))}
-    for it in items:
-        kind, rb, nl, tb, te, pbase, rows, run = it[:8]
-        assert rows == nl * G and te > tb and nl >= 1
-        for f in range(3):   # the first tiles' half-block sources ride in the record
-            want_src = 2 * tiles[tb + f][0] + (tiles[tb + f][2] & 1) if tb + f < te else -1
-            assert it[8 + f] == want_src
+    pieces, rowsets, tiles, n_streams = ctx.export_plan(leaves, mode)
+    hkv = ctx.cfg.num_kv_heads
+    G = ctx.cfg.num_q_heads // hkv
+    covered = {(x, g): [] for x in range(len(leaves)) for g in range(hkv)}
+    spans = []
+    stream_next = {}
+    seg_next = {}
+    for pc in pieces:
+        rb, nl, rows, g, stile, nt, pbase, seg, run, stream, ptile, nq = pc[:12]
+        assert rows == nl * G and nt >= 1 and nl >= 1 and 0 <= g < hkv and rows <= 128
+        assert 0 <= stream < n_streams and (pc[12:] == 0).all()
+        assert nq == -(-rows // 64)          # 64 query rows per query tile
+        # pieces of a stream are consecutive and tile its list from 0:
+        # the piece's query tiles, then its KV tiles
+        assert stile == stream_next.get(stream, 0)
+        stream_next[stream] = stile + nq + nt
+        assert stile + nq + nt <= MAX_STREAM_TILES
+        assert seg == seg_next.get(stream, 0)
+        seg_next[stream] = seg + nl
+        assert seg + nl <= 256
+        spans.append((pbase, 2 * rows if rows <= SPLIT_MAX_ROWS else rows))
         for pos in rowsets[rb:rb + nl]:
-            for t in tiles[tb:te]:
-                covered[pos].append(tuple(t))
+            for t in tiles[ptile:ptile + nt]:
+                covered[(pos, g)].append(tuple(t))
+    assert sorted(stream_next) == list(range(n_streams))
     for pos, x in enumerate(leaves):
-        got = sorted(covered[pos])
         want = []
         for n in model.chain(x):
             ln = model.nodes[n]["len"]
             for k in range((ln + 31) // 32):     # 32-token tiles, two per 64-token block
                 want.append((model.nodes[n]["block_begin"] + k // 2, n, k, min(32, ln - 32 * k)))
-        assert got == sorted(want), (mode, pos)
+        for g in range(hkv):
+            assert sorted(covered[(pos, g)]) == sorted(want), (mode, pos, g)
     # partial rows are laid out back to back without overlap
-    bases = sorted((it[5], it[6] * ctx.cfg.num_kv_heads) for it in items)
-    for (b0, s0), (b1, _) in zip(bases, bases[1:]):
+    spans.sort()
+    assert spans[0][0] == 0
+    for (b0, s0), (b1, _) in zip(spans, spans[1:]):
         assert b0 + s0 == b1
-    return items, tiles
+    return pieces, tiles, n_streams
+
+
+def _stream_costs(pieces, n_streams):
+    cost = np.zeros(n_streams)
+    for pc in pieces:
+        cost[pc[9]] += pc[5] * _tile_cost(pc[2]) + 0.25 * pc[11]
+    return cost
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
@@ -95,14 +124,33 @@ def test_plan_covers_each_chain_token_once(cfg):
     ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
     replay_host(ctx, log)
     model = oracle_model(log)
-    items_t, tiles_t = _plan_checks(ctx, model, log.leaves, 0)
-    items_n, tiles_n = _plan_checks(ctx, model, log.leaves, 1)
+    p_t, tiles_t, _ = _plan_checks(ctx, model, log.leaves, 0)
+    p_n, tiles_n, _ = _plan_checks(ctx, model, log.leaves, 1)
     # the tree plan streams every node once per leaf group; the naive plan once per leaf
-    tree_tok = sum(int(t[3]) for it in items_t for t in tiles_t[it[3]:it[4]])
-    naive_tok = sum(int(t[3]) for it in items_n for t in tiles_n[it[3]:it[4]])
-    logical = sum(model.chain_len(x) for x in log.leaves)
+    tree_tok = sum(int(t[3]) for pc in p_t for t in tiles_t[pc[10]:pc[10] + pc[5]])
+    naive_tok = sum(int(t[3]) for pc in p_n for t in tiles_n[pc[10]:pc[10] + pc[5]])
+    logical = sum(model.chain_len(x) for x in log.leaves) * c.hkv
     assert naive_tok == logical
     assert tree_tok <= naive_tok
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_streams_are_balanced(cfg):
+    """One stream per resident workgroup slot (512), equal estimated cost to
+    within about two tiles."""
+    log = build_call_log(cfg)
+    from workloads import CONFIGS
+    c = CONFIGS[cfg]
+    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    replay_host(ctx, log)
+    model = oracle_model(log)
+    for mode in (0, 1):
+        pieces, tiles, n_streams = _plan_checks(ctx, model, log.leaves, mode)
+        total = len(tiles)
+        rounds = -(-total // (512 * 192))
+        assert n_streams <= min(total, 512 * rounds) and n_streams >= 0.95 * min(total, 512 * rounds)
+        cost = _stream_costs(pieces, n_streams)
+        assert cost.max() <= cost.mean() + 2 * 2.0 + 1.0, (mode, cost.mean(), cost.max())
 
 
 def test_duplicate_and_interior_leaves():
@@ -115,33 +163,3 @@ def test_duplicate_and_interior_leaves():
     model = oracle_model(log)
     _compare(ctx, model, leaves)
     _plan_checks(ctx, model, leaves, 0)
-
-
-def test_schedule_option_sets_item_kinds():
-    """VALU_MAX_ROWS moves items between the shuffle and MFMA partials; the
-    plan's coverage is unchanged and out-of-range values are rejected."""
-    from paper_2508_17445_amd import OPT_VALU_MAX_ROWS, TreePOError
-    from workloads import CONFIGS
-    log = build_call_log(2)
-    c = CONFIGS[2]
-    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
-    replay_host(ctx, log)
-    model = oracle_model(log)
-    kinds = {}
-    for v in (0, 8):
-        ctx.set_option(OPT_VALU_MAX_ROWS, v)
-        assert ctx.get_option(OPT_VALU_MAX_ROWS) == v
-        items, _ = _plan_checks(ctx, model, log.leaves, 0)
-        kinds[v] = items[:, 0]
-        if v == 0:
-            assert (items[:, 0] == 1).all()
-        else:
-            # VALU items are exactly those of at most 8 rows, and come first
-            assert ((items[:, 0] == 0) == (items[:, 6] <= 8)).all()
-            assert (np.diff(items[:, 0]) >= 0).all()
-    assert (kinds[8] == 0).any()
-    for bad in (-1, 9):
-        with pytest.raises(TreePOError):
-            ctx.set_option(OPT_VALU_MAX_ROWS, bad)
-    with pytest.raises(TreePOError):
-        ctx.set_option(12345, 0)
