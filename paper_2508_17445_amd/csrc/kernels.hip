@@ -200,16 +200,11 @@ __device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int ntot, int k
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
                                                  0, 0, 0);
-}
-__device__ __forceinline__ f32x4 mfma16k16(const uint2& a, const uint2& b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a), __builtin_bit_cast(s16x4, b), c,
-                                                   0, 0, 0);
 }
 
 // QK: S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 K rows, B = Q^T).  The
@@ -255,29 +250,31 @@ __device__ __forceinline__ uint2 mask_v4(uint2 v, int tok0, int valid) {
   return v;
 }
 
-// ---- token-split piece (at most 32 rows) -----------------------------------------
+// ---- column-split piece (at most 32 rows) ------------------------------------------
 //
 // One or two 16-row blocks: one leaf's GQA group, or a few leaves of a shared
-// node.  Splitting rows over waves would leave most waves idle, so the tile is
-// split by tokens instead: wave w takes row block w/2 and token block b = w%2
-// of every tile -- the 16 tokens tau(b, 0..15) -- and keeps its own
-// online-softmax state, written as its own partial rows (no cross-wave merge).
-//   QK: four MFMAs per row block; each lane's four scores are the consecutive
-//       tokens 8(lane/16) + 4b + 0..3.
-//   PV: O^T += V^T P^T with v_mfma_f32_16x16x16_bf16: the B operand (four
-//       tokens x row) is exactly the lane's four scores, the A operand four
-//       consecutive tokens of one V^T row (8 bytes).
-template <int D>
-__device__ __forceinline__ void split_piece(TREEPO_PARTIAL_PARAMS, const int32_t* __restrict__ pc, int ntot,
-                                            uint32_t buf0, Smem<D>& sm) {
-  constexpr int kKS = D / 32;  // QK k-steps
-  constexpr int kDB = D / 16;  // PV output d-blocks
+// node.  Splitting rows over waves would leave most waves idle, so the waves
+// of a row block split the output columns instead: wave w takes row block
+// w / DSPLIT and d columns [D/DSPLIT * (w % DSPLIT), +D/DSPLIT) (DSPLIT = 4 for
+// one row block, 2 for two).  Every wave scores all 32 tokens of the tile for
+// its rows -- the waves of a row block compute the same scores and softmax
+// state bit for bit -- and accumulates its own slice of O, so each query row
+// gets one partial with no cross-wave merge.
+//   QK: S^T = K Q^T, eight MFMAs (two token blocks x D/32 k-steps).
+//   PV: O^T += V^T P^T with v_mfma_f32_16x16x32_bf16 over all 32 tokens for
+//       the wave's d-blocks (A = 16 d-rows of V^T, B = P^T: the lane's eight
+//       scores, tokens 8(lane/16) + 0..7).
+template <int D, int DSPLIT>
+__device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const int32_t* __restrict__ pc, int ntot,
+                                             uint32_t buf0, Smem<D>& sm) {
+  constexpr int kKS = D / 32;             // QK k-steps
+  constexpr int kDBw = D / 16 / DSPLIT;   // PV output d-blocks of this wave
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int a = lane >> 4;    // lane group
   const int r16 = lane & 15;  // row within the 16-row block
-  const int rb = wave >> 1;   // row block
-  const int tb = wave & 1;    // token block
+  const int rb = wave / DSPLIT;
+  const int db0 = (wave % DSPLIT) * kDBw;
   const int rows = pc[2], k0 = pc[4], nk = pc[5], pbase = pc[6];
   const bool active = 16 * rb < rows;  // wave-uniform
   const int m = 16 * rb + r16;         // this lane's query row
@@ -292,12 +289,11 @@ __device__ __forceinline__ void split_piece(TREEPO_PARTIAL_PARAMS, const int32_t
     for (int ks = 0; ks < kKS; ++ks) qb[ks] = m < rows ? qt[4 * ks + a] : make_uint4(0, 0, 0, 0);
   }
 
-  f32x4 acc[kDB];
+  f32x4 acc[kDBw];
 #pragma unroll
-  for (int db = 0; db < kDB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int db = 0; db < kDBw; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_ref = -INFINITY;  // per row (equal on the row's four lane groups)
   float l_sum = 0.f;        // per lane: this lane's tokens only
-  const int tok0 = 8 * a + 4 * tb;  // first of the lane's four tokens
 
   for (int k = k0 + 1; k <= k0 + nk; ++k) {
     wait_tile<D>(k, ntot);
@@ -306,25 +302,28 @@ __device__ __forceinline__ void split_piece(TREEPO_PARTIAL_PARAMS, const int32_t
     if (!active) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
-    // ---- S^T = K Q^T for the wave's 16 tokens
-    f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
-    {
-      const int tok = tau(tb, r16);
+    // ---- S^T = K Q^T for the 32 tokens
+    f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-      for (int ks = 0; ks < kKS; ++ks) {
+    for (int ks = 0; ks < kKS; ++ks) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int tok = tau(b, r16);
         const int c = 4 * ks + a;
         const uint4 ka = *reinterpret_cast<const uint4*>(kt + tok * (D * 2) + ((c ^ k_swz(tok)) << 4));
-        S = mfma16(ka, qb[ks], S);
+        S[b] = mfma16(ka, qb[ks], S[b]);
       }
     }
     // ---- scores (log2 units), masked past the node's length; lazy reference
-    float x[4];
+    float x[2][4];
     float mx = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = tok0 + e < valid ? S[e] * sc.scale_log2 : -INFINITY;
-      mx = fmaxf(mx, x[e]);
-    }
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[b][e] = 8 * a + 4 * b + e < valid ? S[b][e] * sc.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, x[b][e]);
+      }
     if (__builtin_amdgcn_ballot_w64(mx > m_ref + kLazyMaxSlack) != 0) {
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -333,28 +332,34 @@ __device__ __forceinline__ void split_piece(TREEPO_PARTIAL_PARAMS, const int32_t
       m_ref = mn;
       l_sum *= alpha;
 #pragma unroll
-      for (int db = 0; db < kDB; ++db) acc[db] *= alpha;
+      for (int db = 0; db < kDBw; ++db) acc[db] *= alpha;
     }
-    uint2 P, PL;
-    l_sum += softmax_p4(x, m_ref, P, PL);
-    // ---- O^T += V^T P^T
+    uint2 p0, pl0, p1, pl1;
+    l_sum += softmax_p4(x[0], m_ref, p0, pl0) + softmax_p4(x[1], m_ref, p1, pl1);
+    const uint4 P = make_uint4(p0.x, p0.y, p1.x, p1.y), PL = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
+    // ---- O^T += V^T P^T for the wave's d-blocks
 #pragma unroll
-    for (int db = 0; db < kDB; ++db) {
-      const int d = 16 * db + r16;
-      uint2 va = *reinterpret_cast<const uint2*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4) + tb * 8);
-      if (valid < kSub) va = mask_v4(va, tok0, valid);
-      acc[db] = mfma16k16(va, PL, mfma16k16(va, P, acc[db]));
+    for (int db = 0; db < kDBw; ++db) {
+      const int d = 16 * (db0 + db) + r16;
+      uint4 va = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
+      if (valid < kSub) {
+        const uint2 lo = mask_v4(make_uint2(va.x, va.y), 8 * a, valid);
+        const uint2 hi = mask_v4(make_uint2(va.z, va.w), 8 * a + 4, valid);
+        va = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+      acc[db] = mfma16(va, PL, mfma16(va, P, acc[db]));
     }
   }
 
-  // ---- partial rows of this wave's token half
+  // ---- partial rows: this wave's column slice
   l_sum += __shfl_xor(l_sum, 16);
   l_sum += __shfl_xor(l_sum, 32);
   if (active && m < rows) {
-    const int64_t slot = static_cast<int64_t>(pbase) + tb * rows + m;
+    const int64_t slot = static_cast<int64_t>(pbase) + m;
 #pragma unroll
-    for (int db = 0; db < kDB; ++db) *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * db + 4 * a) = acc[db];
-    if (a == 0) {
+    for (int db = 0; db < kDBw; ++db)
+      *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * (db0 + db) + 4 * a) = acc[db];
+    if (a == 0 && db0 == 0) {
       part_ml[slot * 2 + 0] = m_ref;
       part_ml[slot * 2 + 1] = l_sum;
     }
@@ -537,8 +542,10 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(TREEPO_PAR
   for (int pi = pb; pi < pe; ++pi) {
     const int32_t* pc = pieces + kPieceInts * pi;
     const int rows = pc[2];
-    if (rows <= kSplitMaxRows) {
-      split_piece<D>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);
+    if (rows <= 16) {
+      dsplit_piece<D, 4>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);
+    } else if (rows <= kSplitMaxRows) {
+      dsplit_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);
     } else {
       const int nrb = (((rows + 15) >> 4) + 3) >> 2;
       if (nrb == 1)

@@ -358,7 +358,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         }
         st->n_tiles += nq;
         acc += kQTileCost * nq;
-        const int64_t prow = rows <= kSplitMaxRows ? 2 * static_cast<int64_t>(rows) : rows;
+        const int64_t prow = rows;
         if (partial + prow > INT32_MAX) {
           if (err) *err = "too many partial rows";
           return kEUnsupported;
@@ -391,7 +391,6 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       for (int32_t j = 0; j < pc.n_leaves; ++j) {
         const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
         f(key, pc.partial_base + j * G);
-        if (pc.rows <= kSplitMaxRows) f(key, pc.partial_base + pc.rows + j * G);
       }
     }
   };

@@ -97,17 +97,15 @@ constexpr int32_t kMaxStreamTiles = 256;
 constexpr int32_t kMaxStreamSegs = 256;
 // Query rows carried by one query tile (a tile buffer holds 64 rows of D).
 constexpr int32_t kQTileRows = 64;
-// Query rows of a piece that the token-split kernel path handles (two 16-row
+// Query rows of a piece that the column-split kernel path handles (two 16-row
 // blocks); larger row groups use the row-split path.
 constexpr int32_t kSplitMaxRows = 32;
 
 // A piece: consecutive tiles of one (run, leaf group, KV head) sequence, all
 // in one stream.  Rows are (leaf j of the group, head h' of the GQA group):
 // row = j * G + h'.  In its stream's tile list a piece is n_qtiles query tiles
-// (its query rows, 64 per tile) followed by n_tiles KV tiles.  A token-split
-// piece (rows <= 32) writes two partial rows per query row (one per token half
-// of each tile): rows [base, base + rows) and [base + rows, base + 2 rows); a
-// row-split piece writes rows partial rows.
+// (its query rows, 64 per tile) followed by n_tiles KV tiles.  It writes one
+// partial row per query row: rows [partial_base, partial_base + rows).
 struct Piece {
   int32_t rowset_begin;  // index into Plan::rowsets (the group's call positions)
   int32_t n_leaves;

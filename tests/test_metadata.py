@@ -59,7 +59,6 @@ def test_kv_slots_follow_block_reservation():
     assert list(ctx.kv_slots([a], [2])) == [138, 139]
 
 
-SPLIT_MAX_ROWS = 32      # pieces up to this many rows write two partial rows per query row
 MAX_STREAM_TILES = 256
 
 
@@ -88,7 +87,7 @@ def _plan_checks(ctx, model, leaves, mode):
         assert seg == seg_next.get(stream, 0)
         seg_next[stream] = seg + nl
         assert seg + nl <= 256
-        spans.append((pbase, 2 * rows if rows <= SPLIT_MAX_ROWS else rows))
+        spans.append((pbase, rows))
         for pos in rowsets[rb:rb + nl]:
             for t in tiles[ptile:ptile + nt]:
                 covered[(pos, g)].append(tuple(t))
