@@ -33,6 +33,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+# HBM bytes per partial-kernel launch measured with rocprofv3 counters
+# (FETCH_SIZE and WRITE_SIZE passes, calibrated on a plain copy kernel); the
+# summary records the hash of the kernel source it was taken on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "partial_kernel_config2_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2508_17445_amd", "csrc", "kernels.hip")
 METRIC = "tree-decode leaf-token-steps/sec + achieved HBM GB/s on unique KV (1 MI355X)"
 
 
@@ -50,6 +55,21 @@ def _parse():
                     help="short run for hardware counters: a few decode steps of the workload, then one "
                          "1 GiB device copy whose byte counters calibrate the kernels'")
     return ap.parse_args()
+
+
+def _measured_traffic(config_id):
+    """Counter-measured HBM bytes per partial-kernel launch, or None when no
+    summary exists for this workload or the kernel source changed since."""
+    import hashlib
+    try:
+        kv = dict(line.split(":", 1) for line in open(TRAFFIC_FILE).read().splitlines() if ":" in line)
+        kv = {k.strip(): v.strip() for k, v in kv.items()}
+        src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        if kv.get("kernels.hip sha256") != src or int(kv.get("config", -1)) != config_id:
+            return None
+        return int(kv["traffic bytes per launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def _ensure_built():
@@ -242,7 +262,7 @@ def main():
         },
         "achieved_unique_kv_GBps_step": round(achieved_step, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved_kern, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(achieved_kern / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "frac": round(achieved_kern / PEAK_HBM_GBPS, 4), "traffic": _measured_traffic(args.config),
                      "kernel": "partial_kernel<128>", "kernel_avg_ms": round(kern_ms, 5),
                      "launches_per_step": launches,
                      "algorithmic_bytes_per_launch": uniq_bytes},
