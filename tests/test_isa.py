@@ -1,0 +1,63 @@
+"""Machine-code invariants of the node-partial kernel (CPU: compiles only).
+
+The kernel's load pipeline is counted by hand: tiles are global->LDS loads
+waited for with explicit vmcnt barriers that allow the two newest tiles to
+stay in flight.  That only holds if the compiler adds no vector-memory loads
+or waits of its own and spills nothing to scratch (scratch traffic is vector
+memory too); these tests read the gfx950 assembly built with the library's
+flags and check exactly that.
+"""
+
+from __future__ import annotations
+
+import re
+import sys
+
+import pytest
+
+from tests.conftest import ROOT
+
+sys.path.insert(0, f"{ROOT}/paper_2508_17445_amd")
+
+
+@pytest.fixture(scope="module")
+def partial_kernels(tmp_path_factory):
+    import build
+    asm = open(build.device_asm("kernels.hip", str(tmp_path_factory.mktemp("asm")))).read().split("\n")
+    out = {}
+    for i, line in enumerate(asm):
+        m = re.match(r"^(_ZN6treepo\S*partial_kernelILi(\d+)\S*):", line)
+        if m:
+            end = next(j for j in range(i, len(asm)) if asm[j].startswith(".Lfunc_end"))
+            body = [x.strip() for x in asm[i + 1:end]]
+            out[int(m.group(2))] = [x for x in body if x and not x.startswith((";", "."))]
+    return out, "\n".join(asm)
+
+
+def test_both_head_dims_present(partial_kernels):
+    kernels, _ = partial_kernels
+    assert sorted(kernels) == [64, 128]
+
+
+def test_only_global_to_lds_loads(partial_kernels):
+    kernels, _ = partial_kernels
+    for d, body in kernels.items():
+        loads = [x for x in body if re.match(r"^(global_load|buffer_load|flat_load|scratch_|global_atomic)", x)
+                 and not x.startswith("global_load_lds_dwordx4")]
+        assert not loads, (d, loads[:5])
+        assert any(x.startswith("global_load_lds_dwordx4") and x.endswith(" nt") for x in body), d
+
+
+def test_no_scratch(partial_kernels):
+    _, meta = partial_kernels
+    sizes = re.findall(r"\.private_segment_fixed_size:\s+(\d+)\n(?:.*\n){0,40}?\s+\.symbol:\s+\S*partial_kernel", meta)
+    assert len(sizes) == 2 and all(int(s) == 0 for s in sizes), sizes
+
+
+def test_every_vector_memory_wait_is_a_pipeline_barrier(partial_kernels):
+    kernels, _ = partial_kernels
+    for d, body in kernels.items():
+        for i, x in enumerate(body):
+            if x.startswith("s_waitcnt") and "vmcnt" in x:
+                assert re.match(r"^s_waitcnt vmcnt\(\d+\) lgkmcnt\(0\)$", x), (d, x)
+                assert body[i + 1] == "s_barrier", (d, body[i:i + 2])
