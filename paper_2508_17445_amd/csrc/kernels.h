@@ -25,8 +25,8 @@ struct DecodeArgs {
   const int32_t* segs;     // query segment offsets
   float* part_o;           // fp32 [partial_rows][D], unnormalised
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
-  const int32_t* leaf_off; // [n_leaves * Hkv + 1]
-  const int32_t* entries;
+  const int32_t* comb;     // per (leaf, KV head): count, then the partial rows to merge
+  int32_t comb_stride;
   int32_t n_leaves;
   float* out;              // fp32 [n_leaves][Hq][D]
   float* lse;              // fp32 [n_leaves][Hq] or null

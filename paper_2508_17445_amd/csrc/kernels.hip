@@ -559,16 +559,16 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(TREEPO_PAR
 // ---- combine ------------------------------------------------------------------
 //
 // One wave per (leaf, query head h = g G + h'): over the partial rows
-// entries[e] + h' of (leaf, g), m* = max m_i, L = sum l_i 2^(m_i - m*),
+// comb[1 + e] + h' of (leaf, g), m* = max m_i, L = sum l_i 2^(m_i - m*),
 // out = sum 2^(m_i - m*) O_i / L, lse = (m* + log2 L) ln 2.  Partials without
-// tokens (m = -inf) contribute nothing.  Entries are taken 64 at a time: the
-// lanes load their (m, l) pairs in parallel, then the weights are broadcast
-// with readlane while every lane accumulates its d-slice of the O rows, 16
-// rows per batch of independent loads.  The order of the sum is fixed by the
-// plan, so results are deterministic.
+// tokens (m = -inf) contribute nothing.  The merge list has a fixed stride, so
+// its count and rows arrive in one round of loads; the (m, l) pairs (one per
+// lane) and the first 16 O rows (every lane its d-slice) are then loaded
+// together, so a leaf with up to 16 partials costs two memory round trips.
+// Later rows follow in batches of 16 independent loads.  The order of the sum
+// is fixed by the plan, so results are deterministic.
 template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __restrict__ leaf_off,
-                                                           const int32_t* __restrict__ entries,
+__global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __restrict__ comb, int32_t comb_stride,
                                                            const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml,
                                                            float* __restrict__ out, float* __restrict__ lse,
@@ -582,17 +582,25 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
   const int h = gw % hq;
   const int g = h / group;
   const int hp = h % group;
-  const int key = x * hkv + g;
-  const int e0 = leaf_off[key], e1 = leaf_off[key + 1];
+  const int32_t* blk = comb + static_cast<int64_t>(x * hkv + g) * comb_stride;
+  const int n = blk[0];
   float run_m = -INFINITY, run_l = 0.f;
   float o[kPL];
 #pragma unroll
   for (int i = 0; i < kPL; ++i) o[i] = 0.f;
-  for (int base = e0; base < e1; base += 64) {
-    const int cnt = e1 - base < 64 ? e1 - base : 64;
+  for (int base = 0; base < n; base += 64) {
+    const int cnt = n - base < 64 ? n - base : 64;
     const bool mine = lane < cnt;
-    const int e = base + (mine ? lane : 0);
-    const int slot = entries[e] + hp;
+    const int slot = blk[1 + base + (mine ? lane : 0)] + hp;
+    // first batch of O rows, issued with the (m, l) loads
+    float v[kGroup][kPL];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const int k = i < cnt ? i : cnt - 1;
+      const float* po = part_o + static_cast<int64_t>(__builtin_amdgcn_readlane(slot, k)) * D + lane * kPL;
+#pragma unroll
+      for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+    }
     const float mi = mine ? part_ml[2 * static_cast<int64_t>(slot)] : -INFINITY;
     const float li = mine ? part_ml[2 * static_cast<int64_t>(slot) + 1] : 0.f;
     float cm = mi;
@@ -608,16 +616,15 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
 #pragma unroll
     for (int i = 0; i < kPL; ++i) o[i] *= keep;
     run_m = nm;
-    // O rows in groups of 16: all loads of a group are issued before the first
-    // use, so a group costs one memory latency
     for (int k0 = 0; k0 < cnt; k0 += kGroup) {
-      float v[kGroup][kPL];
+      if (k0 > 0) {
 #pragma unroll
-      for (int i = 0; i < kGroup; ++i) {
-        const int k = k0 + i < cnt ? k0 + i : cnt - 1;
-        const float* po = part_o + static_cast<int64_t>(__builtin_amdgcn_readlane(slot, k)) * D + lane * kPL;
+        for (int i = 0; i < kGroup; ++i) {
+          const int k = k0 + i < cnt ? k0 + i : cnt - 1;
+          const float* po = part_o + static_cast<int64_t>(__builtin_amdgcn_readlane(slot, k)) * D + lane * kPL;
 #pragma unroll
-        for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+          for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+        }
       }
 #pragma unroll
       for (int i = 0; i < kGroup; ++i) {
@@ -704,10 +711,10 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   const int64_t waves = static_cast<int64_t>(a.n_leaves) * a.hq;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
   if (a.d == 128)
-    combine_kernel<128><<<grid, kThreads, 0, s>>>(a.leaf_off, a.entries, a.part_o, a.part_ml, a.out, a.lse,
+    combine_kernel<128><<<grid, kThreads, 0, s>>>(a.comb, a.comb_stride, a.part_o, a.part_ml, a.out, a.lse,
                                                   a.n_leaves, a.hq, a.hkv, a.group);
   else
-    combine_kernel<64><<<grid, kThreads, 0, s>>>(a.leaf_off, a.entries, a.part_o, a.part_ml, a.out, a.lse,
+    combine_kernel<64><<<grid, kThreads, 0, s>>>(a.comb, a.comb_stride, a.part_o, a.part_ml, a.out, a.lse,
                                                  a.n_leaves, a.hq, a.hkv, a.group);
   return hipGetLastError();
 }

@@ -383,22 +383,27 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   pad_to(&out->segs, 4, 0);
   out->partial_rows = partial;
 
-  // ---- per (leaf, KV head) merge entries -----------------------------------------
+  // ---- per (leaf, KV head) merge lists -------------------------------------------
   const int64_t nkeys = static_cast<int64_t>(n_leaves) * Hkv;
-  out->leaf_off.assign(nkeys + 1, 0);
-  auto for_each_entry = [&](auto&& f) {
-    for (const Piece& pc : out->pieces) {
-      for (int32_t j = 0; j < pc.n_leaves; ++j) {
-        const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
-        f(key, pc.partial_base + j * G);
-      }
+  std::vector<int32_t> count(nkeys, 0);
+  for (const Piece& pc : out->pieces)
+    for (int32_t j = 0; j < pc.n_leaves; ++j)
+      ++count[static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g];
+  int32_t emax = 1;
+  for (int32_t c : count) emax = std::max(emax, c);
+  out->comb_stride = 1 + emax;
+  if (nkeys * out->comb_stride > INT32_MAX) {
+    if (err) *err = "merge lists too large";
+    return kEUnsupported;
+  }
+  out->comb.assign(nkeys * out->comb_stride, 0);
+  for (const Piece& pc : out->pieces) {
+    for (int32_t j = 0; j < pc.n_leaves; ++j) {
+      const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
+      int32_t* blk = &out->comb[key * out->comb_stride];
+      blk[1 + blk[0]++] = pc.partial_base + j * G;
     }
-  };
-  for_each_entry([&](int64_t key, int32_t) { ++out->leaf_off[key + 1]; });
-  for (int64_t k = 0; k < nkeys; ++k) out->leaf_off[k + 1] += out->leaf_off[k];
-  out->entries.assign(out->leaf_off.back(), 0);
-  std::vector<int32_t> cursor(out->leaf_off.begin(), out->leaf_off.end() - 1);
-  for_each_entry([&](int64_t key, int32_t row) { out->entries[cursor[key]++] = row; });
+  }
   return kOk;
 }
 

@@ -176,10 +176,11 @@ struct Plan {
   // Query segments: element offset in the query tensor of the G rows of one
   // leaf for one KV head (contiguous there), one per (piece, leaf).
   std::vector<int32_t> segs;
-  // Per (leaf x, KV head g): partial rows to merge for query head g * G + h'
-  // are entries[e] + h' for e in [leaf_off[x * Hkv + g], leaf_off[x * Hkv + g + 1]).
-  std::vector<int32_t> leaf_off;
-  std::vector<int32_t> entries;
+  // Per (leaf x, KV head g), key = x * Hkv + g: the partial rows to merge for
+  // query head g * G + h' are comb[key * comb_stride + 1 + e] + h' for
+  // e < comb[key * comb_stride] (fixed stride, so one load finds them).
+  std::vector<int32_t> comb;
+  int32_t comb_stride = 0;
   int64_t partial_rows = 0;
   int64_t unique_kv_tokens = 0;   // tokens streamed per KV head (tree: unique)
   int64_t kv_token_visits = 0;    // tokens streamed, summed over leaf groups (per KV head)

@@ -33,7 +33,7 @@ struct CachedPlan {
   Plan plan;
   std::vector<char> blob;  // host image of the plan region
   size_t off_streams = 0, off_pieces = 0, off_rowsets = 0, off_stiles = 0, off_segs = 0;
-  size_t off_leaf_off = 0, off_entries = 0;
+  size_t off_comb = 0;
   size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;
   uint64_t uid = 0;
   uint64_t last_use = 0;
@@ -198,16 +198,14 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   place(&cp.off_rowsets, p.rowsets.size() * sizeof(int32_t));
   place(&cp.off_stiles, p.stream_tiles.size() * sizeof(treepo::StreamTile));
   place(&cp.off_segs, p.segs.size() * sizeof(int32_t));
-  place(&cp.off_leaf_off, p.leaf_off.size() * sizeof(int32_t));
-  place(&cp.off_entries, p.entries.size() * sizeof(int32_t));
+  place(&cp.off_comb, p.comb.size() * sizeof(int32_t));
   cp.blob.assign(off, 0);
   put(cp.blob, cp.off_streams, p.streams);
   put(cp.blob, cp.off_pieces, p.pieces);
   put(cp.blob, cp.off_rowsets, p.rowsets);
   put(cp.blob, cp.off_stiles, p.stream_tiles);
   put(cp.blob, cp.off_segs, p.segs);
-  put(cp.blob, cp.off_leaf_off, p.leaf_off);
-  put(cp.blob, cp.off_entries, p.entries);
+  put(cp.blob, cp.off_comb, p.comb);
   cp.off_part_o = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
   cp.off_part_ml = off;
@@ -274,8 +272,8 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.segs = reinterpret_cast<const int32_t*>(wsb + cp->off_segs);
   a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
   a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
-  a.leaf_off = reinterpret_cast<const int32_t*>(wsb + cp->off_leaf_off);
-  a.entries = reinterpret_cast<const int32_t*>(wsb + cp->off_entries);
+  a.comb = reinterpret_cast<const int32_t*>(wsb + cp->off_comb);
+  a.comb_stride = p.comb_stride;
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;
