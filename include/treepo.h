@@ -203,9 +203,12 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  * piece is the part of one sequence inside one stream.  Pieces,
  * TREEPO_PIECE_FIELDS int32 each, in stream order:
  *   {rowset_begin, n_leaves, rows, kv_head, stream_tile, n_tiles,
- *    partial_base, q_row, run, stream, plan_tile, 0, 0, 0, 0, 0}
+ *    partial_base, seg_begin, run, stream, plan_tile, n_qtiles, 0, 0, 0, 0}
  * rows = n_leaves * (Hq / Hkv); the piece's leaves are rowsets[rowset_begin ..
- * + n_leaves) (call positions); its tiles are tiles[plan_tile .. + n_tiles),
+ * + n_leaves) (call positions); in its stream's tile list it is n_qtiles
+ * query tiles (64 rows each) from stream_tile on, then n_tiles KV tiles, and
+ * its query segments start at seg_begin there; its KV tiles are
+ * tiles[plan_tile .. + n_tiles),
  * TREEPO_TILE_FIELDS int32 each {block, node, tile_in_node, valid_tokens}:
  * tile k of a node holds its tokens [32k, 32k+32) and lives in pool block
  * block_begin + k/2.  *n_streams receives the stream count.  Pass null arrays
@@ -214,6 +217,21 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
                            int32_t mode, int32_t* pieces, int32_t* rowsets, int32_t* tiles,
                            int32_t* n_pieces, int32_t* n_rowsets, int32_t* n_tiles,
                            int32_t* n_streams);
+
+/* The device copy of the same schedule, as the node-partial kernel reads it:
+ * one block of *block_ints int32 per stream (a multiple of 4; stream s at
+ * s * block_ints, *n_streams blocks):
+ *   {n_pieces, n_tiles, n_segs, 0};
+ *   per piece {rows, stream_tile, n_tiles, partial_base};
+ *   per stream tile {hb, valid}, padded to an even count: a KV tile has
+ *     hb = 2 * (kv_head * num_blocks + block) + tile_in_node % 2 and valid =
+ *     its tokens; a query tile has hb = -1 - (its piece's seg_begin) and
+ *     valid = first_row | (n_rows << 16);
+ *   per query segment, the element offset (x * Hq + kv_head * G) * D of the
+ *     G query rows of the piece's leaf x, padded to a multiple of 4.
+ * Pass a null array to query the sizes only. */
+int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t mode,
+                             int32_t* blocks, int32_t* block_ints, int32_t* n_streams);
 
 /* ---- kernel timing ------------------------------------------------------ */
 

@@ -17,12 +17,9 @@ struct DecodeArgs {
   int32_t hq, hkv, group, d;
   const uint16_t* q;       // bf16 [n_leaves][Hq][D]
   float scale_log2;        // softmax scale * log2(e)
-  const int32_t* streams;  // Stream records
+  const int32_t* blocks;   // stream blocks, block_ints int32 each (layout in tree_core.h)
+  int32_t block_ints;
   int32_t n_streams;
-  const int32_t* pieces;   // Piece records
-  const int32_t* rowsets;
-  const int32_t* stiles;   // StreamTile records
-  const int32_t* segs;     // query segment offsets
   float* part_o;           // fp32 [partial_rows][D], unnormalised
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
   const int32_t* comb;     // per (leaf, KV head): count, then the partial rows to merge

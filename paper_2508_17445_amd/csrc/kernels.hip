@@ -64,8 +64,13 @@ template <int D>
 struct Smem {
   static constexpr int kElems = kSub * D;  // K (or V^T) elements per tile
   uint16_t kv[kNBuf][2 * kElems];
-  int2 tile_meta[kMaxStreamTiles];         // the stream's tile records
-  int32_t segs[kMaxStreamSegs];            // the stream's query segment offsets
+  int32_t blk[kMaxBlockInts];              // the stream's block (pieces, tiles, segments)
+};
+
+// LDS views of the stream block's tables.
+struct BlockTables {
+  const int2* tiles;    // StreamTile records
+  const int32_t* segs;  // query segment offsets
 };
 
 __device__ __forceinline__ int k_swz(int r) { return (r & 3) | ((r >> 1) & 4); }
@@ -140,8 +145,7 @@ __device__ __forceinline__ void wait_tile(int k, int ntot) {
     barrier_tile_landed<0>();
 }
 
-// Kernel arguments: the pointers are passed as separate __restrict__ kernel
-// parameters so that uniform metadata reads become scalar loads.
+// Kernel arguments, passed as separate __restrict__ kernel parameters.
 struct Scalars {
   int32_t hq, hkv, group;
   float scale_log2;
@@ -149,11 +153,8 @@ struct Scalars {
 
 #define TREEPO_PARTIAL_PARAMS                                                         \
   const uint16_t *__restrict__ kpool, const uint16_t *__restrict__ vpool,            \
-      const uint16_t *__restrict__ q, const int32_t *__restrict__ streams,           \
-      const int32_t *__restrict__ pieces, const int32_t *__restrict__ rowsets,       \
-      const int32_t *__restrict__ stiles, const int32_t *__restrict__ segs,          \
-      float *__restrict__ part_o, float *__restrict__ part_ml, Scalars sc
-#define TREEPO_PARTIAL_ARGS kpool, vpool, q, streams, pieces, rowsets, stiles, segs, part_o, part_ml, sc
+      const uint16_t *__restrict__ q, float *__restrict__ part_o, float *__restrict__ part_ml, Scalars sc
+#define TREEPO_PARTIAL_ARGS kpool, vpool, q, part_o, part_ml, sc
 
 // Stages rows [row0, row0 + n) of a piece's queries into the LDS buffer at
 // `dst` as [64][D]: row r of the piece is head h' = r % G of its leaf j = r / G,
@@ -161,7 +162,7 @@ struct Scalars {
 // lane issues the same loads as for a KV tile (rows past n repeat the last row).
 template <int D>
 __device__ __forceinline__ void dma_qtile(const uint16_t* __restrict__ q, int seg_base, int row0, int n, int G,
-                                          const Smem<D>& sm, uint32_t dst, int wave, int lane) {
+                                          const BlockTables& bt, uint32_t dst, int wave, int lane) {
   constexpr int kCPR = D / 8;       // 16-byte chunks per row
   constexpr int kPerWave = D / 32;  // 1 KiB slots per wave
 #pragma unroll
@@ -172,32 +173,37 @@ __device__ __forceinline__ void dma_qtile(const uint16_t* __restrict__ q, int se
     const int row = row0 + (r < n ? r : n - 1);
     const int leaf = row / G;
     const int h = row - leaf * G;
-    const uint16_t* src = q + sm.segs[seg_base + leaf] + h * D + (c % kCPR) * 8;
+    const uint16_t* src = q + bt.segs[seg_base + leaf] + h * D + (c % kCPR) * 8;
     dma16(src, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
   }
 }
 
 // Issues tile k of the stream (KV or query) into buffer k mod 4.
 template <int D>
-__device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, uint32_t buf0, const Smem<D>& sm,
+__device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, uint32_t buf0, const BlockTables& bt,
                                                 int wave, int lane) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
-  const int hb = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].x);
+  const int hb = __builtin_amdgcn_readfirstlane(bt.tiles[k].x);
   const uint32_t dst = buf0 + (k & (kNBuf - 1)) * kBufBytes;
   if (hb >= 0) {
     dma_tile<D>(kpool, vpool, hb, dst, wave, lane);
   } else {
-    const int y = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
-    dma_qtile<D>(q, -1 - hb, y & 0xFFFF, y >> 16, sc.group, sm, dst, wave, lane);
+    const int y = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
+    dma_qtile<D>(q, -1 - hb, y & 0xFFFF, y >> 16, sc.group, bt, dst, wave, lane);
   }
 }
 
 // After tile k is published: prefetch tile k + 3 into the buffer tile k - 1 used.
 template <int D>
-__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int ntot, int k, uint32_t buf0, const Smem<D>& sm,
-                                          int wave, int lane) {
-  if (k + kDepth < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, k + kDepth, buf0, sm, wave, lane);
+__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int ntot, int k, uint32_t buf0,
+                                          const BlockTables& bt, int wave, int lane) {
+  if (k + kDepth < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, k + kDepth, buf0, bt, wave, lane);
 }
+
+// A piece's record in the stream block.
+struct PieceRec {
+  int rows, k0, nk, pbase;
+};
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -265,8 +271,8 @@ __device__ __forceinline__ uint2 mask_v4(uint2 v, int tok0, int valid) {
 //       the wave's d-blocks (A = 16 d-rows of V^T, B = P^T: the lane's eight
 //       scores, tokens 8(lane/16) + 0..7).
 template <int D, int DSPLIT>
-__device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const int32_t* __restrict__ pc, int ntot,
-                                             uint32_t buf0, Smem<D>& sm) {
+__device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceRec& pc, int ntot, uint32_t buf0,
+                                             Smem<D>& sm, const BlockTables& bt) {
   constexpr int kKS = D / 32;             // QK k-steps
   constexpr int kDBw = D / 16 / DSPLIT;   // PV output d-blocks of this wave
   const int lane = threadIdx.x & 63;
@@ -275,14 +281,14 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const int32_
   const int r16 = lane & 15;  // row within the 16-row block
   const int rb = wave / DSPLIT;
   const int db0 = (wave % DSPLIT) * kDBw;
-  const int rows = pc[2], k0 = pc[4], nk = pc[5], pbase = pc[6];
+  const int rows = pc.rows, k0 = pc.k0, nk = pc.nk, pbase = pc.pbase;
   const bool active = 16 * rb < rows;  // wave-uniform
   const int m = 16 * rb + r16;         // this lane's query row
 
   // ---- the piece's query tile: Q^T operands, lane holds row m, d chunk 4 ks + a
   uint4 qb[kKS];
   wait_tile<D>(k0, ntot);
-  dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k0, buf0, sm, wave, lane);
+  dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k0, buf0, bt, wave, lane);
   {
     const uint4* qt = reinterpret_cast<const uint4*>(sm.kv[k0 & (kNBuf - 1)]) + m * (D / 8);
 #pragma unroll
@@ -297,8 +303,8 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const int32_
 
   for (int k = k0 + 1; k <= k0 + nk; ++k) {
     wait_tile<D>(k, ntot);
-    const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k, buf0, sm, wave, lane);
+    const int valid = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k, buf0, bt, wave, lane);
     if (!active) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
@@ -377,15 +383,16 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const int32_
 //   PV: O^T += V^T P^T with v_mfma_f32_16x16x32_bf16 over all 32 tokens (A =
 //       16 d-rows of the transposed V tile, B = P^T: the lane's eight scores).
 template <int D, int NRB>
-__device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const int32_t* __restrict__ pc, int ntot,
-                                           uint32_t buf0, Smem<D>& sm) {
+__device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec& pc, int ntot, uint32_t buf0,
+                                           Smem<D>& sm, const BlockTables& bt) {
   constexpr int kKS = D / 32;
   constexpr int kDB = D / 16;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int a = lane >> 4;
   const int r16 = lane & 15;
-  const int rows = pc[2], k0 = pc[4], nk = pc[5], pbase = pc[6], nq = pc[11];
+  const int rows = pc.rows, k0 = pc.k0, nk = pc.nk, pbase = pc.pbase;
+  const int nq = (rows + kQTileRows - 1) / kQTileRows;
   const int nrb_total = (rows + 15) >> 4;
   const int my_rb = nrb_total > wave ? (nrb_total - wave + 3) >> 2 : 0;  // row blocks of this wave (<= NRB)
 
@@ -396,7 +403,7 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const int32_t*
   for (int i = 0; i < NRB; ++i) {
     if (i >= nq) continue;
     wait_tile<D>(k0 + i, ntot);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k0 + i, buf0, sm, wave, lane);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k0 + i, buf0, bt, wave, lane);
     const int m = 16 * (wave + 4 * i) + r16;
     const uint4* qt =
         reinterpret_cast<const uint4*>(sm.kv[(k0 + i) & (kNBuf - 1)]) + (m - kQTileRows * i) * (D / 8);
@@ -416,8 +423,8 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const int32_t*
 
   for (int k = k0 + nq; k < k0 + nq + nk; ++k) {
     wait_tile<D>(k, ntot);
-    const int valid = __builtin_amdgcn_readfirstlane(sm.tile_meta[k].y);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k, buf0, sm, wave, lane);
+    const int valid = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k, buf0, bt, wave, lane);
     if (my_rb == 0) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
@@ -507,51 +514,50 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const int32_t*
 
 // ---- the node-partial kernel ----------------------------------------------------
 //
-// One workgroup per stream.  Prologue: the stream's tile list and query
-// segment offsets into LDS; then the first three tiles.  The pieces run in
-// order over one continuous tile pipeline: every load is a global->LDS load
-// counted by hand, so no compiler-inserted wait ever drains it.
+// One workgroup per stream.  Prologue: the stream's block (its piece records,
+// tile list and query segment offsets) into LDS with one round of
+// global->LDS loads from an address computed from the workgroup index, so
+// the first tiles are issued one memory round trip after the start; then the
+// first three tiles.  The pieces run in order over one continuous tile
+// pipeline: every load is a global->LDS load counted by hand and every piece
+// record comes from LDS, so no compiler-inserted wait ever drains it.
 template <int D>
-__global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(TREEPO_PARTIAL_PARAMS) {
+__global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int32_t* __restrict__ blocks,
+                                                                     int32_t block_ints, TREEPO_PARTIAL_PARAMS) {
   __shared__ __attribute__((aligned(1024))) Smem<D> sm;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int32_t* sr = streams + kStreamInts * static_cast<int>(blockIdx.x);
-  const int pb = sr[0], pe = sr[1], toff = sr[2], ntot = sr[3], soff = sr[4], nseg = sr[5];
   const uint32_t buf0 = lds_addr(sm.kv[0]);
   {
-    // tile list: two 8-byte records per 16-byte load (tile_off even, list padded)
-    const char* src = reinterpret_cast<const char*>(stiles + 2 * static_cast<int64_t>(toff));
-    const uint32_t dst = lds_addr(sm.tile_meta);
-    const int nch = (ntot + 1) >> 1;
-    for (int c0 = wave * 64; c0 < nch; c0 += kThreads)
-      if (c0 + lane < nch) dma16(src + 16 * (c0 + lane), dst + 16 * c0);
-  }
-  {
-    // segment offsets: four per 16-byte load (seg_off a multiple of 4, list padded)
-    const char* src = reinterpret_cast<const char*>(segs + soff);
-    const uint32_t dst = lds_addr(sm.segs);
-    const int nch = (nseg + 3) >> 2;
+    // the block: block_ints (a multiple of 4, at most kMaxBlockInts) in 16-byte loads
+    const char* src = reinterpret_cast<const char*>(blocks + static_cast<int64_t>(blockIdx.x) * block_ints);
+    const uint32_t dst = lds_addr(sm.blk);
+    const int nch = block_ints >> 2;
     for (int c0 = wave * 64; c0 < nch; c0 += kThreads)
       if (c0 + lane < nch) dma16(src + 16 * (c0 + lane), dst + 16 * c0);
   }
   barrier_tile_landed<0>();
+  const int np = __builtin_amdgcn_readfirstlane(sm.blk[0]);
+  const int ntot = __builtin_amdgcn_readfirstlane(sm.blk[1]);
+  const int tile_at = kBlockHeaderInts + kBlockPieceInts * np;
+  const BlockTables bt{reinterpret_cast<const int2*>(sm.blk + tile_at), sm.blk + tile_at + 2 * ((ntot + 1) & ~1)};
 #pragma unroll
   for (int t = 0; t < kDepth; ++t)
-    if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, buf0, sm, wave, lane);
-  for (int pi = pb; pi < pe; ++pi) {
-    const int32_t* pc = pieces + kPieceInts * pi;
-    const int rows = pc[2];
-    if (rows <= 16) {
-      dsplit_piece<D, 4>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);
-    } else if (rows <= kSplitMaxRows) {
-      dsplit_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);
+    if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, buf0, bt, wave, lane);
+  for (int pi = 0; pi < np; ++pi) {
+    const int4 r = *reinterpret_cast<const int4*>(sm.blk + kBlockHeaderInts + kBlockPieceInts * pi);
+    const PieceRec pc{__builtin_amdgcn_readfirstlane(r.x), __builtin_amdgcn_readfirstlane(r.y),
+                      __builtin_amdgcn_readfirstlane(r.z), __builtin_amdgcn_readfirstlane(r.w)};
+    if (pc.rows <= 16) {
+      dsplit_piece<D, 4>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);
+    } else if (pc.rows <= kSplitMaxRows) {
+      dsplit_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);
     } else {
-      const int nrb = (((rows + 15) >> 4) + 3) >> 2;
+      const int nrb = (((pc.rows + 15) >> 4) + 3) >> 2;
       if (nrb == 1)
-        rows_piece<D, 1>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);
+        rows_piece<D, 1>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);
       else
-        rows_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm);  // the planner keeps pieces at <= 128 rows
+        rows_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);  // the planner keeps pieces at <= 128 rows
     }
   }
 }
@@ -698,12 +704,13 @@ hipError_t launch_partial(const DecodeArgs& a, hipStream_t s) {
   if (a.n_streams <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(a.n_streams));
   const Scalars sc{a.hq, a.hkv, a.group, a.scale_log2};
+  if (a.block_ints <= 0 || a.block_ints > kMaxBlockInts || a.block_ints % 4 != 0) return hipErrorInvalidValue;
   if (a.d == 128)
-    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.streams, a.pieces, a.rowsets, a.stiles,
-                                                  a.segs, a.part_o, a.part_ml, sc);
+    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.k_pool, a.v_pool, a.q, a.part_o,
+                                                  a.part_ml, sc);
   else
-    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.k_pool, a.v_pool, a.q, a.streams, a.pieces, a.rowsets, a.stiles,
-                                                 a.segs, a.part_o, a.part_ml, sc);
+    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.k_pool, a.v_pool, a.q, a.part_o,
+                                                 a.part_ml, sc);
   return hipGetLastError();
 }
 

@@ -297,9 +297,25 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   const int64_t per_round = S0 * (3 * kMaxStreamTiles / 4);
   const int64_t rounds = std::max<int64_t>(1, (total_tiles + per_round - 1) / per_round);
   const int64_t planned = std::min<int64_t>(total_tiles, S0 * rounds);
-  // every stream may start with a cut piece's query tiles; the slack keeps the
-  // last stream from collecting the rounding remainder
-  const double target = total_cost / static_cast<double>(planned) + 2 * kQTileCost;
+  // Stream s closes once the running cost passes quota[s]: its share of the
+  // total in proportion to its placement's speed (one round only: later
+  // rounds start wherever a slot frees up), plus slack for the query tiles of
+  // a cut piece that every stream may start with, so that the last stream
+  // does not collect the rounding remainder.
+  std::vector<double> quota(static_cast<size_t>(planned));
+  {
+    std::vector<double> w(static_cast<size_t>(planned), 1.0);
+    if (planned <= S0 && p.compute_units > 0) {
+      for (int64_t s = 0; s < planned; ++s) w[s] = p.slot_speed[s < p.compute_units ? 0 : 1];
+    }
+    double wsum = 0.0;
+    for (double x : w) wsum += x;
+    double cum = 0.0;
+    for (int64_t s = 0; s < planned; ++s) {
+      cum += w[s];
+      quota[s] = total_cost * cum / wsum + 2 * kQTileCost * static_cast<double>(s + 1);
+    }
+  }
   double acc = 0.0;
   int64_t partial = 0;
   auto pad_to = [](auto* v, size_t m, auto fill) {
@@ -325,10 +341,11 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     for (const Tile& tl : r.tiles) {
       Stream* st = &out->streams.back();
       const int64_t s = static_cast<int64_t>(out->streams.size()) - 1;
-      const bool quota = acc >= target * static_cast<double>(s + 1) && s + 1 < planned;
+      const bool full = s + 1 < planned && acc >= quota[s];
       const bool room = st->n_tiles + (new_piece ? nq + 1 : 1) <= kMaxStreamTiles &&
-                        st->n_segs + (new_piece ? sq.n_leaves : 0) <= kMaxStreamSegs;
-      if (st->n_tiles > 0 && (quota || !room)) {
+                        st->n_segs + (new_piece ? sq.n_leaves : 0) <= kMaxStreamSegs &&
+                        st->piece_end - st->piece_begin + (new_piece ? 1 : 0) <= kMaxStreamPieces;
+      if (st->n_tiles > 0 && (full || !room)) {
         open_stream();
         st = &out->streams.back();
         new_piece = true;
@@ -382,6 +399,37 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   pad_to(&out->stream_tiles, 2, StreamTile{0, 0});
   pad_to(&out->segs, 4, 0);
   out->partial_rows = partial;
+
+  // ---- stream blocks ----------------------------------------------------------------
+  auto round_up = [](int32_t x, int32_t m) { return (x + m - 1) / m * m; };
+  int32_t bi = kBlockHeaderInts;
+  for (const Stream& st : out->streams)
+    bi = std::max(bi, kBlockHeaderInts + kBlockPieceInts * (st.piece_end - st.piece_begin) +
+                          2 * round_up(st.n_tiles, 2) + round_up(st.n_segs, 4));
+  out->block_ints = round_up(bi, 4);
+  out->blocks.assign(out->streams.size() * static_cast<size_t>(out->block_ints), 0);
+  for (size_t si = 0; si < out->streams.size(); ++si) {
+    const Stream& st = out->streams[si];
+    int32_t* b = &out->blocks[si * out->block_ints];
+    const int32_t np = st.piece_end - st.piece_begin;
+    b[0] = np;
+    b[1] = st.n_tiles;
+    b[2] = st.n_segs;
+    int32_t* w = b + kBlockHeaderInts;
+    for (int32_t i = st.piece_begin; i < st.piece_end; ++i) {
+      const Piece& pc = out->pieces[i];
+      *w++ = pc.rows;
+      *w++ = pc.tile_begin;
+      *w++ = pc.n_tiles;
+      *w++ = pc.partial_base;
+    }
+    for (int32_t k = 0; k < st.n_tiles; ++k) {
+      *w++ = out->stream_tiles[st.tile_off + k].hb;
+      *w++ = out->stream_tiles[st.tile_off + k].valid;
+    }
+    w += 2 * (round_up(st.n_tiles, 2) - st.n_tiles);
+    for (int32_t k = 0; k < st.n_segs; ++k) *w++ = out->segs[st.seg_off + k];
+  }
 
   // ---- per (leaf, KV head) merge lists -------------------------------------------
   const int64_t nkeys = static_cast<int64_t>(n_leaves) * Hkv;

@@ -91,10 +91,12 @@ enum PlanMode : int32_t { kModeTree = 0, kModeNaive = 1 };
 
 // Tokens per decode tile (half of a 64-token pool block).
 constexpr int32_t kPlanTileTokens = 32;
-// Upper bounds on the tiles and query segments of one stream (sized for the
-// kernel's LDS tables).
+// Upper bounds on the tiles, query segments and pieces of one stream (sized
+// for the kernel's LDS copy of its stream block).  A piece holds at least one
+// query tile and one KV tile.
 constexpr int32_t kMaxStreamTiles = 256;
 constexpr int32_t kMaxStreamSegs = 256;
+constexpr int32_t kMaxStreamPieces = kMaxStreamTiles / 2;
 // Query rows carried by one query tile (a tile buffer holds 64 rows of D).
 constexpr int32_t kQTileRows = 64;
 // Query rows of a piece that the column-split kernel path handles (two 16-row
@@ -147,6 +149,19 @@ struct StreamTile {
   int32_t valid;
 };
 
+// Device copy of one stream, all a workgroup needs to run it: stream s is the
+// block of block_ints int32 at s * block_ints (the same size for every stream
+// of a plan, a multiple of 4 ints, so the kernel fetches it with one round of
+// 16-byte loads from an address it computes itself):
+//   [0, 4)                   n_pieces, n_tiles, n_segs, 0
+//   [4, 4 + 4 n_pieces)      per piece: rows, tile_begin, n_tiles, partial_base
+//   then n_tiles StreamTile records (two ints each, padded to an even count)
+//   then n_segs query segment offsets (padded to a multiple of 4)
+constexpr int32_t kBlockHeaderInts = 4;
+constexpr int32_t kBlockPieceInts = 4;
+constexpr int32_t kMaxBlockInts =
+    kBlockHeaderInts + kBlockPieceInts * kMaxStreamPieces + 2 * kMaxStreamTiles + kMaxStreamSegs;
+
 // Host record of a KV tile, for inspection: tokens [32 k, 32 k + 32) of node
 // `node` (k = tile_in_node) in pool block `block` (= block_begin + k / 2).
 struct Tile {
@@ -164,6 +179,12 @@ struct PlanParams {
   int64_t num_blocks;       // pool blocks per KV head
   int32_t max_rows;         // query rows of a piece at most (leaf groups are split to fit)
   int32_t concurrent_wgs;   // workgroups resident at once (streams per round)
+  // Relative speed of a first-round stream by its slot on the CU.  The
+  // dispatcher fills every CU's first slot before any second one, so stream s
+  // runs in slot s / compute_units; streams are sized in proportion to
+  // slot_speed[slot] (both 1.0: equal cost per stream).
+  int32_t compute_units;
+  double slot_speed[2];
 };
 
 struct Plan {
@@ -176,6 +197,9 @@ struct Plan {
   // Query segments: element offset in the query tensor of the G rows of one
   // leaf for one KV head (contiguous there), one per (piece, leaf).
   std::vector<int32_t> segs;
+  // The device copy of the streams (layout above kBlockHeaderInts).
+  std::vector<int32_t> blocks;
+  int32_t block_ints = 0;
   // Per (leaf x, KV head g), key = x * Hkv + g: the partial rows to merge for
   // query head g * G + h' are comb[key * comb_stride + 1 + e] + h' for
   // e < comb[key * comb_stride] (fixed stride, so one load finds them).

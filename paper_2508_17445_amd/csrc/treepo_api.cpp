@@ -32,7 +32,7 @@ struct CachedPlan {
   std::vector<int32_t> leaves;
   Plan plan;
   std::vector<char> blob;  // host image of the plan region
-  size_t off_streams = 0, off_pieces = 0, off_rowsets = 0, off_stiles = 0, off_segs = 0;
+  size_t off_blocks = 0;
   size_t off_comb = 0;
   size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;
   uint64_t uid = 0;
@@ -193,18 +193,10 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
     *at = off;
     off = align_up(off + bytes);
   };
-  place(&cp.off_streams, p.streams.size() * sizeof(treepo::Stream));
-  place(&cp.off_pieces, p.pieces.size() * sizeof(treepo::Piece));
-  place(&cp.off_rowsets, p.rowsets.size() * sizeof(int32_t));
-  place(&cp.off_stiles, p.stream_tiles.size() * sizeof(treepo::StreamTile));
-  place(&cp.off_segs, p.segs.size() * sizeof(int32_t));
+  place(&cp.off_blocks, p.blocks.size() * sizeof(int32_t));
   place(&cp.off_comb, p.comb.size() * sizeof(int32_t));
   cp.blob.assign(off, 0);
-  put(cp.blob, cp.off_streams, p.streams);
-  put(cp.blob, cp.off_pieces, p.pieces);
-  put(cp.blob, cp.off_rowsets, p.rowsets);
-  put(cp.blob, cp.off_stiles, p.stream_tiles);
-  put(cp.blob, cp.off_segs, p.segs);
+  put(cp.blob, cp.off_blocks, p.blocks);
   put(cp.blob, cp.off_comb, p.comb);
   cp.off_part_o = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
@@ -264,12 +256,9 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.d = ctx->cfg.head_dim;
   a.q = static_cast<const uint16_t*>(q);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.streams = reinterpret_cast<const int32_t*>(wsb + cp->off_streams);
+  a.blocks = reinterpret_cast<const int32_t*>(wsb + cp->off_blocks);
+  a.block_ints = p.block_ints;
   a.n_streams = static_cast<int32_t>(p.streams.size());
-  a.pieces = reinterpret_cast<const int32_t*>(wsb + cp->off_pieces);
-  a.rowsets = reinterpret_cast<const int32_t*>(wsb + cp->off_rowsets);
-  a.stiles = reinterpret_cast<const int32_t*>(wsb + cp->off_stiles);
-  a.segs = reinterpret_cast<const int32_t*>(wsb + cp->off_segs);
   a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
   a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
   a.comb = reinterpret_cast<const int32_t*>(wsb + cp->off_comb);
@@ -336,6 +325,12 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   ctx->params.num_blocks = c.num_blocks;
   ctx->params.max_rows = 128;
   ctx->params.concurrent_wgs = treepo::kComputeUnits * treepo::partial_workgroups_per_cu();
+  // The second workgroup on a CU gets the smaller share of its issue and
+  // memory bandwidth (measured on config-2 decodes: about 0.85 of the first's
+  // progress over the same time).
+  ctx->params.compute_units = treepo::kComputeUnits;
+  ctx->params.slot_speed[0] = 1.0;
+  ctx->params.slot_speed[1] = 0.85;
   *out = ctx;
   return TREEPO_OK;
 }
@@ -546,6 +541,24 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
     std::memcpy(rowsets, p.rowsets.data(), p.rowsets.size() * sizeof(int32_t));
     std::memcpy(tiles, p.tiles.data(), p.tiles.size() * sizeof(treepo::Tile));
   }
+  return TREEPO_OK;
+}
+
+int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t mode,
+                             int32_t* blocks, int32_t* block_ints, int32_t* n_streams) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (!block_ints || !n_streams || (mode != TREEPO_MODE_TREE && mode != TREEPO_MODE_NAIVE))
+    return fail(ctx, TREEPO_EINVAL, "null count pointer or bad mode");
+  std::string err;
+  int32_t st = ctx->tree.check_leaves(n_leaves, leaves, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  CachedPlan* cp = nullptr;
+  st = get_plan(ctx, n_leaves, leaves, mode, &cp);
+  if (st != TREEPO_OK) return st;
+  const Plan& p = cp->plan;
+  *block_ints = p.block_ints;
+  *n_streams = static_cast<int32_t>(p.streams.size());
+  if (blocks) std::memcpy(blocks, p.blocks.data(), p.blocks.size() * sizeof(int32_t));
   return TREEPO_OK;
 }
 

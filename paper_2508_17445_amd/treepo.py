@@ -73,6 +73,7 @@ def load_library(path: str = LIB_PATH):
         "treepo_export_chains": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
         "treepo_export_desc": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
         "treepo_export_plan": (_i32, [_p, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
+        "treepo_export_blocks": (_i32, [_p, _i32, _pi32, _i32, _pi32, _pi32, _pi32]),
         "treepo_set_profiling": (_i32, [_p, _i32]),
         "treepo_profile_read": (_i32, [_p, _i32, ctypes.POINTER(ctypes.c_double), _pi64]),
         "treepo_strerror": (ctypes.c_char_p, [_i32]),
@@ -256,6 +257,17 @@ class Context:
                                                 ctypes.byref(ns)),
                     "treepo_export_plan")
         return pieces[:ni.value], rowsets[:nr.value], tiles[:nt.value], ns.value
+
+    def export_blocks(self, leaves, mode: int = MODE_TREE):
+        """Stream blocks as the kernel reads them: int32 [n_streams, block_ints]."""
+        lv = _arr32(leaves)
+        bi, ns = _i32(), _i32()
+        self._check(self.lib.treepo_export_blocks(self.h, len(lv), _ptr32(lv), mode, ctypes.cast(None, _pi32),
+                                                  ctypes.byref(bi), ctypes.byref(ns)), "treepo_export_blocks")
+        out = np.zeros((max(ns.value, 1), max(bi.value, 1)), np.int32)
+        self._check(self.lib.treepo_export_blocks(self.h, len(lv), _ptr32(lv), mode, _ptr32(out), ctypes.byref(bi),
+                                                  ctypes.byref(ns)), "treepo_export_blocks")
+        return out[:ns.value]
 
     # ---- timing ------------------------------------------------------------
     def set_profiling(self, enable: bool):

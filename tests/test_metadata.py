@@ -60,6 +60,7 @@ def test_kv_slots_follow_block_reservation():
 
 
 MAX_STREAM_TILES = 256
+MAX_BLOCK_INTS = 4 + 4 * 128 + 2 * 256 + 256   # header, pieces, tile records, segments
 
 
 def _tile_cost(rows):
@@ -105,7 +106,46 @@ def _plan_checks(ctx, model, leaves, mode):
     assert spans[0][0] == 0
     for (b0, s0), (b1, _) in zip(spans, spans[1:]):
         assert b0 + s0 == b1
+    _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_next, seg_next)
     return pieces, tiles, n_streams
+
+
+def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_next, seg_next):
+    """The kernel's stream blocks restate the exported schedule exactly, and
+    every pool and query address they lead to is in bounds."""
+    blocks = ctx.export_blocks(leaves, mode)
+    hq, hkv, d, nb = ctx.cfg.num_q_heads, ctx.cfg.num_kv_heads, ctx.cfg.head_dim, ctx.cfg.num_blocks
+    G = hq // hkv
+    bi = blocks.shape[1]
+    assert blocks.shape[0] == n_streams and bi % 4 == 0 and bi <= MAX_BLOCK_INTS
+    by_stream = {}
+    for pc in pieces:
+        by_stream.setdefault(int(pc[9]), []).append(pc)
+    for s in range(n_streams):
+        b = blocks[s]
+        n_p, n_t, n_s = int(b[0]), int(b[1]), int(b[2])
+        pcs = by_stream[s]
+        assert (n_p, n_t, n_s, b[3]) == (len(pcs), stream_next[s], seg_next[s], 0)
+        tiles_at = 4 + 4 * n_p
+        segs_at = tiles_at + 2 * (n_t + n_t % 2)
+        assert segs_at + n_s <= bi
+        assert (b[tiles_at + 2 * n_t:segs_at] == 0).all() and (b[segs_at + n_s:] == 0).all()
+        recs = b[4:tiles_at].reshape(-1, 4)
+        st = b[tiles_at:tiles_at + 2 * n_t].reshape(-1, 2)
+        sg = b[segs_at:segs_at + n_s]
+        for i, pc in enumerate(pcs):
+            rb, nl, rows, g, stile, nt, pbase, seg, _, _, ptile, nq = (int(v) for v in pc[:12])
+            assert tuple(recs[i]) == (rows, stile, nt, pbase)
+            for t in range(nq):
+                assert tuple(st[stile + t]) == (-1 - seg, (64 * t) | (min(64, rows - 64 * t) << 16))
+            for t in range(nt):
+                blk, _, tin, valid = (int(v) for v in tiles[ptile + t])
+                hb, v = (int(x) for x in st[stile + nq + t])
+                assert hb == 2 * (g * nb + blk) + tin % 2 and v == valid
+                assert 0 <= hb < 2 * hkv * nb and 1 <= v <= 32
+            for j in range(nl):
+                x = int(rowsets[rb + j])
+                assert 0 <= x < len(leaves) and sg[seg + j] == (x * hq + g * G) * d
 
 
 def _stream_costs(pieces, n_streams):
@@ -135,8 +175,8 @@ def test_plan_covers_each_chain_token_once(cfg):
 
 @pytest.mark.parametrize("cfg", [2, 4])
 def test_streams_are_balanced(cfg):
-    """One stream per resident workgroup slot (512), equal estimated cost to
-    within about two tiles."""
+    """One stream per resident workgroup slot (512), estimated cost in
+    proportion to the slot's speed to within about two tiles."""
     log = build_call_log(cfg)
     from workloads import CONFIGS
     c = CONFIGS[cfg]
@@ -149,7 +189,11 @@ def test_streams_are_balanced(cfg):
         rounds = -(-total // (512 * 192))
         assert n_streams <= min(total, 512 * rounds) and n_streams >= 0.95 * min(total, 512 * rounds)
         cost = _stream_costs(pieces, n_streams)
+        if rounds == 1:
+            # the second slot of a CU (streams 256 on) is sized at 0.85 of the first
+            cost = cost / np.where(np.arange(n_streams) < 256, 1.0, 0.85)
         assert cost.max() <= cost.mean() + 2 * 2.0 + 1.0, (mode, cost.mean(), cost.max())
+        assert cost.min() >= cost.mean() - 2 * 2.0 - 1.0 or n_streams < 512 * rounds
 
 
 def test_duplicate_and_interior_leaves():
