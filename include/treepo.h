@@ -203,7 +203,7 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  * piece is the part of one sequence inside one stream.  Pieces,
  * TREEPO_PIECE_FIELDS int32 each, in stream order:
  *   {rowset_begin, n_leaves, rows, kv_head, stream_tile, n_tiles,
- *    partial_base, seg_begin, run, stream, plan_tile, n_qtiles, 0, 0, 0, 0}
+ *    0, seg_begin, run, stream, plan_tile, n_qtiles, 0, 0, 0, 0}
  * rows = n_leaves * (Hq / Hkv); the piece's leaves are rowsets[rowset_begin ..
  * + n_leaves) (call positions); in its stream's tile list it is n_qtiles
  * query tiles (64 rows each) from stream_tile on, then n_tiles KV tiles, and
@@ -222,13 +222,17 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  * one block of *block_ints int32 per stream (a multiple of 4; stream s at
  * s * block_ints, *n_streams blocks):
  *   {n_pieces, n_tiles, n_segs, 0};
- *   per piece {rows, stream_tile, n_tiles, partial_base};
+ *   per piece {rows, stream_tile, n_tiles, seg_begin};
  *   per stream tile {hb, valid}, padded to an even count: a KV tile has
  *     hb = 2 * (kv_head * num_blocks + block) + tile_in_node % 2 and valid =
  *     its tokens; a query tile has hb = -1 - (its piece's seg_begin) and
  *     valid = first_row | (n_rows << 16);
  *   per query segment, the element offset (x * Hq + kv_head * G) * D of the
- *     G query rows of the piece's leaf x, padded to a multiple of 4.
+ *     G query rows of the piece's leaf x, padded to a multiple of 4;
+ *   per query segment, the partial row (key * E + e) * G of the piece's entry
+ *     for its leaf x, key = x * Hkv + kv_head, where e counts the pieces
+ *     before it (plan order) that cover the same key and E is the largest
+ *     count over the keys; padded to a multiple of 4.
  * Pass a null array to query the sizes only. */
 int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t mode,
                              int32_t* blocks, int32_t* block_ints, int32_t* n_streams);
@@ -237,7 +241,7 @@ int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* l
 
 /* Kernel kinds for treepo_profile_read. */
 #define TREEPO_KERNEL_APPEND 0  /* KV scatter into the pools                      */
-#define TREEPO_KERNEL_PARTIAL 1 /* node partials, VALU and MFMA work items        */
+#define TREEPO_KERNEL_PARTIAL 1 /* node partials, one workgroup per stream         */
 #define TREEPO_KERNEL_COMBINE 2 /* log-sum-exp merge of each leaf's partials      */
 #define TREEPO_KERNEL_KINDS 3
 

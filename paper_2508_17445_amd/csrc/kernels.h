@@ -22,8 +22,8 @@ struct DecodeArgs {
   int32_t n_streams;
   float* part_o;           // fp32 [partial_rows][D], unnormalised
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
-  const int32_t* comb;     // per (leaf, KV head): count, then the partial rows to merge
-  int32_t comb_stride;
+  const int32_t* comb_count;  // per key (leaf, KV head): partial entries to merge
+  int32_t emax;               // entries per key at most (partial slot stride)
   int32_t n_leaves;
   float* out;              // fp32 [n_leaves][Hq][D]
   float* lse;              // fp32 [n_leaves][Hq] or null

@@ -69,8 +69,9 @@ struct Smem {
 
 // LDS views of the stream block's tables.
 struct BlockTables {
-  const int2* tiles;    // StreamTile records
-  const int32_t* segs;  // query segment offsets
+  const int2* tiles;     // StreamTile records
+  const int32_t* segs;   // query segment offsets
+  const int32_t* dests;  // per (piece, leaf): partial row of its h' = 0
 };
 
 __device__ __forceinline__ int k_swz(int r) { return (r & 3) | ((r >> 1) & 4); }
@@ -202,8 +203,14 @@ __device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int ntot, int k
 
 // A piece's record in the stream block.
 struct PieceRec {
-  int rows, k0, nk, pbase;
+  int rows, k0, nk, seg;
 };
+
+// Partial row of the piece's query row m (leaf j = m / G, head h' = m % G).
+__device__ __forceinline__ int64_t partial_row(const BlockTables& bt, int seg, int m, int G) {
+  const int j = m / G;
+  return static_cast<int64_t>(bt.dests[seg + j]) + (m - j * G);
+}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -281,7 +288,7 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
   const int r16 = lane & 15;  // row within the 16-row block
   const int rb = wave / DSPLIT;
   const int db0 = (wave % DSPLIT) * kDBw;
-  const int rows = pc.rows, k0 = pc.k0, nk = pc.nk, pbase = pc.pbase;
+  const int rows = pc.rows, k0 = pc.k0, nk = pc.nk;
   const bool active = 16 * rb < rows;  // wave-uniform
   const int m = 16 * rb + r16;         // this lane's query row
 
@@ -361,7 +368,7 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
   l_sum += __shfl_xor(l_sum, 16);
   l_sum += __shfl_xor(l_sum, 32);
   if (active && m < rows) {
-    const int64_t slot = static_cast<int64_t>(pbase) + m;
+    const int64_t slot = partial_row(bt, pc.seg, m, sc.group);
 #pragma unroll
     for (int db = 0; db < kDBw; ++db)
       *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * (db0 + db) + 4 * a) = acc[db];
@@ -391,7 +398,7 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int a = lane >> 4;
   const int r16 = lane & 15;
-  const int rows = pc.rows, k0 = pc.k0, nk = pc.nk, pbase = pc.pbase;
+  const int rows = pc.rows, k0 = pc.k0, nk = pc.nk;
   const int nq = (rows + kQTileRows - 1) / kQTileRows;
   const int nrb_total = (rows + 15) >> 4;
   const int my_rb = nrb_total > wave ? (nrb_total - wave + 3) >> 2 : 0;  // row blocks of this wave (<= NRB)
@@ -500,7 +507,7 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
     l += __shfl_xor(l, 32);
     const int m = 16 * (wave + 4 * i) + r16;
     if (m < rows) {
-      const int64_t slot = static_cast<int64_t>(pbase) + m;
+      const int64_t slot = partial_row(bt, pc.seg, m, sc.group);
 #pragma unroll
       for (int db = 0; db < kDB; ++db)
         *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * db + 4 * a) = acc[i][db];
@@ -539,8 +546,11 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
   barrier_tile_landed<0>();
   const int np = __builtin_amdgcn_readfirstlane(sm.blk[0]);
   const int ntot = __builtin_amdgcn_readfirstlane(sm.blk[1]);
+  const int nseg = __builtin_amdgcn_readfirstlane(sm.blk[2]);
   const int tile_at = kBlockHeaderInts + kBlockPieceInts * np;
-  const BlockTables bt{reinterpret_cast<const int2*>(sm.blk + tile_at), sm.blk + tile_at + 2 * ((ntot + 1) & ~1)};
+  const int seg_at = tile_at + 2 * ((ntot + 1) & ~1);
+  const BlockTables bt{reinterpret_cast<const int2*>(sm.blk + tile_at), sm.blk + seg_at,
+                       sm.blk + seg_at + ((nseg + 3) & ~3)};
 #pragma unroll
   for (int t = 0; t < kDepth; ++t)
     if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, buf0, bt, wave, lane);
@@ -564,17 +574,46 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
 
 // ---- combine ------------------------------------------------------------------
 //
-// One wave per (leaf, query head h = g G + h'): over the partial rows
-// comb[1 + e] + h' of (leaf, g), m* = max m_i, L = sum l_i 2^(m_i - m*),
-// out = sum 2^(m_i - m*) O_i / L, lse = (m* + log2 L) ln 2.  Partials without
-// tokens (m = -inf) contribute nothing.  The merge list has a fixed stride, so
-// its count and rows arrive in one round of loads; the (m, l) pairs (one per
-// lane) and the first 16 O rows (every lane its d-slice) are then loaded
-// together, so a leaf with up to 16 partials costs two memory round trips.
-// Later rows follow in batches of 16 independent loads.  The order of the sum
-// is fixed by the plan, so results are deterministic.
+// One wave per (leaf, query head h = g G + h'): over the n = comb_count[key]
+// partial entries of key = (leaf, g), m* = max m_e, L = sum l_e 2^(m_e - m*),
+// out = sum 2^(m_e - m*) O_e / L, lse = (m* + log2 L) ln 2.  Partials without
+// tokens (m = -inf) contribute nothing.  Entry e sits at the fixed row
+// (key emax + e) G + h', so the (m, l) pairs (one entry per lane) and the
+// first 16 O rows (every lane its d-slice) are loaded in the same round as the
+// count, for all emax entries the slots can hold; entries past the count
+// (stale values of earlier calls) are masked out by selection.  A key with up
+// to 16 entries costs one memory round trip; later rows follow in batches of
+// 16 independent loads.  The sum runs in the plan's fixed entry order, so
+// results are deterministic.
+// Adds sum over entries k in [k0, cnt) of the round starting at entry `base`
+// of w_k O_k to o (w_k in lane k of w), 16 independent row loads at a time.
 template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __restrict__ comb, int32_t comb_stride,
+__device__ __forceinline__ void combine_rows(float (&o)[D / 64], const float* __restrict__ part_o, int64_t row0,
+                                             int group, int base, int k0, int cnt, float w, int lane) {
+  constexpr int kPL = D / 64;
+  constexpr int kGroup = 16;
+  for (; k0 < cnt; k0 += kGroup) {
+    float v[kGroup][kPL];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const int k = k0 + i < cnt ? k0 + i : cnt - 1;
+      const float* po = part_o + (row0 + static_cast<int64_t>(base + k) * group) * D + lane * kPL;
+#pragma unroll
+      for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), k0 + i));
+      if (k0 + i < cnt) {
+#pragma unroll
+        for (int j = 0; j < kPL; ++j) o[j] += wk * v[i][j];
+      }
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __restrict__ comb_count, int32_t emax,
                                                            const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml,
                                                            float* __restrict__ out, float* __restrict__ lse,
@@ -582,70 +621,85 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
   constexpr int kPL = D / 64;
   constexpr int kGroup = 16;
   const int lane = threadIdx.x & 63;
-  const int gw = static_cast<int>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+  const int gw = static_cast<int>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (gw >= n_leaves * hq) return;
   const int x = gw / hq;
   const int h = gw % hq;
   const int g = h / group;
   const int hp = h % group;
-  const int32_t* blk = comb + static_cast<int64_t>(x * hkv + g) * comb_stride;
-  const int n = blk[0];
-  float run_m = -INFINITY, run_l = 0.f;
+  const int key = x * hkv + g;
+  const int64_t row0 = static_cast<int64_t>(key) * emax * group + hp;  // entry e: row0 + e * group
+  const int n = comb_count[key];
+
+  // round 0, issued before the count is known: (m, l) of entries 0..63 and O
+  // rows of entries 0..15, each clamped to the slots
+  const int avail = emax < 64 ? emax : 64;
+  const int64_t my_row = row0 + static_cast<int64_t>(lane < avail ? lane : avail - 1) * group;
+  float v[kGroup][kPL];
+#pragma unroll
+  for (int i = 0; i < kGroup; ++i) {
+    const int k = i < avail ? i : avail - 1;
+    const float* po = part_o + (row0 + static_cast<int64_t>(k) * group) * D + lane * kPL;
+#pragma unroll
+    for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+  }
+  const float m_ld = part_ml[2 * my_row];
+  const float l_ld = part_ml[2 * my_row + 1];
+  // keeps every round-0 load ahead of the count-dependent code (otherwise the
+  // compiler may sink a load under the weight test, a second round trip)
+#pragma unroll
+  for (int i = 0; i < kGroup; ++i)
+#pragma unroll
+    for (int j = 0; j < kPL; ++j) asm volatile("" ::"v"(v[i][j]));
+  asm volatile("" ::"v"(m_ld), "v"(l_ld));
+
   float o[kPL];
+  int cnt = n < 64 ? n : 64;
+  float mi = lane < cnt ? m_ld : -INFINITY;
+  float li = lane < cnt ? l_ld : 0.f;
+  float run_m = mi;
 #pragma unroll
-  for (int i = 0; i < kPL; ++i) o[i] = 0.f;
-  for (int base = 0; base < n; base += 64) {
-    const int cnt = n - base < 64 ? n - base : 64;
-    const bool mine = lane < cnt;
-    const int slot = blk[1 + base + (mine ? lane : 0)] + hp;
-    // first batch of O rows, issued with the (m, l) loads
-    float v[kGroup][kPL];
+  for (int sh = 1; sh < 64; sh <<= 1) run_m = fmaxf(run_m, __shfl_xor(run_m, sh));
+  float w = mi == -INFINITY ? 0.f : fast_exp2(mi - run_m);
+  float run_l = w * li;
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      const int k = i < cnt ? i : cnt - 1;
-      const float* po = part_o + static_cast<int64_t>(__builtin_amdgcn_readlane(slot, k)) * D + lane * kPL;
+  for (int sh = 1; sh < 64; sh <<= 1) run_l += __shfl_xor(run_l, sh);
 #pragma unroll
-      for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
-    }
-    const float mi = mine ? part_ml[2 * static_cast<int64_t>(slot)] : -INFINITY;
-    const float li = mine ? part_ml[2 * static_cast<int64_t>(slot) + 1] : 0.f;
-    float cm = mi;
+  for (int j = 0; j < kPL; ++j) o[j] = 0.f;
 #pragma unroll
-    for (int sh = 1; sh < 64; sh <<= 1) cm = fmaxf(cm, __shfl_xor(cm, sh));
-    const float nm = fmaxf(run_m, cm);
-    const float keep = run_m == -INFINITY ? 0.f : fast_exp2(run_m - nm);
-    const float w = mi == -INFINITY ? 0.f : fast_exp2(mi - nm);
-    float wl = w * li;
+  for (int i = 0; i < kGroup; ++i) {
+    // entries past the count have w = 0 and may hold anything: select, not multiply
+    const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), i));
 #pragma unroll
-    for (int sh = 1; sh < 64; sh <<= 1) wl += __shfl_xor(wl, sh);
-    run_l = run_l * keep + wl;
+    for (int j = 0; j < kPL; ++j) o[j] = wk == 0.f ? o[j] : fmaf(wk, v[i][j], o[j]);
+  }
+  if (n > kGroup) {
+    combine_rows<D>(o, part_o, row0, group, 0, kGroup, cnt, w, lane);
+    for (int base = 64; base < n; base += 64) {
+      cnt = n - base < 64 ? n - base : 64;
+      const int64_t r = row0 + static_cast<int64_t>(base + (lane < cnt ? lane : 0)) * group;
+      mi = lane < cnt ? part_ml[2 * r] : -INFINITY;
+      li = lane < cnt ? part_ml[2 * r + 1] : 0.f;
+      float cm = mi;
 #pragma unroll
-    for (int i = 0; i < kPL; ++i) o[i] *= keep;
-    run_m = nm;
-    for (int k0 = 0; k0 < cnt; k0 += kGroup) {
-      if (k0 > 0) {
+      for (int sh = 1; sh < 64; sh <<= 1) cm = fmaxf(cm, __shfl_xor(cm, sh));
+      const float nm = fmaxf(run_m, cm);
+      const float keep = fast_exp2(run_m - nm);  // run_m is finite: some entry holds tokens
+      w = mi == -INFINITY ? 0.f : fast_exp2(mi - nm);
+      float wl = w * li;
 #pragma unroll
-        for (int i = 0; i < kGroup; ++i) {
-          const int k = k0 + i < cnt ? k0 + i : cnt - 1;
-          const float* po = part_o + static_cast<int64_t>(__builtin_amdgcn_readlane(slot, k)) * D + lane * kPL;
+      for (int sh = 1; sh < 64; sh <<= 1) wl += __shfl_xor(wl, sh);
+      run_l = run_l * keep + wl;
 #pragma unroll
-          for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < kGroup; ++i) {
-        const float wk = k0 + i < cnt
-                             ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), k0 + i))
-                             : 0.f;
-#pragma unroll
-        for (int j = 0; j < kPL; ++j) o[j] += wk * v[i][j];
-      }
+      for (int j = 0; j < kPL; ++j) o[j] *= keep;
+      run_m = nm;
+      combine_rows<D>(o, part_o, row0, group, base, 0, cnt, w, lane);
     }
   }
   const float inv = 1.f / run_l;
   float* op = out + (static_cast<int64_t>(x) * hq + h) * D + lane * kPL;
 #pragma unroll
-  for (int i = 0; i < kPL; ++i) op[i] = o[i] * inv;
+  for (int j = 0; j < kPL; ++j) op[j] = o[j] * inv;
   if (lse != nullptr && lane == 0) lse[static_cast<int64_t>(x) * hq + h] = (run_m + __log2f(run_l)) * kLn2;
 }
 
@@ -718,10 +772,10 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   const int64_t waves = static_cast<int64_t>(a.n_leaves) * a.hq;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
   if (a.d == 128)
-    combine_kernel<128><<<grid, kThreads, 0, s>>>(a.comb, a.comb_stride, a.part_o, a.part_ml, a.out, a.lse,
+    combine_kernel<128><<<grid, kThreads, 0, s>>>(a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
                                                   a.n_leaves, a.hq, a.hkv, a.group);
   else
-    combine_kernel<64><<<grid, kThreads, 0, s>>>(a.comb, a.comb_stride, a.part_o, a.part_ml, a.out, a.lse,
+    combine_kernel<64><<<grid, kThreads, 0, s>>>(a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
                                                  a.n_leaves, a.hq, a.hkv, a.group);
   return hipGetLastError();
 }

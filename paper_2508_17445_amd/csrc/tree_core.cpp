@@ -317,7 +317,6 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     }
   }
   double acc = 0.0;
-  int64_t partial = 0;
   auto pad_to = [](auto* v, size_t m, auto fill) {
     while (v->size() % m) v->push_back(fill);
   };
@@ -375,13 +374,6 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         }
         st->n_tiles += nq;
         acc += kQTileCost * nq;
-        const int64_t prow = rows;
-        if (partial + prow > INT32_MAX) {
-          if (err) *err = "too many partial rows";
-          return kEUnsupported;
-        }
-        pc.partial_base = static_cast<int32_t>(partial);
-        partial += prow;
         out->pieces.push_back(pc);
         st->piece_end = static_cast<int32_t>(out->pieces.size());
         new_piece = false;
@@ -398,14 +390,40 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   }
   pad_to(&out->stream_tiles, 2, StreamTile{0, 0});
   pad_to(&out->segs, 4, 0);
-  out->partial_rows = partial;
+
+  // ---- partial slots: entry e of key (leaf x, KV head g) -------------------------------
+  // Every piece adds one entry to each of its leaves' keys, in piece order (the
+  // fixed merge order); entry e of key k holds rows (k * emax + e) * G + h'.
+  const int64_t nkeys = static_cast<int64_t>(n_leaves) * Hkv;
+  out->comb_count.assign(nkeys, 0);
+  for (const Piece& pc : out->pieces)
+    for (int32_t j = 0; j < pc.n_leaves; ++j)
+      ++out->comb_count[static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g];
+  out->emax = 1;
+  for (int32_t c : out->comb_count) out->emax = std::max(out->emax, c);
+  out->partial_rows = nkeys * out->emax * G;
+  if (out->partial_rows > INT32_MAX) {
+    if (err) *err = "too many partial rows";
+    return kEUnsupported;
+  }
+  out->dests.assign(out->segs.size(), 0);
+  {
+    std::vector<int32_t> next(nkeys, 0);
+    for (const Piece& pc : out->pieces) {
+      const Stream& st = out->streams[pc.stream];
+      for (int32_t j = 0; j < pc.n_leaves; ++j) {
+        const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
+        out->dests[st.seg_off + pc.seg_begin + j] = static_cast<int32_t>((key * out->emax + next[key]++) * G);
+      }
+    }
+  }
 
   // ---- stream blocks ----------------------------------------------------------------
   auto round_up = [](int32_t x, int32_t m) { return (x + m - 1) / m * m; };
   int32_t bi = kBlockHeaderInts;
   for (const Stream& st : out->streams)
     bi = std::max(bi, kBlockHeaderInts + kBlockPieceInts * (st.piece_end - st.piece_begin) +
-                          2 * round_up(st.n_tiles, 2) + round_up(st.n_segs, 4));
+                          2 * round_up(st.n_tiles, 2) + 2 * round_up(st.n_segs, 4));
   out->block_ints = round_up(bi, 4);
   out->blocks.assign(out->streams.size() * static_cast<size_t>(out->block_ints), 0);
   for (size_t si = 0; si < out->streams.size(); ++si) {
@@ -421,37 +439,18 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       *w++ = pc.rows;
       *w++ = pc.tile_begin;
       *w++ = pc.n_tiles;
-      *w++ = pc.partial_base;
+      *w++ = pc.seg_begin;
     }
     for (int32_t k = 0; k < st.n_tiles; ++k) {
       *w++ = out->stream_tiles[st.tile_off + k].hb;
       *w++ = out->stream_tiles[st.tile_off + k].valid;
     }
     w += 2 * (round_up(st.n_tiles, 2) - st.n_tiles);
-    for (int32_t k = 0; k < st.n_segs; ++k) *w++ = out->segs[st.seg_off + k];
+    for (int32_t k = 0; k < st.n_segs; ++k) w[k] = out->segs[st.seg_off + k];
+    w += round_up(st.n_segs, 4);
+    for (int32_t k = 0; k < st.n_segs; ++k) w[k] = out->dests[st.seg_off + k];
   }
 
-  // ---- per (leaf, KV head) merge lists -------------------------------------------
-  const int64_t nkeys = static_cast<int64_t>(n_leaves) * Hkv;
-  std::vector<int32_t> count(nkeys, 0);
-  for (const Piece& pc : out->pieces)
-    for (int32_t j = 0; j < pc.n_leaves; ++j)
-      ++count[static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g];
-  int32_t emax = 1;
-  for (int32_t c : count) emax = std::max(emax, c);
-  out->comb_stride = 1 + emax;
-  if (nkeys * out->comb_stride > INT32_MAX) {
-    if (err) *err = "merge lists too large";
-    return kEUnsupported;
-  }
-  out->comb.assign(nkeys * out->comb_stride, 0);
-  for (const Piece& pc : out->pieces) {
-    for (int32_t j = 0; j < pc.n_leaves; ++j) {
-      const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
-      int32_t* blk = &out->comb[key * out->comb_stride];
-      blk[1 + blk[0]++] = pc.partial_base + j * G;
-    }
-  }
   return kOk;
 }
 

@@ -107,7 +107,8 @@ constexpr int32_t kSplitMaxRows = 32;
 // in one stream.  Rows are (leaf j of the group, head h' of the GQA group):
 // row = j * G + h'.  In its stream's tile list a piece is n_qtiles query tiles
 // (its query rows, 64 per tile) followed by n_tiles KV tiles.  It writes one
-// partial row per query row: rows [partial_base, partial_base + rows).
+// partial row per query row, at the partial slot of its leaf's key (see
+// Plan::dests).
 struct Piece {
   int32_t rowset_begin;  // index into Plan::rowsets (the group's call positions)
   int32_t n_leaves;
@@ -115,7 +116,7 @@ struct Piece {
   int32_t g;             // KV head
   int32_t tile_begin;    // its first query tile, index into the stream's tile list
   int32_t n_tiles;       // KV tiles
-  int32_t partial_base;
+  int32_t reserved;      // 0
   int32_t seg_begin;     // its first query segment, index into the stream's segment list
   int32_t run;
   int32_t stream;
@@ -154,13 +155,14 @@ struct StreamTile {
 // of a plan, a multiple of 4 ints, so the kernel fetches it with one round of
 // 16-byte loads from an address it computes itself):
 //   [0, 4)                   n_pieces, n_tiles, n_segs, 0
-//   [4, 4 + 4 n_pieces)      per piece: rows, tile_begin, n_tiles, partial_base
+//   [4, 4 + 4 n_pieces)      per piece: rows, tile_begin, n_tiles, seg_begin
 //   then n_tiles StreamTile records (two ints each, padded to an even count)
 //   then n_segs query segment offsets (padded to a multiple of 4)
+//   then n_segs partial destinations, Plan::dests (padded to a multiple of 4)
 constexpr int32_t kBlockHeaderInts = 4;
 constexpr int32_t kBlockPieceInts = 4;
 constexpr int32_t kMaxBlockInts =
-    kBlockHeaderInts + kBlockPieceInts * kMaxStreamPieces + 2 * kMaxStreamTiles + kMaxStreamSegs;
+    kBlockHeaderInts + kBlockPieceInts * kMaxStreamPieces + 2 * kMaxStreamTiles + 2 * kMaxStreamSegs;
 
 // Host record of a KV tile, for inspection: tokens [32 k, 32 k + 32) of node
 // `node` (k = tile_in_node) in pool block `block` (= block_begin + k / 2).
@@ -200,11 +202,14 @@ struct Plan {
   // The device copy of the streams (layout above kBlockHeaderInts).
   std::vector<int32_t> blocks;
   int32_t block_ints = 0;
-  // Per (leaf x, KV head g), key = x * Hkv + g: the partial rows to merge for
-  // query head g * G + h' are comb[key * comb_stride + 1 + e] + h' for
-  // e < comb[key * comb_stride] (fixed stride, so one load finds them).
-  std::vector<int32_t> comb;
-  int32_t comb_stride = 0;
+  // Partial slots.  Key (leaf x, KV head g) = x * Hkv + g has comb_count[key]
+  // entries (one per piece over its chain, in plan order, at most emax); entry
+  // e holds the partial rows (key * emax + e) * G + h' for query heads
+  // g * G + h'.  dests (parallel to segs) gives, per (piece, leaf), the row of
+  // its entry's h' = 0.
+  std::vector<int32_t> comb_count;
+  int32_t emax = 0;
+  std::vector<int32_t> dests;
   int64_t partial_rows = 0;
   int64_t unique_kv_tokens = 0;   // tokens streamed per KV head (tree: unique)
   int64_t kv_token_visits = 0;    // tokens streamed, summed over leaf groups (per KV head)

@@ -194,10 +194,10 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
     off = align_up(off + bytes);
   };
   place(&cp.off_blocks, p.blocks.size() * sizeof(int32_t));
-  place(&cp.off_comb, p.comb.size() * sizeof(int32_t));
+  place(&cp.off_comb, p.comb_count.size() * sizeof(int32_t));
   cp.blob.assign(off, 0);
   put(cp.blob, cp.off_blocks, p.blocks);
-  put(cp.blob, cp.off_comb, p.comb);
+  put(cp.blob, cp.off_comb, p.comb_count);
   cp.off_part_o = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
   cp.off_part_ml = off;
@@ -261,8 +261,8 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.n_streams = static_cast<int32_t>(p.streams.size());
   a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
   a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
-  a.comb = reinterpret_cast<const int32_t*>(wsb + cp->off_comb);
-  a.comb_stride = p.comb_stride;
+  a.comb_count = reinterpret_cast<const int32_t*>(wsb + cp->off_comb);
+  a.emax = p.emax;
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;

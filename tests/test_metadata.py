@@ -72,12 +72,11 @@ def _plan_checks(ctx, model, leaves, mode):
     hkv = ctx.cfg.num_kv_heads
     G = ctx.cfg.num_q_heads // hkv
     covered = {(x, g): [] for x in range(len(leaves)) for g in range(hkv)}
-    spans = []
     stream_next = {}
     seg_next = {}
     for pc in pieces:
-        rb, nl, rows, g, stile, nt, pbase, seg, run, stream, ptile, nq = pc[:12]
-        assert rows == nl * G and nt >= 1 and nl >= 1 and 0 <= g < hkv and rows <= 128
+        rb, nl, rows, g, stile, nt, reserved, seg, run, stream, ptile, nq = pc[:12]
+        assert rows == nl * G and nt >= 1 and nl >= 1 and 0 <= g < hkv and rows <= 128 and reserved == 0
         assert 0 <= stream < n_streams and (pc[12:] == 0).all()
         assert nq == -(-rows // 64)          # 64 query rows per query tile
         # pieces of a stream are consecutive and tile its list from 0:
@@ -88,7 +87,6 @@ def _plan_checks(ctx, model, leaves, mode):
         assert seg == seg_next.get(stream, 0)
         seg_next[stream] = seg + nl
         assert seg + nl <= 256
-        spans.append((pbase, rows))
         for pos in rowsets[rb:rb + nl]:
             for t in tiles[ptile:ptile + nt]:
                 covered[(pos, g)].append(tuple(t))
@@ -101,26 +99,28 @@ def _plan_checks(ctx, model, leaves, mode):
                 want.append((model.nodes[n]["block_begin"] + k // 2, n, k, min(32, ln - 32 * k)))
         for g in range(hkv):
             assert sorted(covered[(pos, g)]) == sorted(want), (mode, pos, g)
-    # partial rows are laid out back to back without overlap
-    spans.sort()
-    assert spans[0][0] == 0
-    for (b0, s0), (b1, _) in zip(spans, spans[1:]):
-        assert b0 + s0 == b1
     _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_next, seg_next)
     return pieces, tiles, n_streams
 
 
 def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_next, seg_next):
-    """The kernel's stream blocks restate the exported schedule exactly, and
-    every pool and query address they lead to is in bounds."""
+    """The kernel's stream blocks restate the exported schedule exactly, every
+    pool and query address they lead to is in bounds, and the partial slots
+    give each (leaf, KV head) key entries 0..count-1 in piece order."""
     blocks = ctx.export_blocks(leaves, mode)
     hq, hkv, d, nb = ctx.cfg.num_q_heads, ctx.cfg.num_kv_heads, ctx.cfg.head_dim, ctx.cfg.num_blocks
     G = hq // hkv
     bi = blocks.shape[1]
     assert blocks.shape[0] == n_streams and bi % 4 == 0 and bi <= MAX_BLOCK_INTS
     by_stream = {}
+    count = {}
     for pc in pieces:
         by_stream.setdefault(int(pc[9]), []).append(pc)
+        for x in rowsets[pc[0]:pc[0] + pc[1]]:
+            count[(int(x), int(pc[3]))] = count.get((int(x), int(pc[3])), 0) + 1
+    assert sorted(count) == [(x, g) for x in range(len(leaves)) for g in range(hkv)]
+    emax = max(count.values())
+    entry = {}
     for s in range(n_streams):
         b = blocks[s]
         n_p, n_t, n_s = int(b[0]), int(b[1]), int(b[2])
@@ -128,14 +128,17 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
         assert (n_p, n_t, n_s, b[3]) == (len(pcs), stream_next[s], seg_next[s], 0)
         tiles_at = 4 + 4 * n_p
         segs_at = tiles_at + 2 * (n_t + n_t % 2)
-        assert segs_at + n_s <= bi
-        assert (b[tiles_at + 2 * n_t:segs_at] == 0).all() and (b[segs_at + n_s:] == 0).all()
+        dests_at = segs_at + n_s + (-n_s) % 4
+        assert dests_at + n_s <= bi
+        assert (b[tiles_at + 2 * n_t:segs_at] == 0).all() and (b[segs_at + n_s:dests_at] == 0).all()
+        assert (b[dests_at + n_s:] == 0).all()
         recs = b[4:tiles_at].reshape(-1, 4)
         st = b[tiles_at:tiles_at + 2 * n_t].reshape(-1, 2)
         sg = b[segs_at:segs_at + n_s]
+        dst = b[dests_at:dests_at + n_s]
         for i, pc in enumerate(pcs):
-            rb, nl, rows, g, stile, nt, pbase, seg, _, _, ptile, nq = (int(v) for v in pc[:12])
-            assert tuple(recs[i]) == (rows, stile, nt, pbase)
+            rb, nl, rows, g, stile, nt, _, seg, _, _, ptile, nq = (int(v) for v in pc[:12])
+            assert tuple(recs[i]) == (rows, stile, nt, seg)
             for t in range(nq):
                 assert tuple(st[stile + t]) == (-1 - seg, (64 * t) | (min(64, rows - 64 * t) << 16))
             for t in range(nt):
@@ -146,6 +149,10 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
             for j in range(nl):
                 x = int(rowsets[rb + j])
                 assert 0 <= x < len(leaves) and sg[seg + j] == (x * hq + g * G) * d
+                e = entry.get((x, g), 0)
+                entry[(x, g)] = e + 1
+                assert dst[seg + j] == ((x * hkv + g) * emax + e) * G
+    assert entry == count
 
 
 def _stream_costs(pieces, n_streams):
