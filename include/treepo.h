@@ -144,6 +144,7 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
  * decoding; Sec. 2.3 chains).  leaves: host node ids (any node, duplicates
  * allowed), call position i.
  *   q     device bf16 [n_leaves][Hq][D]   the step's queries (16-byte aligned)
+ *   scale softmax scale, positive and finite (e.g. 1/sqrt(D))
  *   out   device fp32 [n_leaves][Hq][D]   softmax(scale q K^T) V over the chain
  *   lse   device fp32 [n_leaves][Hq] or null: natural-log sum exp(scale q.k)
  *   workspace  device, 256-byte aligned, >= treepo_decode_workspace_size(..., TREEPO_MODE_TREE)
@@ -152,7 +153,8 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
  * per-node partials are merged with a log-sum-exp combine.  The library keeps
  * the plan it uploaded into the workspace and reuses it while the tree and
  * the leaf list are unchanged: do not modify the workspace between calls.
- * EINVAL (bad id, null pointer, n_leaves < 1, q not 16-byte aligned),
+ * EINVAL (bad id, null pointer, n_leaves < 1, q not 16-byte aligned, scale
+ * not positive and finite),
  * EEMPTY (a chain holds no tokens), EWORKSPACE (missing, too small or not
  * 256-byte aligned), EHIP. */
 int32_t treepo_tree_decode(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,

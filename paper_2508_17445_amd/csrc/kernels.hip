@@ -89,37 +89,62 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
                :: "v"(g), "s"(lds) : "memory", "m0");
 }
 
+// The same load from a wave-uniform base address (SGPRs) plus a per-lane byte
+// offset: no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+               :: "v"(voff), "s"(sbase), "s"(lds) : "memory", "m0");
+}
+
 // Loads per lane per tile.
 template <int D>
 constexpr int dma_per_tile() { return D / 32; }
+
+// The tile pipeline of a workgroup: LDS buffers, this lane's byte offsets in
+// a tile's K and V^T ranges for each of its loads (the swizzles of the LDS
+// layout applied on the global side), and the record of the next tile to
+// issue, read from LDS one step early so that a tile's loads go out right
+// after the barrier that frees its buffer.
+template <int D>
+struct Pipe {
+  static constexpr int kPerWave = D / 64;  // 1 KiB slots per wave for each of K and V
+  uint32_t buf0;                           // LDS byte address of buffer 0
+  int ntot;                                // tiles of the stream
+  uint32_t koff[kPerWave], voff[kPerWave];
+  int2 next;                               // record of tile k + kDepth while tile k is current
+};
+
+template <int D>
+__device__ __forceinline__ void pipe_init(Pipe<D>& p, uint32_t buf0, int ntot, int wave, int lane) {
+  constexpr int kKChunks = D / 8;  // 16-byte chunks per K row
+  p.buf0 = buf0;
+  p.ntot = ntot;
+  p.next = make_int2(0, 0);
+#pragma unroll
+  for (int j = 0; j < Pipe<D>::kPerWave; ++j) {
+    const int c = (wave * Pipe<D>::kPerWave + j) * 64 + lane;
+    const int row = c / kKChunks;
+    p.koff[j] = row * (D * 2) + (((c % kKChunks) ^ k_swz(row)) << 4);
+    const int vrow = c >> 2;
+    p.voff[j] = vrow * (kSub * 2) + (((c & 3) ^ v_swz(vrow)) << 4);
+  }
+}
 
 // Stages half block `hb` (= 2 * (g * num_blocks + block) + half) into the LDS
 // buffer at byte address `dst`.
 template <int D>
 __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                         int hb, uint32_t dst, int wave, int lane) {
-  constexpr int kKChunks = D / 8;   // 16-byte chunks per K row
-  constexpr int kPerWave = D / 64;  // 1 KiB slots per wave for each of K and V
+                                         int hb, uint32_t dst, const Pipe<D>& p, int wave) {
   const int64_t off = static_cast<int64_t>(hb) * kSub * D;
-  const char* kg = reinterpret_cast<const char*>(kpool + off);
-  const char* vg = reinterpret_cast<const char*>(vpool + off);
+  const uint16_t* kg = kpool + off;
+  const uint16_t* vg = vpool + off;
   const uint32_t vd = dst + kSub * D * 2;
 #pragma unroll
-  for (int j = 0; j < kPerWave; ++j) {
-    const int slot = wave * kPerWave + j;
-    const int c = slot * 64 + lane;
-    const int row = c / kKChunks;
-    const int col = (c % kKChunks) ^ k_swz(row);
-    dma16(kg + row * (D * 2) + col * 16, __builtin_amdgcn_readfirstlane(dst + slot * 1024));
-  }
+  for (int j = 0; j < Pipe<D>::kPerWave; ++j)
+    dma16s(kg, p.koff[j], __builtin_amdgcn_readfirstlane(dst + (wave * Pipe<D>::kPerWave + j) * 1024));
 #pragma unroll
-  for (int j = 0; j < kPerWave; ++j) {
-    const int slot = wave * kPerWave + j;
-    const int c = slot * 64 + lane;
-    const int row = c >> 2;
-    const int col = (c & 3) ^ v_swz(row);
-    dma16(vg + row * (kSub * 2) + col * 16, __builtin_amdgcn_readfirstlane(vd + slot * 1024));
-  }
+  for (int j = 0; j < Pipe<D>::kPerWave; ++j)
+    dma16s(vg, p.voff[j], __builtin_amdgcn_readfirstlane(vd + (wave * Pipe<D>::kPerWave + j) * 1024));
 }
 
 // Barrier after which this workgroup's global->LDS loads, except the newest N
@@ -179,26 +204,31 @@ __device__ __forceinline__ void dma_qtile(const uint16_t* __restrict__ q, int se
   }
 }
 
-// Issues tile k of the stream (KV or query) into buffer k mod 4.
+// Issues tile k of the stream (KV or query; `rec` its record) into buffer
+// k mod 4.
 template <int D>
-__device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, uint32_t buf0, const BlockTables& bt,
-                                                int wave, int lane) {
+__device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, int2 rec, const BlockTables& bt,
+                                                const Pipe<D>& p, int wave, int lane) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
-  const int hb = __builtin_amdgcn_readfirstlane(bt.tiles[k].x);
-  const uint32_t dst = buf0 + (k & (kNBuf - 1)) * kBufBytes;
+  const int hb = __builtin_amdgcn_readfirstlane(rec.x);
+  const uint32_t dst = p.buf0 + (k & (kNBuf - 1)) * kBufBytes;
   if (hb >= 0) {
-    dma_tile<D>(kpool, vpool, hb, dst, wave, lane);
+    dma_tile<D>(kpool, vpool, hb, dst, p, wave);
   } else {
-    const int y = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
+    const int y = __builtin_amdgcn_readfirstlane(rec.y);
     dma_qtile<D>(q, -1 - hb, y & 0xFFFF, y >> 16, sc.group, bt, dst, wave, lane);
   }
 }
 
-// After tile k is published: prefetch tile k + 3 into the buffer tile k - 1 used.
+// After tile k is published: tile k + 3 into the buffer tile k - 1 used (its
+// record is already in registers), then the record of tile k + 4.
 template <int D>
-__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int ntot, int k, uint32_t buf0,
-                                          const BlockTables& bt, int wave, int lane) {
-  if (k + kDepth < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, k + kDepth, buf0, bt, wave, lane);
+__device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int k, const BlockTables& bt, Pipe<D>& p,
+                                          int wave, int lane) {
+  if (k + kDepth < p.ntot) {
+    dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, k + kDepth, p.next, bt, p, wave, lane);
+    if (k + kDepth + 1 < p.ntot) p.next = bt.tiles[k + kDepth + 1];
+  }
 }
 
 // A piece's record in the stream block.
@@ -255,6 +285,31 @@ __device__ __forceinline__ float softmax_p4(const float (&x)[4], float ref, uint
   return ls;
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Full tile (every token holds data): P = 2^(s scale - ref) for the lane's
+// four raw scores s as hi + lo bf16 pairs.  ref is finite here (a piece's
+// first tile always moves it off -inf).  Returns the sum of the four fp32
+// weights (the represented hi + lo differ from them by < 2^-17 relative).
+__device__ __forceinline__ float weights4(const f32x4& s, float scale_log2, float neg_ref, uint2& P, uint2& PL) {
+  float ls = 0.f;
+  uint32_t ph[2], pl[2];
+#pragma unroll
+  for (int e = 0; e < 4; e += 2) {
+    const float f0 = fast_exp2(fmaf(s[e], scale_log2, neg_ref));
+    const float f1 = fast_exp2(fmaf(s[e + 1], scale_log2, neg_ref));
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){f0, f1}, bf16x2));
+    const float h0 = __builtin_bit_cast(float, h << 16), h1 = __builtin_bit_cast(float, h & 0xFFFF0000u);
+    pl[e >> 1] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){f0 - h0, f1 - h1}, bf16x2));
+    ph[e >> 1] = h;
+    ls += f0 + f1;
+  }
+  P = make_uint2(ph[0], ph[1]);
+  PL = make_uint2(pl[0], pl[1]);
+  return ls;
+}
+
 // Clears the V^T entries of tokens tok0..tok0+3 past the node's length (their
 // P is 0, but the pool may hold any bits there).
 __device__ __forceinline__ uint2 mask_v4(uint2 v, int tok0, int valid) {
@@ -278,8 +333,8 @@ __device__ __forceinline__ uint2 mask_v4(uint2 v, int tok0, int valid) {
 //       the wave's d-blocks (A = 16 d-rows of V^T, B = P^T: the lane's eight
 //       scores, tokens 8(lane/16) + 0..7).
 template <int D, int DSPLIT>
-__device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceRec& pc, int ntot, uint32_t buf0,
-                                             Smem<D>& sm, const BlockTables& bt) {
+__device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceRec& pc, Pipe<D>& pp, Smem<D>& sm,
+                                             const BlockTables& bt) {
   constexpr int kKS = D / 32;             // QK k-steps
   constexpr int kDBw = D / 16 / DSPLIT;   // PV output d-blocks of this wave
   const int lane = threadIdx.x & 63;
@@ -294,8 +349,8 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
 
   // ---- the piece's query tile: Q^T operands, lane holds row m, d chunk 4 ks + a
   uint4 qb[kKS];
-  wait_tile<D>(k0, ntot);
-  dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k0, buf0, bt, wave, lane);
+  wait_tile<D>(k0, pp.ntot);
+  dma_ahead<D>(TREEPO_PARTIAL_ARGS, k0, bt, pp, wave, lane);
   {
     const uint4* qt = reinterpret_cast<const uint4*>(sm.kv[k0 & (kNBuf - 1)]) + m * (D / 8);
 #pragma unroll
@@ -309,9 +364,9 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
   float l_sum = 0.f;        // per lane: this lane's tokens only
 
   for (int k = k0 + 1; k <= k0 + nk; ++k) {
-    wait_tile<D>(k, ntot);
+    wait_tile<D>(k, pp.ntot);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, k, bt, pp, wave, lane);
     const int valid = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k, buf0, bt, wave, lane);
     if (!active) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
@@ -327,7 +382,36 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
         S[b] = mfma16(ka, qb[ks], S[b]);
       }
     }
-    // ---- scores (log2 units), masked past the node's length; lazy reference
+    // ---- scores (log2 units) with a lazy reference: O and the sum are
+    // rescaled only when a row's maximum passes it by more than the slack
+    if (valid == kSub) {
+      // full tile (the common case): no masking; max over the raw scores
+      // (the scale is positive)
+      float mx = fmaxf(fmaxf(fmaxf(S[0][0], S[0][1]), fmaxf(S[0][2], S[0][3])),
+                       fmaxf(fmaxf(S[1][0], S[1][1]), fmaxf(S[1][2], S[1][3]))) * sc.scale_log2;
+      if (__builtin_amdgcn_ballot_w64(mx > m_ref + kLazyMaxSlack) != 0) {
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mn = fmaxf(m_ref, mx);
+        const float alpha = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - mn);
+        m_ref = mn;
+        l_sum *= alpha;
+#pragma unroll
+        for (int db = 0; db < kDBw; ++db) acc[db] *= alpha;
+      }
+      uint2 p0, pl0, p1, pl1;
+      l_sum += weights4(S[0], sc.scale_log2, -m_ref, p0, pl0) + weights4(S[1], sc.scale_log2, -m_ref, p1, pl1);
+      const uint4 P = make_uint4(p0.x, p0.y, p1.x, p1.y), PL = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
+      // ---- O^T += V^T P^T for the wave's d-blocks
+#pragma unroll
+      for (int db = 0; db < kDBw; ++db) {
+        const int d = 16 * (db0 + db) + r16;
+        const uint4 va = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
+        acc[db] = mfma16(va, PL, mfma16(va, P, acc[db]));
+      }
+      continue;
+    }
+    // the node's last tile: tokens past its length are masked
     float x[2][4];
     float mx = -INFINITY;
 #pragma unroll
@@ -350,16 +434,13 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
     uint2 p0, pl0, p1, pl1;
     l_sum += softmax_p4(x[0], m_ref, p0, pl0) + softmax_p4(x[1], m_ref, p1, pl1);
     const uint4 P = make_uint4(p0.x, p0.y, p1.x, p1.y), PL = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
-    // ---- O^T += V^T P^T for the wave's d-blocks
 #pragma unroll
     for (int db = 0; db < kDBw; ++db) {
       const int d = 16 * (db0 + db) + r16;
       uint4 va = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
-      if (valid < kSub) {
-        const uint2 lo = mask_v4(make_uint2(va.x, va.y), 8 * a, valid);
-        const uint2 hi = mask_v4(make_uint2(va.z, va.w), 8 * a + 4, valid);
-        va = make_uint4(lo.x, lo.y, hi.x, hi.y);
-      }
+      const uint2 lo = mask_v4(make_uint2(va.x, va.y), 8 * a, valid);
+      const uint2 hi = mask_v4(make_uint2(va.z, va.w), 8 * a + 4, valid);
+      va = make_uint4(lo.x, lo.y, hi.x, hi.y);
       acc[db] = mfma16(va, PL, mfma16(va, P, acc[db]));
     }
   }
@@ -390,8 +471,8 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
 //   PV: O^T += V^T P^T with v_mfma_f32_16x16x32_bf16 over all 32 tokens (A =
 //       16 d-rows of the transposed V tile, B = P^T: the lane's eight scores).
 template <int D, int NRB>
-__device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec& pc, int ntot, uint32_t buf0,
-                                           Smem<D>& sm, const BlockTables& bt) {
+__device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec& pc, Pipe<D>& pp, Smem<D>& sm,
+                                           const BlockTables& bt) {
   constexpr int kKS = D / 32;
   constexpr int kDB = D / 16;
   const int lane = threadIdx.x & 63;
@@ -409,8 +490,8 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
 #pragma unroll
   for (int i = 0; i < NRB; ++i) {
     if (i >= nq) continue;
-    wait_tile<D>(k0 + i, ntot);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k0 + i, buf0, bt, wave, lane);
+    wait_tile<D>(k0 + i, pp.ntot);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, k0 + i, bt, pp, wave, lane);
     const int m = 16 * (wave + 4 * i) + r16;
     const uint4* qt =
         reinterpret_cast<const uint4*>(sm.kv[(k0 + i) & (kNBuf - 1)]) + (m - kQTileRows * i) * (D / 8);
@@ -429,9 +510,9 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
   }
 
   for (int k = k0 + nq; k < k0 + nq + nk; ++k) {
-    wait_tile<D>(k, ntot);
+    wait_tile<D>(k, pp.ntot);
+    dma_ahead<D>(TREEPO_PARTIAL_ARGS, k, bt, pp, wave, lane);
     const int valid = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
-    dma_ahead<D>(TREEPO_PARTIAL_ARGS, ntot, k, buf0, bt, wave, lane);
     if (my_rb == 0) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
@@ -551,23 +632,26 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
   const int seg_at = tile_at + 2 * ((ntot + 1) & ~1);
   const BlockTables bt{reinterpret_cast<const int2*>(sm.blk + tile_at), sm.blk + seg_at,
                        sm.blk + seg_at + ((nseg + 3) & ~3)};
+  Pipe<D> pp;
+  pipe_init<D>(pp, buf0, ntot, wave, lane);
 #pragma unroll
   for (int t = 0; t < kDepth; ++t)
-    if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, buf0, bt, wave, lane);
+    if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, bt.tiles[t], bt, pp, wave, lane);
+  if (kDepth < ntot) pp.next = bt.tiles[kDepth];
   for (int pi = 0; pi < np; ++pi) {
     const int4 r = *reinterpret_cast<const int4*>(sm.blk + kBlockHeaderInts + kBlockPieceInts * pi);
     const PieceRec pc{__builtin_amdgcn_readfirstlane(r.x), __builtin_amdgcn_readfirstlane(r.y),
                       __builtin_amdgcn_readfirstlane(r.z), __builtin_amdgcn_readfirstlane(r.w)};
     if (pc.rows <= 16) {
-      dsplit_piece<D, 4>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);
+      dsplit_piece<D, 4>(TREEPO_PARTIAL_ARGS, pc, pp, sm, bt);
     } else if (pc.rows <= kSplitMaxRows) {
-      dsplit_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);
+      dsplit_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, pp, sm, bt);
     } else {
       const int nrb = (((pc.rows + 15) >> 4) + 3) >> 2;
       if (nrb == 1)
-        rows_piece<D, 1>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);
+        rows_piece<D, 1>(TREEPO_PARTIAL_ARGS, pc, pp, sm, bt);
       else
-        rows_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, ntot, buf0, sm, bt);  // the planner keeps pieces at <= 128 rows
+        rows_piece<D, 2>(TREEPO_PARTIAL_ARGS, pc, pp, sm, bt);  // the planner keeps pieces at <= 128 rows
     }
   }
 }

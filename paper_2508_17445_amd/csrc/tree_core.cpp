@@ -177,6 +177,9 @@ struct Run {
 
 // A piece's query tiles cost little next to its KV tiles (a few rows each).
 constexpr double kQTileCost = 0.25;
+// Guided stream sizes when the work takes several rounds of workgroups.
+constexpr double kGuide = 2.0;
+constexpr double kGuideMinCost = 8.0;
 
 // Estimated cost of one KV tile for a piece of `rows` query rows, in units of
 // one tile's load time at full load (measured): the token-split path (up to
@@ -292,22 +295,27 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     return kEEmpty;
   }
 
-  // ---- streams: cut the concatenated sequences at equal cumulative cost --------
+  // ---- streams ------------------------------------------------------------------
+  // One round (every stream resident at once): the concatenated sequences are
+  // cut at equal cumulative cost, each stream's share in proportion to its
+  // slot's speed.  Several rounds: later streams start wherever a slot frees
+  // up, so the hardware dispatcher balances them; stream sizes shrink with the
+  // work left (each takes 1/kGuide of an even share of the remainder, between
+  // kGuideMinCost and a full LDS table), so the last streams to start are
+  // short and the slots drain together.
   const int64_t S0 = std::max(1, p.concurrent_wgs);
-  const int64_t per_round = S0 * (3 * kMaxStreamTiles / 4);
-  const int64_t rounds = std::max<int64_t>(1, (total_tiles + per_round - 1) / per_round);
-  const int64_t planned = std::min<int64_t>(total_tiles, S0 * rounds);
-  // Stream s closes once the running cost passes quota[s]: its share of the
-  // total in proportion to its placement's speed (one round only: later
-  // rounds start wherever a slot frees up), plus slack for the query tiles of
-  // a cut piece that every stream may start with, so that the last stream
-  // does not collect the rounding remainder.
-  std::vector<double> quota(static_cast<size_t>(planned));
-  {
+  const double full_stream = 3 * kMaxStreamTiles / 4;
+  const bool one_round = total_cost <= static_cast<double>(S0) * full_stream;
+  const int64_t planned = one_round ? std::min<int64_t>(total_tiles, S0) : INT64_MAX;
+  // One round: stream s closes once the running cost passes quota[s], plus
+  // slack for the query tiles of a cut piece that every stream may start
+  // with, so that the last stream does not collect the rounding remainder.
+  std::vector<double> quota;
+  if (one_round) {
+    quota.resize(static_cast<size_t>(planned));
     std::vector<double> w(static_cast<size_t>(planned), 1.0);
-    if (planned <= S0 && p.compute_units > 0) {
+    if (p.compute_units > 0)
       for (int64_t s = 0; s < planned; ++s) w[s] = p.slot_speed[s < p.compute_units ? 0 : 1];
-    }
     double wsum = 0.0;
     for (double x : w) wsum += x;
     double cum = 0.0;
@@ -316,6 +324,16 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       quota[s] = total_cost * cum / wsum + 2 * kQTileCost * static_cast<double>(s + 1);
     }
   }
+  // Several rounds: the open stream closes once the running cost reaches
+  // guided_end; its size follows the KV work not yet assigned (kv_acc counts
+  // KV tiles only, as total_kv_cost does).
+  double total_kv_cost = 0.0, kv_acc = 0.0, guided_end = 0.0;
+  for (const Seq& sq : seqs)
+    total_kv_cost += tile_cost(sq.n_leaves * G) * static_cast<double>(runs[sq.run].tiles.size());
+  auto guided_quota = [&](double acc_now) {
+    const double share = (total_kv_cost - kv_acc) / (kGuide * static_cast<double>(S0));
+    return acc_now + std::min(full_stream, std::max(kGuideMinCost, share));
+  };
   double acc = 0.0;
   auto pad_to = [](auto* v, size_t m, auto fill) {
     while (v->size() % m) v->push_back(fill);
@@ -330,6 +348,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     out->streams.push_back(st);
   };
   open_stream();
+  if (!one_round) guided_end = guided_quota(0.0);
   for (int32_t si = 0; si < static_cast<int32_t>(seqs.size()); ++si) {
     const Seq& sq = seqs[si];
     const Run& r = runs[sq.run];
@@ -340,7 +359,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     for (const Tile& tl : r.tiles) {
       Stream* st = &out->streams.back();
       const int64_t s = static_cast<int64_t>(out->streams.size()) - 1;
-      const bool full = s + 1 < planned && acc >= quota[s];
+      const bool full = one_round ? s + 1 < planned && acc >= quota[s] : acc >= guided_end;
       const bool room = st->n_tiles + (new_piece ? nq + 1 : 1) <= kMaxStreamTiles &&
                         st->n_segs + (new_piece ? sq.n_leaves : 0) <= kMaxStreamSegs &&
                         st->piece_end - st->piece_begin + (new_piece ? 1 : 0) <= kMaxStreamPieces;
@@ -348,6 +367,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         open_stream();
         st = &out->streams.back();
         new_piece = true;
+        if (!one_round) guided_end = guided_quota(acc);
       }
       if (new_piece) {
         Piece pc{};
@@ -386,6 +406,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       ++st->n_tiles;
       ++out->pieces.back().n_tiles;
       acc += c;
+      kv_acc += c;
     }
   }
   pad_to(&out->stream_tiles, 2, StreamTile{0, 0});

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <array>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <string>
@@ -225,6 +226,7 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   if (!ctx) return TREEPO_EINVAL;
   if (!q || !out) return fail(ctx, TREEPO_EINVAL, "null q or out");
   if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return fail(ctx, TREEPO_EINVAL, "q must be 16-byte aligned");
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(ctx, TREEPO_EINVAL, "scale must be positive and finite");
   std::string err;
   int32_t st = ctx->tree.check_leaves(n, leaves, &err);
   if (st != treepo::kOk) return fail(ctx, st, err);

@@ -63,6 +63,9 @@ def test_each_code_and_no_state_change():
     # decode: workspace is checked before any device work
     assert _code(ctx.tree_decode, [a], FAKE_POOL, 0.1, FAKE_POOL, None, None, 0) == T.EWORKSPACE
     assert _code(ctx.tree_decode, [a], None, 0.1, FAKE_POOL, None, FAKE_POOL, 1 << 30) == T.EINVAL
+    for bad_scale in (0.0, -0.1, float("inf"), float("nan")):
+        assert _code(ctx.tree_decode, [a], FAKE_POOL, bad_scale, FAKE_POOL, None, FAKE_POOL, 1 << 30) == T.EINVAL
+        assert "scale" in ctx.lib.treepo_last_error(ctx.h).decode()
     # append with tokens but no K/V buffers
     assert _code(ctx.kv_append, [a], [1], None, None, 0) == T.EINVAL
     assert ctx.export_nodes()[a][3] == 0

@@ -155,10 +155,10 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
     assert entry == count
 
 
-def _stream_costs(pieces, n_streams):
+def _stream_costs(pieces, n_streams, q_cost=0.25):
     cost = np.zeros(n_streams)
     for pc in pieces:
-        cost[pc[9]] += pc[5] * _tile_cost(pc[2]) + 0.25 * pc[11]
+        cost[pc[9]] += pc[5] * _tile_cost(pc[2]) + q_cost * pc[11]
     return cost
 
 
@@ -181,26 +181,43 @@ def test_plan_covers_each_chain_token_once(cfg):
 
 
 @pytest.mark.parametrize("cfg", [2, 4])
-def test_streams_are_balanced(cfg):
-    """One stream per resident workgroup slot (512), estimated cost in
-    proportion to the slot's speed to within about two tiles."""
+def test_stream_sizes(cfg):
+    """One round of resident workgroups (at most 512 x 192 cost units): one
+    stream per slot, estimated cost in proportion to the slot's speed to
+    within about two tiles.  More work: guided sizes, each stream 1/2 of an
+    even 512-way share of the work not yet assigned, clamped to [8, 192]."""
     log = build_call_log(cfg)
     from workloads import CONFIGS
     c = CONFIGS[cfg]
     ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
     replay_host(ctx, log)
     model = oracle_model(log)
+    seen = set()
     for mode in (0, 1):
         pieces, tiles, n_streams = _plan_checks(ctx, model, log.leaves, mode)
-        total = len(tiles)
-        rounds = -(-total // (512 * 192))
-        assert n_streams <= min(total, 512 * rounds) and n_streams >= 0.95 * min(total, 512 * rounds)
         cost = _stream_costs(pieces, n_streams)
-        if rounds == 1:
-            # the second slot of a CU (streams 256 on) is sized at 0.85 of the first
-            cost = cost / np.where(np.arange(n_streams) < 256, 1.0, 0.85)
-        assert cost.max() <= cost.mean() + 2 * 2.0 + 1.0, (mode, cost.mean(), cost.max())
-        assert cost.min() >= cost.mean() - 2 * 2.0 - 1.0 or n_streams < 512 * rounds
+        total = cost.sum()
+        if total <= 512 * 192:
+            seen.add("one round")
+            assert n_streams == min(len(tiles), 512) or n_streams >= 0.95 * min(len(tiles), 512)
+            rel = cost / np.where(np.arange(n_streams) < 256, 1.0, 0.85)
+            assert rel.max() <= rel.mean() + 2 * 2.0 + 1.0, (mode, rel.mean(), rel.max())
+            assert rel.min() >= rel.mean() - 2 * 2.0 - 1.0 or n_streams < 512
+        else:
+            seen.add("guided")
+            kv = _stream_costs(pieces, n_streams, q_cost=0.0)
+            before = np.concatenate([[0.0], np.cumsum(kv)[:-1]])
+            want = np.clip((kv.sum() - before) / (2 * 512), 8, 192)
+            # a stream closes on the first tile that reaches its size (plus the
+            # query tiles of a piece it opens) unless its tile table fills first
+            assert (cost[:-1] <= want[:-1] + 2.0 + 0.5).all()
+            # ... or one of its tables (tiles, query segments, pieces) fills first
+            hdr = ctx.export_blocks(log.leaves, mode)[:, :3]
+            table_full = (hdr[:, 1] >= 256 - 3) | (hdr[:, 2] > 256 - 128 // (c.hq // c.hkv)) | (hdr[:, 0] >= 127)
+            short = cost[:-1] < want[:-1] - 1e-6
+            assert table_full[:-1][short].all()
+            assert cost[-1] <= want[-1] + 2.5
+    assert seen == {2: {"one round"}, 4: {"guided"}}[cfg]
 
 
 def test_duplicate_and_interior_leaves():
