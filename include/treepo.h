@@ -65,6 +65,16 @@ typedef struct treepo_ctx treepo_ctx;
  * stream 32-token half blocks), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned,
  * 16-byte aligned, and must stay valid until treepo_destroy; their contents
  * need no initialisation.
+ *
+ * node_len (optional, device int32[max_nodes], caller-owned, contents kept by
+ * the library, valid until treepo_destroy): the nodes' token counts on the
+ * device.  With it, a decode plan stays valid while the tree only grows by
+ * appends (segment-level decoding: one append and one decode per step until
+ * the next fork, Sec. 2.2): the plan covers every unfrozen node up to its
+ * capacity and the kernels read the current lengths from node_len, so no
+ * re-plan or re-upload happens between forks.  treepo_kv_append updates it on
+ * the stream; after treepo_kv_commit, new_root or fork the next decode
+ * re-uploads the table on its stream.  NULL: every length change re-plans.
  */
 typedef struct treepo_config {
   int32_t num_q_heads;  /* Hq  */
@@ -76,6 +86,7 @@ typedef struct treepo_config {
   int32_t reserved;     /* must be 0                                    */
   void* k_pool;         /* device, see above                            */
   void* v_pool;         /* device, see above                            */
+  void* node_len;       /* device int32[max_nodes] or NULL, see above   */
 } treepo_config;
 
 /* Records exported by treepo_export_plan. */
@@ -211,7 +222,9 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  * query tiles (64 rows each) from stream_tile on, then n_tiles KV tiles, and
  * its query segments start at seg_begin there; its KV tiles are
  * tiles[plan_tile .. + n_tiles),
- * TREEPO_TILE_FIELDS int32 each {block, node, tile_in_node, valid_tokens}:
+ * TREEPO_TILE_FIELDS int32 each {block, node, tile_in_node, valid_tokens}
+ * (valid_tokens as of planning; with node_len a plan is reused while nodes
+ * grow and the kernels read the current counts of tiles not yet full):
  * tile k of a node holds its tokens [32k, 32k+32) and lives in pool block
  * block_begin + k/2.  *n_streams receives the stream count.  Pass null arrays
  * to query the counts only. */

@@ -10,7 +10,8 @@ hipError_t launch_partial(const DecodeArgs&, hipStream_t) { return hipErrorNoDev
 hipError_t launch_combine(const DecodeArgs&, hipStream_t) { return hipErrorNoDevice; }
 int32_t partial_workgroups_per_cu() { return 2; }
 hipError_t launch_kv_append(const uint16_t*, const uint16_t*, uint16_t*, uint16_t*, int64_t, int32_t, int32_t,
-                            const AppendPiece*, int32_t, hipStream_t) {
+                            const AppendPiece*, int32_t, const int32_t*, const int32_t*, int32_t, int32_t*,
+                            hipStream_t) {
   return hipErrorNoDevice;
 }
 

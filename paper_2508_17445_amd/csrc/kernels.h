@@ -17,6 +17,7 @@ struct DecodeArgs {
   int32_t hq, hkv, group, d;
   const uint16_t* q;       // bf16 [n_leaves][Hq][D]
   float scale_log2;        // softmax scale * log2(e)
+  const int32_t* node_len; // device token count per node (live tiles), or null
   const int32_t* blocks;   // stream blocks, block_ints int32 each (layout in tree_core.h)
   int32_t block_ints;
   int32_t n_streams;
@@ -46,8 +47,11 @@ struct AppendPiece {
   int32_t count;
 };
 
+// node_len (device lengths table or null) receives len[i] at node[i] for the
+// n_upd appended nodes (n_upd <= n_pieces).
 hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool,
                             uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
-                            const AppendPiece* pieces, int32_t n_pieces, hipStream_t s);
+                            const AppendPiece* pieces, int32_t n_pieces, const int32_t* upd_node,
+                            const int32_t* upd_len, int32_t n_upd, int32_t* node_len, hipStream_t s);
 
 }  // namespace treepo

@@ -64,15 +64,27 @@ template <int D>
 struct Smem {
   static constexpr int kElems = kSub * D;  // K (or V^T) elements per tile
   uint16_t kv[kNBuf][2 * kElems];
-  int32_t blk[kMaxBlockInts];              // the stream's block (pieces, tiles, segments)
+  int32_t blk[kMaxBlockInts];              // the stream's block (pieces, tiles, segments, live tiles)
+  int32_t live_len[kMaxStreamLive];        // current length of each live tile's node
 };
 
 // LDS views of the stream block's tables.
 struct BlockTables {
-  const int2* tiles;     // StreamTile records
-  const int32_t* segs;   // query segment offsets
-  const int32_t* dests;  // per (piece, leaf): partial row of its h' = 0
+  const int2* tiles;        // StreamTile records
+  const int32_t* segs;      // query segment offsets
+  const int32_t* dests;     // per (piece, leaf): partial row of its h' = 0
+  const int32_t* live;      // per live tile: node, base (first token of the tile)
+  const int32_t* live_len;  // per live tile: its node's length at this decode
 };
+
+// Tokens of a KV tile from its record's valid field: the planned count, or,
+// for a live tile, the tokens its node holds now past the tile's first.
+__device__ __forceinline__ int tile_tokens(int y, const BlockTables& bt) {
+  if (y >= 0) return y;
+  const int i = -1 - y;
+  const int v = __builtin_amdgcn_readfirstlane(bt.live_len[i]) - __builtin_amdgcn_readfirstlane(bt.live[2 * i + 1]);
+  return v < 0 ? 0 : (v > kSub ? kSub : v);
+}
 
 __device__ __forceinline__ int k_swz(int r) { return (r & 3) | ((r >> 1) & 4); }
 __device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
@@ -86,6 +98,13 @@ __device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 3; }
 // barrier that publishes a tile.
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
+               :: "v"(g), "s"(lds) : "memory", "m0");
+}
+
+// One 4-byte global->LDS load per lane (lane l writes bytes [4 l, 4 l + 4) at
+// `lds`).
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                :: "v"(g), "s"(lds) : "memory", "m0");
 }
 
@@ -132,19 +151,21 @@ __device__ __forceinline__ void pipe_init(Pipe<D>& p, uint32_t buf0, int ntot, i
 
 // Stages half block `hb` (= 2 * (g * num_blocks + block) + half) into the LDS
 // buffer at byte address `dst`.
+// An empty live tile keeps its place in the load count, but every lane reads
+// the tile's first 16 bytes (one request per load instruction).
 template <int D>
 __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                         int hb, uint32_t dst, const Pipe<D>& p, int wave) {
+                                         int hb, bool empty, uint32_t dst, const Pipe<D>& p, int wave) {
   const int64_t off = static_cast<int64_t>(hb) * kSub * D;
   const uint16_t* kg = kpool + off;
   const uint16_t* vg = vpool + off;
   const uint32_t vd = dst + kSub * D * 2;
 #pragma unroll
   for (int j = 0; j < Pipe<D>::kPerWave; ++j)
-    dma16s(kg, p.koff[j], __builtin_amdgcn_readfirstlane(dst + (wave * Pipe<D>::kPerWave + j) * 1024));
+    dma16s(kg, empty ? 0u : p.koff[j], __builtin_amdgcn_readfirstlane(dst + (wave * Pipe<D>::kPerWave + j) * 1024));
 #pragma unroll
   for (int j = 0; j < Pipe<D>::kPerWave; ++j)
-    dma16s(vg, p.voff[j], __builtin_amdgcn_readfirstlane(vd + (wave * Pipe<D>::kPerWave + j) * 1024));
+    dma16s(vg, empty ? 0u : p.voff[j], __builtin_amdgcn_readfirstlane(vd + (wave * Pipe<D>::kPerWave + j) * 1024));
 }
 
 // Barrier after which this workgroup's global->LDS loads, except the newest N
@@ -213,7 +234,8 @@ __device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, in
   const int hb = __builtin_amdgcn_readfirstlane(rec.x);
   const uint32_t dst = p.buf0 + (k & (kNBuf - 1)) * kBufBytes;
   if (hb >= 0) {
-    dma_tile<D>(kpool, vpool, hb, dst, p, wave);
+    const int y = __builtin_amdgcn_readfirstlane(rec.y);
+    dma_tile<D>(kpool, vpool, hb, y < 0 && tile_tokens(y, bt) == 0, dst, p, wave);
   } else {
     const int y = __builtin_amdgcn_readfirstlane(rec.y);
     dma_qtile<D>(q, -1 - hb, y & 0xFFFF, y >> 16, sc.group, bt, dst, wave, lane);
@@ -366,8 +388,8 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
   for (int k = k0 + 1; k <= k0 + nk; ++k) {
     wait_tile<D>(k, pp.ntot);
     dma_ahead<D>(TREEPO_PARTIAL_ARGS, k, bt, pp, wave, lane);
-    const int valid = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
-    if (!active) continue;
+    const int valid = tile_tokens(__builtin_amdgcn_readfirstlane(bt.tiles[k].y), bt);
+    if (!active || valid == 0) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
     // ---- S^T = K Q^T for the 32 tokens
@@ -512,8 +534,8 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
   for (int k = k0 + nq; k < k0 + nq + nk; ++k) {
     wait_tile<D>(k, pp.ntot);
     dma_ahead<D>(TREEPO_PARTIAL_ARGS, k, bt, pp, wave, lane);
-    const int valid = __builtin_amdgcn_readfirstlane(bt.tiles[k].y);
-    if (my_rb == 0) continue;
+    const int valid = tile_tokens(__builtin_amdgcn_readfirstlane(bt.tiles[k].y), bt);
+    if (my_rb == 0 || valid == 0) continue;
     const char* kt = reinterpret_cast<const char*>(sm.kv[k & (kNBuf - 1)]);
     const char* vt = kt + kSub * D * 2;
     // ---- S^T = K Q^T for the wave's row blocks
@@ -611,7 +633,9 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
 // record comes from LDS, so no compiler-inserted wait ever drains it.
 template <int D>
 __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int32_t* __restrict__ blocks,
-                                                                     int32_t block_ints, TREEPO_PARTIAL_PARAMS) {
+                                                                     int32_t block_ints,
+                                                                     const int32_t* __restrict__ node_len,
+                                                                     TREEPO_PARTIAL_PARAMS) {
   __shared__ __attribute__((aligned(1024))) Smem<D> sm;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -628,10 +652,17 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
   const int np = __builtin_amdgcn_readfirstlane(sm.blk[0]);
   const int ntot = __builtin_amdgcn_readfirstlane(sm.blk[1]);
   const int nseg = __builtin_amdgcn_readfirstlane(sm.blk[2]);
+  const int n_live = __builtin_amdgcn_readfirstlane(sm.blk[3]);
   const int tile_at = kBlockHeaderInts + kBlockPieceInts * np;
   const int seg_at = tile_at + 2 * ((ntot + 1) & ~1);
+  const int live_at = seg_at + 2 * ((nseg + 3) & ~3);
   const BlockTables bt{reinterpret_cast<const int2*>(sm.blk + tile_at), sm.blk + seg_at,
-                       sm.blk + seg_at + ((nseg + 3) & ~3)};
+                       sm.blk + seg_at + ((nseg + 3) & ~3), sm.blk + live_at, sm.live_len};
+  // live tiles: their nodes' current lengths, gathered into LDS ahead of the
+  // first tile loads (older loads, so they have landed when tile 0 has)
+  for (int c0 = wave * 64; c0 < n_live; c0 += kThreads)
+    if (c0 + lane < n_live)
+      dma4(node_len + bt.live[2 * (c0 + lane)], __builtin_amdgcn_readfirstlane(lds_addr(sm.live_len + c0)));
   Pipe<D> pp;
   pipe_init<D>(pp, buf0, ntot, wave, lane);
 #pragma unroll
@@ -795,9 +826,10 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
 // blocks.
 constexpr int kMaxPieces = 128;
 struct AppendBatch {
-  int32_t n;
-  int32_t pad;
+  int32_t n;      // pieces
+  int32_t n_upd;  // length updates (node, length)
   AppendPiece p[kMaxPieces];
+  int2 upd[kMaxPieces];
 };
 
 template <int D>
@@ -806,9 +838,12 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
                                                              uint16_t* __restrict__ kpool,
                                                              uint16_t* __restrict__ vpool,
                                                              int64_t num_blocks, int32_t hkv,
-                                                             AppendBatch b) {
+                                                             int32_t* __restrict__ node_len, AppendBatch b) {
   constexpr int kPad = D + 2;
   __shared__ uint16_t vt[kTile * kPad];
+  if (node_len != nullptr && blockIdx.y == 0 && threadIdx.x == 0 && static_cast<int>(blockIdx.x) < b.n_upd)
+    node_len[b.upd[blockIdx.x].x] = b.upd[blockIdx.x].y;
+  if (static_cast<int>(blockIdx.x) >= b.n) return;
   const AppendPiece pc = b.p[blockIdx.x];
   const int g = blockIdx.y;
   const int64_t blk = static_cast<int64_t>(g) * num_blocks + pc.block;
@@ -844,11 +879,11 @@ hipError_t launch_partial(const DecodeArgs& a, hipStream_t s) {
   const Scalars sc{a.hq, a.hkv, a.group, a.scale_log2};
   if (a.block_ints <= 0 || a.block_ints > kMaxBlockInts || a.block_ints % 4 != 0) return hipErrorInvalidValue;
   if (a.d == 128)
-    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.k_pool, a.v_pool, a.q, a.part_o,
-                                                  a.part_ml, sc);
+    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,
+                                                  a.part_o, a.part_ml, sc);
   else
-    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.k_pool, a.v_pool, a.q, a.part_o,
-                                                 a.part_ml, sc);
+    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,
+                                                 a.part_o, a.part_ml, sc);
   return hipGetLastError();
 }
 
@@ -866,16 +901,21 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
 
 hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool,
                             uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
-                            const AppendPiece* pieces, int32_t n_pieces, hipStream_t s) {
-  for (int32_t p0 = 0; p0 < n_pieces; p0 += kMaxPieces) {
+                            const AppendPiece* pieces, int32_t n_pieces, const int32_t* upd_node,
+                            const int32_t* upd_len, int32_t n_upd, int32_t* node_len, hipStream_t s) {
+  if (node_len == nullptr) n_upd = 0;
+  for (int32_t p0 = 0; p0 < n_pieces || p0 < n_upd; p0 += kMaxPieces) {
     AppendBatch b{};
-    b.n = n_pieces - p0 < kMaxPieces ? n_pieces - p0 : kMaxPieces;
+    b.n = n_pieces - p0 < kMaxPieces ? (n_pieces > p0 ? n_pieces - p0 : 0) : kMaxPieces;
+    b.n_upd = n_upd - p0 < kMaxPieces ? (n_upd > p0 ? n_upd - p0 : 0) : kMaxPieces;
     for (int32_t i = 0; i < b.n; ++i) b.p[i] = pieces[p0 + i];
-    const dim3 grid(static_cast<unsigned>(b.n), static_cast<unsigned>(hkv));
+    for (int32_t i = 0; i < b.n_upd; ++i) b.upd[i] = make_int2(upd_node[p0 + i], upd_len[p0 + i]);
+    const int32_t gx = b.n > b.n_upd ? b.n : b.n_upd;
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(hkv));
     if (d == 128)
-      kv_append_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, b);
+      kv_append_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len, b);
     else
-      kv_append_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, b);
+      kv_append_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len, b);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -54,6 +54,7 @@ int32_t Tree::new_root(int32_t cap, int32_t* node_out, std::string* err) {
   if (st != kOk) return st;
   *node_out = make(-1, 0, 0, cap, n_roots_++);
   ++version_;
+  ++shape_version_;
   return kOk;
 }
 
@@ -72,6 +73,7 @@ int32_t Tree::fork(int32_t parent, int32_t n, int32_t cap, int32_t* out, std::st
   for (int32_t i = 0; i < n; ++i) out[i] = make(parent, p.depth + 1, p.start + p.len, cap, p.tree_id);
   nodes_[parent].n_children += n;
   ++version_;
+  ++shape_version_;
   return kOk;
 }
 
@@ -172,6 +174,8 @@ struct Run {
   std::vector<int32_t> nodes;   // root-first
   std::vector<int32_t> leaves;  // ascending call positions
   std::vector<Tile> tiles;
+  std::vector<char> live;       // per tile: token count read at decode time
+  double weight = 0.0;          // tiles, an empty live tile counting kLiveEmptyWeight
   int32_t group_leaves = 1;     // leaves per group
 };
 
@@ -180,6 +184,10 @@ constexpr double kQTileCost = 0.25;
 // Guided stream sizes when the work takes several rounds of workgroups.
 constexpr double kGuide = 2.0;
 constexpr double kGuideMinCost = 8.0;
+// A live tile empty at planning time costs a few loads and no compute until it
+// fills; the plan serves a whole segment, so it is weighted at about its
+// average over the segment.
+constexpr double kLiveEmptyWeight = 0.5;
 
 // Estimated cost of one KV tile for a piece of `rows` query rows, in units of
 // one tile's load time at full load (measured): the token-split path (up to
@@ -247,13 +255,19 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       const int32_t ln = nd[n].len;
       constexpr int32_t T = kPlanTileTokens;
       const int32_t per_block = B / T;
-      for (int32_t k = 0; k * T < ln; ++k) {
+      // with device lengths an unfrozen node is planned up to its capacity
+      const bool grows = p.live_lengths && nd[n].n_children == 0 && ln < nd[n].cap;
+      const int32_t span = grows ? nd[n].cap : ln;
+      for (int32_t k = 0; k * T < span; ++k) {
         Tile tl;
         tl.block = nd[n].block_begin + k / per_block;
         tl.node = n;
         tl.tile_in_node = k;
-        tl.valid = std::min(T, ln - k * T);
+        tl.valid = std::max(0, std::min(T, ln - k * T));
+        const bool live = grows && (k + 1) * T > ln;
         r.tiles.push_back(tl);
+        r.live.push_back(live ? 1 : 0);
+        r.weight += live && tl.valid == 0 ? kLiveEmptyWeight : 1.0;
         out->unique_kv_tokens += tl.valid;
       }
     }
@@ -284,7 +298,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       out->kv_token_visits += tok;
       for (int32_t g = 0; g < Hkv; ++g) {
         seqs.push_back(Seq{ri, rs, l1 - l0, g});
-        total_cost += tile_cost((l1 - l0) * G) * static_cast<double>(r.tiles.size()) +
+        total_cost += tile_cost((l1 - l0) * G) * r.weight +
                       kQTileCost * ((l1 - l0) * G + kQTileRows - 1) / kQTileRows;
         total_tiles += static_cast<int64_t>(r.tiles.size());
       }
@@ -328,8 +342,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   // guided_end; its size follows the KV work not yet assigned (kv_acc counts
   // KV tiles only, as total_kv_cost does).
   double total_kv_cost = 0.0, kv_acc = 0.0, guided_end = 0.0;
-  for (const Seq& sq : seqs)
-    total_kv_cost += tile_cost(sq.n_leaves * G) * static_cast<double>(runs[sq.run].tiles.size());
+  for (const Seq& sq : seqs) total_kv_cost += tile_cost(sq.n_leaves * G) * runs[sq.run].weight;
   auto guided_quota = [&](double acc_now) {
     const double share = (total_kv_cost - kv_acc) / (kGuide * static_cast<double>(S0));
     return acc_now + std::min(full_stream, std::max(kGuideMinCost, share));
@@ -345,6 +358,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     st.piece_begin = st.piece_end = static_cast<int32_t>(out->pieces.size());
     st.tile_off = static_cast<int32_t>(out->stream_tiles.size());
     st.seg_off = static_cast<int32_t>(out->segs.size());
+    st.live_off = static_cast<int32_t>(out->live.size() / 2);
     out->streams.push_back(st);
   };
   open_stream();
@@ -356,13 +370,16 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     const int32_t nq = (rows + kQTileRows - 1) / kQTileRows;
     const double c = tile_cost(rows);
     bool new_piece = true;
-    for (const Tile& tl : r.tiles) {
+    for (size_t ti = 0; ti < r.tiles.size(); ++ti) {
+      const Tile& tl = r.tiles[ti];
+      const bool live = r.live[ti] != 0;
       Stream* st = &out->streams.back();
       const int64_t s = static_cast<int64_t>(out->streams.size()) - 1;
       const bool full = one_round ? s + 1 < planned && acc >= quota[s] : acc >= guided_end;
       const bool room = st->n_tiles + (new_piece ? nq + 1 : 1) <= kMaxStreamTiles &&
                         st->n_segs + (new_piece ? sq.n_leaves : 0) <= kMaxStreamSegs &&
-                        st->piece_end - st->piece_begin + (new_piece ? 1 : 0) <= kMaxStreamPieces;
+                        st->piece_end - st->piece_begin + (new_piece ? 1 : 0) <= kMaxStreamPieces &&
+                        st->n_live + (live ? 1 : 0) <= kMaxStreamLive;
       if (st->n_tiles > 0 && (full || !room)) {
         open_stream();
         st = &out->streams.back();
@@ -399,14 +416,20 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         new_piece = false;
       }
       const int32_t half = tl.tile_in_node & 1;
+      int32_t valid = tl.valid;
+      if (live) {
+        valid = -1 - st->n_live++;
+        out->live.push_back(tl.node);
+        out->live.push_back(tl.tile_in_node * kPlanTileTokens);
+      }
       out->stream_tiles.push_back(
-          StreamTile{static_cast<int32_t>(2 * (static_cast<int64_t>(sq.g) * p.num_blocks + tl.block) + half),
-                     tl.valid});
+          StreamTile{static_cast<int32_t>(2 * (static_cast<int64_t>(sq.g) * p.num_blocks + tl.block) + half), valid});
       out->tiles.push_back(tl);
       ++st->n_tiles;
       ++out->pieces.back().n_tiles;
-      acc += c;
-      kv_acc += c;
+      const double w = live && tl.valid == 0 ? kLiveEmptyWeight : 1.0;
+      acc += c * w;
+      kv_acc += c * w;
     }
   }
   pad_to(&out->stream_tiles, 2, StreamTile{0, 0});
@@ -444,7 +467,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   int32_t bi = kBlockHeaderInts;
   for (const Stream& st : out->streams)
     bi = std::max(bi, kBlockHeaderInts + kBlockPieceInts * (st.piece_end - st.piece_begin) +
-                          2 * round_up(st.n_tiles, 2) + 2 * round_up(st.n_segs, 4));
+                          2 * round_up(st.n_tiles, 2) + 2 * round_up(st.n_segs, 4) + 2 * st.n_live);
   out->block_ints = round_up(bi, 4);
   out->blocks.assign(out->streams.size() * static_cast<size_t>(out->block_ints), 0);
   for (size_t si = 0; si < out->streams.size(); ++si) {
@@ -454,6 +477,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     b[0] = np;
     b[1] = st.n_tiles;
     b[2] = st.n_segs;
+    b[3] = st.n_live;
     int32_t* w = b + kBlockHeaderInts;
     for (int32_t i = st.piece_begin; i < st.piece_end; ++i) {
       const Piece& pc = out->pieces[i];
@@ -470,6 +494,8 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     for (int32_t k = 0; k < st.n_segs; ++k) w[k] = out->segs[st.seg_off + k];
     w += round_up(st.n_segs, 4);
     for (int32_t k = 0; k < st.n_segs; ++k) w[k] = out->dests[st.seg_off + k];
+    w += round_up(st.n_segs, 4);
+    for (int32_t k = 0; k < 2 * st.n_live; ++k) w[k] = out->live[2 * st.live_off + k];
   }
 
   return kOk;

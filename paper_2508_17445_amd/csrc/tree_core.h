@@ -57,6 +57,8 @@ class Tree {
   int32_t block_tokens() const { return B_; }
   // Bumped by every mutation; plans are cached against it.
   uint64_t version() const { return version_; }
+  // Bumped by new_root and fork only (appends change lengths, not shape).
+  uint64_t shape_version() const { return shape_version_; }
   void chain(int32_t x, std::vector<int32_t>* out) const;
   int64_t chain_tokens(int32_t x) const;
 
@@ -70,6 +72,7 @@ class Tree {
   int64_t next_block_ = 0;
   int32_t n_roots_ = 0;
   uint64_t version_ = 0;
+  uint64_t shape_version_ = 0;
   std::vector<Node> nodes_;
 };
 
@@ -97,6 +100,8 @@ constexpr int32_t kPlanTileTokens = 32;
 constexpr int32_t kMaxStreamTiles = 256;
 constexpr int32_t kMaxStreamSegs = 256;
 constexpr int32_t kMaxStreamPieces = kMaxStreamTiles / 2;
+// Live tiles (token count read on the device at decode time) of one stream.
+constexpr int32_t kMaxStreamLive = kMaxStreamTiles;
 // Query rows carried by one query tile (a tile buffer holds 64 rows of D).
 constexpr int32_t kQTileRows = 64;
 // Query rows of a piece that the column-split kernel path handles (two 16-row
@@ -128,23 +133,26 @@ constexpr int32_t kPieceInts = 16;
 static_assert(sizeof(Piece) == kPieceInts * sizeof(int32_t), "piece record size");
 
 // A stream: pieces [piece_begin, piece_end) processed in order by one
-// workgroup; its tiles are Plan::stream_tiles[tile_off, tile_off + n_tiles)
-// and its query segments Plan::segs[seg_off, seg_off + n_segs).  tile_off is
-// even and seg_off a multiple of 4; both arrays are padded so that a stream's
-// lists can be read in 16-byte pieces.
+// workgroup; its tiles are Plan::stream_tiles[tile_off, tile_off + n_tiles),
+// its query segments Plan::segs[seg_off, seg_off + n_segs) and its live tiles
+// Plan::live[2 live_off, 2 (live_off + n_live)).  tile_off is even and seg_off
+// a multiple of 4; both arrays are padded so that a stream's lists can be
+// read in 16-byte pieces.
 struct Stream {
   int32_t piece_begin, piece_end;
   int32_t tile_off, n_tiles;
   int32_t seg_off, n_segs;
-  int32_t pad[2];
+  int32_t live_off, n_live;
 };
 constexpr int32_t kStreamInts = 8;
 static_assert(sizeof(Stream) == kStreamInts * sizeof(int32_t), "stream record size");
 
 // Device record of a tile.  KV tile: hb = 2 * (g * num_blocks + block) + half
-// >= 0 locates its K and V data, valid = tokens holding data (1..32).  Query
-// tile: hb = -1 - (the piece's first segment, stream-local), valid =
-// row0 | (n_rows << 16): rows [row0, row0 + n_rows) of the piece.
+// >= 0 locates its K and V data, valid = tokens holding data (1..32), or, for
+// a live tile, valid = -1 - i: entry i = {node, base} of the stream's live
+// table, and the tile holds min(32, max(0, len(node) - base)) tokens at decode
+// time.  Query tile: hb = -1 - (the piece's first segment, stream-local),
+// valid = row0 | (n_rows << 16): rows [row0, row0 + n_rows) of the piece.
 struct StreamTile {
   int32_t hb;
   int32_t valid;
@@ -159,10 +167,11 @@ struct StreamTile {
 //   then n_tiles StreamTile records (two ints each, padded to an even count)
 //   then n_segs query segment offsets (padded to a multiple of 4)
 //   then n_segs partial destinations, Plan::dests (padded to a multiple of 4)
+//   then n_live live-tile entries {node, base} (header[3] = n_live)
 constexpr int32_t kBlockHeaderInts = 4;
 constexpr int32_t kBlockPieceInts = 4;
-constexpr int32_t kMaxBlockInts =
-    kBlockHeaderInts + kBlockPieceInts * kMaxStreamPieces + 2 * kMaxStreamTiles + 2 * kMaxStreamSegs;
+constexpr int32_t kMaxBlockInts = kBlockHeaderInts + kBlockPieceInts * kMaxStreamPieces + 2 * kMaxStreamTiles +
+                                  2 * kMaxStreamSegs + 2 * kMaxStreamLive;
 
 // Host record of a KV tile, for inspection: tokens [32 k, 32 k + 32) of node
 // `node` (k = tile_in_node) in pool block `block` (= block_begin + k / 2).
@@ -187,6 +196,9 @@ struct PlanParams {
   // slot_speed[slot] (both 1.0: equal cost per stream).
   int32_t compute_units;
   double slot_speed[2];
+  // Lengths are read on the device: unfrozen nodes are planned up to their
+  // capacity, tiles not yet full become live tiles.
+  bool live_lengths;
 };
 
 struct Plan {
@@ -199,6 +211,8 @@ struct Plan {
   // Query segments: element offset in the query tensor of the G rows of one
   // leaf for one KV head (contiguous there), one per (piece, leaf).
   std::vector<int32_t> segs;
+  // Live tiles: {node, base} per live tile, stream order.
+  std::vector<int32_t> live;
   // The device copy of the streams (layout above kBlockHeaderInts).
   std::vector<int32_t> blocks;
   int32_t block_ints = 0;

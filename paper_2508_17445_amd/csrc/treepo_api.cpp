@@ -68,6 +68,10 @@ struct treepo_ctx {
   bool profiling = false;
   std::vector<TimedLaunch> timed;
   std::vector<hipEvent_t> spare_events;
+  // Device lengths (cfg.node_len): stale after kv_commit, new_root or fork;
+  // the next decode uploads the host table on its stream.
+  bool live = false;
+  bool dev_len_stale = true;
   double prof_ms[TREEPO_KERNEL_KINDS] = {0, 0, 0};
   int64_t prof_n[TREEPO_KERNEL_KINDS] = {0, 0, 0};
 
@@ -175,7 +179,10 @@ void put(std::vector<char>& blob, size_t off, const std::vector<T>& v) {
 int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode, CachedPlan** out) {
   ++ctx->clock;
   for (CachedPlan& cp : ctx->plans) {
-    if (cp.version == ctx->tree.version() && cp.mode == mode &&
+    // with device lengths a plan outlives appends (it covers unfrozen nodes up
+    // to their capacity); otherwise any mutation invalidates it
+    const uint64_t v = ctx->live ? ctx->tree.shape_version() : ctx->tree.version();
+    if (cp.version == v && cp.mode == mode &&
         cp.leaves.size() == static_cast<size_t>(n) &&
         std::equal(cp.leaves.begin(), cp.leaves.end(), leaves)) {
       cp.last_use = ctx->clock;
@@ -204,7 +211,7 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   cp.off_part_ml = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * 2 * sizeof(float));
   cp.ws_bytes = off;
-  cp.version = ctx->tree.version();
+  cp.version = ctx->live ? ctx->tree.shape_version() : ctx->tree.version();
   cp.mode = mode;
   cp.leaves.assign(leaves, leaves + n);
   cp.uid = ctx->next_uid++;
@@ -247,6 +254,16 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
     else
       up->second = cp->uid;
   }
+  if (ctx->live && ctx->dev_len_stale) {
+    const auto& nd = ctx->tree.nodes();
+    std::vector<int32_t> lens(nd.size());
+    for (size_t i = 0; i < nd.size(); ++i) lens[i] = nd[i].len;
+    if (!lens.empty()) {
+      hipError_t e = upload(ctx, ctx->cfg.node_len, lens.data(), lens.size() * sizeof(int32_t), stream);
+      if (e != hipSuccess) return hip_fail(ctx, e, "length table upload");
+    }
+    ctx->dev_len_stale = false;
+  }
   const Plan& p = cp->plan;
   treepo::DecodeArgs a;
   a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
@@ -258,6 +275,7 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.d = ctx->cfg.head_dim;
   a.q = static_cast<const uint16_t*>(q);
   a.scale_log2 = scale * 1.4426950408889634f;
+  a.node_len = static_cast<const int32_t*>(ctx->cfg.node_len);
   a.blocks = reinterpret_cast<const int32_t*>(wsb + cp->off_blocks);
   a.block_ints = p.block_ints;
   a.n_streams = static_cast<int32_t>(p.streams.size());
@@ -277,7 +295,8 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
 
 // Splits a validated append into block-aligned pieces (source rows in call order).
 void append_pieces(const treepo::Tree& t, int32_t n, const int32_t* nodes, const int32_t* ntok,
-                   std::vector<treepo::AppendPiece>* out) {
+                   std::vector<treepo::AppendPiece>* out,
+                   std::vector<std::pair<int32_t, int32_t>>* upd = nullptr) {
   const int32_t B = t.block_tokens();
   std::vector<std::pair<int32_t, int32_t>> pending;  // node -> len so far in this call
   out->clear();
@@ -301,6 +320,10 @@ void append_pieces(const treepo::Tree& t, int32_t n, const int32_t* nodes, const
     else
       it->second = cur;
   }
+  // the nodes that received tokens, with their lengths after the whole call
+  if (upd)
+    for (const auto& pr : pending)
+      if (pr.second != t.nodes()[pr.first].len) upd->push_back(pr);
 }
 
 }  // namespace
@@ -313,7 +336,7 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   if (c.num_q_heads < 1 || c.num_kv_heads < 1 || c.num_q_heads % c.num_kv_heads != 0 ||
       c.num_blocks < 0 || c.num_blocks > INT32_MAX || c.max_nodes < 0 || c.reserved != 0 ||
       !c.k_pool || !c.v_pool || reinterpret_cast<uintptr_t>(c.k_pool) % 16 != 0 ||
-      reinterpret_cast<uintptr_t>(c.v_pool) % 16 != 0)
+      reinterpret_cast<uintptr_t>(c.v_pool) % 16 != 0 || reinterpret_cast<uintptr_t>(c.node_len) % 4 != 0)
     return TREEPO_EINVAL;
   if ((c.head_dim != 64 && c.head_dim != 128) || c.block_tokens != treepo::kTile ||
       c.num_q_heads / c.num_kv_heads > 128)
@@ -333,6 +356,8 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   ctx->params.compute_units = treepo::kComputeUnits;
   ctx->params.slot_speed[0] = 1.0;
   ctx->params.slot_speed[1] = 0.85;
+  ctx->live = c.node_len != nullptr;
+  ctx->params.live_lengths = ctx->live;
   *out = ctx;
   return TREEPO_OK;
 }
@@ -358,6 +383,7 @@ int32_t treepo_new_root(treepo_ctx* ctx, int32_t cap_tokens, int32_t* node_out) 
   if (!ctx) return TREEPO_EINVAL;
   std::string err;
   const int32_t st = ctx->tree.new_root(cap_tokens, node_out, &err);
+  if (st == treepo::kOk) ctx->dev_len_stale = true;
   return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
 }
 
@@ -366,6 +392,7 @@ int32_t treepo_fork(treepo_ctx* ctx, int32_t parent, int32_t n_children, int32_t
   if (!ctx) return TREEPO_EINVAL;
   std::string err;
   const int32_t st = ctx->tree.fork(parent, n_children, child_cap, children_out, &err);
+  if (st == treepo::kOk) ctx->dev_len_stale = true;
   return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
 }
 
@@ -389,6 +416,7 @@ int32_t treepo_kv_commit(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
   const int32_t st = ctx->tree.check_append(n, nodes, ntok, nullptr, &err);
   if (st != treepo::kOk) return fail(ctx, st, err);
   ctx->tree.apply_append(n, nodes, ntok);
+  ctx->dev_len_stale = true;
   return TREEPO_OK;
 }
 
@@ -403,13 +431,21 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
   if (total > 0) {
     if (!k || !v) return fail(ctx, TREEPO_EINVAL, "null k or v with tokens to append");
     std::vector<treepo::AppendPiece> pieces;
-    append_pieces(ctx->tree, n, nodes, ntok, &pieces);
+    std::vector<std::pair<int32_t, int32_t>> upd;
+    append_pieces(ctx->tree, n, nodes, ntok, &pieces, &upd);
+    std::vector<int32_t> upd_node(upd.size()), upd_len(upd.size());
+    for (size_t i = 0; i < upd.size(); ++i) {
+      upd_node[i] = upd[i].first;
+      upd_len[i] = upd[i].second;
+    }
     const hipError_t e = timed_launch(ctx, TREEPO_KERNEL_APPEND, stream, [&] {
       return treepo::launch_kv_append(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                                       static_cast<uint16_t*>(ctx->cfg.k_pool),
                                       static_cast<uint16_t*>(ctx->cfg.v_pool), ctx->cfg.num_blocks,
                                       ctx->cfg.num_kv_heads, ctx->cfg.head_dim, pieces.data(),
-                                      static_cast<int32_t>(pieces.size()), stream);
+                                      static_cast<int32_t>(pieces.size()), upd_node.data(), upd_len.data(),
+                                      static_cast<int32_t>(upd.size()), static_cast<int32_t*>(ctx->cfg.node_len),
+                                      stream);
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "append kernel launch");
   }

@@ -43,7 +43,7 @@ class TreePOError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [("num_q_heads", _i32), ("num_kv_heads", _i32), ("head_dim", _i32),
                 ("block_tokens", _i32), ("num_blocks", _i64), ("max_nodes", _i32),
-                ("reserved", _i32), ("k_pool", _p), ("v_pool", _p)]
+                ("reserved", _i32), ("k_pool", _p), ("v_pool", _p), ("node_len", _p)]
 
 
 _lib = None
@@ -125,11 +125,12 @@ class Context:
     """One segment-tree KV cache over caller-owned K/V pools."""
 
     def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, num_blocks: int,
-                 max_nodes: int, k_pool, v_pool, block_tokens: int = BLOCK_TOKENS):
+                 max_nodes: int, k_pool, v_pool, block_tokens: int = BLOCK_TOKENS, node_len=None):
         self.lib = load_library()
         self.cfg = Config(num_q_heads, num_kv_heads, head_dim, block_tokens, num_blocks,
-                          max_nodes, 0, _dev(k_pool), _dev(v_pool))
-        self._keep = (k_pool, v_pool)
+                          max_nodes, 0, _dev(k_pool), _dev(v_pool),
+                          _dev(node_len) if node_len is not None else None)
+        self._keep = (k_pool, v_pool, node_len)
         h = _p()
         st = self.lib.treepo_create(ctypes.byref(self.cfg), ctypes.byref(h))
         if st != OK:

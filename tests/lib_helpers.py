@@ -17,10 +17,11 @@ def ensure_lib():
     return load_library()
 
 
-def host_ctx(hq=4, hkv=1, d=64, num_blocks=1 << 20, max_nodes=1 << 20, block_tokens=64):
+def host_ctx(hq=4, hkv=1, d=64, num_blocks=1 << 20, max_nodes=1 << 20, block_tokens=64, live=False):
     ensure_lib()
     from paper_2508_17445_amd import Context
-    return Context(hq, hkv, d, num_blocks, max_nodes, FAKE_POOL, FAKE_POOL + 64, block_tokens)
+    return Context(hq, hkv, d, num_blocks, max_nodes, FAKE_POOL, FAKE_POOL + 64, block_tokens,
+                   node_len=FAKE_POOL + 128 if live else None)
 
 
 def replay_host(ctx, log, step_append=True):

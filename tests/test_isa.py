@@ -40,10 +40,12 @@ def test_both_head_dims_present(partial_kernels):
 
 
 def test_only_global_to_lds_loads(partial_kernels):
+    """Tiles, the stream block and the live tiles' lengths all arrive by
+    global->LDS loads (16-byte tile chunks, non-temporal; 4-byte lengths)."""
     kernels, _ = partial_kernels
     for d, body in kernels.items():
         loads = [x for x in body if re.match(r"^(global_load|buffer_load|flat_load|scratch_|global_atomic)", x)
-                 and not x.startswith("global_load_lds_dwordx4")]
+                 and not re.match(r"^global_load_lds_dword(x4)?\s", x)]
         assert not loads, (d, loads[:5])
         assert any(x.startswith("global_load_lds_dwordx4") and x.endswith(" nt") for x in body), d
 

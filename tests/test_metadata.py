@@ -60,7 +60,7 @@ def test_kv_slots_follow_block_reservation():
 
 
 MAX_STREAM_TILES = 256
-MAX_BLOCK_INTS = 4 + 4 * 128 + 2 * 256 + 256   # header, pieces, tile records, segments
+MAX_BLOCK_INTS = 4 + 4 * 128 + 2 * 256 + 2 * 256 + 2 * 256   # header, pieces, tiles, segments, dests, live
 
 
 def _tile_cost(rows):
@@ -91,14 +91,21 @@ def _plan_checks(ctx, model, leaves, mode):
             for t in tiles[ptile:ptile + nt]:
                 covered[(pos, g)].append(tuple(t))
     assert sorted(stream_next) == list(range(n_streams))
+    live_mode = ctx.cfg.node_len is not None
     for pos, x in enumerate(leaves):
         want = []
         for n in model.chain(x):
-            ln = model.nodes[n]["len"]
-            for k in range((ln + 31) // 32):     # 32-token tiles, two per 64-token block
-                want.append((model.nodes[n]["block_begin"] + k // 2, n, k, min(32, ln - 32 * k)))
+            ln, cap = model.nodes[n]["len"], model.nodes[n]["cap"]
+            # with device lengths an unfrozen node is covered up to its capacity
+            span = cap if live_mode and model.n_children[n] == 0 and ln < cap else ln
+            for k in range((span + 31) // 32):     # 32-token tiles, two per 64-token block
+                want.append((model.nodes[n]["block_begin"] + k // 2, n, k, max(0, min(32, ln - 32 * k))))
         for g in range(hkv):
-            assert sorted(covered[(pos, g)]) == sorted(want), (mode, pos, g)
+            got = sorted(covered[(pos, g)])
+            # a reused live plan reports the counts of its planning time (the
+            # device reads the current ones): compare those of full tiles only
+            assert [t[:3] for t in got] == [t[:3] for t in sorted(want)], (mode, pos, g)
+            assert all(a[3] == b[3] or (live_mode and a[3] < b[3]) for a, b in zip(got, sorted(want))), (mode, pos, g)
     _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_next, seg_next)
     return pieces, tiles, n_streams
 
@@ -121,37 +128,59 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
     assert sorted(count) == [(x, g) for x in range(len(leaves)) for g in range(hkv)]
     emax = max(count.values())
     entry = {}
+    nodes = ctx.export_nodes()
+    kids = np.bincount(nodes[:, 0][nodes[:, 0] >= 0], minlength=len(nodes))
+    live_mode = ctx.cfg.node_len is not None
     for s in range(n_streams):
         b = blocks[s]
-        n_p, n_t, n_s = int(b[0]), int(b[1]), int(b[2])
+        n_p, n_t, n_s, n_l = int(b[0]), int(b[1]), int(b[2]), int(b[3])
         pcs = by_stream[s]
-        assert (n_p, n_t, n_s, b[3]) == (len(pcs), stream_next[s], seg_next[s], 0)
+        assert (n_p, n_t, n_s) == (len(pcs), stream_next[s], seg_next[s])
+        assert live_mode or n_l == 0
         tiles_at = 4 + 4 * n_p
         segs_at = tiles_at + 2 * (n_t + n_t % 2)
         dests_at = segs_at + n_s + (-n_s) % 4
-        assert dests_at + n_s <= bi
+        live_at = dests_at + n_s + (-n_s) % 4
+        assert live_at + 2 * n_l <= bi
         assert (b[tiles_at + 2 * n_t:segs_at] == 0).all() and (b[segs_at + n_s:dests_at] == 0).all()
-        assert (b[dests_at + n_s:] == 0).all()
+        assert (b[dests_at + n_s:live_at] == 0).all() and (b[live_at + 2 * n_l:] == 0).all()
         recs = b[4:tiles_at].reshape(-1, 4)
         st = b[tiles_at:tiles_at + 2 * n_t].reshape(-1, 2)
         sg = b[segs_at:segs_at + n_s]
         dst = b[dests_at:dests_at + n_s]
+        live = b[live_at:live_at + 2 * n_l].reshape(-1, 2)
+        used_live = set()
         for i, pc in enumerate(pcs):
             rb, nl, rows, g, stile, nt, _, seg, _, _, ptile, nq = (int(v) for v in pc[:12])
             assert tuple(recs[i]) == (rows, stile, nt, seg)
             for t in range(nq):
                 assert tuple(st[stile + t]) == (-1 - seg, (64 * t) | (min(64, rows - 64 * t) << 16))
             for t in range(nt):
-                blk, _, tin, valid = (int(v) for v in tiles[ptile + t])
+                blk, node, tin, valid = (int(v) for v in tiles[ptile + t])
                 hb, v = (int(x) for x in st[stile + nq + t])
-                assert hb == 2 * (g * nb + blk) + tin % 2 and v == valid
-                assert 0 <= hb < 2 * hkv * nb and 1 <= v <= 32
+                assert hb == 2 * (g * nb + blk) + tin % 2
+                assert 0 <= hb < 2 * hkv * nb
+                # a tile of an unfrozen node that was not full when planned is
+                # live: its count is read on the device (such nodes are planned
+                # up to their capacity); `valid` is the count at planning time
+                n_len, n_cap, n_kids = int(nodes[node][3]), int(nodes[node][4]), int(kids[node])
+                assert tin * 32 < (n_cap if live_mode and n_kids == 0 else n_len)
+                assert 0 <= valid <= max(0, min(32, n_len - 32 * tin))
+                if v < 0:
+                    assert live_mode and n_kids == 0 and valid < 32
+                    assert -1 - v < n_l and -1 - v not in used_live
+                    used_live.add(-1 - v)
+                    assert tuple(live[-1 - v]) == (node, 32 * tin)
+                else:
+                    assert v == valid == min(32, n_len - 32 * tin) and 1 <= v <= 32
+                    assert valid == 32 or not live_mode or n_kids > 0 or n_len == n_cap
             for j in range(nl):
                 x = int(rowsets[rb + j])
                 assert 0 <= x < len(leaves) and sg[seg + j] == (x * hq + g * G) * d
                 e = entry.get((x, g), 0)
                 entry[(x, g)] = e + 1
                 assert dst[seg + j] == ((x * hkv + g) * emax + e) * G
+        assert used_live == set(range(n_l))
     assert entry == count
 
 
@@ -230,3 +259,57 @@ def test_duplicate_and_interior_leaves():
     model = oracle_model(log)
     _compare(ctx, model, leaves)
     _plan_checks(ctx, model, leaves, 0)
+
+
+def test_live_plans_outlive_appends():
+    """With device lengths, a plan covers every unfrozen node up to its
+    capacity (tiles not yet full are live) and is reused across appends --
+    also ones that cross tile and block boundaries -- until the next fork."""
+    log = build_call_log(1)
+    from workloads import CONFIGS
+    c = CONFIGS[1]
+    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d, live=True)
+    replay_host(ctx, log)
+    model = oracle_model(log)
+    # a new 100-token segment under every leaf (the next step of Alg. 1), 5 tokens in
+    leaves = []
+    for x in log.leaves:
+        kid, = ctx.fork(x, 1, 100)
+        assert model.fork(x, 1, 100) == [kid]
+        leaves.append(kid)
+    ctx.kv_commit(leaves, [5] * len(leaves))
+    model.append(leaves, [5] * len(leaves))
+    for mode in (0, 1):
+        _plan_checks(ctx, model, leaves, mode)
+    b0 = ctx.export_blocks(leaves, 0)
+    assert b0[:, 3].sum() == len(leaves) * c.hkv * 4      # 100 tokens: 4 tiles per leaf and KV head, none full
+    for step in (1, 40, 53):                            # 6, 46 (past 32), 99 (past 64)
+        ctx.kv_commit(leaves, [step] * len(leaves))
+        model.append(leaves, [step] * len(leaves))
+        _plan_checks(ctx, model, leaves, 0)
+        assert np.array_equal(ctx.export_blocks(leaves, 0), b0)   # the same plan serves every step
+    # a fork changes the shape: a new plan; the frozen node is static, the others
+    # have one live tile left (tokens 96..99 of 100)
+    ctx.fork(leaves[0], 2, 64)
+    model.fork(leaves[0], 2, 64)
+    b1 = ctx.export_blocks(leaves, 0)
+    assert not np.array_equal(b1, b0) and b1[:, 3].sum() == (len(leaves) - 1) * c.hkv
+    _plan_checks(ctx, model, leaves, 0)
+
+
+def test_static_plans_follow_appends():
+    """Without device lengths every append re-plans (counts baked in)."""
+    log = build_call_log(1)
+    from workloads import CONFIGS
+    c = CONFIGS[1]
+    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    replay_host(ctx, log)
+    leaves = list(log.leaves)
+    b0 = ctx.export_blocks(leaves, 0)
+    assert (b0[:, 3] == 0).all()
+    nodes = ctx.export_nodes()
+    frozen = set(int(p) for p in nodes[:, 0] if p >= 0)
+    grow = [x for x in leaves if nodes[x][3] < nodes[x][4] and x not in frozen]
+    if grow:
+        ctx.kv_commit(grow[:1], [1])
+        assert not np.array_equal(ctx.export_blocks(leaves, 0), b0)

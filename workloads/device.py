@@ -54,7 +54,7 @@ class DeviceTree:
 
     def __init__(self, cfg_id: int | None = None, cfg: Config | None = None, log: CallLog | None = None,
                  device: str = "cuda", keep_host_data: bool = False, extra_blocks: int = 0,
-                 apply_step_append: bool = True):
+                 apply_step_append: bool = True, live: bool = False):
         import torch
         from paper_2508_17445_amd import Context
 
@@ -66,8 +66,10 @@ class DeviceTree:
         elems = c.hkv * self.num_blocks * c.block_tokens * c.d
         self.k_pool = torch.empty(elems, dtype=torch.bfloat16, device=device)
         self.v_pool = torch.empty(elems, dtype=torch.bfloat16, device=device)
+        # live: node lengths on the device, plans reused across appends
+        self.node_len = torch.zeros(max(self.log.n_nodes, 1), dtype=torch.int32, device=device) if live else None
         self.ctx = Context(c.hq, c.hkv, c.d, self.num_blocks, max(self.log.n_nodes, 1),
-                           self.k_pool, self.v_pool, c.block_tokens)
+                           self.k_pool, self.v_pool, c.block_tokens, node_len=self.node_len)
         self.data = NodeData(c, self.log)
         self._len: dict[int, int] = {}
         self._replay(keep_host_data)
@@ -160,8 +162,9 @@ class DeviceTree:
         r.k_pool = self.k_pool.clone()
         r.v_pool = self.v_pool.clone()
         c = self.cfg
+        r.node_len = torch.zeros_like(self.node_len) if self.node_len is not None else None
         r.ctx = Context(c.hq, c.hkv, c.d, r.num_blocks, max(self.log.n_nodes, 1), r.k_pool, r.v_pool,
-                        c.block_tokens)
+                        c.block_tokens, node_len=r.node_len)
         for op in self.log.ops:
             if op[0] == "root":
                 r.ctx.new_root(op[1])
