@@ -51,6 +51,11 @@ def _parse():
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--segment-loop", action="store_true",
+                    help="instead of the default line: segment-level decoding after a fork, every step one "
+                         "append per leaf then a decode, over --layers layers, steady state over the segment")
+    ap.add_argument("--seg-len", type=int, default=512, help="segment capacity for --segment-loop")
+    ap.add_argument("--layers", type=int, default=4, help="layers (each its own pools) for --segment-loop")
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for hardware counters: a few decode steps of the workload, then one "
                          "1 GiB device copy whose byte counters calibrate the kernels'")
@@ -211,6 +216,72 @@ def _profile_pass(dt, args):
     print(json.dumps({"profile_pass": True, "steps_per_mode": args.steps, "copy_bytes": nbytes}), flush=True)
 
 
+def _segment_loop(args):
+    """Segment-level decoding (the paper's Sec. 2.2 step loop): the config's
+    tree gets a new --seg-len segment under every leaf; each step appends one
+    token per leaf and decodes, on every layer.  Modes: cascade with device
+    lengths (one plan for the whole segment), per-leaf baseline with device
+    lengths, cascade without them (a new plan and upload every step)."""
+    import torch
+    from workloads import CONFIGS, CallLog, build_call_log
+    from workloads.device import DeviceTree
+    cfg = CONFIGS[args.config]
+    base = build_call_log(args.config)
+    ops, rows, nid, leaves = list(base.ops), dict(base.rows), base.n_nodes, []
+    for x in base.leaves:
+        ops.append(("fork", x, 1, args.seg_len))
+        rows[nid] = 0
+        leaves.append(nid)
+        nid += 1
+    log = CallLog(ops=ops, step_append=None, leaves=leaves, rows=rows, n_nodes=nid)
+    n = len(leaves)
+    if args.warmup + args.steps > args.seg_len:
+        args.steps = args.seg_len - args.warmup
+    g = torch.Generator(device="cuda").manual_seed(7)
+    k_step = torch.randn(n, cfg.hkv, cfg.d, device="cuda", generator=g).to(torch.bfloat16)
+    v_step = torch.randn(n, cfg.hkv, cfg.d, device="cuda", generator=g).to(torch.bfloat16)
+    ones = [1] * n
+    res = {}
+    for name, mode, live in (("tree_live", 0, True), ("naive_live", 1, True), ("tree_replan", 0, False)):
+        first = DeviceTree(cfg=cfg, log=log, live=live)
+        layers = [first] + [first.clone() for _ in range(args.layers - 1)]
+        bufs = [(L.outputs(), L.workspace(mode)) for L in layers]
+
+        def step():
+            for i, L in enumerate(layers):
+                L.ctx.kv_append(leaves, ones, k_step, v_step)
+                ws = bufs[i][1] if live else L.workspace(mode)
+                fn = L.ctx.tree_decode if mode == 0 else L.ctx.paged_decode_naive
+                fn(leaves, L.q, cfg.scale, bufs[i][0][0], bufs[i][0][1], ws)
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        res[name] = {"ms_per_step": round(ms, 4), "ms_per_layer": round(ms / args.layers, 4),
+                     "value": round(n / (ms * 1e-3), 1)}
+        del layers, bufs, first
+        torch.cuda.empty_cache()
+    line = {
+        "metric": "segment decode loop: leaf-token-steps/sec (one append + one decode per leaf, all layers)",
+        "value": res["tree_live"]["value"], "unit": "leaf-token-steps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["tree_live"]["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 tree; random bf16 appended rows)",
+        "config": {"workload": f"config {args.config}: {cfg.name} + a {args.seg_len}-token segment per leaf",
+                   "leaves": n, "layers": args.layers, "hq": cfg.hq, "hkv": cfg.hkv, "head_dim": cfg.d,
+                   "segment_tokens": args.seg_len},
+        "modes": res,
+        "speedup_live_vs_replan": round(res["tree_replan"]["ms_per_step"] / res["tree_live"]["ms_per_step"], 3),
+        "speedup_tree_vs_naive": round(res["naive_live"]["ms_per_step"] / res["tree_live"]["ms_per_step"], 3),
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -223,6 +294,9 @@ def main():
     from workloads import CONFIGS
     from workloads.device import DeviceTree
 
+    if args.segment_loop:
+        _segment_loop(args)
+        return
     cfg = CONFIGS[args.config]
     base = DeviceTree(cfg_id=args.config)
     if args.profile_pass:
