@@ -161,9 +161,12 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
  *   workspace  device, 256-byte aligned, >= treepo_decode_workspace_size(..., TREEPO_MODE_TREE)
  * Cascade schedule: every node's K/V is read once and scored against all of
  * its descendant leaves' query rows (the nested sub-groups G_j of Sec. 2.3);
- * per-node partials are merged with a log-sum-exp combine.  The library keeps
- * the plan it uploaded into the workspace and reuses it while the tree and
- * the leaf list are unchanged: do not modify the workspace between calls.
+ * per-node partials are merged with a log-sum-exp combine.  The schedule
+ * (plan) is cached per context (the last four leaf lists and modes) and its
+ * device copy lives in memory the context allocates on the first decode with
+ * it and frees in treepo_destroy; the workspace holds only this call's
+ * partial results, so the caller may reuse it freely between calls (calls
+ * that overlap on one workspace race).
  * EINVAL (bad id, null pointer, n_leaves < 1, q not 16-byte aligned, scale
  * not positive and finite),
  * EEMPTY (a chain holds no tokens), EWORKSPACE (missing, too small or not

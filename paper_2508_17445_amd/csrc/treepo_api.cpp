@@ -1,6 +1,7 @@
 // C-ABI of the segment-tree decode-attention library: argument validation,
-// plan caching, pinned-staging uploads into the caller's workspace, kernel
-// launches on the caller's stream, metadata export and kernel timing.
+// plan caching (each cached plan's device image in memory the context owns,
+// uploaded through pinned staging), kernel launches on the caller's stream,
+// metadata export and kernel timing.
 #include "treepo.h"
 
 #include <algorithm>
@@ -32,12 +33,23 @@ struct CachedPlan {
   int32_t mode = 0;
   std::vector<int32_t> leaves;
   Plan plan;
-  std::vector<char> blob;  // host image of the plan region
+  std::vector<char> blob;  // host image of the plan's device data
   size_t off_blocks = 0;
   size_t off_comb = 0;
-  size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;
-  uint64_t uid = 0;
+  size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;  // partials, in the caller's workspace
   uint64_t last_use = 0;
+  // Device copy of `blob`, owned by the context (the buffer stays with the
+  // cache entry when a new plan replaces it).  Uploaded on the first decode
+  // with the plan, on that call's stream; decodes on other streams wait for
+  // the upload's event.  done_ev follows the last decode that read it.
+  void* dev = nullptr;
+  size_t dev_cap = 0;
+  bool dev_valid = false;
+  hipStream_t up_stream = nullptr;
+  hipEvent_t up_ev = nullptr;
+  hipEvent_t done_ev = nullptr;
+  bool used = false;          // done_ev recorded
+  bool multi_stream = false;  // read on more than one stream
 };
 
 struct PinnedSlot {
@@ -60,9 +72,7 @@ struct treepo_ctx {
   PlanParams params;
   std::string last_error;
   std::vector<CachedPlan> plans;
-  uint64_t next_uid = 1;
   uint64_t clock = 0;
-  std::vector<std::pair<void*, uint64_t>> uploaded;  // workspace -> plan uid
   std::array<PinnedSlot, kRing> ring;
   int ring_next = 0;
   bool profiling = false;
@@ -176,6 +186,58 @@ void put(std::vector<char>& blob, size_t off, const std::vector<T>& v) {
   if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
 }
 
+// Waits until no queued kernel reads the entry's device image.
+hipError_t retire_image(CachedPlan& cp) {
+  hipError_t e = hipSuccess;
+  if (cp.multi_stream)
+    e = hipDeviceSynchronize();
+  else if (cp.used)
+    e = hipEventSynchronize(cp.done_ev);
+  cp.used = false;
+  cp.multi_stream = false;
+  cp.dev_valid = false;
+  return e;
+}
+
+// Makes the plan's device image current for a decode on `s`: uploads it on
+// the first use (growing the entry's buffer if needed), else orders `s`
+// after the upload.
+hipError_t stage_image(treepo_ctx* ctx, CachedPlan& cp, hipStream_t s) {
+  hipError_t e;
+  if (cp.dev_valid) {
+    if (s == cp.up_stream) return hipSuccess;
+    cp.multi_stream = true;
+    return hipStreamWaitEvent(s, cp.up_ev, 0);
+  }
+  const size_t bytes = std::max<size_t>(cp.blob.size(), kAlign);
+  if (cp.dev_cap < bytes) {
+    if (cp.dev) {
+      e = hipFree(cp.dev);
+      cp.dev = nullptr;
+      cp.dev_cap = 0;
+      if (e != hipSuccess) return e;
+    }
+    e = hipMalloc(&cp.dev, bytes);
+    if (e != hipSuccess) return e;
+    cp.dev_cap = bytes;
+  }
+  if (!cp.up_ev) {
+    e = hipEventCreateWithFlags(&cp.up_ev, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+  }
+  if (!cp.done_ev) {
+    e = hipEventCreateWithFlags(&cp.done_ev, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+  }
+  e = upload(ctx, cp.dev, cp.blob.data(), cp.blob.size(), s);
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(cp.up_ev, s);
+  if (e != hipSuccess) return e;
+  cp.up_stream = s;
+  cp.dev_valid = true;
+  return hipSuccess;
+}
+
 int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode, CachedPlan** out) {
   ++ctx->clock;
   for (CachedPlan& cp : ctx->plans) {
@@ -206,6 +268,7 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   cp.blob.assign(off, 0);
   put(cp.blob, cp.off_blocks, p.blocks);
   put(cp.blob, cp.off_comb, p.comb_count);
+  off = 0;
   cp.off_part_o = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
   cp.off_part_ml = off;
@@ -214,11 +277,17 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   cp.version = ctx->live ? ctx->tree.shape_version() : ctx->tree.version();
   cp.mode = mode;
   cp.leaves.assign(leaves, leaves + n);
-  cp.uid = ctx->next_uid++;
   cp.last_use = ctx->clock;
   if (static_cast<int>(ctx->plans.size()) >= kPlanCache) {
     auto lru = std::min_element(ctx->plans.begin(), ctx->plans.end(),
                                 [](const CachedPlan& a, const CachedPlan& b) { return a.last_use < b.last_use; });
+    // the new plan takes over the entry's device buffer once no kernel reads it
+    hipError_t e = retire_image(*lru);
+    if (e != hipSuccess) return hip_fail(ctx, e, "plan cache");
+    cp.dev = lru->dev;
+    cp.dev_cap = lru->dev_cap;
+    cp.up_ev = lru->up_ev;
+    cp.done_ev = lru->done_ev;
     *lru = std::move(cp);
     *out = &*lru;
   } else {
@@ -244,16 +313,11 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
     return fail(ctx, TREEPO_EWORKSPACE,
                 "workspace missing, smaller than treepo_decode_workspace_size or not 256-byte aligned");
   char* wsb = static_cast<char*>(ws);
-  auto up = std::find_if(ctx->uploaded.begin(), ctx->uploaded.end(),
-                         [&](const std::pair<void*, uint64_t>& u) { return u.first == ws; });
-  if (up == ctx->uploaded.end() || up->second != cp->uid) {
-    hipError_t e = upload(ctx, wsb, cp->blob.data(), cp->blob.size(), stream);
+  {
+    const hipError_t e = stage_image(ctx, *cp, stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "plan upload");
-    if (up == ctx->uploaded.end())
-      ctx->uploaded.emplace_back(ws, cp->uid);
-    else
-      up->second = cp->uid;
   }
+  const char* img = static_cast<const char*>(cp->dev);
   if (ctx->live && ctx->dev_len_stale) {
     const auto& nd = ctx->tree.nodes();
     std::vector<int32_t> lens(nd.size());
@@ -276,12 +340,12 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.q = static_cast<const uint16_t*>(q);
   a.scale_log2 = scale * 1.4426950408889634f;
   a.node_len = static_cast<const int32_t*>(ctx->cfg.node_len);
-  a.blocks = reinterpret_cast<const int32_t*>(wsb + cp->off_blocks);
+  a.blocks = reinterpret_cast<const int32_t*>(img + cp->off_blocks);
   a.block_ints = p.block_ints;
   a.n_streams = static_cast<int32_t>(p.streams.size());
   a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
   a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
-  a.comb_count = reinterpret_cast<const int32_t*>(wsb + cp->off_comb);
+  a.comb_count = reinterpret_cast<const int32_t*>(img + cp->off_comb);
   a.emax = p.emax;
   a.n_leaves = n;
   a.out = out;
@@ -290,6 +354,9 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
   e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
+  e = hipEventRecord(cp->done_ev, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "plan event");
+  cp->used = true;
   return TREEPO_OK;
 }
 
@@ -375,6 +442,12 @@ int32_t treepo_destroy(treepo_ctx* ctx) {
     (void)hipEventDestroy(t.stop);
   }
   for (hipEvent_t e : ctx->spare_events) (void)hipEventDestroy(e);
+  for (CachedPlan& cp : ctx->plans) {
+    (void)retire_image(cp);
+    if (cp.dev) (void)hipFree(cp.dev);
+    if (cp.up_ev) (void)hipEventDestroy(cp.up_ev);
+    if (cp.done_ev) (void)hipEventDestroy(cp.done_ev);
+  }
   delete ctx;
   return TREEPO_OK;
 }

@@ -128,3 +128,28 @@ def test_large_configs_sampled(cfg_id):
         _check(dt, mode, positions=pos, tag=f"cfg{cfg_id}")
     del dt
     torch.cuda.empty_cache()
+
+
+def test_shared_workspace_between_contexts():
+    """One workspace buffer used in turn by two contexts (different shapes and
+    plans) and filled with 0xFF before every call: the plans live in memory
+    each context owns and every partial the combine reads is written by the
+    same call, so each context keeps giving its own, bitwise equal results."""
+    import torch
+    t1, t2 = _dt(1), _dt(2)
+    refs = {}
+    for t in (t1, t2):
+        for mode in (0, 1):
+            out, _ = t.decode(mode)
+            refs[(id(t), mode)] = out.clone()
+    torch.cuda.synchronize()
+    nbytes = max(t.ctx.workspace_size(t.leaves, m) for t in (t1, t2) for m in (0, 1))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    for it in range(2):
+        for t in (t1, t2):
+            for mode in (0, 1):
+                ws.fill_(255)
+                out, _ = t.decode(mode, ws=ws)
+                torch.cuda.synchronize()
+                print(f"[shared workspace it={it} cfg={t.cfg.name} mode={mode}]", flush=True)
+                assert torch.equal(out, refs[(id(t), mode)])
