@@ -226,16 +226,18 @@ __device__ __forceinline__ void dma_qtile(const uint16_t* __restrict__ q, int se
 }
 
 // Issues tile k of the stream (KV or query; `rec` its record) into buffer
-// k mod 4.
+// k mod 4.  `lengths` says whether the live tiles' lengths have landed in LDS;
+// before that a live tile is loaded in full (it lies inside its node's
+// reserved blocks) and only the compute looks at its length.
 template <int D>
 __device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, int2 rec, const BlockTables& bt,
-                                                const Pipe<D>& p, int wave, int lane) {
+                                                const Pipe<D>& p, int wave, int lane, bool lengths) {
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
   const int hb = __builtin_amdgcn_readfirstlane(rec.x);
   const uint32_t dst = p.buf0 + (k & (kNBuf - 1)) * kBufBytes;
   if (hb >= 0) {
     const int y = __builtin_amdgcn_readfirstlane(rec.y);
-    dma_tile<D>(kpool, vpool, hb, y < 0 && tile_tokens(y, bt) == 0, dst, p, wave);
+    dma_tile<D>(kpool, vpool, hb, lengths && y < 0 && tile_tokens(y, bt) == 0, dst, p, wave);
   } else {
     const int y = __builtin_amdgcn_readfirstlane(rec.y);
     dma_qtile<D>(q, -1 - hb, y & 0xFFFF, y >> 16, sc.group, bt, dst, wave, lane);
@@ -243,12 +245,13 @@ __device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, in
 }
 
 // After tile k is published: tile k + 3 into the buffer tile k - 1 used (its
-// record is already in registers), then the record of tile k + 4.
+// record is already in registers), then the record of tile k + 4.  The live
+// lengths were gathered before tile 0 was issued, so they have landed.
 template <int D>
 __device__ __forceinline__ void dma_ahead(TREEPO_PARTIAL_PARAMS, int k, const BlockTables& bt, Pipe<D>& p,
                                           int wave, int lane) {
   if (k + kDepth < p.ntot) {
-    dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, k + kDepth, p.next, bt, p, wave, lane);
+    dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, k + kDepth, p.next, bt, p, wave, lane, true);
     if (k + kDepth + 1 < p.ntot) p.next = bt.tiles[k + kDepth + 1];
   }
 }
@@ -659,7 +662,8 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
   const BlockTables bt{reinterpret_cast<const int2*>(sm.blk + tile_at), sm.blk + seg_at,
                        sm.blk + seg_at + ((nseg + 3) & ~3), sm.blk + live_at, sm.live_len};
   // live tiles: their nodes' current lengths, gathered into LDS ahead of the
-  // first tile loads (older loads, so they have landed when tile 0 has)
+  // first tile loads (older loads, so they have landed when tile 0 has; the
+  // first tiles are issued before that and load live tiles in full)
   for (int c0 = wave * 64; c0 < n_live; c0 += kThreads)
     if (c0 + lane < n_live)
       dma4(node_len + bt.live[2 * (c0 + lane)], __builtin_amdgcn_readfirstlane(lds_addr(sm.live_len + c0)));
@@ -667,7 +671,7 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
   pipe_init<D>(pp, buf0, ntot, wave, lane);
 #pragma unroll
   for (int t = 0; t < kDepth; ++t)
-    if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, bt.tiles[t], bt, pp, wave, lane);
+    if (t < ntot) dma_stream_tile<D>(TREEPO_PARTIAL_ARGS, t, bt.tiles[t], bt, pp, wave, lane, false);
   if (kDepth < ntot) pp.next = bt.tiles[kDepth];
   for (int pi = 0; pi < np; ++pi) {
     const int4 r = *reinterpret_cast<const int4*>(sm.blk + kBlockHeaderInts + kBlockPieceInts * pi);
