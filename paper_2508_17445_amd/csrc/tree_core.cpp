@@ -179,8 +179,11 @@ struct Run {
   int32_t group_leaves = 1;     // leaves per group
 };
 
-// A piece's query tiles cost little next to its KV tiles (a few rows each).
-constexpr double kQTileCost = 0.25;
+// A piece's query tile takes a step of the tile pipeline like a KV tile (the
+// loads of 64 rows, repeats of the last row for a small piece); per-workgroup
+// timestamps of config-2 decodes put a piece's query tiles and start at about
+// one KV tile each.
+constexpr double kQTileCost = 1.0;
 // Guided stream sizes when the work takes several rounds of workgroups.
 constexpr double kGuide = 2.0;
 constexpr double kGuideMinCost = 8.0;
@@ -192,8 +195,8 @@ constexpr double kLiveEmptyWeight = 0.5;
 // Estimated cost of one KV tile for a piece of `rows` query rows, in units of
 // one tile's load time at full load (measured): the token-split path (up to
 // 32 rows) hides its compute under the loads; the row-split path takes about
-// 1.4 (one 16-row block per wave) and 2 (two per wave) times as long.
-double tile_cost(int32_t rows) { return rows <= 32 ? 1.0 : rows <= 64 ? 1.4 : 2.0; }
+// 1.4 (one 16-row block per wave) and 2.3 (two per wave) times as long.
+double tile_cost(int32_t rows) { return rows <= 32 ? 1.0 : rows <= 64 ? 1.4 : 2.3; }
 
 }  // namespace
 
@@ -312,30 +315,38 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   // ---- streams ------------------------------------------------------------------
   // One round (every stream resident at once): the concatenated sequences are
   // cut at equal cumulative cost, each stream's share in proportion to its
-  // slot's speed.  Several rounds: later streams start wherever a slot frees
-  // up, so the hardware dispatcher balances them; stream sizes shrink with the
-  // work left (each takes 1/kGuide of an even share of the remainder, between
+  // slot's and its die's speed.  Several rounds: later streams start wherever
+  // a slot of their die frees up, so the hardware dispatcher balances them
+  // within a die; stream sizes shrink with the work left (each takes 1/kGuide
+  // of an even share of the remainder, scaled by its die's speed, between
   // kGuideMinCost and a full LDS table), so the last streams to start are
   // short and the slots drain together.
   const int64_t S0 = std::max(1, p.concurrent_wgs);
+  const int32_t nx = p.xcds >= 1 && p.xcds <= 8 ? p.xcds : 1;
+  auto xcd_speed = [&](int64_t s) { return nx > 1 ? p.xcd_speed[s % nx] : 1.0; };
+  double xcd_mean = 0.0;
+  for (int32_t x = 0; x < nx; ++x) xcd_mean += xcd_speed(x);
+  xcd_mean /= nx;
   const double full_stream = 3 * kMaxStreamTiles / 4;
   const bool one_round = total_cost <= static_cast<double>(S0) * full_stream;
   const int64_t planned = one_round ? std::min<int64_t>(total_tiles, S0) : INT64_MAX;
-  // One round: stream s closes once the running cost passes quota[s], plus
-  // slack for the query tiles of a cut piece that every stream may start
-  // with, so that the last stream does not collect the rounding remainder.
+  // One round: stream s closes once the running cost passes quota[s], its
+  // share of the total cost in proportion to its slot's and die's speed.  The
+  // total counts one more query tile per stream: a stream starting inside a
+  // sequence loads the query rows of that piece again.
   std::vector<double> quota;
   if (one_round) {
     quota.resize(static_cast<size_t>(planned));
     std::vector<double> w(static_cast<size_t>(planned), 1.0);
     if (p.compute_units > 0)
       for (int64_t s = 0; s < planned; ++s) w[s] = p.slot_speed[s < p.compute_units ? 0 : 1];
+    for (int64_t s = 0; s < planned; ++s) w[s] *= xcd_speed(s);
     double wsum = 0.0;
     for (double x : w) wsum += x;
     double cum = 0.0;
     for (int64_t s = 0; s < planned; ++s) {
       cum += w[s];
-      quota[s] = total_cost * cum / wsum + 2 * kQTileCost * static_cast<double>(s + 1);
+      quota[s] = (total_cost + kQTileCost * static_cast<double>(planned)) * cum / wsum;
     }
   }
   // Several rounds: the open stream closes once the running cost reaches
@@ -344,7 +355,8 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   double total_kv_cost = 0.0, kv_acc = 0.0, guided_end = 0.0;
   for (const Seq& sq : seqs) total_kv_cost += tile_cost(sq.n_leaves * G) * runs[sq.run].weight;
   auto guided_quota = [&](double acc_now) {
-    const double share = (total_kv_cost - kv_acc) / (kGuide * static_cast<double>(S0));
+    const double speed = xcd_speed(static_cast<int64_t>(out->streams.size()) - 1) / xcd_mean;  // the open stream
+    const double share = speed * (total_kv_cost - kv_acc) / (kGuide * static_cast<double>(S0));
     return acc_now + std::min(full_stream, std::max(kGuideMinCost, share));
   };
   double acc = 0.0;

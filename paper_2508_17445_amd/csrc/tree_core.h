@@ -196,6 +196,11 @@ struct PlanParams {
   // slot_speed[slot] (both 1.0: equal cost per stream).
   int32_t compute_units;
   double slot_speed[2];
+  // Relative speed by accelerator die (XCD): workgroups are dealt to the
+  // xcds dies round robin, so stream s runs on die s % xcds; stream sizes
+  // (every round) are scaled by xcd_speed[s % xcds] (all 1.0: no scaling).
+  int32_t xcds;
+  double xcd_speed[8];
   // Lengths are read on the device: unfrozen nodes are planned up to their
   // capacity, tiles not yet full become live tiles.
   bool live_lengths;

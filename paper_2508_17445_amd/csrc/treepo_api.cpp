@@ -418,11 +418,16 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   ctx->params.max_rows = 128;
   ctx->params.concurrent_wgs = treepo::kComputeUnits * treepo::partial_workgroups_per_cu();
   // The second workgroup on a CU gets the smaller share of its issue and
-  // memory bandwidth (measured on config-2 decodes: about 0.85 of the first's
+  // memory bandwidth (measured on config-2 decodes: about 0.80 of the first's
   // progress over the same time).
   ctx->params.compute_units = treepo::kComputeUnits;
   ctx->params.slot_speed[0] = 1.0;
-  ctx->params.slot_speed[1] = 0.85;
+  ctx->params.slot_speed[1] = 0.80;
+  // Workgroups are dealt to the eight XCDs round robin; the odd-numbered
+  // ones streamed about 0.93-0.94 as many tiles per microsecond as the even
+  // ones in per-workgroup timestamps of config-2 decodes.
+  ctx->params.xcds = 8;
+  for (int x = 0; x < 8; ++x) ctx->params.xcd_speed[x] = x % 2 ? 0.935 : 1.0;
   ctx->live = c.node_len != nullptr;
   ctx->params.live_lengths = ctx->live;
   *out = ctx;
