@@ -332,8 +332,9 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
   const int64_t planned = one_round ? std::min<int64_t>(total_tiles, S0) : INT64_MAX;
   // One round: stream s closes once the running cost passes quota[s], its
   // share of the total cost in proportion to its slot's and die's speed.  The
-  // total counts one more query tile per stream: a stream starting inside a
-  // sequence loads the query rows of that piece again.
+  // query tiles that a stream starting inside a sequence loads again are left
+  // out of the running cost (each stream has about one such start), so the
+  // last stream's share stays proportional.
   std::vector<double> quota;
   if (one_round) {
     quota.resize(static_cast<size_t>(planned));
@@ -346,7 +347,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     double cum = 0.0;
     for (int64_t s = 0; s < planned; ++s) {
       cum += w[s];
-      quota[s] = (total_cost + kQTileCost * static_cast<double>(planned)) * cum / wsum;
+      quota[s] = total_cost * cum / wsum;
     }
   }
   // Several rounds: the open stream closes once the running cost reaches
@@ -422,7 +423,10 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
           out->stream_tiles.push_back(StreamTile{-1 - pc.seg_begin, row0 | (n << 16)});
         }
         st->n_tiles += nq;
-        acc += kQTileCost * nq;
+        // the sequence's own query tiles are part of total_cost; those a cut
+        // piece loads again are a per-stream overhead left out of the running
+        // cost (one-round quotas are fractions of total_cost)
+        if (ti == 0) acc += kQTileCost * nq;
         out->pieces.push_back(pc);
         st->piece_end = static_cast<int32_t>(out->pieces.size());
         new_piece = false;

@@ -194,10 +194,18 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
     assert entry == count
 
 
-def _stream_costs(pieces, n_streams, q_cost=1.0):
+def _stream_costs(pieces, n_streams, q_cost=1.0, cut_q=False):
+    """The planner's estimated cost per stream: KV tiles by piece height,
+    plus the query tiles of each sequence's first piece (and with cut_q also
+    those that a piece continuing a sequence cut at a stream boundary loads
+    again, which the planner leaves out as a per-stream overhead)."""
     cost = np.zeros(n_streams)
+    prev = None
     for pc in pieces:
-        cost[pc[9]] += pc[5] * _tile_cost(pc[2]) + q_cost * pc[11]
+        key = (pc[8], pc[0], pc[3])  # run, rowset, KV head
+        first = key != prev
+        prev = key
+        cost[pc[9]] += pc[5] * _tile_cost(pc[2]) + (q_cost * pc[11] if first or cut_q else 0.0)
     return cost
 
 
