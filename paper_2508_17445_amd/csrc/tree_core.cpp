@@ -180,10 +180,11 @@ struct Run {
 };
 
 // A piece's query tile takes a step of the tile pipeline like a KV tile (the
-// loads of 64 rows, repeats of the last row for a small piece); per-workgroup
-// timestamps of config-2 decodes put a piece's query tiles and start at about
-// one KV tile each.
-constexpr double kQTileCost = 1.0;
+// loads of 64 rows, repeats of the last row for a small piece) but no
+// matrix work.  Swept on the five workloads (0.25-1.0): 0.5 is within 0.3% of the
+// best on each; 1.0 makes 192-cost streams of long one-leaf sequences hold
+// 191 KV tiles, 5% slower on config 5's per-leaf plan.
+constexpr double kQTileCost = 0.5;
 // Guided stream sizes when the work takes several rounds of workgroups.
 constexpr double kGuide = 2.0;
 constexpr double kGuideMinCost = 8.0;

@@ -194,7 +194,7 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
     assert entry == count
 
 
-def _stream_costs(pieces, n_streams, q_cost=1.0, cut_q=False):
+def _stream_costs(pieces, n_streams, q_cost=0.5, cut_q=False):
     """The planner's estimated cost per stream: KV tiles by piece height,
     plus the query tiles of each sequence's first piece (and with cut_q also
     those that a piece continuing a sequence cut at a stream boundary loads
