@@ -38,19 +38,29 @@ struct CachedPlan {
   size_t off_comb = 0;
   size_t off_part_o = 0, off_part_ml = 0, ws_bytes = 0;  // partials, in the caller's workspace
   uint64_t last_use = 0;
-  // Device copy of `blob`, owned by the context (the buffer stays with the
-  // cache entry when a new plan replaces it).  Uploaded on the first decode
-  // with the plan, on that call's stream; decodes on other streams wait for
-  // the upload's event.  done_ev follows the last decode that read it.
+  // Device copy of `blob` in memory the context owns.  Uploaded on the first
+  // decode with the plan, on that call's stream; decodes on other streams
+  // wait for the upload's event.  No event follows each decode: when the plan
+  // leaves the cache its buffer is retired with one event recorded on the
+  // stream of its last decode (see RetiredImage).
   void* dev = nullptr;
   size_t dev_cap = 0;
   bool dev_valid = false;
   hipStream_t up_stream = nullptr;
   hipEvent_t up_ev = nullptr;
-  hipEvent_t done_ev = nullptr;
-  bool used = false;          // done_ev recorded
-  bool multi_stream = false;  // read on more than one stream
+  hipStream_t last_stream = nullptr;  // stream of the latest decode with this plan
+  bool multi_stream = false;          // read on more than one stream
 };
+
+// A plan image buffer no longer in the cache: reused for a new plan, or
+// freed, once `ev` (recorded after every decode that read it; null if none
+// did) has completed.
+struct RetiredImage {
+  void* dev;
+  size_t cap;
+  hipEvent_t ev;
+};
+constexpr size_t kMaxRetired = 8;
 
 struct PinnedSlot {
   void* p = nullptr;
@@ -78,6 +88,7 @@ struct treepo_ctx {
   bool profiling = false;
   std::vector<TimedLaunch> timed;
   std::vector<hipEvent_t> spare_events;
+  std::vector<RetiredImage> retired;
   // Device lengths (cfg.node_len): stale after kv_commit, new_root or fork;
   // the next decode uploads the host table on its stream.
   bool live = false;
@@ -186,37 +197,94 @@ void put(std::vector<char>& blob, size_t off, const std::vector<T>& v) {
   if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
 }
 
-// Waits until no queued kernel reads the entry's device image.
-hipError_t retire_image(CachedPlan& cp) {
+// Frees a retired buffer after its last reader has finished.
+hipError_t free_retired(RetiredImage& r) {
   hipError_t e = hipSuccess;
-  if (cp.multi_stream)
-    e = hipDeviceSynchronize();
-  else if (cp.used)
-    e = hipEventSynchronize(cp.done_ev);
-  cp.used = false;
-  cp.multi_stream = false;
+  if (r.ev) {
+    e = hipEventSynchronize(r.ev);
+    (void)hipEventDestroy(r.ev);
+    r.ev = nullptr;
+  }
+  if (r.dev) {
+    const hipError_t f = hipFree(r.dev);
+    if (e == hipSuccess) e = f;
+    r.dev = nullptr;
+  }
+  return e;
+}
+
+// Moves a cache entry's image buffer to the retired list: one event on the
+// stream of its last decode marks when no kernel reads it any more (a device
+// synchronisation if it was read on several streams).  Keeps the list short
+// by freeing the oldest buffers.
+hipError_t retire_image(treepo_ctx* ctx, CachedPlan& cp) {
+  hipError_t e = hipSuccess;
+  if (cp.up_ev) {
+    (void)hipEventDestroy(cp.up_ev);
+    cp.up_ev = nullptr;
+  }
+  if (cp.dev) {
+    RetiredImage r{cp.dev, cp.dev_cap, nullptr};
+    if (cp.dev_valid) {
+      if (cp.multi_stream) {
+        e = hipDeviceSynchronize();
+      } else {
+        e = hipEventCreateWithFlags(&r.ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventRecord(r.ev, cp.last_stream);
+      }
+    }
+    if (e != hipSuccess) {
+      // cannot tell when its readers finish: wait for the whole device
+      if (r.ev) (void)hipEventDestroy(r.ev);
+      r.ev = nullptr;
+      e = hipDeviceSynchronize();
+    }
+    ctx->retired.push_back(r);
+  }
+  cp.dev = nullptr;
+  cp.dev_cap = 0;
   cp.dev_valid = false;
+  cp.multi_stream = false;
+  while (ctx->retired.size() > kMaxRetired) {
+    const hipError_t f = free_retired(ctx->retired.front());
+    ctx->retired.erase(ctx->retired.begin());
+    if (e == hipSuccess) e = f;
+  }
   return e;
 }
 
 // Makes the plan's device image current for a decode on `s`: uploads it on
-// the first use (growing the entry's buffer if needed), else orders `s`
-// after the upload.
+// the first use (into a retired buffer whose readers have finished, or a new
+// one), else orders `s` after the upload.
 hipError_t stage_image(treepo_ctx* ctx, CachedPlan& cp, hipStream_t s) {
   hipError_t e;
   if (cp.dev_valid) {
-    if (s == cp.up_stream) return hipSuccess;
-    cp.multi_stream = true;
-    return hipStreamWaitEvent(s, cp.up_ev, 0);
-  }
-  const size_t bytes = std::max<size_t>(cp.blob.size(), kAlign);
-  if (cp.dev_cap < bytes) {
-    if (cp.dev) {
-      e = hipFree(cp.dev);
-      cp.dev = nullptr;
-      cp.dev_cap = 0;
+    if (s != cp.up_stream) {
+      cp.multi_stream = true;
+      e = hipStreamWaitEvent(s, cp.up_ev, 0);
       if (e != hipSuccess) return e;
     }
+    cp.last_stream = s;
+    return hipSuccess;
+  }
+  const size_t bytes = std::max<size_t>(cp.blob.size(), kAlign);
+  if (!cp.dev) {
+    for (size_t i = 0; i < ctx->retired.size(); ++i) {
+      RetiredImage& r = ctx->retired[i];
+      if (r.cap < bytes) continue;
+      if (r.ev) {
+        const hipError_t q = hipEventQuery(r.ev);
+        if (q == hipErrorNotReady) continue;
+        if (q != hipSuccess) return q;
+        (void)hipEventDestroy(r.ev);
+      }
+      cp.dev = r.dev;
+      cp.dev_cap = r.cap;
+      ctx->retired.erase(ctx->retired.begin() + static_cast<std::ptrdiff_t>(i));
+      break;
+    }
+  }
+  if (!cp.dev) {
     e = hipMalloc(&cp.dev, bytes);
     if (e != hipSuccess) return e;
     cp.dev_cap = bytes;
@@ -225,15 +293,12 @@ hipError_t stage_image(treepo_ctx* ctx, CachedPlan& cp, hipStream_t s) {
     e = hipEventCreateWithFlags(&cp.up_ev, hipEventDisableTiming);
     if (e != hipSuccess) return e;
   }
-  if (!cp.done_ev) {
-    e = hipEventCreateWithFlags(&cp.done_ev, hipEventDisableTiming);
-    if (e != hipSuccess) return e;
-  }
   e = upload(ctx, cp.dev, cp.blob.data(), cp.blob.size(), s);
   if (e != hipSuccess) return e;
   e = hipEventRecord(cp.up_ev, s);
   if (e != hipSuccess) return e;
   cp.up_stream = s;
+  cp.last_stream = s;
   cp.dev_valid = true;
   return hipSuccess;
 }
@@ -281,13 +346,8 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   if (static_cast<int>(ctx->plans.size()) >= kPlanCache) {
     auto lru = std::min_element(ctx->plans.begin(), ctx->plans.end(),
                                 [](const CachedPlan& a, const CachedPlan& b) { return a.last_use < b.last_use; });
-    // the new plan takes over the entry's device buffer once no kernel reads it
-    hipError_t e = retire_image(*lru);
+    hipError_t e = retire_image(ctx, *lru);
     if (e != hipSuccess) return hip_fail(ctx, e, "plan cache");
-    cp.dev = lru->dev;
-    cp.dev_cap = lru->dev_cap;
-    cp.up_ev = lru->up_ev;
-    cp.done_ev = lru->done_ev;
     *lru = std::move(cp);
     *out = &*lru;
   } else {
@@ -354,9 +414,6 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
   e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
-  e = hipEventRecord(cp->done_ev, stream);
-  if (e != hipSuccess) return hip_fail(ctx, e, "plan event");
-  cp->used = true;
   return TREEPO_OK;
 }
 
@@ -447,12 +504,8 @@ int32_t treepo_destroy(treepo_ctx* ctx) {
     (void)hipEventDestroy(t.stop);
   }
   for (hipEvent_t e : ctx->spare_events) (void)hipEventDestroy(e);
-  for (CachedPlan& cp : ctx->plans) {
-    (void)retire_image(cp);
-    if (cp.dev) (void)hipFree(cp.dev);
-    if (cp.up_ev) (void)hipEventDestroy(cp.up_ev);
-    if (cp.done_ev) (void)hipEventDestroy(cp.done_ev);
-  }
+  for (CachedPlan& cp : ctx->plans) (void)retire_image(ctx, cp);
+  for (RetiredImage& r : ctx->retired) (void)free_retired(r);
   delete ctx;
   return TREEPO_OK;
 }
