@@ -263,8 +263,11 @@ int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* l
 #define TREEPO_KERNEL_COMBINE 2 /* log-sum-exp merge of each leaf's partials      */
 #define TREEPO_KERNEL_KINDS 3
 
-/* When enabled, every kernel launch of this context is bracketed by HIP events
- * on the launch stream.  Enabling or disabling clears the totals. */
+/* When enabled, every kernel launch of this context is timed with HIP events
+ * on the launch stream: the decode kernels (partial, combine) get events that
+ * the launch attaches to the kernel itself (hipExtLaunchKernelGGL: recorded
+ * at its start and end), the append kernel's launches are bracketed by
+ * events.  Enabling or disabling clears the totals. */
 int32_t treepo_set_profiling(treepo_ctx* ctx, int32_t enable);
 /* Total milliseconds and launch count per kernel kind since profiling was
  * enabled; waits for the recorded events to complete. */

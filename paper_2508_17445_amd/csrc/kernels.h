@@ -25,6 +25,9 @@ struct DecodeArgs {
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
   const int32_t* comb_count;  // per key (leaf, KV head): partial entries to merge
   int32_t emax;               // entries per key at most (partial slot stride)
+  // Profiling: when set, the launch records these events at the kernel's
+  // start and end (hipExtLaunchKernelGGL), so they time the kernel alone.
+  hipEvent_t ev_start = nullptr, ev_stop = nullptr;
   int32_t n_leaves;
   float* out;              // fp32 [n_leaves][Hq][D]
   float* lse;              // fp32 [n_leaves][Hq] or null

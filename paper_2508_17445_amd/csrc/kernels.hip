@@ -17,6 +17,8 @@
 // (32-token tiles), each one contiguous 8 KiB (D = 128) range per pool.
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 #include <math.h>
 
 #include "tree_core.h"
@@ -877,17 +879,27 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
 
 int32_t partial_workgroups_per_cu() { return kWgsPerCu; }
 
+// Launches `kernel` on `s`; with a.ev_start set, the events record the
+// kernel's own start and end.
+template <typename... Args, typename F>
+void launch_timed(const DecodeArgs& a, F kernel, dim3 grid, hipStream_t s, Args... args) {
+  if (a.ev_start)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a.ev_start, a.ev_stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, args...);
+}
+
 hipError_t launch_partial(const DecodeArgs& a, hipStream_t s) {
   if (a.n_streams <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(a.n_streams));
   const Scalars sc{a.hq, a.hkv, a.group, a.scale_log2};
   if (a.block_ints <= 0 || a.block_ints > kMaxBlockInts || a.block_ints % 4 != 0) return hipErrorInvalidValue;
   if (a.d == 128)
-    partial_kernel<128><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,
-                                                  a.part_o, a.part_ml, sc);
+    launch_timed(a, partial_kernel<128>, grid, s, a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,
+                 a.part_o, a.part_ml, sc);
   else
-    partial_kernel<64><<<grid, kThreads, 0, s>>>(a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,
-                                                 a.part_o, a.part_ml, sc);
+    launch_timed(a, partial_kernel<64>, grid, s, a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,
+                 a.part_o, a.part_ml, sc);
   return hipGetLastError();
 }
 
@@ -895,11 +907,11 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   const int64_t waves = static_cast<int64_t>(a.n_leaves) * a.hq;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
   if (a.d == 128)
-    combine_kernel<128><<<grid, kThreads, 0, s>>>(a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
-                                                  a.n_leaves, a.hq, a.hkv, a.group);
+    launch_timed(a, combine_kernel<128>, grid, s, a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
+                 a.n_leaves, a.hq, a.hkv, a.group);
   else
-    combine_kernel<64><<<grid, kThreads, 0, s>>>(a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
-                                                 a.n_leaves, a.hq, a.hkv, a.group);
+    launch_timed(a, combine_kernel<64>, grid, s, a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
+                 a.n_leaves, a.hq, a.hkv, a.group);
   return hipGetLastError();
 }
 

@@ -136,6 +136,26 @@ hipError_t drain_timings(treepo_ctx* ctx) {
   return hipSuccess;
 }
 
+// Runs `launch(start, stop)`; with profiling on it gets two timing events
+// that the launch attaches to its kernel (recorded at the kernel's own start
+// and end), otherwise two null events.
+template <class F>
+hipError_t timed_launch_attached(treepo_ctx* ctx, int kind, F launch) {
+  if (!ctx->profiling) return launch(nullptr, nullptr);
+  if (ctx->timed.size() > 8192) {
+    hipError_t e = drain_timings(ctx);
+    if (e != hipSuccess) return e;
+  }
+  TimedLaunch t{kind, nullptr, nullptr};
+  hipError_t e = get_event(ctx, &t.start);
+  if (e == hipSuccess) e = get_event(ctx, &t.stop);
+  if (e != hipSuccess) return e;
+  e = launch(t.start, t.stop);
+  if (e != hipSuccess) return e;
+  ctx->timed.push_back(t);
+  return hipSuccess;
+}
+
 // Runs `launch` bracketed by events when profiling is on.
 template <class F>
 hipError_t timed_launch(treepo_ctx* ctx, int kind, hipStream_t s, F launch) {
@@ -410,9 +430,17 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;
-  hipError_t e = timed_launch(ctx, TREEPO_KERNEL_PARTIAL, stream, [&] { return treepo::launch_partial(a, stream); });
+  hipError_t e = timed_launch_attached(ctx, TREEPO_KERNEL_PARTIAL, [&](hipEvent_t t0, hipEvent_t t1) {
+    a.ev_start = t0;
+    a.ev_stop = t1;
+    return treepo::launch_partial(a, stream);
+  });
   if (e != hipSuccess) return hip_fail(ctx, e, "partial kernel launch");
-  e = timed_launch(ctx, TREEPO_KERNEL_COMBINE, stream, [&] { return treepo::launch_combine(a, stream); });
+  e = timed_launch_attached(ctx, TREEPO_KERNEL_COMBINE, [&](hipEvent_t t0, hipEvent_t t1) {
+    a.ev_start = t0;
+    a.ev_stop = t1;
+    return treepo::launch_combine(a, stream);
+  });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
   return TREEPO_OK;
 }
