@@ -194,10 +194,11 @@ constexpr double kGuideMinCost = 8.0;
 constexpr double kLiveEmptyWeight = 0.5;
 
 // Estimated cost of one KV tile for a piece of `rows` query rows, in units of
-// one tile's load time at full load (measured): the token-split path (up to
-// 32 rows) hides its compute under the loads; the row-split path takes about
-// 1.4 (one 16-row block per wave) and 2.3 (two per wave) times as long.
-double tile_cost(int32_t rows) { return rows <= 32 ? 1.0 : rows <= 64 ? 1.4 : 2.3; }
+// one tile's load time at full load (fitted to per-workgroup timestamps and
+// swept on the five workloads): the token-split path hides its compute under
+// the loads (1.0 for one 16-row block, 1.1 for two); the row-split path takes
+// about 1.4 (one 16-row block per wave) and 2.6 (two per wave) times as long.
+double tile_cost(int32_t rows) { return rows <= 16 ? 1.0 : rows <= 32 ? 1.1 : rows <= 64 ? 1.4 : 2.6; }
 
 }  // namespace
 
