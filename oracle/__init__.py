@@ -19,6 +19,8 @@ What it computes follows TreePO (arXiv 2508.17445):
   prefixes are represented once).
 * ``cascade`` -- the log-sum-exp algebra that lets per-node partial results be
   merged into the per-leaf result; it is pinned against ``attention``.
+* ``advantage`` -- the TreePO advantage over the same descendant sets
+  (Sec. 2.3, Eq. tree_ae; the size-weighted variant Eq. tree_ae_sgw).
 """
 
-from . import metadata, attention, cascade  # noqa: F401
+from . import metadata, attention, cascade, advantage  # noqa: F401

@@ -120,3 +120,96 @@ def test_mutation_is_caught(name, monkeypatch):
         except (AssertionError, IndexError, ValueError):
             failed.append(pin.__name__)
     assert failed, f"mutation {name} passed every pin"
+
+
+# ---- the TreePO advantage oracle ----------------------------------------------
+
+from oracle import advantage as ADV  # noqa: E402
+from tests import advantage_pins as AP  # noqa: E402
+
+
+def _adv_factory(kind):
+    def subgroups(parents, leaves, rewards):
+        chains = [ADV.chain(parents, int(x)) for x in leaves]
+        members = {}
+        for p, ch in enumerate(chains):
+            for a in ch:
+                members.setdefault(a, []).append(p)
+        R = np.asarray(rewards, dtype=np.float64)
+        rows = []
+        for p, ch in enumerate(chains):
+            preds = ch if kind == "own_node_group" else ch[:-1]
+            row = []
+            for a in preds:
+                g = members[a]
+                if kind == "leave_one_out":
+                    others = [k for k in g if k != p] or g
+                    base = R[others].mean()
+                else:
+                    base = R[g].mean()
+                row.append((a, len(g), R[p] - base))
+            rows.append(row)
+        return rows, chains
+
+    def tree_advantage(parents, leaves, rewards, weighting="mean"):
+        R = np.asarray(rewards, dtype=np.float64)
+        n = len(leaves)
+        rows, chains = subgroups(parents, leaves, rewards)
+        roots = [ch[0] for ch in chains]
+        kept = []
+        for p in range(n):
+            g = [k for k in range(n) if roots[k] == roots[p]]
+            kept.append(kind == "no_rejection" or bool(np.std(R[g]) != 0.0))
+        adv = np.zeros(n)
+        pooled = np.zeros(n)
+        for p in range(n):
+            if not rows[p]:
+                continue
+            a = np.array([x for (_, _, x) in rows[p]])
+            w = np.array([s for (_, s, _) in rows[p]], dtype=float)
+            if kind == "inverse_size":
+                w = 1.0 / w
+            pooled[p] = a.mean() if weighting == "mean" else (w * a).sum() / w.sum()
+        pairs = [x for p in range(n) if kept[p] for (_, _, x) in rows[p]]
+        if not pairs:
+            return adv
+        if kind == "ddof1":
+            sigma = float(np.std(pairs, ddof=1))
+        elif kind == "pooled_std":
+            sigma = float(np.std([pooled[p] for p in range(n) if kept[p] and rows[p]]))
+        else:
+            sigma = float(np.std(pairs))
+        for p in range(n):
+            if kept[p] and rows[p]:
+                s = sigma
+                if kind == "per_query_std":
+                    s = float(np.std([x for k in range(n) if roots[k] == roots[p] for (_, _, x) in rows[k]]))
+                adv[p] = pooled[p] / s if s > 0 else 0.0
+        return adv
+
+    return subgroups, tree_advantage
+
+
+@pytest.mark.parametrize("kind", ["own_node_group", "leave_one_out", "no_rejection", "inverse_size", "ddof1",
+                                  "pooled_std", "per_query_std"])
+def test_advantage_mutation_caught(kind, monkeypatch):
+    subgroups, adv = _adv_factory(kind)
+    monkeypatch.setattr(ADV, "subgroup_advantages", subgroups)
+    monkeypatch.setattr(ADV, "tree_advantage", adv)
+    failed = []
+    for pin in AP.ALL:
+        try:
+            pin()
+        except AssertionError:
+            failed.append(pin.__name__)
+    assert failed, f"mutation {kind} passed every advantage pin"
+
+
+def test_advantage_mutation_factory_faithful():
+    """The unmutated copy used above reproduces the oracle (so a caught
+    mutation is caught for its planted mistake)."""
+    _, adv = _adv_factory("none")
+    parents, leaves = AP.random_forest(5)
+    R = np.random.default_rng(5).normal(size=len(leaves))
+    for w in ("mean", "size"):
+        assert np.abs(adv(parents, leaves, R, w) - ADV.tree_advantage(parents, leaves, R, w)).max() <= 1e-12
