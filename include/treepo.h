@@ -184,6 +184,42 @@ int32_t treepo_paged_decode_naive(treepo_ctx* ctx, int32_t n_leaves, const int32
                                   const void* q, float scale, float* out, float* lse,
                                   void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ---- TreePO advantage ---------------------------------------------------- */
+
+/* Aggregations for treepo_tree_advantage. */
+#define TREEPO_ADV_MEAN 0           /* mean over sub-groups (Sec. 2.3, Eq. tree_ae)         */
+#define TREEPO_ADV_SIZE_WEIGHTED 1  /* |G_j|-weighted mean (Sec. 4.1, Eq. tree_ae_sgw)      */
+
+/* Workspace bytes that treepo_tree_advantage needs for these leaves. */
+int32_t treepo_advantage_workspace_size(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                                        size_t* bytes);
+
+/* TreePO advantage of every trajectory (Sec. 2.3: Eq. groups, Eq. tree_ae;
+ * Fig. 3 caption).  Call position p is a trajectory: the chain of node
+ * leaves[p] (any node; duplicates allowed).  A query is a root; its group G
+ * holds every position under it.  The sub-groups of p are, for each strict
+ * predecessor a of leaves[p] (root first), G_a = the positions whose chain
+ * contains a.  With R = rewards:
+ *   A_{p,a} = R_p - mean over G_a of R;
+ *   pooled_p = mean over a of A_{p,a} (TREEPO_ADV_MEAN), or the
+ *              |G_a|-weighted mean (TREEPO_ADV_SIZE_WEIGHTED);
+ *   adv_p = pooled_p / sigma, sigma = the population standard deviation of
+ *           every A_{p,a} of every kept query (one global normalisation).
+ * A query whose rewards are all equal is rejected (the paper's constraint
+ * std(R over G) != 0): its positions get 0 and add nothing to sigma; so does
+ * a position with no predecessor (a root).  If sigma is 0, every adv is 0.
+ *   rewards   device fp32 [n_leaves]
+ *   adv       device fp32 [n_leaves] (written)
+ *   workspace device, 256-byte aligned, >= treepo_advantage_workspace_size;
+ *             the call uploads its index arrays there (contents need not
+ *             survive between calls)
+ * Arithmetic in fp64 on the device, in a fixed order (deterministic).
+ * EINVAL (bad id, null pointer, n_leaves < 1, bad weighting), EWORKSPACE,
+ * EHIP.  Leaves need not hold tokens. */
+int32_t treepo_tree_advantage(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                              const float* rewards, int32_t weighting, float* adv, void* workspace,
+                              size_t ws_bytes, hipStream_t stream);
+
 /* ---- metadata export (host arrays) -------------------------------------- */
 
 /* Number of nodes created so far. */
@@ -261,7 +297,8 @@ int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* l
 #define TREEPO_KERNEL_APPEND 0  /* KV scatter into the pools                      */
 #define TREEPO_KERNEL_PARTIAL 1 /* node partials, one workgroup per stream         */
 #define TREEPO_KERNEL_COMBINE 2 /* log-sum-exp merge of each leaf's partials      */
-#define TREEPO_KERNEL_KINDS 3
+#define TREEPO_KERNEL_ADVANTAGE 3 /* TreePO advantage over the leaves' sub-groups  */
+#define TREEPO_KERNEL_KINDS 4
 
 /* When enabled, every kernel launch of this context is timed with HIP events
  * on the launch stream: the decode kernels (partial, combine) get events that

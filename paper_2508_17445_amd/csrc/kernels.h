@@ -39,6 +39,29 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // Node-partial workgroups resident per compute unit (set by the kernel's
 // register and LDS budget); the planner makes one stream per resident slot.
 int32_t partial_workgroups_per_cu();
+
+// TreePO advantage (advantage.hip): one workgroup over index arrays built on
+// the host from the leaves' chains.  Sub-group g = the call positions whose
+// chain contains node g (members grp_mem[grp_off[g], grp_off[g+1]));
+// position p's strict predecessors are the sub-groups
+// pos_grp[pos_off[p], pos_off[p+1]) (root first), its query's group
+// pos_root[p].
+struct AdvantageArgs {
+  const int32_t* grp_off;
+  const int32_t* grp_mem;
+  int32_t n_groups;
+  const int32_t* pos_off;
+  const int32_t* pos_grp;
+  const int32_t* pos_root;
+  int32_t n_pos;
+  const float* rewards;    // [n_pos], device
+  int32_t size_weighted;   // 0: mean over sub-groups, 1: |G|-weighted mean
+  double* gmean;           // [n_groups] scratch
+  int32_t* gkeep;          // [n_groups] scratch: rewards of the sub-group not all equal
+  double* pooled;          // [n_pos] scratch
+  float* adv;              // [n_pos], device
+};
+hipError_t launch_advantage(const AdvantageArgs& a, hipStream_t s);
 constexpr int32_t kComputeUnits = 256;  // MI355X
 
 // One block-aligned run of appended tokens: source rows [src_row, +count) go

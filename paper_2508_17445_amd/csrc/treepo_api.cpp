@@ -93,8 +93,8 @@ struct treepo_ctx {
   // the next decode uploads the host table on its stream.
   bool live = false;
   bool dev_len_stale = true;
-  double prof_ms[TREEPO_KERNEL_KINDS] = {0, 0, 0};
-  int64_t prof_n[TREEPO_KERNEL_KINDS] = {0, 0, 0};
+  double prof_ms[TREEPO_KERNEL_KINDS] = {};
+  int64_t prof_n[TREEPO_KERNEL_KINDS] = {};
 
   treepo_ctx(const treepo_config& c)
       : cfg(c), tree(c.block_tokens, c.num_blocks, c.max_nodes) {}
@@ -480,6 +480,79 @@ void append_pieces(const treepo::Tree& t, int32_t n, const int32_t* nodes, const
 
 }  // namespace
 
+namespace {
+
+// Index arrays of the advantage kernel for a leaf list, as one int32 image
+// (uploaded into the workspace), plus the scratch that follows it.
+struct AdvPlan {
+  std::vector<int32_t> ints;
+  int32_t n_groups = 0;
+  size_t off_grp_off = 0, off_grp_mem = 0, off_pos_off = 0, off_pos_grp = 0, off_pos_root = 0;  // in ints
+  size_t off_gmean = 0, off_gkeep = 0, off_pooled = 0, ws_bytes = 0;                           // in bytes
+};
+
+// Sub-group g = a node on some leaf's chain, numbered in order of first
+// appearance (positions ascending, chains root first); its members are the
+// positions whose chain contains it, ascending.
+void build_adv_plan(const treepo::Tree& t, int32_t n, const int32_t* leaves, AdvPlan* ap) {
+  std::vector<std::vector<int32_t>> chains(n);
+  std::vector<int32_t> gid(t.nodes().size(), -1);
+  std::vector<std::vector<int32_t>> members;
+  for (int32_t p = 0; p < n; ++p) {
+    t.chain(leaves[p], &chains[p]);
+    for (int32_t x : chains[p]) {
+      if (gid[x] < 0) {
+        gid[x] = static_cast<int32_t>(members.size());
+        members.emplace_back();
+      }
+      members[gid[x]].push_back(p);
+    }
+  }
+  const int32_t G = static_cast<int32_t>(members.size());
+  std::vector<int32_t>& v = ap->ints;
+  v.clear();
+  ap->n_groups = G;
+  ap->off_grp_off = v.size();
+  int32_t acc = 0;
+  for (int32_t g = 0; g < G; ++g) {
+    v.push_back(acc);
+    acc += static_cast<int32_t>(members[g].size());
+  }
+  v.push_back(acc);
+  ap->off_grp_mem = v.size();
+  for (const auto& m : members) v.insert(v.end(), m.begin(), m.end());
+  ap->off_pos_off = v.size();
+  acc = 0;
+  for (int32_t p = 0; p < n; ++p) {
+    v.push_back(acc);
+    acc += static_cast<int32_t>(chains[p].size()) - 1;
+  }
+  v.push_back(acc);
+  ap->off_pos_grp = v.size();
+  for (int32_t p = 0; p < n; ++p)
+    for (size_t j = 0; j + 1 < chains[p].size(); ++j) v.push_back(gid[chains[p][j]]);
+  ap->off_pos_root = v.size();
+  for (int32_t p = 0; p < n; ++p) v.push_back(gid[chains[p][0]]);
+  size_t off = align_up(v.size() * sizeof(int32_t));
+  ap->off_gmean = off;
+  off = align_up(off + static_cast<size_t>(G) * sizeof(double));
+  ap->off_gkeep = off;
+  off = align_up(off + static_cast<size_t>(G) * sizeof(int32_t));
+  ap->off_pooled = off;
+  off = align_up(off + static_cast<size_t>(n) * sizeof(double));
+  ap->ws_bytes = off;
+}
+
+int32_t check_ids(treepo_ctx* ctx, int32_t n, const int32_t* leaves) {
+  if (n < 1 || !leaves) return fail(ctx, TREEPO_EINVAL, "need at least one leaf");
+  for (int32_t i = 0; i < n; ++i)
+    if (leaves[i] < 0 || leaves[i] >= static_cast<int32_t>(ctx->tree.nodes().size()))
+      return fail(ctx, TREEPO_EINVAL, "unknown leaf id");
+  return TREEPO_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
@@ -609,6 +682,55 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
     if (e != hipSuccess) return hip_fail(ctx, e, "append kernel launch");
   }
   ctx->tree.apply_append(n, nodes, ntok);
+  return TREEPO_OK;
+}
+
+int32_t treepo_advantage_workspace_size(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
+                                        size_t* bytes) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (!bytes) return fail(ctx, TREEPO_EINVAL, "null bytes");
+  const int32_t st = check_ids(ctx, n_leaves, leaves);
+  if (st != TREEPO_OK) return st;
+  AdvPlan ap;
+  build_adv_plan(ctx->tree, n_leaves, leaves, &ap);
+  *bytes = ap.ws_bytes;
+  return TREEPO_OK;
+}
+
+int32_t treepo_tree_advantage(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, const float* rewards,
+                              int32_t weighting, float* adv, void* workspace, size_t ws_bytes,
+                              hipStream_t stream) {
+  if (!ctx) return TREEPO_EINVAL;
+  int32_t st = check_ids(ctx, n_leaves, leaves);
+  if (st != TREEPO_OK) return st;
+  if (!rewards || !adv) return fail(ctx, TREEPO_EINVAL, "null rewards or adv");
+  if (weighting != TREEPO_ADV_MEAN && weighting != TREEPO_ADV_SIZE_WEIGHTED)
+    return fail(ctx, TREEPO_EINVAL, "bad weighting");
+  AdvPlan ap;
+  build_adv_plan(ctx->tree, n_leaves, leaves, &ap);
+  if (!workspace || ws_bytes < ap.ws_bytes || reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(ctx, TREEPO_EWORKSPACE,
+                "workspace missing, smaller than treepo_advantage_workspace_size or not 256-byte aligned");
+  char* wsb = static_cast<char*>(workspace);
+  hipError_t e = upload(ctx, wsb, ap.ints.data(), ap.ints.size() * sizeof(int32_t), stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "advantage index upload");
+  const int32_t* ints = reinterpret_cast<const int32_t*>(wsb);
+  treepo::AdvantageArgs a;
+  a.grp_off = ints + ap.off_grp_off;
+  a.grp_mem = ints + ap.off_grp_mem;
+  a.n_groups = ap.n_groups;
+  a.pos_off = ints + ap.off_pos_off;
+  a.pos_grp = ints + ap.off_pos_grp;
+  a.pos_root = ints + ap.off_pos_root;
+  a.n_pos = n_leaves;
+  a.rewards = rewards;
+  a.size_weighted = weighting == TREEPO_ADV_SIZE_WEIGHTED;
+  a.gmean = reinterpret_cast<double*>(wsb + ap.off_gmean);
+  a.gkeep = reinterpret_cast<int32_t*>(wsb + ap.off_gkeep);
+  a.pooled = reinterpret_cast<double*>(wsb + ap.off_pooled);
+  a.adv = adv;
+  e = timed_launch(ctx, TREEPO_KERNEL_ADVANTAGE, stream, [&] { return treepo::launch_advantage(a, stream); });
+  if (e != hipSuccess) return hip_fail(ctx, e, "advantage kernel launch");
   return TREEPO_OK;
 }
 

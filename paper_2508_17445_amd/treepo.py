@@ -21,7 +21,8 @@ LIB_PATH = os.environ.get("TREEPO_LIBRARY") or os.path.join(HERE, "libtreepo.so"
 
 OK, EINVAL, ENOMEM, EFULL, EFROZEN, EEMPTY, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 MODE_TREE, MODE_NAIVE = 0, 1
-KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE = 0, 1, 2
+KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE, KERNEL_ADVANTAGE = 0, 1, 2, 3
+ADV_MEAN, ADV_SIZE_WEIGHTED = 0, 1
 NODE_FIELDS = ("parent", "depth", "start", "len", "cap", "block_begin", "n_blocks", "tree_id")
 BLOCK_TOKENS = 64
 PIECE_FIELDS = 16
@@ -78,6 +79,8 @@ def load_library(path: str = LIB_PATH):
         "treepo_profile_read": (_i32, [_p, _i32, ctypes.POINTER(ctypes.c_double), _pi64]),
         "treepo_strerror": (ctypes.c_char_p, [_i32]),
         "treepo_last_error": (ctypes.c_char_p, [_p]),
+        "treepo_advantage_workspace_size": (_i32, [_p, _i32, _pi32, ctypes.POINTER(ctypes.c_size_t)]),
+        "treepo_tree_advantage": (_i32, [_p, _i32, _pi32, _p, _i32, _p, _p, ctypes.c_size_t, _p]),
         "treepo_bench_copy": (_i32, [_p, _p, ctypes.c_size_t, _p]),
         "treepo_bench_read": (_i32, [_p, ctypes.c_size_t, _p, _p]),
         "treepo_bench_stream": (_i32, [_p, ctypes.c_size_t, _p, _i32, _i32, _p]),
@@ -269,6 +272,21 @@ class Context:
         self._check(self.lib.treepo_export_blocks(self.h, len(lv), _ptr32(lv), mode, _ptr32(out), ctypes.byref(bi),
                                                   ctypes.byref(ns)), "treepo_export_blocks")
         return out[:ns.value]
+
+    # ---- TreePO advantage --------------------------------------------------
+    def advantage_workspace_size(self, leaves) -> int:
+        lv = _arr32(leaves)
+        n = ctypes.c_size_t()
+        self._check(self.lib.treepo_advantage_workspace_size(self.h, len(lv), _ptr32(lv), ctypes.byref(n)),
+                    "treepo_advantage_workspace_size")
+        return n.value
+
+    def tree_advantage(self, leaves, rewards, adv, workspace, weighting: int = 0, ws_bytes=None, stream=None):
+        """adv[p] = TreePO advantage of call position p (rewards, adv: device fp32)."""
+        lv = _arr32(leaves)
+        nb = int(workspace.numel() * workspace.element_size()) if ws_bytes is None else ws_bytes
+        self._check(self.lib.treepo_tree_advantage(self.h, len(lv), _ptr32(lv), _dev(rewards), weighting, _dev(adv),
+                                                   _dev(workspace), nb, _stream(stream)), "treepo_tree_advantage")
 
     # ---- timing ------------------------------------------------------------
     def set_profiling(self, enable: bool):

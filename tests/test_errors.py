@@ -108,3 +108,22 @@ def test_codes_match_oracle_on_random_ops(seed):
             assert r_lib == r_ref
         ref = np.array([model.record(i) for i in range(len(model.nodes))], dtype=np.int32).reshape(-1, 8)
         assert np.array_equal(ctx.export_nodes().reshape(-1, 8), ref)
+
+
+def test_advantage_codes():
+    """treepo_tree_advantage validates before any device work; leaves need no tokens."""
+    ctx = host_ctx()
+    r = ctx.new_root(64)
+    a, b = ctx.fork(r, 2, 64)
+    nb = ctx.advantage_workspace_size([a, b])
+    assert nb >= 256 and nb % 256 == 0
+    assert _code(ctx.advantage_workspace_size, []) == T.EINVAL
+    assert _code(ctx.advantage_workspace_size, [a, 99]) == T.EINVAL
+    assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, FAKE_POOL, 2, 1 << 20) == T.EINVAL
+    assert "weighting" in ctx.lib.treepo_last_error(ctx.h).decode()
+    assert _code(ctx.tree_advantage, [a, b], None, FAKE_POOL, FAKE_POOL, 0, 1 << 20) == T.EINVAL
+    assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, None, FAKE_POOL, 0, 1 << 20) == T.EINVAL
+    assert _code(ctx.tree_advantage, [a, 99], FAKE_POOL, FAKE_POOL, FAKE_POOL, 0, 1 << 20) == T.EINVAL
+    assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, FAKE_POOL, 0, nb - 1) == T.EWORKSPACE
+    assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, FAKE_POOL + 8, 0, nb) == T.EWORKSPACE
+    assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, None, 0, nb) == T.EWORKSPACE
