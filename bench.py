@@ -58,6 +58,8 @@ def _parse():
                          "append per leaf then a decode, over --layers layers, steady state over the segment")
     ap.add_argument("--seg-len", type=int, default=512, help="segment capacity for --segment-loop")
     ap.add_argument("--layers", type=int, default=4, help="layers (each its own pools) for --segment-loop")
+    ap.add_argument("--advantage", action="store_true",
+                    help="TreePO advantage (Sec. 2.3, Eq. tree_ae) over the config's decoded leaves: one JSON line")
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for hardware counters: a few decode steps of the workload, then one "
                          "1 GiB device copy whose byte counters calibrate the kernels'")
@@ -238,6 +240,81 @@ def _profile_pass(dt, args):
     print(json.dumps({"profile_pass": True, "steps_per_mode": args.steps, "copy_bytes": nbytes}), flush=True)
 
 
+def _advantage(args):
+    """TreePO advantage over the config's decoded leaves, 0/1 rewards: the
+    kernel's duration (events attached to it), a whole call's time (host index
+    arrays + upload + kernel, calls back to back), and the fp64 oracle on the
+    host."""
+    import numpy as np
+    import torch
+    from paper_2508_17445_amd import KERNEL_ADVANTAGE, Context
+    from workloads import CONFIGS, build_call_log
+    cfg, log = CONFIGS[args.config], build_call_log(args.config)
+    dummy = torch.empty(256, dtype=torch.uint8, device="cuda")  # the advantage never reads the pools
+    ctx = Context(cfg.hq, cfg.hkv, cfg.d, 1 << 30, max(log.n_nodes, 1), dummy, dummy, cfg.block_tokens)
+    parents = []
+    for op in log.ops:
+        if op[0] == "root":
+            ctx.new_root(op[1])
+            parents.append(-1)
+        elif op[0] == "fork":
+            ctx.fork(op[1], op[2], op[3])
+            parents += [op[1]] * op[2]
+        else:
+            ctx.kv_commit(op[1], op[2])
+    leaves = log.leaves
+    n = len(leaves)
+    R = np.random.default_rng(args.config).integers(0, 2, size=n).astype(np.float32)
+    rw = torch.tensor(R, device="cuda")
+    out = torch.empty(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(ctx.advantage_workspace_size(leaves), 256), dtype=torch.uint8, device="cuda")
+    for _ in range(args.warmup):
+        ctx.tree_advantage(leaves, rw, out, ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ctx.tree_advantage(leaves, rw, out, ws)
+    torch.cuda.synchronize()
+    call_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ctx.set_profiling(True)
+    for _ in range(args.steps):
+        ctx.tree_advantage(leaves, rw, out, ws)
+    torch.cuda.synchronize()
+    tot, cnt = ctx.profile_read(KERNEL_ADVANTAGE)
+    kern_ms = tot / max(cnt, 1)
+    ctx.set_profiling(False)
+    pairs = sum(len(_chain(parents, x)) - 1 for x in leaves)
+    line = {"metric": "TreePO advantage: trajectories/s (one call per batch of decoded leaves)",
+            "value": round(n / (call_ms * 1e-3), 1), "unit": "trajectories/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "dtype": "f64",
+            "data": "synthetic (seeded 0/1 rewards on the config's call-log-built forest)",
+            "config": {"workload": f"config {args.config}: {cfg.name}", "trajectories": n,
+                       "queries": sum(1 for p in parents if p < 0), "subgroup_pairs": pairs},
+            "call_ms": round(call_ms, 5), "kernel_avg_ms": round(kern_ms, 5),
+            "roofline": {"bound": "latency", "note": "one workgroup over a few thousand sub-groups; the kernel "
+                         "moves ~KiB, far from any throughput roof"}}
+    if not args.no_cpu:
+        from oracle import advantage as ADV
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            ADV.tree_advantage(parents, leaves, R.astype(np.float64))
+            reps += 1
+            if time.perf_counter() - t0 >= min(args.cpu_seconds, 5.0):
+                break
+        dt = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": round(n * reps / dt, 1), "unit": "trajectories/s", "cores": 1,
+                                "kind": "oracle", "sample": f"{reps} full batch(es) of {n} trajectories in {dt:.1f} s"}
+    print(json.dumps(line), flush=True)
+
+
+def _chain(parents, x):
+    c = []
+    while x >= 0:
+        c.append(x)
+        x = parents[x]
+    return c
+
+
 def _segment_loop(args):
     """Segment-level decoding (the paper's Sec. 2.2 step loop): the config's
     tree gets a new --seg-len segment under every leaf; each step appends one
@@ -316,6 +393,9 @@ def main():
     from workloads import CONFIGS
     from workloads.device import DeviceTree
 
+    if args.advantage:
+        _advantage(args)
+        return
     if args.segment_loop:
         _segment_loop(args)
         return

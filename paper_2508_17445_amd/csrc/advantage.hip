@@ -18,12 +18,22 @@ namespace treepo {
 namespace {
 
 constexpr int kAdvThreads = 1024;
+// Rewards of up to this many positions are staged in LDS first, so that the
+// member loops' reads are LDS reads instead of dependent global loads.
+constexpr int kAdvLdsRewards = 8192;
 
 __global__ __launch_bounds__(kAdvThreads) void advantage_kernel(AdvantageArgs a) {
   __shared__ double red_s1[kAdvThreads];
   __shared__ double red_s2[kAdvThreads];
   __shared__ int32_t red_n[kAdvThreads];
+  __shared__ float rew[kAdvLdsRewards];
   const int tid = threadIdx.x;
+  const bool staged = a.n_pos <= kAdvLdsRewards;
+  if (staged) {
+    for (int p = tid; p < a.n_pos; p += kAdvThreads) rew[p] = a.rewards[p];
+    __syncthreads();
+  }
+  const float* R = staged ? rew : a.rewards;
 
   // 1. sub-group means and the all-equal test
   for (int g = tid; g < a.n_groups; g += kAdvThreads) {
@@ -31,7 +41,7 @@ __global__ __launch_bounds__(kAdvThreads) void advantage_kernel(AdvantageArgs a)
     double sum = 0.0;
     float lo = INFINITY, hi = -INFINITY;
     for (int k = b; k < e; ++k) {
-      const float r = a.rewards[a.grp_mem[k]];
+      const float r = R[a.grp_mem[k]];
       sum += static_cast<double>(r);
       lo = fminf(lo, r);
       hi = fmaxf(hi, r);
@@ -48,7 +58,7 @@ __global__ __launch_bounds__(kAdvThreads) void advantage_kernel(AdvantageArgs a)
     const int b = a.pos_off[p], e = a.pos_off[p + 1];
     double pooled = 0.0;
     if (a.gkeep[a.pos_root[p]] && e > b) {
-      const double r = static_cast<double>(a.rewards[p]);
+      const double r = static_cast<double>(R[p]);
       double num = 0.0, den = 0.0;
       for (int k = b; k < e; ++k) {
         const int g = a.pos_grp[k];

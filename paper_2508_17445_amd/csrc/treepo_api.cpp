@@ -69,6 +69,17 @@ struct PinnedSlot {
   bool pending = false;
 };
 
+// Index arrays of the advantage kernel for a leaf list, as one int32 image
+// (uploaded into the workspace), plus the scratch that follows it.
+struct AdvPlan {
+  std::vector<int32_t> ints;
+  int32_t n_groups = 0;
+  size_t off_grp_off = 0, off_grp_mem = 0, off_pos_off = 0, off_pos_grp = 0, off_pos_root = 0;  // in ints
+  size_t off_gmean = 0, off_gkeep = 0, off_pooled = 0, ws_bytes = 0;                           // in bytes
+  uint64_t shape_version = 0;  // the tree shape it was built for
+  std::vector<int32_t> leaves;
+};
+
 struct TimedLaunch {
   int kind;
   hipEvent_t start, stop;
@@ -89,6 +100,7 @@ struct treepo_ctx {
   std::vector<TimedLaunch> timed;
   std::vector<hipEvent_t> spare_events;
   std::vector<RetiredImage> retired;
+  AdvPlan adv;  // the last advantage call's index arrays (reused for the same shape and leaves)
   // Device lengths (cfg.node_len): stale after kv_commit, new_root or fork;
   // the next decode uploads the host table on its stream.
   bool live = false;
@@ -482,15 +494,6 @@ void append_pieces(const treepo::Tree& t, int32_t n, const int32_t* nodes, const
 
 namespace {
 
-// Index arrays of the advantage kernel for a leaf list, as one int32 image
-// (uploaded into the workspace), plus the scratch that follows it.
-struct AdvPlan {
-  std::vector<int32_t> ints;
-  int32_t n_groups = 0;
-  size_t off_grp_off = 0, off_grp_mem = 0, off_pos_off = 0, off_pos_grp = 0, off_pos_root = 0;  // in ints
-  size_t off_gmean = 0, off_gkeep = 0, off_pooled = 0, ws_bytes = 0;                           // in bytes
-};
-
 // Sub-group g = a node on some leaf's chain, numbered in order of first
 // appearance (positions ascending, chains root first); its members are the
 // positions whose chain contains it, ascending.
@@ -706,8 +709,13 @@ int32_t treepo_tree_advantage(treepo_ctx* ctx, int32_t n_leaves, const int32_t* 
   if (!rewards || !adv) return fail(ctx, TREEPO_EINVAL, "null rewards or adv");
   if (weighting != TREEPO_ADV_MEAN && weighting != TREEPO_ADV_SIZE_WEIGHTED)
     return fail(ctx, TREEPO_EINVAL, "bad weighting");
-  AdvPlan ap;
-  build_adv_plan(ctx->tree, n_leaves, leaves, &ap);
+  AdvPlan& ap = ctx->adv;
+  if (ap.ints.empty() || ap.shape_version != ctx->tree.shape_version() ||
+      ap.leaves.size() != static_cast<size_t>(n_leaves) || !std::equal(ap.leaves.begin(), ap.leaves.end(), leaves)) {
+    build_adv_plan(ctx->tree, n_leaves, leaves, &ap);
+    ap.shape_version = ctx->tree.shape_version();
+    ap.leaves.assign(leaves, leaves + n_leaves);
+  }
   if (!workspace || ws_bytes < ap.ws_bytes || reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
     return fail(ctx, TREEPO_EWORKSPACE,
                 "workspace missing, smaller than treepo_advantage_workspace_size or not 256-byte aligned");
