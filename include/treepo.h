@@ -184,6 +184,28 @@ int32_t treepo_paged_decode_naive(treepo_ctx* ctx, int32_t n_leaves, const int32
                                   const void* q, float scale, float* out, float* lse,
                                   void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ---- branching budget ---------------------------------------------------- */
+
+#define TREEPO_BUDGET_EVEN 0       /* budget transfer: spread evenly (Sec. 2.2)                */
+#define TREEPO_BUDGET_HIGH_PROB 1  /* softmax(score / T): higher probability favoured (Sec. 4.4) */
+#define TREEPO_BUDGET_LOW_PROB 2   /* softmax(-score / T): lower probability favoured (Sec. 4.4) */
+
+/* Branches per active path before the next segment step (Sec. 2.2 "Branching
+ * Budget Transfer"; Sec. 4.4 probability-based assignment, temperature 2.0
+ * there).  Host only, no context.
+ *   scores      host [n_paths]: the log probability of each path's last
+ *               segment (ignored, may be null, for TREEPO_BUDGET_EVEN)
+ *   total       the depth's branching budget (e.g. N^d)
+ *   budget_out  host [n_paths] (written): every path gets 1; the other
+ *               max(total - n_paths, 0) are split in proportion to 1/n or
+ *               the softmax weights (double, maximum subtracted) by largest
+ *               remainders, ties to the lower index.  Sums to
+ *               max(total, n_paths).
+ * EINVAL (n_paths < 1, null budget_out, total < 0, bad mode, non-finite
+ * score, temperature not positive and finite). */
+int32_t treepo_branch_budget(int32_t n_paths, const float* scores, int32_t total, int32_t mode,
+                             float temperature, int32_t* budget_out);
+
 /* ---- TreePO advantage ---------------------------------------------------- */
 
 /* Aggregations for treepo_tree_advantage. */

@@ -1,6 +1,8 @@
 // Node table, block allocator and decode planner (host, C++17).
 #include "tree_core.h"
 
+#include <cmath>
+
 #include <algorithm>
 #include <unordered_map>
 
@@ -145,6 +147,58 @@ int32_t Tree::check_leaves(int32_t n, const int32_t* leaves, std::string* err) c
       return kEEmpty;
     }
   }
+  return kOk;
+}
+
+int32_t branch_budget(int32_t n, const float* scores, int32_t total, int32_t mode, double temperature,
+                      int32_t* out, std::string* err) {
+  if (n < 1 || !out || total < 0) {
+    if (err) *err = "need at least one path, an output array and a non-negative total";
+    return kEInval;
+  }
+  if (mode != kBudgetEven && mode != kBudgetHighProb && mode != kBudgetLowProb) {
+    if (err) *err = "bad budget mode";
+    return kEInval;
+  }
+  std::vector<double> w(n);
+  if (mode == kBudgetEven) {
+    for (double& x : w) x = 1.0 / n;
+  } else {
+    if (!scores || !(temperature > 0.0) || !std::isfinite(temperature)) {
+      if (err) *err = "probability modes need scores and a positive finite temperature";
+      return kEInval;
+    }
+    const double sign = mode == kBudgetHighProb ? 1.0 : -1.0;
+    double m = -INFINITY;
+    for (int32_t k = 0; k < n; ++k) {
+      if (!std::isfinite(scores[k])) {
+        if (err) *err = "scores must be finite";
+        return kEInval;
+      }
+      w[k] = sign * static_cast<double>(scores[k]) / temperature;
+      m = std::max(m, w[k]);
+    }
+    double tot = 0.0;
+    for (double& x : w) {
+      x = std::exp(x - m);
+      tot += x;
+    }
+    for (double& x : w) x /= tot;
+  }
+  const int32_t rest = std::max(total - n, 0);
+  std::vector<double> frac(n);
+  int64_t left = rest;
+  for (int32_t k = 0; k < n; ++k) {
+    const double q = rest * w[k];
+    const double f = std::floor(q);
+    out[k] = 1 + static_cast<int32_t>(f);
+    frac[k] = q - f;
+    left -= static_cast<int64_t>(f);
+  }
+  std::vector<int32_t> order(n);
+  for (int32_t k = 0; k < n; ++k) order[k] = k;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return frac[a] > frac[b]; });
+  for (int64_t i = 0; i < left && i < n; ++i) ++out[order[i]];
   return kOk;
 }
 

@@ -234,6 +234,16 @@ struct Plan {
   int64_t kv_token_visits = 0;    // tokens streamed, summed over leaf groups (per KV head)
 };
 
+// Branching budget over n active paths (TreePO Sec. 2.2 budget transfer;
+// Sec. 4.4 probability-based assignment): every path gets one branch, the
+// other max(total - n, 0) are split in proportion to the weights by largest
+// remainders (ties to the lower index).  Weights: 1/n (kBudgetEven),
+// softmax(scores / T) (kBudgetHighProb) or softmax(-scores / T)
+// (kBudgetLowProb), in double with the maximum subtracted.
+enum BudgetMode : int32_t { kBudgetEven = 0, kBudgetHighProb = 1, kBudgetLowProb = 2 };
+int32_t branch_budget(int32_t n, const float* scores, int32_t total, int32_t mode, double temperature,
+                      int32_t* out, std::string* err);
+
 // Builds the decode schedule for `leaves` (validated by the caller).
 int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanMode mode,
                    const PlanParams& p, Plan* out, std::string* err);

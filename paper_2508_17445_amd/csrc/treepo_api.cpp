@@ -688,6 +688,13 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
   return TREEPO_OK;
 }
 
+int32_t treepo_branch_budget(int32_t n_paths, const float* scores, int32_t total, int32_t mode,
+                             float temperature, int32_t* budget_out) {
+  return treepo::branch_budget(n_paths, scores, total, mode, temperature, budget_out, nullptr) == treepo::kOk
+             ? TREEPO_OK
+             : TREEPO_EINVAL;
+}
+
 int32_t treepo_advantage_workspace_size(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
                                         size_t* bytes) {
   if (!ctx) return TREEPO_EINVAL;

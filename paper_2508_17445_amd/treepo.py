@@ -79,6 +79,7 @@ def load_library(path: str = LIB_PATH):
         "treepo_profile_read": (_i32, [_p, _i32, ctypes.POINTER(ctypes.c_double), _pi64]),
         "treepo_strerror": (ctypes.c_char_p, [_i32]),
         "treepo_last_error": (ctypes.c_char_p, [_p]),
+        "treepo_branch_budget": (_i32, [_i32, ctypes.POINTER(ctypes.c_float), _i32, _i32, ctypes.c_float, _pi32]),
         "treepo_advantage_workspace_size": (_i32, [_p, _i32, _pi32, ctypes.POINTER(ctypes.c_size_t)]),
         "treepo_tree_advantage": (_i32, [_p, _i32, _pi32, _p, _i32, _p, _p, ctypes.c_size_t, _p]),
         "treepo_bench_copy": (_i32, [_p, _p, ctypes.c_size_t, _p]),
@@ -297,6 +298,21 @@ class Context:
         self._check(self.lib.treepo_profile_read(self.h, kind, ctypes.byref(ms), ctypes.byref(n)),
                     "treepo_profile_read")
         return ms.value, n.value
+
+
+BUDGET_EVEN, BUDGET_HIGH_PROB, BUDGET_LOW_PROB = 0, 1, 2
+
+
+def branch_budget(scores, total: int, mode: int = BUDGET_EVEN, temperature: float = 2.0) -> list[int]:
+    """Branches per active path (treepo_branch_budget); scores: last-segment log probabilities."""
+    lib = load_library()
+    sc = np.ascontiguousarray(np.asarray(scores, dtype=np.float32))
+    out = np.zeros(max(len(sc), 1), dtype=np.int32)
+    st = lib.treepo_branch_budget(len(sc), sc.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), int(total), int(mode),
+                                  float(temperature), _ptr32(out))
+    if st != OK:
+        raise TreePOError(st, "treepo_branch_budget: " + lib.treepo_strerror(st).decode())
+    return [int(x) for x in out[:len(sc)]]
 
 
 def bench_copy(dst, src, nbytes: int, stream=None):

@@ -213,3 +213,48 @@ def test_advantage_mutation_factory_faithful():
     R = np.random.default_rng(5).normal(size=len(leaves))
     for w in ("mean", "size"):
         assert np.abs(adv(parents, leaves, R, w) - ADV.tree_advantage(parents, leaves, R, w)).max() <= 1e-12
+
+
+# ---- the branching-budget oracle ----------------------------------------------
+
+import math  # noqa: E402
+
+from oracle import budget as BUD  # noqa: E402
+from tests import test_oracle_budget as BP  # noqa: E402
+
+
+def _budget_factory(kind):
+    orig_weights = BUD.weights
+
+    def branch_budget(scores, total, mode="even", temperature=2.0):
+        n = len(scores)
+        t = 1.0 if kind == "no_temperature" and mode != "even" else temperature
+        w = orig_weights(scores, mode, t)
+        rest = total if kind == "no_min_one" else max(total - n, 0)
+        quota = [rest * x for x in w]
+        base = [int(math.floor(q)) for q in quota]
+        left = rest - sum(base)
+        if kind == "ties_high_index":
+            order = sorted(range(n), key=lambda k: (-(quota[k] - base[k]), -k))
+        else:
+            order = sorted(range(n), key=lambda k: (-(quota[k] - base[k]), k))
+        if kind != "drop_remainder":
+            for k in order[:left]:
+                base[k] += 1
+        return base if kind == "no_min_one" else [1 + b for b in base]
+    return branch_budget
+
+
+@pytest.mark.parametrize("kind", ["no_temperature", "no_min_one", "ties_high_index", "drop_remainder"])
+def test_budget_mutation_caught(kind, monkeypatch):
+    monkeypatch.setattr(BUD, "branch_budget", _budget_factory(kind))
+    pins = [BP.test_even_transfer_closed_form, lambda: BP.test_sum_min_one_and_order("high"),
+            lambda: BP.test_sum_min_one_and_order("low"), BP.test_two_paths_closed_form,
+            BP.test_largest_remainder_ties_to_lower_index]
+    failed = 0
+    for pin in pins:
+        try:
+            pin()
+        except AssertionError:
+            failed += 1
+    assert failed, f"budget mutation {kind} passed every pin"
