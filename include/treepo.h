@@ -120,6 +120,22 @@ int32_t treepo_new_root(treepo_ctx* ctx, int32_t cap_tokens, int32_t* node_out);
 int32_t treepo_fork(treepo_ctx* ctx, int32_t parent, int32_t n_children,
                     int32_t child_cap, int32_t* children_out);
 
+/* Fallback inside a segment (Alg. 1 Fallback; Sec. 2.2 fallback at segment
+ * level; Sec. 4.1 "misaligned fallback", a fallback granularity finer than
+ * the segment): forks n_children (>= 0) children after the first `offset`
+ * tokens of `node`.  The node keeps tokens [0, offset); a new tail node (the
+ * next id, written to *tail_out) takes tokens [offset, len), the rest of the
+ * node's capacity and blocks (no KV is copied), and the node's children,
+ * whose subtrees move one level down; every existing trajectory keeps
+ * exactly its tokens (an active path now continues in the tail).  The
+ * children (consecutive ids after the tail, children_out) start after the
+ * kept prefix and reserve ceil(child_cap/B) blocks each.  offset == len is a
+ * plain treepo_fork (*tail_out = -1).  EINVAL (bad node, offset outside
+ * [0, len], offset < len not a multiple of B, n_children < 0, or < 1 for a
+ * plain fork, child_cap < 1 with children), ENOMEM (nodes or blocks). */
+int32_t treepo_fork_at(treepo_ctx* ctx, int32_t node, int32_t offset, int32_t n_children, int32_t child_cap,
+                       int32_t* children_out, int32_t* tail_out);
+
 /* Appends generated tokens (Alg. 1: the segment s_k joins its path).  nodes and
  * ntok are host arrays of n entries; node i gets ntok[i] >= 0 tokens whose
  * K and V rows are rows [sum(ntok[0..i)), +ntok[i]) of k and v (device bf16,

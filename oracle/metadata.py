@@ -97,6 +97,55 @@ class TreeModel:
         self.n_children[parent] += n
         return ids
 
+    def fork_at(self, node: int, offset: int, n: int, cap: int):
+        """Fork n children from node `node` after its first `offset` tokens: a
+        fallback that branches inside a segment (Sec. 2.2 fallback at segment
+        level; Sec. 4.1 "misaligned fallback" with a fallback granularity finer
+        than the segment).  The node keeps tokens [0, offset); a new tail node
+        (the next id) takes tokens [offset, len), the rest of the node's
+        capacity and blocks, and the node's children, so every existing
+        trajectory keeps its tokens; the tail's subtree moves one level down.
+        Then the n children (consecutive ids, n may be 0) start after the
+        kept prefix.  offset == len is a plain fork (tail -1); otherwise the
+        offset must be a multiple of the block size (the tail starts on a
+        block of its own, no KV is copied).  Returns (children, tail)."""
+        if not (0 <= node < len(self.nodes)):
+            raise TreeError(EINVAL, "unknown node")
+        x = self.nodes[node]
+        if not (0 <= offset <= x["len"]) or n < 0:
+            raise TreeError(EINVAL, "bad offset or child count")
+        if offset == x["len"]:
+            return self.fork(node, n, cap), -1
+        if offset % self.B:
+            raise TreeError(EINVAL, "split offset not a multiple of the block size")
+        if n > 0 and cap <= 0:
+            raise TreeError(EINVAL, "cap must be positive")
+        if len(self.nodes) + 1 + n > self.max_nodes:
+            raise TreeError(ENOMEM, "node table full")
+        if n > 0 and self.next_block + n * _ceil_div(cap, self.B) > self.num_blocks:
+            raise TreeError(ENOMEM, "pool blocks exhausted")
+        keep = offset // self.B
+        tail = dict(parent=node, depth=x["depth"] + 1, start=x["start"] + offset, len=x["len"] - offset,
+                    cap=x["cap"] - offset, block_begin=x["block_begin"] + keep, n_blocks=x["n_blocks"] - keep,
+                    tree_id=x["tree_id"])
+        self.nodes.append(tail)
+        t = len(self.nodes) - 1
+        self.n_children.append(self.n_children[node])
+        moved = [c for c in range(len(self.nodes) - 1) if self.nodes[c]["parent"] == node]
+        for c in moved:
+            self.nodes[c]["parent"] = t
+        stack = list(moved)
+        while stack:
+            c = stack.pop()
+            self.nodes[c]["depth"] += 1
+            stack += [d for d in range(len(self.nodes)) if self.nodes[d]["parent"] == c]
+        x["len"] = offset
+        x["cap"] = offset
+        x["n_blocks"] = keep
+        self.n_children[node] = 1
+        kids = self.fork(node, n, cap) if n > 0 else []
+        return kids, t
+
     def append(self, nodes, ntok) -> None:
         """Batched append: validated as a whole first, then applied in order."""
         if len(nodes) != len(ntok):
@@ -159,6 +208,8 @@ def replay(log, block_tokens: int, num_blocks: int, max_nodes: int,
             m.new_root(op[1])
         elif op[0] == "fork":
             m.fork(op[1], op[2], op[3])
+        elif op[0] == "fork_at":
+            m.fork_at(op[1], op[2], op[3], op[4])
         elif op[0] == "append":
             m.append(op[1], op[2])
         else:

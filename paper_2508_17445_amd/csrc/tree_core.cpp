@@ -79,6 +79,84 @@ int32_t Tree::fork(int32_t parent, int32_t n, int32_t cap, int32_t* out, std::st
   return kOk;
 }
 
+int32_t Tree::fork_at(int32_t node, int32_t offset, int32_t n, int32_t cap, int32_t* out, int32_t* tail,
+                      std::string* err) {
+  if (!tail || (n > 0 && !out)) {
+    if (err) *err = "null output pointer";
+    return kEInval;
+  }
+  if (node < 0 || node >= static_cast<int32_t>(nodes_.size())) {
+    if (err) *err = "fork of an unknown node";
+    return kEInval;
+  }
+  const Node x = nodes_[node];
+  if (offset < 0 || offset > x.len || n < 0) {
+    if (err) *err = "split offset outside the node's tokens or negative child count";
+    return kEInval;
+  }
+  if (offset == x.len) {
+    int32_t st = fork(node, n, cap, out, err);
+    if (st == kOk) *tail = -1;
+    return st;
+  }
+  if (offset % B_ != 0) {
+    if (err) *err = "split offset is not a multiple of the block size";
+    return kEInval;
+  }
+  if (n > 0 && cap < 1) {
+    if (err) *err = "capacity must be >= 1 token";
+    return kEInval;
+  }
+  if (static_cast<int64_t>(nodes_.size()) + 1 + n > max_nodes_) {
+    if (err) *err = "node table full";
+    return kENoMem;
+  }
+  if (n > 0 && next_block_ + static_cast<int64_t>(n) * ceil_div64(cap, B_) > num_blocks_) {
+    if (err) *err = "pool blocks exhausted";
+    return kENoMem;
+  }
+  const int32_t keep = offset / B_;
+  Node t;
+  t.parent = node;
+  t.depth = x.depth + 1;
+  t.start = x.start + offset;
+  t.len = x.len - offset;
+  t.cap = x.cap - offset;
+  t.block_begin = x.block_begin + keep;
+  t.n_blocks = x.n_blocks - keep;
+  t.tree_id = x.tree_id;
+  t.n_children = x.n_children;
+  nodes_.push_back(t);
+  const int32_t tid = static_cast<int32_t>(nodes_.size() - 1);
+  // the node's children move under the tail; their subtrees one level down
+  std::vector<int32_t> stack;
+  for (int32_t c = 0; c < tid; ++c)
+    if (nodes_[c].parent == node) {
+      nodes_[c].parent = tid;
+      stack.push_back(c);
+    }
+  if (!stack.empty()) {
+    std::vector<std::vector<int32_t>> kids(nodes_.size());
+    for (int32_t c = 0; c < tid; ++c)
+      if (nodes_[c].parent >= 0) kids[nodes_[c].parent].push_back(c);
+    while (!stack.empty()) {
+      const int32_t c = stack.back();
+      stack.pop_back();
+      ++nodes_[c].depth;
+      for (int32_t d : kids[c]) stack.push_back(d);
+    }
+  }
+  nodes_[node].len = offset;
+  nodes_[node].cap = offset;
+  nodes_[node].n_blocks = keep;
+  nodes_[node].n_children = 1;
+  ++version_;
+  ++shape_version_;
+  *tail = tid;
+  if (n > 0) return fork(node, n, cap, out, err);  // checked above: cannot fail
+  return kOk;
+}
+
 int32_t Tree::check_append(int32_t n, const int32_t* nodes, const int32_t* ntok,
                            std::vector<int64_t>* dest_rows, std::string* err) const {
   if (n < 0 || (n > 0 && (!nodes || !ntok))) {

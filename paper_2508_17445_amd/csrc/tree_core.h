@@ -45,6 +45,13 @@ class Tree {
 
   int32_t new_root(int32_t cap, int32_t* node_out, std::string* err);
   int32_t fork(int32_t parent, int32_t n, int32_t cap, int32_t* out, std::string* err);
+  // Fork n (>= 0) children after the first `offset` tokens of `node`: the
+  // node keeps [0, offset), a new tail node (next id) takes [offset, len),
+  // the rest of the capacity and blocks and the node's children (their
+  // subtree one level deeper); offset == len is a plain fork (tail -1), any
+  // other offset must be a multiple of the block size.
+  int32_t fork_at(int32_t node, int32_t offset, int32_t n, int32_t cap, int32_t* out, int32_t* tail,
+                  std::string* err);
   // Validates a batched append; on success fills `dest_rows` (if non-null)
   // with the pool token row of every appended token, in call order.
   int32_t check_append(int32_t n, const int32_t* nodes, const int32_t* ntok,

@@ -631,6 +631,15 @@ int32_t treepo_fork(treepo_ctx* ctx, int32_t parent, int32_t n_children, int32_t
   return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
 }
 
+int32_t treepo_fork_at(treepo_ctx* ctx, int32_t node, int32_t offset, int32_t n_children, int32_t child_cap,
+                       int32_t* children_out, int32_t* tail_out) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  const int32_t st = ctx->tree.fork_at(node, offset, n_children, child_cap, children_out, tail_out, &err);
+  if (st == treepo::kOk) ctx->dev_len_stale = true;
+  return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
+}
+
 int32_t treepo_kv_slots(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
                         int64_t* rows_out) {
   if (!ctx) return TREEPO_EINVAL;

@@ -63,6 +63,7 @@ def load_library(path: str = LIB_PATH):
         "treepo_destroy": (_i32, [_p]),
         "treepo_new_root": (_i32, [_p, _i32, _pi32]),
         "treepo_fork": (_i32, [_p, _i32, _i32, _i32, _pi32]),
+        "treepo_fork_at": (_i32, [_p, _i32, _i32, _i32, _i32, _pi32, _pi32]),
         "treepo_kv_append": (_i32, [_p, _i32, _pi32, _pi32, _p, _p, _p]),
         "treepo_kv_slots": (_i32, [_p, _i32, _pi32, _pi32, _pi64]),
         "treepo_kv_commit": (_i32, [_p, _i32, _pi32, _pi32]),
@@ -167,6 +168,14 @@ class Context:
         out = np.zeros(max(n_children, 1), dtype=np.int32)
         self._check(self.lib.treepo_fork(self.h, parent, n_children, child_cap, _ptr32(out)), "treepo_fork")
         return [int(x) for x in out[:n_children]]
+
+    def fork_at(self, node: int, offset: int, n_children: int, child_cap: int):
+        """Fork after the first `offset` tokens of `node`: (children, tail id or -1)."""
+        out = np.zeros(max(n_children, 1), dtype=np.int32)
+        tail = _i32()
+        self._check(self.lib.treepo_fork_at(self.h, node, offset, n_children, child_cap, _ptr32(out),
+                                            ctypes.byref(tail)), "treepo_fork_at")
+        return [int(x) for x in out[:n_children]], tail.value
 
     def kv_append(self, nodes, ntok, k, v, stream=None):
         nd, nt = _arr32(nodes), _arr32(ntok)

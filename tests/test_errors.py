@@ -79,8 +79,14 @@ def test_codes_match_oracle_on_random_ops(seed):
     model = M.TreeModel(64, 40, 25)
     for _ in range(60):
         n = len(model.nodes)
-        kind = rng.integers(4)
-        if kind == 0 or n == 0:
+        kind = rng.integers(5)
+        if kind == 4 and n > 0:
+            x = int(rng.integers(-1, n + 1))
+            ln = model.nodes[x]["len"] if 0 <= x < n else 0
+            offset = int(rng.choice([-1, 0, 64, 128, ln, int(rng.integers(0, max(ln, 1) + 1))]))
+            args = (x, offset, int(rng.integers(-1, 3)), int(rng.integers(0, 200)))
+            f_lib, f_ref = ctx.fork_at, model.fork_at
+        elif kind == 0 or n == 0:
             cap = int(rng.integers(-1, 300))
             args = (cap,)
             f_lib, f_ref = ctx.new_root, model.new_root
@@ -105,7 +111,7 @@ def test_codes_match_oracle_on_random_ops(seed):
             c_lib, r_lib = e.code, None
         assert c_lib == c_ref, (args, c_lib, c_ref)
         if c_ref == 0 and r_ref is not None:
-            assert r_lib == r_ref
+            assert (list(r_lib) if isinstance(r_lib, tuple) else r_lib) == (list(r_ref) if isinstance(r_ref, tuple) else r_ref)
         ref = np.array([model.record(i) for i in range(len(model.nodes))], dtype=np.int32).reshape(-1, 8)
         assert np.array_equal(ctx.export_nodes().reshape(-1, 8), ref)
 
