@@ -260,6 +260,11 @@ def _advantage(args):
         elif op[0] == "fork":
             ctx.fork(op[1], op[2], op[3])
             parents += [op[1]] * op[2]
+        elif op[0] == "fork_at":
+            x = op[1]
+            ctx.fork_at(x, op[2], op[3], op[4])
+            t = len(parents)
+            parents = [t if q == x else q for q in parents] + [x] + [x] * op[3]
         else:
             ctx.kv_commit(op[1], op[2])
     leaves = log.leaves

@@ -222,4 +222,5 @@ def replay(log, block_tokens: int, num_blocks: int, max_nodes: int,
 def pool_blocks_needed(log, block_tokens: int) -> int:
     caps = [op[1] for op in log.ops if op[0] == "root"]
     caps += [op[3] for op in log.ops if op[0] == "fork" for _ in range(op[2])]
+    caps += [op[4] for op in log.ops if op[0] == "fork_at" for _ in range(op[3])]
     return sum(_ceil_div(c, block_tokens) for c in caps)

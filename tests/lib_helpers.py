@@ -32,6 +32,9 @@ def replay_host(ctx, log, step_append=True):
             ids.append(ctx.new_root(op[1]))
         elif op[0] == "fork":
             ids += ctx.fork(op[1], op[2], op[3])
+        elif op[0] == "fork_at":
+            kids, t = ctx.fork_at(op[1], op[2], op[3], op[4])
+            ids += [t] + kids
         else:
             ctx.kv_commit(op[1], op[2])
     if step_append and log.step_append is not None:

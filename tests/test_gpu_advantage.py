@@ -43,7 +43,7 @@ def _check(ctx, parents, leaves, R, tag):
         assert np.isfinite(got).all() and err <= TOL
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4, 5, 6])
 def test_configs(cfg_id):
     c = CONFIGS[cfg_id]
     log = build_call_log(cfg_id)

@@ -117,7 +117,7 @@ def test_ragged_and_degenerate_shapes():
             _check(dt, mode, tag=f"ragged-d{d}")
 
 
-@pytest.mark.parametrize("cfg_id", [3, 4, 5])
+@pytest.mark.parametrize("cfg_id", [3, 4, 5, 6])
 def test_large_configs_sampled(cfg_id):
     import torch
     dt = _dt(cfg_id)

@@ -28,7 +28,7 @@ def _compare(ctx, model, leaves):
     assert np.array_equal(np.diff(off), [len(v) for v in ds.values()])
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_workload_metadata_bit_exact(cfg):
     log = build_call_log(cfg)
     ctx = host_ctx()
@@ -209,7 +209,7 @@ def _stream_costs(pieces, n_streams, q_cost=0.5, cut_q=False):
     return cost
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 4])
+@pytest.mark.parametrize("cfg", [1, 2, 4, 6])
 def test_plan_covers_each_chain_token_once(cfg):
     log = build_call_log(cfg)
     from workloads import CONFIGS
@@ -334,3 +334,23 @@ def test_static_plans_follow_appends():
     if grow:
         ctx.kv_commit(grow[:1], [1])
         assert not np.array_equal(ctx.export_blocks(leaves, 0), b0)
+
+
+def test_misaligned_fallback_workload_shape():
+    """The fork-variant workload cuts 1024-token segments at their 512-token
+    midpoint (the misaligned fallback) and re-forks interior nodes; every
+    node starts on a 512-token boundary after the 512-token prompt."""
+    log = build_call_log(6)
+    cuts = [op for op in log.ops if op[0] == "fork_at"]
+    assert len(cuts) >= 10 and all(op[2] == 512 for op in cuts)
+    model = oracle_model(log)
+    starts = {nd["start"] for nd in model.nodes if nd["parent"] >= 0}
+    assert all((s - 512) % 512 == 0 for s in starts) and any((s - 512) % 1024 for s in starts)
+    kids = {}
+    for i, nd in enumerate(model.nodes):
+        kids.setdefault(nd["parent"], []).append(i)
+    assert any(len(v) > 2 for k, v in kids.items() if k >= 0)      # re-forks of a node that had children
+    per_tree = {}
+    for x in log.leaves:
+        per_tree[model.nodes[x]["tree_id"]] = per_tree.get(model.nodes[x]["tree_id"], 0) + 1
+    assert max(per_tree.values()) == 16

@@ -1,4 +1,4 @@
-"""The five synthetic segment-tree workloads and their call logs.
+"""The six synthetic segment-tree workloads and their call logs.
 
 A call log is the sequence of library calls that builds a rollout forest the
 way TreePO's tree sampler grows it (Alg. 1; Sec. 2.2 "Segment-level Tree
@@ -30,18 +30,25 @@ BLOCK_TOKENS = 64
 class CallLog:
     """Tree construction ops plus the decode step.
 
-    ``ops`` items are ``("root", cap)``, ``("fork", parent, n_children, cap)``
-    or ``("append", nodes, ntok)`` (one batched append call).  The decode step
+    ``ops`` items are ``("root", cap)``, ``("fork", parent, n_children, cap)``,
+    ``("fork_at", node, offset, n_children, cap)`` (a fork after the first
+    ``offset`` tokens of ``node``: a tail node takes the rest, then the
+    children) or ``("append", nodes, ntok)`` (one batched append call).  The decode step
     is an optional fused append ``step_append`` (nodes, ntok) followed by a
     decode of ``leaves``.  ``rows[n]`` is node ``n``'s token count at decode
     time (after the fused append), which fixes how many K/V rows the data
-    generator draws for it.
+    generator draws for it.  A tail made by ``fork_at`` holds rows of the
+    node it was cut from: ``data_src[t] = (source node, first row)``, and a
+    source node's stream is drawn with ``data_rows[n]`` rows when that
+    exceeds ``rows[n]`` (the rows it held before a cut).
     """
     ops: list = field(default_factory=list)
     step_append: tuple | None = None
     leaves: list = field(default_factory=list)
     rows: dict = field(default_factory=dict)
     n_nodes: int = 0
+    data_src: dict = field(default_factory=dict)
+    data_rows: dict = field(default_factory=dict)
 
 
 class _Builder:
@@ -54,27 +61,48 @@ class _Builder:
         self.len: list[int] = []
         self.cap: list[int] = []
         self.children: list[int] = []
+        self.peak: list[int] = []
+        self.src: dict[int, tuple[int, int]] = {}
+
+    def _node(self, parent: int, start: int, cap: int) -> int:
+        self.parent.append(parent); self.start.append(start); self.len.append(0)
+        self.cap.append(cap); self.children.append(0); self.peak.append(0)
+        return len(self.parent) - 1
 
     def root(self, cap: int) -> int:
-        nid = len(self.parent)
-        self.parent.append(-1); self.start.append(0); self.len.append(0)
-        self.cap.append(cap); self.children.append(0)
         self.log.ops.append(("root", cap))
-        return nid
+        return self._node(-1, 0, cap)
 
     def fork(self, p: int, n: int, cap: int) -> list[int]:
-        first = len(self.parent)
-        for _ in range(n):
-            self.parent.append(p); self.start.append(self.start[p] + self.len[p])
-            self.len.append(0); self.cap.append(cap); self.children.append(0)
-        self.children[p] += n
         self.log.ops.append(("fork", p, n, cap))
-        return list(range(first, first + n))
+        return self._kids(p, n, cap)
+
+    def _kids(self, p: int, n: int, cap: int) -> list[int]:
+        self.children[p] += n
+        return [self._node(p, self.start[p] + self.len[p], cap) for _ in range(n)]
+
+    def fork_at(self, x: int, offset: int, n: int, cap: int):
+        """Cut node x after `offset` tokens (a block multiple below its length):
+        the tail takes the rest, x's children and blocks; then n children."""
+        assert 0 <= offset < self.len[x] and offset % BLOCK_TOKENS == 0
+        t = self._node(x, self.start[x] + offset, self.cap[x] - offset)
+        self.len[t] = self.peak[t] = self.len[x] - offset
+        self.children[t] = self.children[x]
+        for c in range(t):
+            if self.parent[c] == x:
+                self.parent[c] = t
+        o, first = self.src.get(x, (x, 0))
+        self.src[t] = (o, first + offset)
+        self.len[x] = self.cap[x] = offset
+        self.children[x] = 1
+        self.log.ops.append(("fork_at", x, offset, n, cap))
+        return self._kids(x, n, cap), t
 
     def append(self, nodes: list[int], ntok: list[int]):
         for n, t in zip(nodes, ntok):
             assert self.len[n] + t <= self.cap[n] and self.children[n] == 0
             self.len[n] += t
+            self.peak[n] = max(self.peak[n], self.len[n])
         if nodes:
             self.log.ops.append(("append", list(nodes), list(ntok)))
 
@@ -82,10 +110,17 @@ class _Builder:
         if step_append is not None:
             for n, t in zip(*step_append):
                 self.len[n] += t
+                self.peak[n] = max(self.peak[n], self.len[n])
             self.log.step_append = (list(step_append[0]), list(step_append[1]))
         self.log.leaves = list(leaves)
         self.log.rows = {i: self.len[i] for i in range(len(self.len))}
         self.log.n_nodes = len(self.len)
+        need = {}
+        for n in range(len(self.len)):
+            o, first = self.src.get(n, (n, 0))
+            need[o] = max(need.get(o, 0), first + self.peak[n])
+        self.log.data_src = dict(self.src)
+        self.log.data_rows = {o: r for o, r in need.items() if r > self.log.rows[o]}
         return self.log
 
 
@@ -213,6 +248,76 @@ def gen_long_context(seed: int) -> CallLog:
     return b.finish(front, step_append=(front, [1] * len(front)))
 
 
+def gen_misaligned_fallback(seed: int) -> CallLog:
+    """32 prompts of 512 tokens, 7 segments of l=1024 (responses up to 7168
+    tokens), width w=16, with a 512-token fallback (the misaligned setting of
+    Sec. 4.1).  Level-synchronous steps: every active path forks into 2
+    children while its prompt holds fewer than w live trajectories (1 after).
+    Each child is pruned with p=0.2 after U[1, avail] tokens (an early stop:
+    it stays in the forest but is no trajectory), ends with an answer with
+    p=0.1 after U[1, avail] tokens, or takes the whole segment (finished at
+    the length limit).  When a prompt has no active path and fewer than w
+    trajectories, it falls back (Sec. 2.2): a random finished trajectory is
+    re-forked into min(2, w - count) branches at a random 512-token boundary
+    of its response; a boundary inside a 1024-token segment cuts that node
+    (``fork_at``).  Every trajectory of the final forest is decoded."""
+    rng = structure_rng(seed)
+    seg, fb, plen, n_prompts, w = 1024, 512, 512, 32, 16
+    p_prune, p_answer = 0.2, 0.1
+    end = plen + 7 * seg
+    b = _Builder()
+    roots = [b.root(plen) for _ in range(n_prompts)]
+    b.append(roots, [plen] * n_prompts)
+    active = [[r] for r in roots]
+    finished: list[list[int]] = [[] for _ in roots]
+    count = [1] * n_prompts                       # active + finished trajectories
+    while True:
+        new_nodes, new_tok = [], []
+        for p in range(n_prompts):
+            if active[p]:
+                grow = []
+                for n in active[p]:
+                    br = min(2 if count[p] < w else 1, w - count[p] + 1)
+                    grow += b.fork(n, br, seg)
+                    count[p] += br - 1
+            elif count[p] < w and finished[p]:
+                leaf = finished[p][int(rng.integers(len(finished[p])))]
+                total = b.start[leaf] + b.len[leaf]
+                pos = plen + fb * int(rng.integers(0, (total - 1 - plen) // fb + 1))
+                x = leaf
+                while b.start[x] > pos:
+                    x = b.parent[x]
+                br = min(2, w - count[p])
+                if pos == b.start[x]:
+                    grow = b.fork(b.parent[x], br, seg)
+                else:
+                    grow, t = b.fork_at(x, pos - b.start[x], br, seg)
+                    if x == leaf:
+                        finished[p][finished[p].index(leaf)] = t
+                count[p] += br
+            else:
+                continue
+            active[p] = []
+            for c in grow:
+                avail = min(seg, end - b.start[c])
+                u = rng.random()
+                if u < p_prune + p_answer:
+                    ln = int(rng.integers(1, avail + 1))
+                    if u < p_prune:
+                        count[p] -= 1
+                    else:
+                        finished[p].append(c)
+                else:
+                    ln = avail
+                    (active[p] if b.start[c] + ln < end else finished[p]).append(c)
+                new_nodes.append(c)
+                new_tok.append(ln)
+        if not new_nodes:
+            break
+        b.append(new_nodes, new_tok)
+    return b.finish([x for f in finished for x in f])
+
+
 @dataclass(frozen=True)
 class Config:
     name: str
@@ -238,6 +343,7 @@ CONFIGS = {
     3: Config("batch-64x16-rollout", 3, 28, 4, 128, gen_batch_rollout),
     4: Config("irregular-32-prompt", 4, 28, 4, 128, gen_irregular),
     5: Config("long-context-8x32-16k", 5, 40, 8, 128, gen_long_context),
+    6: Config("misaligned-fallback-32x16-7x1024", 6, 28, 4, 128, gen_misaligned_fallback),
 }
 
 

@@ -20,33 +20,44 @@ _MAX_STAGE_ROWS = 1 << 16
 def pool_blocks(log: CallLog, block_tokens: int = BLOCK_TOKENS) -> int:
     caps = [op[1] for op in log.ops if op[0] == "root"]
     caps += [op[3] for op in log.ops if op[0] == "fork" for _ in range(op[2])]
+    caps += [op[4] for op in log.ops if op[0] == "fork_at" for _ in range(op[3])]
     return sum(-(-c // block_tokens) for c in caps)
 
 
 class NodeData:
-    """Lazily generated per-node K/V bit patterns (the rows a node holds at decode)."""
+    """Lazily generated per-node K/V bit patterns: ``data(n)`` returns K, V
+    whose row r is node n's r-th token (at least the rows it holds at decode).
+    A tail cut from a node by ``fork_at`` reads that node's stream from the
+    cut on."""
 
     def __init__(self, cfg: Config, log: CallLog):
         self.cfg, self.log = cfg, log
+        self.src = getattr(log, "data_src", {}) or {}
+        self.extra = getattr(log, "data_rows", {}) or {}
         self.cache: dict[int, tuple[np.ndarray, np.ndarray]] = {}
 
+    def _rows(self, o: int) -> int:
+        return self.extra.get(o, self.log.rows[o])
+
     def prefetch(self, nodes):
-        todo = [n for n in dict.fromkeys(nodes) if n not in self.cache]
+        todo = [o for o in dict.fromkeys(self.src.get(n, (n, 0))[0] for n in nodes) if o not in self.cache]
         if not todo:
             return
-        res = many_node_kv_bits(self.cfg.seed, [(n, self.log.rows[n]) for n in todo],
-                                self.cfg.hkv, self.cfg.d)
-        for n, kv in zip(todo, res):
-            self.cache[n] = kv
+        res = many_node_kv_bits(self.cfg.seed, [(o, self._rows(o)) for o in todo], self.cfg.hkv, self.cfg.d)
+        for o, kv in zip(todo, res):
+            self.cache[o] = kv
 
     def __call__(self, n: int):
-        if n not in self.cache:
-            self.cache[n] = node_kv_bits(self.cfg.seed, n, self.log.rows[n], self.cfg.hkv, self.cfg.d)
-        return self.cache[n]
+        o, first = self.src.get(n, (n, 0))
+        if o not in self.cache:
+            self.cache[o] = node_kv_bits(self.cfg.seed, o, self._rows(o), self.cfg.hkv, self.cfg.d)
+        k, v = self.cache[o]
+        return (k, v) if first == 0 else (k[first:], v[first:])
 
     def drop(self, nodes):
         for n in nodes:
-            self.cache.pop(n, None)
+            if n not in self.src and n not in self.extra:
+                self.cache.pop(n, None)
 
 
 class DeviceTree:
@@ -106,6 +117,11 @@ class DeviceTree:
                 self.ctx.new_root(op[1])
             elif op[0] == "fork":
                 self.ctx.fork(op[1], op[2], op[3])
+            elif op[0] == "fork_at":
+                x, off = op[1], op[2]
+                _, t = self.ctx.fork_at(x, off, op[3], op[4])
+                self._len[t] = self._len.get(x, 0) - off
+                self._len[x] = off
             else:
                 nodes, ntok = op[1], op[2]
                 i = 0
@@ -170,6 +186,8 @@ class DeviceTree:
                 r.ctx.new_root(op[1])
             elif op[0] == "fork":
                 r.ctx.fork(op[1], op[2], op[3])
+            elif op[0] == "fork_at":
+                r.ctx.fork_at(op[1], op[2], op[3], op[4])
             else:
                 r.ctx.kv_commit(op[1], op[2])
         r._len = dict(self._len)
