@@ -21,6 +21,9 @@ What it computes follows TreePO (arXiv 2508.17445):
   merged into the per-leaf result; it is pinned against ``attention``.
 * ``advantage`` -- the TreePO advantage over the same descendant sets
   (Sec. 2.3, Eq. tree_ae; the size-weighted variant Eq. tree_ae_sgw).
+* ``budget`` -- the branching budget over active paths (Sec. 2.2, Sec. 4.4).
+* ``prefill`` -- causal attention of newly appended tokens over their chain
+  (the shared prompt prefilled once for all rollouts of a query).
 """
 
-from . import metadata, attention, cascade, advantage  # noqa: F401
+from . import metadata, attention, cascade, advantage, prefill  # noqa: F401
