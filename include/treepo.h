@@ -148,6 +148,33 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes,
                          const int32_t* ntok, const void* k, const void* v,
                          hipStream_t stream);
 
+/* Prefill: appends tokens like treepo_kv_append and computes their causal
+ * attention over their chain (the shared prompt of a query, prefilled once
+ * for all of its rollouts: Sec. 2.2 tree rollout, where the prompt is the
+ * root every path extends; the shared-prefix prefilling of Sec. 4.1).
+ * Node nodes[i] receives ntok[i] tokens; a new token at chain position p
+ * (chain tokens before it, root first) attends to chain positions 0..p:
+ *   out[r, h] = sum_{t <= p} softmax_t(scale <q[r, h], K[t, g]>) V[t, g],
+ *   lse[r, h] = ln sum_{t <= p} exp(scale <q[r, h], K[t, g]>),  g = h / (Hq/Hkv).
+ * Rows r are packed in call order, as for treepo_kv_append.
+ *   q          device bf16 [sum ntok][Hq][D]
+ *   k, v       device bf16 [sum ntok][Hkv][D] (written into the pools)
+ *   scale      softmax scale, positive and finite
+ *   out        device fp32 [sum ntok][Hq][D] (written)
+ *   lse        device fp32 [sum ntok][Hq] (written) or null
+ *   workspace  device, 256-byte aligned, >= treepo_prefill_workspace_size for
+ *              the same arguments; the call uploads its tile tables there
+ *              (contents need not be preserved between calls, but a call's
+ *              kernels read it until they finish on stream).
+ * Validation as treepo_kv_append, plus EINVAL (a node twice in one call, null
+ * q/k/v/out or bad scale with tokens, a chain of 2^25 tokens or more) and
+ * EWORKSPACE.  Nothing is changed on error.  Enqueued on stream. */
+int32_t treepo_prefill_workspace_size(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                                      size_t* bytes);
+int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok, const void* q,
+                       const void* k, const void* v, float scale, float* out, float* lse, void* workspace,
+                       size_t ws_bytes, hipStream_t stream);
+
 /* Pool token rows (block * B + offset) that the next treepo_kv_append /
  * treepo_kv_commit with the same arguments would fill, in call order
  * (rows_out: host, sum(ntok) entries).  For callers that write K/V into the
@@ -336,7 +363,8 @@ int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* l
 #define TREEPO_KERNEL_PARTIAL 1 /* node partials, one workgroup per stream         */
 #define TREEPO_KERNEL_COMBINE 2 /* log-sum-exp merge of each leaf's partials      */
 #define TREEPO_KERNEL_ADVANTAGE 3 /* TreePO advantage over the leaves' sub-groups  */
-#define TREEPO_KERNEL_KINDS 4
+#define TREEPO_KERNEL_PREFILL 4 /* causal attention of prefilled tokens          */
+#define TREEPO_KERNEL_KINDS 5
 
 /* When enabled, every kernel launch of this context is timed with HIP events
  * on the launch stream: the decode kernels (partial, combine) get events that

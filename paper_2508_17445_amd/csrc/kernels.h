@@ -64,6 +64,36 @@ struct AdvantageArgs {
 hipError_t launch_advantage(const AdvantageArgs& a, hipStream_t s);
 constexpr int32_t kComputeUnits = 256;  // MI355X
 
+// Prefill: causal attention of tokens just appended to a node over its chain.
+// A work item is up to kPrefillRows consecutive new tokens of one sequence;
+// the kernel runs it for every query head.  Tile records (int2): x = half
+// block 2 * block + half (32-token tile of the pools, KV head added by the
+// kernel), y = (chain position of the tile's first token) << 6 | tokens.
+constexpr int32_t kPrefillRows = 128;
+struct PrefillItem {
+  int32_t row0;      // packed row (of q, out, lse) of the item's first token
+  int32_t n_rows;    // tokens of the item, 1..kPrefillRows
+  int32_t pos0;      // chain position of the item's first token
+  int32_t tile_off;  // first tile record of the sequence's chain
+  int32_t nk;        // tiles the item streams: those starting at or before its last token
+  int32_t pad[3];
+};
+struct PrefillArgs {
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  int64_t num_blocks;
+  int32_t hq, hkv, d;
+  const uint16_t* q;         // bf16 [rows][Hq][D]
+  const PrefillItem* items;  // n_items, longest first
+  int32_t n_items;
+  const int2* tiles;
+  float scale_log2;
+  float* out;                // fp32 [rows][Hq][D]
+  float* lse;                // fp32 [rows][Hq] or null
+  hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+};
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s);
+
 // One block-aligned run of appended tokens: source rows [src_row, +count) go
 // to token offsets [off, off + count) of pool block `block` (off + count <= 64).
 struct AppendPiece {

@@ -1,5 +1,6 @@
 // gfx950 kernels of the segment-tree decode path: KV append (scatter into the
-// pools), the node-partial kernel, and the log-sum-exp combine.
+// pools), the node-partial kernel, and the log-sum-exp combine; and the
+// prefill of appended tokens (causal attention over their chain).
 //
 // Node-partial attention (cascade schedule): the work is a list of pieces --
 // consecutive KV tiles of one node run, scored against the query rows of a
@@ -875,14 +876,216 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
   }
 }
 
+
+// ---- prefill ------------------------------------------------------------------------
+//
+// Causal attention of tokens just appended to a node, over its chain (a
+// query's shared prompt, prefilled once for all of its rollouts).  A
+// workgroup takes up to 128 consecutive new tokens of one sequence for one
+// query head; wave w owns tokens [32 w, 32 w + 32) as two 16-row blocks that
+// share every K and V operand it reads from LDS.  The workgroup streams the
+// 32-token tiles of the chain up to its last token through the decode's
+// four-buffer global->LDS pipeline.  Tiles that every row of a wave sees in
+// full take the unmasked path; the others mask keys past each row's own
+// position and, at a node's end, past the tile's tokens.
+//
+// Work order: unit u = (item, KV head) in the host's longest-first item
+// order.  Workgroup w runs on XCD w % 8; its index s = w / 8 on that XCD
+// splits into u = (s / G) * 8 + w % 8 and head h = g G + s % G, so the G
+// query heads of one KV head run on one XCD at about the same time and read
+// the same K/V tiles through its L2.
+template <int D>
+__global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
+    const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, const uint16_t* __restrict__ q,
+    const PrefillItem* __restrict__ items, const int2* __restrict__ tiles, float* __restrict__ out,
+    float* __restrict__ lse, int32_t n_units, int32_t num_blocks, int32_t hq, int32_t hkv, float scale_log2) {
+  constexpr int kKS = D / 32;  // QK k-steps
+  constexpr int kDB = D / 16;  // PV output d-blocks
+  constexpr int kRB = 2;       // 16-row blocks per wave
+  constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
+  __shared__ __attribute__((aligned(16))) uint16_t kv[kNBuf][2 * kSub * D];
+
+  const int G = hq / hkv;
+  const int wg = blockIdx.x;
+  const int s_x = wg >> 3;
+  const int unit = (s_x / G) * 8 + (wg & 7);
+  if (unit >= n_units) return;  // whole workgroup
+  const int item_i = unit / hkv;
+  const int g = unit - item_i * hkv;
+  const int h = g * G + s_x % G;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int a = lane >> 4;    // lane group
+  const int r16 = lane & 15;  // row within a 16-row block
+  const PrefillItem it = items[item_i];
+  const int nk = it.nk;
+  const int2* __restrict__ tl = tiles + it.tile_off;
+  const int hb_base = 2 * g * num_blocks;
+
+  // Q^T operands: lane holds row 32 wave + 16 rb + r16, d chunk 4 ks + a
+  uint4 qb[kRB][kKS];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) {
+    const int m = 32 * wave + 16 * rb + r16;
+    if (m < it.n_rows) {
+      const uint4* src = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(it.row0 + m) * hq + h) * D);
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) qb[rb][ks] = src[4 * ks + a];
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) qb[rb][ks] = make_uint4(0, 0, 0, 0);
+    }
+  }
+  // The query loads land before the first tile is issued: otherwise the
+  // compiler, which does not see the tile loads, would wait for them (and so
+  // drain the tile pipeline) at their first use inside the loop.
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) asm volatile("" ::"v"(qb[rb][ks].x));
+
+  Pipe<D> pp;
+  pipe_init<D>(pp, lds_addr(kv[0]), nk, wave, lane);
+  for (int k = 0; k < kDepth && k < nk; ++k)
+    dma_tile<D>(kpool, vpool, hb_base + tl[k].x, false, pp.buf0 + k * kBufBytes, pp, wave);
+  if (kDepth < nk) pp.next = tl[kDepth];
+
+  const int row_w = 32 * wave;  // the wave's first row
+  const bool wave_on = row_w < it.n_rows;
+  const int pos_lo = it.pos0 + row_w;
+  const int pos_hi = it.pos0 + (row_w + 31 < it.n_rows - 1 ? row_w + 31 : it.n_rows - 1);
+  int prow[kRB];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) prow[rb] = it.pos0 + row_w + 16 * rb + r16;
+
+  f32x4 acc[kRB][kDB];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) acc[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_ref[kRB] = {-INFINITY, -INFINITY};
+  float l_sum[kRB] = {0.f, 0.f};
+
+  for (int k = 0; k < nk; ++k) {
+    wait_tile<D>(k, nk);
+    if (k + kDepth < nk) {
+      dma_tile<D>(kpool, vpool, hb_base + pp.next.x, false, pp.buf0 + ((k + kDepth) & (kNBuf - 1)) * kBufBytes, pp,
+                  wave);
+      if (k + kDepth + 1 < nk) pp.next = tl[k + kDepth + 1];
+    }
+    const int2 rec = tl[k];
+    const int first = __builtin_amdgcn_readfirstlane(rec.y >> 6);
+    const int cnt = __builtin_amdgcn_readfirstlane(rec.y & 63);
+    if (!wave_on || first > pos_hi) continue;
+    const char* kt = reinterpret_cast<const char*>(kv[k & (kNBuf - 1)]);
+    const char* vt = kt + kSub * D * 2;
+    // ---- S^T = K Q^T for the 32 tokens, both row blocks
+    f32x4 S[kRB][2];
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) S[rb][0] = S[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int tok = tau(b, r16);
+        const int c = 4 * ks + a;
+        const uint4 ka = *reinterpret_cast<const uint4*>(kt + tok * (D * 2) + ((c ^ k_swz(tok)) << 4));
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) S[rb][b] = mfma16(ka, qb[rb][ks], S[rb][b]);
+      }
+    }
+    // ---- weights: lazy reference per row, as in the decode
+    const bool full = cnt == kSub && first + kSub - 1 <= pos_lo;
+    uint4 P[kRB], PL[kRB];
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) {
+      if (full) {
+        float mx = fmaxf(fmaxf(fmaxf(S[rb][0][0], S[rb][0][1]), fmaxf(S[rb][0][2], S[rb][0][3])),
+                         fmaxf(fmaxf(S[rb][1][0], S[rb][1][1]), fmaxf(S[rb][1][2], S[rb][1][3]))) * scale_log2;
+        if (__builtin_amdgcn_ballot_w64(mx > m_ref[rb] + kLazyMaxSlack) != 0) {
+          mx = fmaxf(mx, __shfl_xor(mx, 16));
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          const float mn = fmaxf(m_ref[rb], mx);
+          const float alpha = m_ref[rb] == -INFINITY ? 0.f : fast_exp2(m_ref[rb] - mn);
+          m_ref[rb] = mn;
+          l_sum[rb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < kDB; ++db) acc[rb][db] *= alpha;
+        }
+        uint2 p0, pl0, p1, pl1;
+        l_sum[rb] += weights4(S[rb][0], scale_log2, -m_ref[rb], p0, pl0) +
+                     weights4(S[rb][1], scale_log2, -m_ref[rb], p1, pl1);
+        P[rb] = make_uint4(p0.x, p0.y, p1.x, p1.y);
+        PL[rb] = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
+      } else {
+        float x[2][4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int t = 8 * a + 4 * b + e;
+            x[b][e] = t < cnt && first + t <= prow[rb] ? S[rb][b][e] * scale_log2 : -INFINITY;
+            mx = fmaxf(mx, x[b][e]);
+          }
+        if (__builtin_amdgcn_ballot_w64(mx > m_ref[rb] + kLazyMaxSlack) != 0) {
+          mx = fmaxf(mx, __shfl_xor(mx, 16));
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          const float mn = fmaxf(m_ref[rb], mx);
+          const float alpha = m_ref[rb] == -INFINITY ? 0.f : fast_exp2(m_ref[rb] - mn);
+          m_ref[rb] = mn;
+          l_sum[rb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < kDB; ++db) acc[rb][db] *= alpha;
+        }
+        uint2 p0, pl0, p1, pl1;
+        l_sum[rb] += softmax_p4(x[0], m_ref[rb], p0, pl0) + softmax_p4(x[1], m_ref[rb], p1, pl1);
+        P[rb] = make_uint4(p0.x, p0.y, p1.x, p1.y);
+        PL[rb] = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
+      }
+    }
+    // ---- O^T += V^T P^T: one V operand per d-block for both row blocks
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+      const int d = 16 * db + r16;
+      uint4 va = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
+      if (cnt < kSub) {
+        const uint2 lo = mask_v4(make_uint2(va.x, va.y), 8 * a, cnt);
+        const uint2 hi = mask_v4(make_uint2(va.z, va.w), 8 * a + 4, cnt);
+        va = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) acc[rb][db] = mfma16(va, PL[rb], mfma16(va, P[rb], acc[rb][db]));
+    }
+  }
+
+  // ---- normalised rows and their log-sum-exp
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) {
+    float l = l_sum[rb];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const int m = row_w + 16 * rb + r16;
+    if (wave_on && m < it.n_rows) {
+      const int64_t orow = static_cast<int64_t>(it.row0 + m) * hq + h;
+      const float inv = 1.f / l;
+#pragma unroll
+      for (int db = 0; db < kDB; ++db)
+        *reinterpret_cast<f32x4*>(out + orow * D + 16 * db + 4 * a) = acc[rb][db] * inv;
+      if (lse != nullptr && a == 0) lse[orow] = (m_ref[rb] + __log2f(l)) * kLn2;
+    }
+  }
+}
+
 }  // namespace
 
 int32_t partial_workgroups_per_cu() { return kWgsPerCu; }
 
 // Launches `kernel` on `s`; with a.ev_start set, the events record the
 // kernel's own start and end.
-template <typename... Args, typename F>
-void launch_timed(const DecodeArgs& a, F kernel, dim3 grid, hipStream_t s, Args... args) {
+template <typename A, typename... Args, typename F>
+void launch_timed(const A& a, F kernel, dim3 grid, hipStream_t s, Args... args) {
   if (a.ev_start)
     hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a.ev_start, a.ev_stop, 0, args...);
   else
@@ -912,6 +1115,24 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   else
     launch_timed(a, combine_kernel<64>, grid, s, a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
                  a.n_leaves, a.hq, a.hkv, a.group);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
+  if (a.n_items <= 0) return hipSuccess;
+  if (a.hkv <= 0 || a.hq % a.hkv != 0 || (a.d != 64 && a.d != 128)) return hipErrorInvalidValue;
+  const int64_t units = static_cast<int64_t>(a.n_items) * a.hkv;
+  const int64_t group = a.hq / a.hkv;
+  const int64_t wgs = (units + 7) / 8 * 8 * group;
+  if (wgs > 0x7FFFFFFF || 2 * a.hkv * a.num_blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(wgs));
+  const int32_t nb = static_cast<int32_t>(a.num_blocks);
+  if (a.d == 128)
+    launch_timed(a, prefill_kernel<128>, grid, s, a.k_pool, a.v_pool, a.q, a.items, a.tiles, a.out, a.lse,
+                 static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
+  else
+    launch_timed(a, prefill_kernel<64>, grid, s, a.k_pool, a.v_pool, a.q, a.items, a.tiles, a.out, a.lse,
+                 static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
   return hipGetLastError();
 }
 

@@ -664,12 +664,12 @@ int32_t treepo_kv_commit(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
   return TREEPO_OK;
 }
 
-int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
-                         const void* k, const void* v, hipStream_t stream) {
-  if (!ctx) return TREEPO_EINVAL;
-  std::string err;
-  int32_t st = ctx->tree.check_append(n, nodes, ntok, nullptr, &err);
-  if (st != treepo::kOk) return fail(ctx, st, err);
+namespace {
+
+// Scatters the rows into the pools and advances the lengths; the call has
+// been validated by check_append.
+int32_t append_validated(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok, const void* k,
+                         const void* v, hipStream_t stream) {
   int64_t total = 0;
   for (int32_t i = 0; i < n; ++i) total += ntok[i];
   if (total > 0) {
@@ -694,6 +694,144 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
     if (e != hipSuccess) return hip_fail(ctx, e, "append kernel launch");
   }
   ctx->tree.apply_append(n, nodes, ntok);
+  return TREEPO_OK;
+}
+
+// Work of a prefill call: each sequence's chain as 32-token tiles (after the
+// append), and items of up to kPrefillRows new tokens, longest first.
+struct PrefillPlan {
+  std::vector<treepo::PrefillItem> items;
+  std::vector<int32_t> tiles;  // int2 records
+  size_t tiles_off = 0, bytes = 0;
+};
+
+int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                           PrefillPlan* pl) {
+  const auto& nd = ctx->tree.nodes();
+  constexpr int32_t kT = 32;
+  std::vector<int32_t> chain;
+  std::vector<int32_t> firsts;
+  int64_t row = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (ntok[i] == 0) continue;
+    const int32_t x = nodes[i];
+    ctx->tree.chain(x, &chain);
+    const int64_t pos0 = ctx->tree.chain_tokens(x);
+    if (pos0 + ntok[i] >= (int64_t{1} << 25)) return fail(ctx, TREEPO_EINVAL, "chain too long for a prefill");
+    const int32_t tile_off = static_cast<int32_t>(pl->tiles.size() / 2);
+    firsts.clear();
+    for (int32_t y : chain) {
+      const treepo::Node& b = nd[y];
+      const int32_t len = y == x ? b.len + ntok[i] : b.len;
+      for (int32_t j = 0; j * kT < len; ++j) {
+        const int32_t first = b.start + j * kT;
+        const int32_t cnt = std::min(kT, len - j * kT);
+        pl->tiles.push_back(2 * (b.block_begin + j / 2) + (j & 1));
+        pl->tiles.push_back((first << 6) | cnt);
+        firsts.push_back(first);
+      }
+    }
+    for (int32_t t0 = 0; t0 < ntok[i]; t0 += treepo::kPrefillRows) {
+      treepo::PrefillItem it{};
+      it.row0 = static_cast<int32_t>(row + t0);
+      it.n_rows = std::min(treepo::kPrefillRows, ntok[i] - t0);
+      it.pos0 = static_cast<int32_t>(pos0 + t0);
+      it.tile_off = tile_off;
+      const int32_t last = it.pos0 + it.n_rows - 1;
+      it.nk = static_cast<int32_t>(std::upper_bound(firsts.begin(), firsts.end(), last) - firsts.begin());
+      pl->items.push_back(it);
+    }
+    row += ntok[i];
+  }
+  if (row >= (int64_t{1} << 31) / 64) return fail(ctx, TREEPO_EINVAL, "too many prefill rows");
+  std::stable_sort(pl->items.begin(), pl->items.end(),
+                   [](const treepo::PrefillItem& a, const treepo::PrefillItem& b) { return a.nk > b.nk; });
+  const size_t ib = pl->items.size() * sizeof(treepo::PrefillItem);
+  pl->tiles_off = (ib + 255) / 256 * 256;
+  pl->bytes = std::max<size_t>(256, pl->tiles_off + pl->tiles.size() * sizeof(int32_t));
+  return TREEPO_OK;
+}
+
+int32_t check_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok) {
+  std::string err;
+  const int32_t st = ctx->tree.check_append(n, nodes, ntok, nullptr, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  std::vector<int32_t> seen(nodes, nodes + n);
+  std::sort(seen.begin(), seen.end());
+  if (std::adjacent_find(seen.begin(), seen.end()) != seen.end())
+    return fail(ctx, TREEPO_EINVAL, "a node appears twice in one prefill");
+  return TREEPO_OK;
+}
+
+}  // namespace
+
+int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                         const void* k, const void* v, hipStream_t stream) {
+  if (!ctx) return TREEPO_EINVAL;
+  std::string err;
+  const int32_t st = ctx->tree.check_append(n, nodes, ntok, nullptr, &err);
+  if (st != treepo::kOk) return fail(ctx, st, err);
+  return append_validated(ctx, n, nodes, ntok, k, v, stream);
+}
+
+int32_t treepo_prefill_workspace_size(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
+                                      size_t* bytes) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (!bytes) return fail(ctx, TREEPO_EINVAL, "null bytes");
+  int32_t st = check_prefill(ctx, n, nodes, ntok);
+  if (st != TREEPO_OK) return st;
+  PrefillPlan pl;
+  st = build_prefill_plan(ctx, n, nodes, ntok, &pl);
+  if (st != TREEPO_OK) return st;
+  *bytes = pl.bytes;
+  return TREEPO_OK;
+}
+
+int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok, const void* q,
+                       const void* k, const void* v, float scale, float* out, float* lse, void* workspace,
+                       size_t ws_bytes, hipStream_t stream) {
+  if (!ctx) return TREEPO_EINVAL;
+  int32_t st = check_prefill(ctx, n, nodes, ntok);
+  if (st != TREEPO_OK) return st;
+  int64_t total = 0;
+  for (int32_t i = 0; i < n; ++i) total += ntok[i];
+  if (total == 0) return TREEPO_OK;
+  if (!q || !k || !v || !out) return fail(ctx, TREEPO_EINVAL, "null q, k, v or out with tokens to prefill");
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(ctx, TREEPO_EINVAL, "scale must be positive and finite");
+  PrefillPlan pl;
+  st = build_prefill_plan(ctx, n, nodes, ntok, &pl);
+  if (st != TREEPO_OK) return st;
+  if (!workspace || ws_bytes < pl.bytes || reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(ctx, TREEPO_EWORKSPACE,
+                "workspace missing, smaller than treepo_prefill_workspace_size or not 256-byte aligned");
+  st = append_validated(ctx, n, nodes, ntok, k, v, stream);
+  if (st != TREEPO_OK) return st;
+  char* wsb = static_cast<char*>(workspace);
+  std::vector<char> blob(pl.bytes, 0);
+  std::memcpy(blob.data(), pl.items.data(), pl.items.size() * sizeof(treepo::PrefillItem));
+  std::memcpy(blob.data() + pl.tiles_off, pl.tiles.data(), pl.tiles.size() * sizeof(int32_t));
+  hipError_t e = upload(ctx, wsb, blob.data(), blob.size(), stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "prefill table upload");
+  treepo::PrefillArgs a;
+  a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
+  a.v_pool = static_cast<const uint16_t*>(ctx->cfg.v_pool);
+  a.num_blocks = ctx->cfg.num_blocks;
+  a.hq = ctx->cfg.num_q_heads;
+  a.hkv = ctx->cfg.num_kv_heads;
+  a.d = ctx->cfg.head_dim;
+  a.q = static_cast<const uint16_t*>(q);
+  a.items = reinterpret_cast<const treepo::PrefillItem*>(wsb);
+  a.n_items = static_cast<int32_t>(pl.items.size());
+  a.tiles = reinterpret_cast<const int2*>(wsb + pl.tiles_off);
+  a.scale_log2 = scale * 1.44269504088896340736f;
+  a.out = out;
+  a.lse = lse;
+  e = timed_launch_attached(ctx, TREEPO_KERNEL_PREFILL, [&](hipEvent_t s0, hipEvent_t s1) {
+    a.ev_start = s0;
+    a.ev_stop = s1;
+    return treepo::launch_prefill(a, stream);
+  });
+  if (e != hipSuccess) return hip_fail(ctx, e, "prefill kernel launch");
   return TREEPO_OK;
 }
 

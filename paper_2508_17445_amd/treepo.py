@@ -21,7 +21,7 @@ LIB_PATH = os.environ.get("TREEPO_LIBRARY") or os.path.join(HERE, "libtreepo.so"
 
 OK, EINVAL, ENOMEM, EFULL, EFROZEN, EEMPTY, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 MODE_TREE, MODE_NAIVE = 0, 1
-KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE, KERNEL_ADVANTAGE = 0, 1, 2, 3
+KERNEL_APPEND, KERNEL_PARTIAL, KERNEL_COMBINE, KERNEL_ADVANTAGE, KERNEL_PREFILL = 0, 1, 2, 3, 4
 ADV_MEAN, ADV_SIZE_WEIGHTED = 0, 1
 NODE_FIELDS = ("parent", "depth", "start", "len", "cap", "block_begin", "n_blocks", "tree_id")
 BLOCK_TOKENS = 64
@@ -83,6 +83,9 @@ def load_library(path: str = LIB_PATH):
         "treepo_branch_budget": (_i32, [_i32, ctypes.POINTER(ctypes.c_float), _i32, _i32, ctypes.c_float, _pi32]),
         "treepo_advantage_workspace_size": (_i32, [_p, _i32, _pi32, ctypes.POINTER(ctypes.c_size_t)]),
         "treepo_tree_advantage": (_i32, [_p, _i32, _pi32, _p, _i32, _p, _p, ctypes.c_size_t, _p]),
+        "treepo_prefill_workspace_size": (_i32, [_p, _i32, _pi32, _pi32, ctypes.POINTER(ctypes.c_size_t)]),
+        "treepo_prefill": (_i32, [_p, _i32, _pi32, _pi32, _p, _p, _p, ctypes.c_float, _p, _p, _p, ctypes.c_size_t,
+                                  _p]),
         "treepo_bench_copy": (_i32, [_p, _p, ctypes.c_size_t, _p]),
         "treepo_bench_read": (_i32, [_p, ctypes.c_size_t, _p, _p]),
         "treepo_bench_stream": (_i32, [_p, ctypes.c_size_t, _p, _i32, _i32, _p]),
@@ -297,6 +300,23 @@ class Context:
         nb = int(workspace.numel() * workspace.element_size()) if ws_bytes is None else ws_bytes
         self._check(self.lib.treepo_tree_advantage(self.h, len(lv), _ptr32(lv), _dev(rewards), weighting, _dev(adv),
                                                    _dev(workspace), nb, _stream(stream)), "treepo_tree_advantage")
+
+    # ---- prefill -------------------------------------------------------------
+    def prefill_workspace_size(self, nodes, ntok) -> int:
+        nd, nt = _arr32(nodes), _arr32(ntok)
+        n = ctypes.c_size_t()
+        self._check(self.lib.treepo_prefill_workspace_size(self.h, len(nd), _ptr32(nd), _ptr32(nt), ctypes.byref(n)),
+                    "treepo_prefill_workspace_size")
+        return n.value
+
+    def prefill(self, nodes, ntok, q, k, v, scale, out, lse, workspace, ws_bytes=None, stream=None):
+        """Append ntok[i] tokens to nodes[i] and write their causal attention
+        over the chain (q, k, v, out, lse: device tensors packed in call order)."""
+        nd, nt = _arr32(nodes), _arr32(ntok)
+        nb = int(workspace.numel() * workspace.element_size()) if ws_bytes is None else ws_bytes
+        self._check(self.lib.treepo_prefill(self.h, len(nd), _ptr32(nd), _ptr32(nt), _dev(q), _dev(k), _dev(v),
+                                            float(scale), _dev(out), _dev(lse), _dev(workspace), nb, _stream(stream)),
+                    "treepo_prefill")
 
     # ---- timing ------------------------------------------------------------
     def set_profiling(self, enable: bool):

@@ -133,3 +133,35 @@ def test_advantage_codes():
     assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, FAKE_POOL, 0, nb - 1) == T.EWORKSPACE
     assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, FAKE_POOL + 8, 0, nb) == T.EWORKSPACE
     assert _code(ctx.tree_advantage, [a, b], FAKE_POOL, FAKE_POOL, None, 0, nb) == T.EWORKSPACE
+
+
+def test_prefill_codes_and_workspace_layout():
+    """Prefill validation happens before any device work; the workspace holds
+    32-byte work items (up to 128 tokens each), then 8-byte tile records of
+    every chain (32 tokens each), at a 256-byte boundary."""
+    ctx = host_ctx(num_blocks=40, max_nodes=8)
+    r = ctx.new_root(300)
+    assert ctx.prefill_workspace_size([r], [300]) == 256 + 10 * 8        # 3 items; 10 tiles
+    assert ctx.prefill_workspace_size([r], [0]) == 256
+    ctx.kv_commit([r], [100])
+    a, b = ctx.fork(r, 2, 200)
+    # a: chain 100 + 129 tokens -> 4 + 5 tiles; 2 items.  b: 100 + 1 -> 4 + 1 tiles; 1 item
+    assert ctx.prefill_workspace_size([a, b], [129, 1]) == 256 + (9 + 5) * 8
+    snap = ctx.export_nodes().copy()
+    F = FAKE_POOL
+    assert _code(ctx.prefill, [a, a], [1, 1], F, F, F, 0.1, F, None, F, 1 << 20) == T.EINVAL   # a node twice
+    assert "twice" in ctx.lib.treepo_last_error(ctx.h).decode()
+    assert _code(ctx.prefill, [r], [1], F, F, F, 0.1, F, None, F, 1 << 20) == T.EFROZEN
+    assert _code(ctx.prefill, [a], [201], F, F, F, 0.1, F, None, F, 1 << 20) == T.EFULL
+    assert _code(ctx.prefill, [a], [1], None, F, F, 0.1, F, None, F, 1 << 20) == T.EINVAL
+    assert _code(ctx.prefill, [a], [1], F, F, F, 0.1, None, None, F, 1 << 20) == T.EINVAL
+    for bad_scale in (0.0, -1.0, float("inf"), float("nan")):
+        assert _code(ctx.prefill, [a], [1], F, F, F, bad_scale, F, None, F, 1 << 20) == T.EINVAL
+    need = ctx.prefill_workspace_size([a], [1])
+    assert _code(ctx.prefill, [a], [1], F, F, F, 0.1, F, None, F, need - 1) == T.EWORKSPACE
+    assert _code(ctx.prefill, [a], [1], F, F, F, 0.1, F, None, F + 16, need) == T.EWORKSPACE
+    assert _code(ctx.prefill, [a], [1], F, F, F, 0.1, F, None, None, need) == T.EWORKSPACE
+    assert np.array_equal(ctx.export_nodes(), snap)
+    # nothing to prefill: no device work, no state change
+    ctx.prefill([a, b], [0, 0], None, None, None, 0.1, None, None, None, 0)
+    assert np.array_equal(ctx.export_nodes(), snap)

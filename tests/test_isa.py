@@ -63,3 +63,37 @@ def test_every_vector_memory_wait_is_a_pipeline_barrier(partial_kernels):
             if x.startswith("s_waitcnt") and "vmcnt" in x:
                 assert re.match(r"^s_waitcnt vmcnt\(\d+\) lgkmcnt\(0\)$", x), (d, x)
                 assert body[i + 1] == "s_barrier", (d, body[i:i + 2])
+
+
+@pytest.fixture(scope="module")
+def prefill_kernels(tmp_path_factory):
+    import build
+    asm = open(build.device_asm("kernels.hip", str(tmp_path_factory.mktemp("asm_pf")))).read()
+    lines = asm.split("\n")
+    out = {}
+    for i, line in enumerate(lines):
+        m = re.match(r"^(_ZN6treepo\S*prefill_kernelILi(\d+)\S*):", line)
+        if m:
+            end = next(j for j in range(i, len(lines)) if lines[j].startswith(".Lfunc_end"))
+            body = [x.strip() for x in lines[i + 1:end]]
+            out[int(m.group(2))] = [x for x in body if x and not x.startswith((";", "."))]
+    return out, asm
+
+
+def test_prefill_pipeline_waits(prefill_kernels):
+    """The prefill kernel's query rows are plain loads waited for before the
+    first tile is issued; after that every vector-memory wait is a tile
+    barrier, so the three tiles in flight are never drained by the compiler."""
+    kernels, asm = prefill_kernels
+    assert sorted(kernels) == [64, 128]
+    for d, body in kernels.items():
+        first_dma = next(i for i, x in enumerate(body) if x.startswith("global_load_lds_dwordx4"))
+        plain = [i for i, x in enumerate(body) if re.match(r"^(global_load|buffer_load|flat_load|scratch_)", x)
+                 and not x.startswith("global_load_lds")]
+        assert plain and max(plain) < first_dma, d
+        for i, x in enumerate(body[first_dma:]):
+            if x.startswith("s_waitcnt") and "vmcnt" in x:
+                assert re.match(r"^s_waitcnt vmcnt\(\d+\) lgkmcnt\(0\)$", x), (d, x)
+                assert body[first_dma + i + 1] == "s_barrier", (d, body[first_dma + i:first_dma + i + 2])
+    sizes = re.findall(r"\.private_segment_fixed_size:\s+(\d+)\n(?:.*\n){0,40}?\s+\.symbol:\s+\S*prefill_kernel", asm)
+    assert len(sizes) == 2 and all(int(s) == 0 for s in sizes), sizes
