@@ -60,6 +60,9 @@ def _parse():
     ap.add_argument("--layers", type=int, default=4, help="layers (each its own pools) for --segment-loop")
     ap.add_argument("--advantage", action="store_true",
                     help="TreePO advantage (Sec. 2.3, Eq. tree_ae) over the config's decoded leaves: one JSON line")
+    ap.add_argument("--prefill", action="store_true",
+                    help="prompt prefill (causal attention of every prompt of the config, written once into the "
+                         "pools for all of its rollouts): one JSON line")
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for hardware counters: a few decode steps of the workload, then one "
                          "1 GiB device copy whose byte counters calibrate the kernels'")
@@ -190,6 +193,14 @@ def _probe_read(nbytes=4 << 30, iters=10):
     return nbytes / (ms * 1e-3) / 1e9
 
 
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        return 1
+
+
 def _cpu_baseline(cfg_id, seconds):
     import numpy as np
     from oracle import attention as A
@@ -312,6 +323,122 @@ def _advantage(args):
     print(json.dumps(line), flush=True)
 
 
+def _prefill(args):
+    """Every prompt of the config prefilled in one call (fresh root nodes per
+    step, the same work each time): prompt tokens/s, the kernel's duration
+    (events attached to it) against the bf16 MFMA peak on the algorithmic
+    FLOPs of causal attention, the per-rollout baseline (each of a prompt's w
+    rollouts prefills its own copy), and the fp64 oracle on a sample."""
+    import numpy as np
+    import torch
+    from paper_2508_17445_amd import KERNEL_PREFILL, Context
+    from workloads import CONFIGS, build_call_log, node_kv_bits, query_bits
+    cfg, log = CONFIGS[args.config], build_call_log(args.config)
+    plens = [op[1] for op in log.ops if op[0] == "root"]
+    n_p, tokens = len(plens), sum(plens)
+    width = max(1, round(len(log.leaves) / n_p))           # rollouts per prompt
+    blocks = sum(-(-p // 64) for p in plens)
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    kb, vb, qb = [], [], []
+    for i, p in enumerate(plens):
+        k, v = node_kv_bits(cfg.seed, 900_000 + i, p, cfg.hkv, cfg.d)
+        kb.append(k); vb.append(v)
+        qb.append(query_bits(cfg.seed, 900_000 + i, p, cfg.hq, cfg.d))
+    k_all, v_all, q_all = dev(np.concatenate(kb)), dev(np.concatenate(vb)), dev(np.concatenate(qb))
+    out = torch.empty((tokens, cfg.hq, cfg.d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((tokens, cfg.hq), dtype=torch.float32, device="cuda")
+
+    def rig(copies):
+        elems = cfg.hkv * blocks * copies * 64 * cfg.d
+        kp = torch.empty(elems, dtype=torch.bfloat16, device="cuda")
+        vp = torch.empty(elems, dtype=torch.bfloat16, device="cuda")
+        return Context(cfg.hq, cfg.hkv, cfg.d, blocks * copies, n_p * copies, kp, vp, 64), kp, vp
+
+    reps = args.warmup + args.steps
+    ctx, kp, vp = rig(reps + 1)
+    sets = [[ctx.new_root(p) for p in plens] for _ in range(reps + 1)]
+    ws = torch.empty(ctx.prefill_workspace_size(sets[0], plens), dtype=torch.uint8, device="cuda")
+    for i in range(args.warmup):
+        ctx.prefill(sets[i], plens, q_all, k_all, v_all, cfg.scale, out, lse, ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, reps):
+        ctx.prefill(sets[i], plens, q_all, k_all, v_all, cfg.scale, out, lse, ws)
+    torch.cuda.synchronize()
+    call_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ctx.set_profiling(True)
+    ctx.prefill(sets[reps], plens, q_all, k_all, v_all, cfg.scale, out, lse, ws)
+    torch.cuda.synchronize()
+    tot, cnt = ctx.profile_read(KERNEL_PREFILL)
+    kern_ms = tot / max(cnt, 1)
+    # algorithmic FLOPs: token p of a prompt scores p + 1 keys (QK) and sums
+    # p + 1 values (PV), 2 D flops each, for every query head
+    flops = sum(p * (p + 1) // 2 for p in plens) * 4 * cfg.d * cfg.hq
+    achieved = flops / (kern_ms * 1e-3) / 1e12
+    del ctx, kp, vp, sets
+    torch.cuda.empty_cache()
+    # per-rollout baseline: each prompt prefilled once per rollout
+    naive = None
+    if not args.no_naive:
+        nrep = 3
+        ctx, kp, vp = rig(width * nrep)
+        plw = plens * width
+        kw, vw, qw = k_all.repeat(width, 1, 1), v_all.repeat(width, 1, 1), q_all.repeat(width, 1, 1)
+        ow = torch.empty((tokens * width, cfg.hq, cfg.d), dtype=torch.float32, device="cuda")
+        lw = torch.empty((tokens * width, cfg.hq), dtype=torch.float32, device="cuda")
+        setw = [[ctx.new_root(p) for p in plw] for _ in range(nrep)]
+        wsw = torch.empty(ctx.prefill_workspace_size(setw[0], plw), dtype=torch.uint8, device="cuda")
+        ctx.prefill(setw[0], plw, qw, kw, vw, cfg.scale, ow, lw, wsw)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(1, nrep):
+            ctx.prefill(setw[i], plw, qw, kw, vw, cfg.scale, ow, lw, wsw)
+        torch.cuda.synchronize()
+        naive = (time.perf_counter() - t0) * 1e3 / (nrep - 1)
+        del ctx, kp, vp, setw, kw, vw, qw, ow, lw
+        torch.cuda.empty_cache()
+    line = {"metric": "prompt prefill: prompt tokens/s (causal attention + KV written once per prompt, 1 MI355X)",
+            "value": round(tokens / (call_ms * 1e-3), 1), "unit": "prompt-tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(call_ms, 5),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded N(0,1) bf16 q/K/V, the config's prompt lengths)",
+            "config": {"workload": f"config {args.config}: {cfg.name} prompts", "prompts": n_p,
+                       "prompt_tokens": tokens, "rollouts_per_prompt": width, "hq": cfg.hq, "hkv": cfg.hkv,
+                       "head_dim": cfg.d},
+            "kernel_avg_ms": round(kern_ms, 5),
+            "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                         "frac": round(achieved / 2500.0, 4), "traffic": None, "kernel": "prefill_kernel",
+                         "kernel_avg_ms": round(kern_ms, 5), "launches_per_step": 1,
+                         "algorithmic_flops_per_launch": flops}}
+    if naive is not None:
+        line["per_rollout_baseline"] = {"ms_per_step": round(naive, 5), "prompt_copies": width,
+                                        "speedup_shared_vs_per_rollout": round(naive / call_ms, 3)}
+    if not args.no_cpu:
+        from oracle import metadata as M
+        from oracle import prefill as PF
+        m = M.TreeModel(64, blocks, n_p)
+        nodes = [m.new_root(p) for p in plens]
+        m.append(nodes, plens)
+        kv = {x: (kb[x], vb[x]) for x in nodes}
+        q_np = np.concatenate(qb)
+        budget = min(args.cpu_seconds, 10.0)
+        rows_done, t0 = 0, time.perf_counter()
+        rng = np.random.default_rng(0)
+        while time.perf_counter() - t0 < budget:
+            r = [int(x) for x in rng.integers(0, tokens, size=16)]
+            PF.prefill(m, kv.__getitem__, nodes, plens, q_np, cfg.scale, rows=r)
+            rows_done += len(r)
+        dt = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": round(rows_done / dt, 1), "unit": "prompt-tokens/s", "cores": _blas_threads(),
+                                "kind": "oracle",
+                                "sample": f"{rows_done} uniformly drawn prompt rows in {dt:.1f} s (fp64 numpy, "
+                                          "chains materialised per call)"}
+    print(json.dumps(line), flush=True)
+
+
 def _chain(parents, x):
     c = []
     while x >= 0:
@@ -389,8 +516,8 @@ def _segment_loop(args):
 def main():
     args = _parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the decode path has no multi-GPU "
-                                   "mode (see DESIGN.md for how it would shard)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "the decode path runs on one GPU only; it has no multi-GPU mode",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
     _ensure_built()
@@ -400,6 +527,9 @@ def main():
 
     if args.advantage:
         _advantage(args)
+        return
+    if args.prefill:
+        _prefill(args)
         return
     if args.segment_loop:
         _segment_loop(args)

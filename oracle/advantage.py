@@ -23,7 +23,7 @@ the paper's order:
    a query whose trajectories all have the same reward is dropped; its
    trajectories get advantage 0 and add nothing to step 5.
 
-Readings of what the paper leaves open (listed in the design doc as well): the
+Readings of what the paper leaves open: the
 garbled `std(...)^{J-1}` term is read as step 5; a leaf with no predecessor
 (a root decoded as a trajectory) gets 0; if no query is kept or the global
 std is 0, every advantage is 0.

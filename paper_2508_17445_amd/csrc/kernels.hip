@@ -195,6 +195,16 @@ __device__ __forceinline__ void wait_tile(int k, int ntot) {
     barrier_tile_landed<0>();
 }
 
+// Waits for tile k when at most one newer tile (k + 1) may have been issued,
+// and publishes it.
+template <int D>
+__device__ __forceinline__ void wait_tile_1ahead(int k, int ntot) {
+  if (ntot - 1 - k >= 1)
+    barrier_tile_landed<dma_per_tile<D>()>();
+  else
+    barrier_tile_landed<0>();
+}
+
 // Kernel arguments, passed as separate __restrict__ kernel parameters.
 struct Scalars {
   int32_t hq, hkv, group;
@@ -967,21 +977,9 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
   float m_ref[kRB] = {-INFINITY, -INFINITY};
   float l_sum[kRB] = {0.f, 0.f};
 
-  for (int k = 0; k < nk; ++k) {
-    wait_tile<D>(k, nk);
-    if (k + kDepth < nk) {
-      dma_tile<D>(kpool, vpool, hb_base + pp.next.x, false, pp.buf0 + ((k + kDepth) & (kNBuf - 1)) * kBufBytes, pp,
-                  wave);
-      if (k + kDepth + 1 < nk) pp.next = tl[k + kDepth + 1];
-    }
-    const int2 rec = tl[k];
-    const int first = __builtin_amdgcn_readfirstlane(rec.y >> 6);
-    const int cnt = __builtin_amdgcn_readfirstlane(rec.y & 63);
-    if (!wave_on || first > pos_hi) continue;
+  // S^T = K Q^T for the 32 tokens of tile k, both row blocks
+  auto qk = [&](int k, f32x4 (&S)[kRB][2]) {
     const char* kt = reinterpret_cast<const char*>(kv[k & (kNBuf - 1)]);
-    const char* vt = kt + kSub * D * 2;
-    // ---- S^T = K Q^T for the 32 tokens, both row blocks
-    f32x4 S[kRB][2];
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) S[rb][0] = S[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -995,32 +993,23 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
         for (int rb = 0; rb < kRB; ++rb) S[rb][b] = mfma16(ka, qb[rb][ks], S[rb][b]);
       }
     }
-    // ---- weights: lazy reference per row, as in the decode
+  };
+
+  // weights of tile k (lazy reference per row, as in the decode), then
+  // O^T += V^T P^T with one V operand per d-block for both row blocks
+  auto softmax_pv = [&](int k, const f32x4 (&S)[kRB][2], int first, int cnt) {
+    const char* vt = reinterpret_cast<const char*>(kv[k & (kNBuf - 1)]) + kSub * D * 2;
     const bool full = cnt == kSub && first + kSub - 1 <= pos_lo;
     uint4 P[kRB], PL[kRB];
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
+      float x[2][4];
+      float mx = -INFINITY;
       if (full) {
-        float mx = fmaxf(fmaxf(fmaxf(S[rb][0][0], S[rb][0][1]), fmaxf(S[rb][0][2], S[rb][0][3])),
-                         fmaxf(fmaxf(S[rb][1][0], S[rb][1][1]), fmaxf(S[rb][1][2], S[rb][1][3]))) * scale_log2;
-        if (__builtin_amdgcn_ballot_w64(mx > m_ref[rb] + kLazyMaxSlack) != 0) {
-          mx = fmaxf(mx, __shfl_xor(mx, 16));
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
-          const float mn = fmaxf(m_ref[rb], mx);
-          const float alpha = m_ref[rb] == -INFINITY ? 0.f : fast_exp2(m_ref[rb] - mn);
-          m_ref[rb] = mn;
-          l_sum[rb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < kDB; ++db) acc[rb][db] *= alpha;
-        }
-        uint2 p0, pl0, p1, pl1;
-        l_sum[rb] += weights4(S[rb][0], scale_log2, -m_ref[rb], p0, pl0) +
-                     weights4(S[rb][1], scale_log2, -m_ref[rb], p1, pl1);
-        P[rb] = make_uint4(p0.x, p0.y, p1.x, p1.y);
-        PL[rb] = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
+        // every key visible: max over the raw scores (the scale is positive)
+        mx = fmaxf(fmaxf(fmaxf(S[rb][0][0], S[rb][0][1]), fmaxf(S[rb][0][2], S[rb][0][3])),
+                   fmaxf(fmaxf(S[rb][1][0], S[rb][1][1]), fmaxf(S[rb][1][2], S[rb][1][3]))) * scale_log2;
       } else {
-        float x[2][4];
-        float mx = -INFINITY;
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -1029,23 +1018,27 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
             x[b][e] = t < cnt && first + t <= prow[rb] ? S[rb][b][e] * scale_log2 : -INFINITY;
             mx = fmaxf(mx, x[b][e]);
           }
-        if (__builtin_amdgcn_ballot_w64(mx > m_ref[rb] + kLazyMaxSlack) != 0) {
-          mx = fmaxf(mx, __shfl_xor(mx, 16));
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
-          const float mn = fmaxf(m_ref[rb], mx);
-          const float alpha = m_ref[rb] == -INFINITY ? 0.f : fast_exp2(m_ref[rb] - mn);
-          m_ref[rb] = mn;
-          l_sum[rb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < kDB; ++db) acc[rb][db] *= alpha;
-        }
-        uint2 p0, pl0, p1, pl1;
-        l_sum[rb] += softmax_p4(x[0], m_ref[rb], p0, pl0) + softmax_p4(x[1], m_ref[rb], p1, pl1);
-        P[rb] = make_uint4(p0.x, p0.y, p1.x, p1.y);
-        PL[rb] = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
       }
+      if (__builtin_amdgcn_ballot_w64(mx > m_ref[rb] + kLazyMaxSlack) != 0) {
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mn = fmaxf(m_ref[rb], mx);
+        const float alpha = m_ref[rb] == -INFINITY ? 0.f : fast_exp2(m_ref[rb] - mn);
+        m_ref[rb] = mn;
+        l_sum[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < kDB; ++db) acc[rb][db] *= alpha;
+      }
+      uint2 p0, pl0, p1, pl1;
+      if (full) {
+        l_sum[rb] += weights4(S[rb][0], scale_log2, -m_ref[rb], p0, pl0) +
+                     weights4(S[rb][1], scale_log2, -m_ref[rb], p1, pl1);
+      } else {
+        l_sum[rb] += softmax_p4(x[0], m_ref[rb], p0, pl0) + softmax_p4(x[1], m_ref[rb], p1, pl1);
+      }
+      P[rb] = make_uint4(p0.x, p0.y, p1.x, p1.y);
+      PL[rb] = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
     }
-    // ---- O^T += V^T P^T: one V operand per d-block for both row blocks
 #pragma unroll
     for (int db = 0; db < kDB; ++db) {
       const int d = 16 * db + r16;
@@ -1058,6 +1051,43 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
 #pragma unroll
       for (int rb = 0; rb < kRB; ++rb) acc[rb][db] = mfma16(va, PL[rb], mfma16(va, P[rb], acc[rb][db]));
     }
+  };
+
+  // Software pipeline: iteration k scores tile k + 1 (its K) while it turns
+  // tile k's scores into weights and accumulates tile k's V, so the matrix
+  // cores work on QK while the vector ALUs do the softmax.  Tile k + 1 must
+  // have landed at the start of iteration k; two tiles stay in flight.
+  f32x4 Sc[kRB][2], Sn[kRB][2];
+  wait_tile<D>(0, nk);
+  int first_c = __builtin_amdgcn_readfirstlane(tl[0].y >> 6);
+  int cnt_c = __builtin_amdgcn_readfirstlane(tl[0].y & 63);
+  bool vis_c = wave_on && first_c <= pos_hi;
+  if (vis_c) qk(0, Sc);
+  for (int k = 0; k < nk; ++k) {
+    int first_n = 0, cnt_n = 0;
+    bool vis_n = false;
+    if (k + 1 < nk) {
+      wait_tile_1ahead<D>(k + 1, nk);
+      if (k + kDepth < nk) {
+        dma_tile<D>(kpool, vpool, hb_base + pp.next.x, false, pp.buf0 + ((k + kDepth) & (kNBuf - 1)) * kBufBytes,
+                    pp, wave);
+        if (k + kDepth + 1 < nk) pp.next = tl[k + kDepth + 1];
+      }
+      const int2 rn = tl[k + 1];
+      first_n = __builtin_amdgcn_readfirstlane(rn.y >> 6);
+      cnt_n = __builtin_amdgcn_readfirstlane(rn.y & 63);
+      vis_n = wave_on && first_n <= pos_hi;
+    }
+    if (vis_n) qk(k + 1, Sn);
+    if (vis_c) softmax_pv(k, Sc, first_c, cnt_c);
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) {
+      Sc[rb][0] = Sn[rb][0];
+      Sc[rb][1] = Sn[rb][1];
+    }
+    first_c = first_n;
+    cnt_c = cnt_n;
+    vis_c = vis_n;
   }
 
   // ---- normalised rows and their log-sum-exp
