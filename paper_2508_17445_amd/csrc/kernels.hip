@@ -62,6 +62,7 @@ constexpr int kSub = 32;   // tokens per tile
 constexpr int kNBuf = 4;   // LDS tile buffers per workgroup
 constexpr int kDepth = 3;  // tiles in flight while one is consumed
 constexpr int kWgsPerCu = 2;
+constexpr int kPrefillWaves = 4;  // waves per prefill workgroup (4 or 8)
 
 template <int D>
 struct Smem {
@@ -191,16 +192,6 @@ __device__ __forceinline__ void wait_tile(int k, int ntot) {
     barrier_tile_landed<2 * kD>();
   else if (ahead == 1)
     barrier_tile_landed<kD>();
-  else
-    barrier_tile_landed<0>();
-}
-
-// Waits for tile k when at most one newer tile (k + 1) may have been issued,
-// and publishes it.
-template <int D>
-__device__ __forceinline__ void wait_tile_1ahead(int k, int ntot) {
-  if (ntot - 1 - k >= 1)
-    barrier_tile_landed<dma_per_tile<D>()>();
   else
     barrier_tile_landed<0>();
 }
@@ -892,8 +883,10 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
 // Causal attention of tokens just appended to a node, over its chain (a
 // query's shared prompt, prefilled once for all of its rollouts).  A
 // workgroup takes up to 128 consecutive new tokens of one sequence for one
-// query head; wave w owns tokens [32 w, 32 w + 32) as two 16-row blocks that
-// share every K and V operand it reads from LDS.  The workgroup streams the
+// query head; with W waves (4 or 8), wave w owns tokens [R w, R w + R),
+// R = 128 / W, as R / 16 row blocks that share every K and V operand it reads
+// from LDS.  Eight waves of 16 rows keep the registers under 128 per lane,
+// so that four waves share each SIMD and hide each other's latencies.  The workgroup streams the
 // 32-token tiles of the chain up to its last token through the decode's
 // four-buffer global->LDS pipeline.  Tiles that every row of a wave sees in
 // full take the unmasked path; the others mask keys past each row's own
@@ -904,14 +897,69 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
 // splits into u = (s / G) * 8 + w % 8 and head h = g G + s % G, so the G
 // query heads of one KV head run on one XCD at about the same time and read
 // the same K/V tiles through its L2.
-template <int D>
-__global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
+// The prefill's tile loads: a 32-token tile is 2 D / 16 slots of 1 KiB (K
+// rows, then V^T rows, swizzled as for the decode); each of the W waves
+// issues D / (8 W) of them per tile, one 16-byte global->LDS load per lane
+// each, so every wave counts the same number of loads per tile.
+template <int D, int W>
+struct PfPipe {
+  static constexpr int kKSlots = kSub * D * 2 / 1024;
+  static constexpr int kSlots = 2 * kKSlots / W;  // per wave
+  uint32_t buf0;
+  uint32_t off[kSlots];
+
+  __device__ __forceinline__ void init(uint32_t b0, int wave, int lane) {
+    constexpr int kKChunks = D / 8;
+    buf0 = b0;
+#pragma unroll
+    for (int j = 0; j < kSlots; ++j) {
+      const int sl = wave * kSlots + j;
+      if (sl < kKSlots) {
+        const int c = sl * 64 + lane;
+        const int row = c / kKChunks;
+        off[j] = row * (D * 2) + (((c % kKChunks) ^ k_swz(row)) << 4);
+      } else {
+        const int c = (sl - kKSlots) * 64 + lane;
+        const int vrow = c >> 2;
+        off[j] = vrow * (kSub * 2) + (((c & 3) ^ v_swz(vrow)) << 4);
+      }
+    }
+  }
+  // Stages half block hb into the buffer at LDS byte address dst.
+  __device__ __forceinline__ void issue(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
+                                        int hb, uint32_t dst, int wave) const {
+    const int64_t o = static_cast<int64_t>(hb) * kSub * D;
+#pragma unroll
+    for (int j = 0; j < kSlots; ++j) {
+      const int sl = wave * kSlots + j;
+      if (sl < kKSlots)
+        dma16s(kpool + o, off[j], __builtin_amdgcn_readfirstlane(dst + sl * 1024));
+      else
+        dma16s(vpool + o, off[j], __builtin_amdgcn_readfirstlane(dst + kSub * D * 2 + (sl - kKSlots) * 1024));
+    }
+  }
+  // Waits for tile k when up to `cap` newer tiles may have been issued, and
+  // publishes it.
+  __device__ __forceinline__ void wait(int k, int ntot, int cap) const {
+    const int ahead = ntot - 1 - k < cap ? ntot - 1 - k : cap;
+    if (ahead >= 2)
+      barrier_tile_landed<2 * kSlots>();
+    else if (ahead == 1)
+      barrier_tile_landed<kSlots>();
+    else
+      barrier_tile_landed<0>();
+  }
+};
+
+template <int D, int W>
+__global__ __launch_bounds__(64 * W, W / 2) void prefill_kernel(
     const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, const uint16_t* __restrict__ q,
     const PrefillItem* __restrict__ items, const int2* __restrict__ tiles, float* __restrict__ out,
     float* __restrict__ lse, int32_t n_units, int32_t num_blocks, int32_t hq, int32_t hkv, float scale_log2) {
   constexpr int kKS = D / 32;  // QK k-steps
   constexpr int kDB = D / 16;  // PV output d-blocks
-  constexpr int kRB = 2;       // 16-row blocks per wave
+  constexpr int kRB = 8 / W;   // 16-row blocks per wave
+  constexpr int kRows = 16 * kRB;
   constexpr uint32_t kBufBytes = 2 * kSub * D * 2;
   __shared__ __attribute__((aligned(16))) uint16_t kv[kNBuf][2 * kSub * D];
 
@@ -933,11 +981,11 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
   const int2* __restrict__ tl = tiles + it.tile_off;
   const int hb_base = 2 * g * num_blocks;
 
-  // Q^T operands: lane holds row 32 wave + 16 rb + r16, d chunk 4 ks + a
+  // Q^T operands: lane holds row kRows wave + 16 rb + r16, d chunk 4 ks + a
   uint4 qb[kRB][kKS];
 #pragma unroll
   for (int rb = 0; rb < kRB; ++rb) {
-    const int m = 32 * wave + 16 * rb + r16;
+    const int m = kRows * wave + 16 * rb + r16;
     if (m < it.n_rows) {
       const uint4* src = reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(it.row0 + m) * hq + h) * D);
 #pragma unroll
@@ -955,16 +1003,15 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) asm volatile("" ::"v"(qb[rb][ks].x));
 
-  Pipe<D> pp;
-  pipe_init<D>(pp, lds_addr(kv[0]), nk, wave, lane);
-  for (int k = 0; k < kDepth && k < nk; ++k)
-    dma_tile<D>(kpool, vpool, hb_base + tl[k].x, false, pp.buf0 + k * kBufBytes, pp, wave);
-  if (kDepth < nk) pp.next = tl[kDepth];
+  PfPipe<D, W> pp;
+  pp.init(lds_addr(kv[0]), wave, lane);
+  for (int k = 0; k < kDepth && k < nk; ++k) pp.issue(kpool, vpool, hb_base + tl[k].x, pp.buf0 + k * kBufBytes, wave);
+  int2 next = kDepth < nk ? tl[kDepth] : make_int2(0, 0);
 
-  const int row_w = 32 * wave;  // the wave's first row
+  const int row_w = kRows * wave;  // the wave's first row
   const bool wave_on = row_w < it.n_rows;
   const int pos_lo = it.pos0 + row_w;
-  const int pos_hi = it.pos0 + (row_w + 31 < it.n_rows - 1 ? row_w + 31 : it.n_rows - 1);
+  const int pos_hi = it.pos0 + (row_w + kRows - 1 < it.n_rows - 1 ? row_w + kRows - 1 : it.n_rows - 1);
   int prow[kRB];
 #pragma unroll
   for (int rb = 0; rb < kRB; ++rb) prow[rb] = it.pos0 + row_w + 16 * rb + r16;
@@ -974,8 +1021,12 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
   for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
     for (int db = 0; db < kDB; ++db) acc[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_ref[kRB] = {-INFINITY, -INFINITY};
-  float l_sum[kRB] = {0.f, 0.f};
+  float m_ref[kRB], l_sum[kRB];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) {
+    m_ref[rb] = -INFINITY;
+    l_sum[rb] = 0.f;
+  }
 
   // S^T = K Q^T for the 32 tokens of tile k, both row blocks
   auto qk = [&](int k, f32x4 (&S)[kRB][2]) {
@@ -1058,7 +1109,7 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
   // cores work on QK while the vector ALUs do the softmax.  Tile k + 1 must
   // have landed at the start of iteration k; two tiles stay in flight.
   f32x4 Sc[kRB][2], Sn[kRB][2];
-  wait_tile<D>(0, nk);
+  pp.wait(0, nk, 2);
   int first_c = __builtin_amdgcn_readfirstlane(tl[0].y >> 6);
   int cnt_c = __builtin_amdgcn_readfirstlane(tl[0].y & 63);
   bool vis_c = wave_on && first_c <= pos_hi;
@@ -1067,11 +1118,10 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void prefill_kernel(
     int first_n = 0, cnt_n = 0;
     bool vis_n = false;
     if (k + 1 < nk) {
-      wait_tile_1ahead<D>(k + 1, nk);
+      pp.wait(k + 1, nk, 1);
       if (k + kDepth < nk) {
-        dma_tile<D>(kpool, vpool, hb_base + pp.next.x, false, pp.buf0 + ((k + kDepth) & (kNBuf - 1)) * kBufBytes,
-                    pp, wave);
-        if (k + kDepth + 1 < nk) pp.next = tl[k + kDepth + 1];
+        pp.issue(kpool, vpool, hb_base + next.x, pp.buf0 + ((k + kDepth) & (kNBuf - 1)) * kBufBytes, wave);
+        if (k + kDepth + 1 < nk) next = tl[k + kDepth + 1];
       }
       const int2 rn = tl[k + 1];
       first_n = __builtin_amdgcn_readfirstlane(rn.y >> 6);
@@ -1115,6 +1165,14 @@ int32_t partial_workgroups_per_cu() { return kWgsPerCu; }
 // Launches `kernel` on `s`; with a.ev_start set, the events record the
 // kernel's own start and end.
 template <typename A, typename... Args, typename F>
+void launch_timed_block(const A& a, F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  if (a.ev_start)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, a.ev_start, a.ev_stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
+
+template <typename A, typename... Args, typename F>
 void launch_timed(const A& a, F kernel, dim3 grid, hipStream_t s, Args... args) {
   if (a.ev_start)
     hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a.ev_start, a.ev_stop, 0, args...);
@@ -1157,12 +1215,13 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
   if (wgs > 0x7FFFFFFF || 2 * a.hkv * a.num_blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(wgs));
   const int32_t nb = static_cast<int32_t>(a.num_blocks);
+  const dim3 block(64 * kPrefillWaves);
   if (a.d == 128)
-    launch_timed(a, prefill_kernel<128>, grid, s, a.k_pool, a.v_pool, a.q, a.items, a.tiles, a.out, a.lse,
-                 static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
+    launch_timed_block(a, prefill_kernel<128, kPrefillWaves>, grid, block, s, a.k_pool, a.v_pool, a.q, a.items,
+                       a.tiles, a.out, a.lse, static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
   else
-    launch_timed(a, prefill_kernel<64>, grid, s, a.k_pool, a.v_pool, a.q, a.items, a.tiles, a.out, a.lse,
-                 static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
+    launch_timed_block(a, prefill_kernel<64, kPrefillWaves>, grid, block, s, a.k_pool, a.v_pool, a.q, a.items,
+                       a.tiles, a.out, a.lse, static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
   return hipGetLastError();
 }
 
