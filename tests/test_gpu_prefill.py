@@ -28,7 +28,7 @@ pytestmark = pytest.mark.gpu
 class _Rig:
     """Pools, a context and the oracle model side by side."""
 
-    def __init__(self, hq, hkv, d, seed, num_blocks, max_nodes=4096):
+    def __init__(self, hq, hkv, d, seed, num_blocks, max_nodes=4096, live=False):
         import torch
         from paper_2508_17445_amd import Context
         self.hq, self.hkv, self.d, self.seed = hq, hkv, d, seed
@@ -37,7 +37,8 @@ class _Rig:
         # pools filled with NaN bit patterns: rows past a node's length must never be read
         self.kp = torch.full((elems,), -1, dtype=torch.int16, device="cuda").view(torch.bfloat16)
         self.vp = torch.full((elems,), -1, dtype=torch.int16, device="cuda").view(torch.bfloat16)
-        self.ctx = Context(hq, hkv, d, num_blocks, max_nodes, self.kp, self.vp, B)
+        self.node_len = torch.zeros(max_nodes, dtype=torch.int32, device="cuda") if live else None
+        self.ctx = Context(hq, hkv, d, num_blocks, max_nodes, self.kp, self.vp, B, node_len=self.node_len)
         self.model = M.TreeModel(B, num_blocks, max_nodes)
         self.kv = {}
 
@@ -137,3 +138,37 @@ def test_workload_prompts_sampled(cfg_id):
     rig.check(roots, plens, qb, out, lse, f"cfg{cfg_id}", rows=rows)
     del rig
     torch.cuda.empty_cache()
+
+
+def test_prefill_then_segment_decode_with_device_lengths():
+    """Prompts prefilled, branches forked, a decode plan built once on device
+    lengths; then branch segments prefilled in chunks (the append inside the
+    prefill advances the device lengths) and the same plan decodes after
+    every chunk."""
+    import torch
+    hq, hkv, d = 28, 4, 128
+    rig = _Rig(hq, hkv, d, 555, num_blocks=200, live=True)
+    lens = [200, 64, 33]
+    roots = [rig.ctx.new_root(n) for n in lens]
+    for n in lens:
+        rig.model.new_root(n)
+    qb, out, lse = rig.prefill(roots, lens, 0)
+    rig.check(roots, lens, qb, out, lse, "live prompts")
+    kids = []
+    for r in roots:
+        c = rig.ctx.fork(r, 2, 96)
+        assert rig.model.fork(r, 2, 96) == c
+        kids += c
+    o = torch.empty((len(kids), hq, d), dtype=torch.float32, device="cuda")
+    l = torch.empty((len(kids), hq), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(rig.ctx.workspace_size(kids, 0), 256), dtype=torch.uint8, device="cuda")
+    for step, chunk in enumerate(([1, 5, 40, 0, 17, 33], [31, 1, 24, 64, 30, 2], [0, 32, 32, 32, 0, 61])):
+        qb, out, lse = rig.prefill(kids, chunk, step + 1)
+        rig.check(kids, chunk, qb, out, lse, f"live chunk {step}")
+        q = query_bits(rig.seed, 500 + step, len(kids), hq, d)
+        rig.ctx.tree_decode(kids, rig.dev(q), rig.scale, o, l, ws)
+        torch.cuda.synchronize()
+        ref, ref_l = A.tree_decode(rig.model, rig.node_kv, kids, q, rig.scale)
+        err = float(np.abs(o.cpu().numpy() - ref).max())
+        print(f"[prefill live decode {step}] max|out-oracle|={err:.3e}", flush=True)
+        assert err <= TOL and float(np.abs(l.cpu().numpy() - ref_l).max()) <= TOL
