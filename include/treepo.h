@@ -163,7 +163,8 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes,
  *   out        device fp32 [sum ntok][Hq][D] (written)
  *   lse        device fp32 [sum ntok][Hq] (written) or null
  *   workspace  device, 256-byte aligned, >= treepo_prefill_workspace_size for
- *              the same arguments; the call uploads its tile tables there
+ *              the same arguments; the call uploads its work items, tile
+ *              tables and per-XCD schedule there
  *              (contents need not be preserved between calls, but a call's
  *              kernels read it until they finish on stream).
  * Validation as treepo_kv_append, plus EINVAL (a node twice in one call, null

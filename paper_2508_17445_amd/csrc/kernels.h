@@ -76,7 +76,7 @@ struct PrefillItem {
   int32_t pos0;      // chain position of the item's first token
   int32_t tile_off;  // first tile record of the sequence's chain
   int32_t nk;        // tiles the item streams: those starting at or before its last token
-  int32_t pad[3];
+  int32_t pad[3];    // pad[0]: the item's sequence (host scheduling only)
 };
 struct PrefillArgs {
   const uint16_t* k_pool;
@@ -87,6 +87,8 @@ struct PrefillArgs {
   const PrefillItem* items;  // n_items, longest first
   int32_t n_items;
   const int2* tiles;
+  const int32_t* sched;      // [slot * 8 + xcd] -> unit = item * Hkv + KV head, or -1
+  int32_t n_sched;           // a multiple of 8
   float scale_log2;
   float* out;                // fp32 [rows][Hq][D]
   float* lse;                // fp32 [rows][Hq] or null

@@ -892,11 +892,12 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
 // full take the unmasked path; the others mask keys past each row's own
 // position and, at a node's end, past the tile's tokens.
 //
-// Work order: unit u = (item, KV head) in the host's longest-first item
-// order.  Workgroup w runs on XCD w % 8; its index s = w / 8 on that XCD
-// splits into u = (s / G) * 8 + w % 8 and head h = g G + s % G, so the G
-// query heads of one KV head run on one XCD at about the same time and read
-// the same K/V tiles through its L2.
+// Work order: a unit is (item, KV head); the host lists each XCD's units,
+// longest first, keeping a sequence's units for one KV head on one XCD where
+// the balance allows.  Workgroup w runs on XCD x = w % 8; its index s = w / 8
+// on that XCD gives slot s / G of the schedule and head h = g G + s % G, so
+// the G query heads of a unit run on one XCD at about the same time and the
+// chain's K/V tiles are reused through that XCD's L2.
 // The prefill's tile loads: a 32-token tile is 2 D / 16 slots of 1 KiB (K
 // rows, then V^T rows, swizzled as for the decode); each of the W waves
 // issues D / (8 W) of them per tile, one 16-byte global->LDS load per lane
@@ -954,8 +955,9 @@ struct PfPipe {
 template <int D, int W>
 __global__ __launch_bounds__(64 * W, W / 2) void prefill_kernel(
     const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, const uint16_t* __restrict__ q,
-    const PrefillItem* __restrict__ items, const int2* __restrict__ tiles, float* __restrict__ out,
-    float* __restrict__ lse, int32_t n_units, int32_t num_blocks, int32_t hq, int32_t hkv, float scale_log2) {
+    const PrefillItem* __restrict__ items, const int2* __restrict__ tiles, const int32_t* __restrict__ sched,
+    float* __restrict__ out, float* __restrict__ lse, int32_t n_sched, int32_t num_blocks, int32_t hq, int32_t hkv,
+    float scale_log2) {
   constexpr int kKS = D / 32;  // QK k-steps
   constexpr int kDB = D / 16;  // PV output d-blocks
   constexpr int kRB = 8 / W;   // 16-row blocks per wave
@@ -966,8 +968,10 @@ __global__ __launch_bounds__(64 * W, W / 2) void prefill_kernel(
   const int G = hq / hkv;
   const int wg = blockIdx.x;
   const int s_x = wg >> 3;
-  const int unit = (s_x / G) * 8 + (wg & 7);
-  if (unit >= n_units) return;  // whole workgroup
+  const int slot = (s_x / G) * 8 + (wg & 7);
+  if (slot >= n_sched) return;  // whole workgroup
+  const int unit = sched[slot];
+  if (unit < 0) return;
   const int item_i = unit / hkv;
   const int g = unit - item_i * hkv;
   const int h = g * G + s_x % G;
@@ -1090,18 +1094,26 @@ __global__ __launch_bounds__(64 * W, W / 2) void prefill_kernel(
       P[rb] = make_uint4(p0.x, p0.y, p1.x, p1.y);
       PL[rb] = make_uint4(pl0.x, pl0.y, pl1.x, pl1.y);
     }
+    // one test per tile (not per d-block), so that the common full tile
+    // issues its V reads together and its MFMAs back to back
+    uint4 va[kDB];
 #pragma unroll
     for (int db = 0; db < kDB; ++db) {
       const int d = 16 * db + r16;
-      uint4 va = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
-      if (cnt < kSub) {
-        const uint2 lo = mask_v4(make_uint2(va.x, va.y), 8 * a, cnt);
-        const uint2 hi = mask_v4(make_uint2(va.z, va.w), 8 * a + 4, cnt);
-        va = make_uint4(lo.x, lo.y, hi.x, hi.y);
-      }
-#pragma unroll
-      for (int rb = 0; rb < kRB; ++rb) acc[rb][db] = mfma16(va, PL[rb], mfma16(va, P[rb], acc[rb][db]));
+      va[db] = *reinterpret_cast<const uint4*>(vt + d * (kSub * 2) + ((a ^ v_swz(d)) << 4));
     }
+    if (cnt < kSub) {
+#pragma unroll
+      for (int db = 0; db < kDB; ++db) {
+        const uint2 lo = mask_v4(make_uint2(va[db].x, va[db].y), 8 * a, cnt);
+        const uint2 hi = mask_v4(make_uint2(va[db].z, va[db].w), 8 * a + 4, cnt);
+        va[db] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+    }
+#pragma unroll
+    for (int db = 0; db < kDB; ++db)
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) acc[rb][db] = mfma16(va[db], PL[rb], mfma16(va[db], P[rb], acc[rb][db]));
   };
 
   // Software pipeline: iteration k scores tile k + 1 (its K) while it turns
@@ -1209,19 +1221,19 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
   if (a.hkv <= 0 || a.hq % a.hkv != 0 || (a.d != 64 && a.d != 128)) return hipErrorInvalidValue;
-  const int64_t units = static_cast<int64_t>(a.n_items) * a.hkv;
+  if (a.n_sched <= 0 || a.n_sched % 8 != 0) return hipErrorInvalidValue;
   const int64_t group = a.hq / a.hkv;
-  const int64_t wgs = (units + 7) / 8 * 8 * group;
+  const int64_t wgs = static_cast<int64_t>(a.n_sched) * group;
   if (wgs > 0x7FFFFFFF || 2 * a.hkv * a.num_blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(wgs));
   const int32_t nb = static_cast<int32_t>(a.num_blocks);
   const dim3 block(64 * kPrefillWaves);
   if (a.d == 128)
     launch_timed_block(a, prefill_kernel<128, kPrefillWaves>, grid, block, s, a.k_pool, a.v_pool, a.q, a.items,
-                       a.tiles, a.out, a.lse, static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
+                       a.tiles, a.sched, a.out, a.lse, a.n_sched, nb, a.hq, a.hkv, a.scale_log2);
   else
     launch_timed_block(a, prefill_kernel<64, kPrefillWaves>, grid, block, s, a.k_pool, a.v_pool, a.q, a.items,
-                       a.tiles, a.out, a.lse, static_cast<int32_t>(units), nb, a.hq, a.hkv, a.scale_log2);
+                       a.tiles, a.sched, a.out, a.lse, a.n_sched, nb, a.hq, a.hkv, a.scale_log2);
   return hipGetLastError();
 }
 

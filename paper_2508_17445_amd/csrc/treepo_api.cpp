@@ -702,8 +702,41 @@ int32_t append_validated(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
 struct PrefillPlan {
   std::vector<treepo::PrefillItem> items;
   std::vector<int32_t> tiles;  // int2 records
-  size_t tiles_off = 0, bytes = 0;
+  std::vector<int32_t> sched;  // [slot * 8 + xcd] -> unit (item * Hkv + KV head), or -1
+  size_t tiles_off = 0, sched_off = 0, bytes = 0;
 };
+
+// Units (item, KV head) onto the 8 XCDs, longest first: a unit goes to the
+// XCD that already holds its (sequence, KV head), so that the chain's tiles
+// stay in that XCD's L2, unless that XCD would pass an even share of the
+// work by more than 5%; then to the least loaded XCD.  Slot p of XCD x runs
+// the p-th unit assigned to it.
+void schedule_prefill(PrefillPlan* pl, int32_t hkv, int32_t n_seq) {
+  constexpr int kX = 8;
+  double total = 0;
+  for (const auto& it : pl->items) total += static_cast<double>(it.nk) * hkv;
+  const double cap = total / kX * 1.05;
+  std::vector<double> load(kX, 0.0);
+  std::vector<int32_t> home(static_cast<size_t>(n_seq) * hkv, -1);
+  std::vector<std::vector<int32_t>> lists(kX);
+  for (size_t i = 0; i < pl->items.size(); ++i) {
+    const auto& it = pl->items[i];
+    for (int32_t g = 0; g < hkv; ++g) {
+      int32_t& h = home[static_cast<size_t>(it.pad[0]) * hkv + g];
+      int x = h;
+      if (x < 0 || load[x] + it.nk > cap)
+        x = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+      if (h < 0) h = x;
+      load[x] += it.nk;
+      lists[x].push_back(static_cast<int32_t>(i) * hkv + g);
+    }
+  }
+  size_t depth = 0;
+  for (const auto& l : lists) depth = std::max(depth, l.size());
+  pl->sched.assign(depth * kX, -1);
+  for (int x = 0; x < kX; ++x)
+    for (size_t p = 0; p < lists[x].size(); ++p) pl->sched[p * kX + x] = lists[x][p];
+}
 
 int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
                            PrefillPlan* pl) {
@@ -712,8 +745,10 @@ int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, con
   std::vector<int32_t> chain;
   std::vector<int32_t> firsts;
   int64_t row = 0;
+  int32_t n_seq = 0;
   for (int32_t i = 0; i < n; ++i) {
     if (ntok[i] == 0) continue;
+    ++n_seq;
     const int32_t x = nodes[i];
     ctx->tree.chain(x, &chain);
     const int64_t pos0 = ctx->tree.chain_tokens(x);
@@ -739,6 +774,7 @@ int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, con
       it.tile_off = tile_off;
       const int32_t last = it.pos0 + it.n_rows - 1;
       it.nk = static_cast<int32_t>(std::upper_bound(firsts.begin(), firsts.end(), last) - firsts.begin());
+      it.pad[0] = n_seq - 1;  // sequence index, for the XCD schedule
       pl->items.push_back(it);
     }
     row += ntok[i];
@@ -746,9 +782,11 @@ int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, con
   if (row >= (int64_t{1} << 31) / 64) return fail(ctx, TREEPO_EINVAL, "too many prefill rows");
   std::stable_sort(pl->items.begin(), pl->items.end(),
                    [](const treepo::PrefillItem& a, const treepo::PrefillItem& b) { return a.nk > b.nk; });
+  schedule_prefill(pl, ctx->cfg.num_kv_heads, n_seq);
   const size_t ib = pl->items.size() * sizeof(treepo::PrefillItem);
   pl->tiles_off = (ib + 255) / 256 * 256;
-  pl->bytes = std::max<size_t>(256, pl->tiles_off + pl->tiles.size() * sizeof(int32_t));
+  pl->sched_off = (pl->tiles_off + pl->tiles.size() * sizeof(int32_t) + 255) / 256 * 256;
+  pl->bytes = std::max<size_t>(256, pl->sched_off + pl->sched.size() * sizeof(int32_t));
   return TREEPO_OK;
 }
 
@@ -810,6 +848,7 @@ int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const i
   std::vector<char> blob(pl.bytes, 0);
   std::memcpy(blob.data(), pl.items.data(), pl.items.size() * sizeof(treepo::PrefillItem));
   std::memcpy(blob.data() + pl.tiles_off, pl.tiles.data(), pl.tiles.size() * sizeof(int32_t));
+  std::memcpy(blob.data() + pl.sched_off, pl.sched.data(), pl.sched.size() * sizeof(int32_t));
   hipError_t e = upload(ctx, wsb, blob.data(), blob.size(), stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "prefill table upload");
   treepo::PrefillArgs a;
@@ -823,6 +862,8 @@ int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const i
   a.items = reinterpret_cast<const treepo::PrefillItem*>(wsb);
   a.n_items = static_cast<int32_t>(pl.items.size());
   a.tiles = reinterpret_cast<const int2*>(wsb + pl.tiles_off);
+  a.sched = reinterpret_cast<const int32_t*>(wsb + pl.sched_off);
+  a.n_sched = static_cast<int32_t>(pl.sched.size());
   a.scale_log2 = scale * 1.44269504088896340736f;
   a.out = out;
   a.lse = lse;
