@@ -169,7 +169,9 @@ int32_t treepo_kv_append(treepo_ctx* ctx, int32_t n, const int32_t* nodes,
  *              kernels read it until they finish on stream).
  * Validation as treepo_kv_append, plus EINVAL (a node twice in one call, null
  * q/k/v/out or bad scale with tokens, a chain of 2^25 tokens or more) and
- * EWORKSPACE.  Nothing is changed on error.  Enqueued on stream. */
+ * EWORKSPACE; a call that fails validation changes nothing.  EHIP (a failed
+ * upload or launch) comes after the append was enqueued: the lengths have
+ * advanced and the out/lse contents are undefined.  Enqueued on stream. */
 int32_t treepo_prefill_workspace_size(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok,
                                       size_t* bytes);
 int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const int32_t* ntok, const void* q,
