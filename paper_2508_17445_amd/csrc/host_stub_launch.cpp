@@ -11,6 +11,10 @@ hipError_t launch_combine(const DecodeArgs&, hipStream_t) { return hipErrorNoDev
 int32_t partial_workgroups_per_cu() { return 2; }
 hipError_t launch_advantage(const AdvantageArgs&, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_prefill(const PrefillArgs&, hipStream_t) { return hipErrorNoDevice; }
+hipError_t launch_kv_append_dev(const uint16_t*, const uint16_t*, uint16_t*, uint16_t*, int64_t, int32_t, int32_t,
+                                const AppendPiece*, int32_t, const int2*, int32_t, int32_t*, hipStream_t) {
+  return hipErrorNoDevice;
+}
 hipError_t launch_kv_append(const uint16_t*, const uint16_t*, uint16_t*, uint16_t*, int64_t, int32_t, int32_t,
                             const AppendPiece*, int32_t, const int32_t*, const int32_t*, int32_t, int32_t*,
                             hipStream_t) {

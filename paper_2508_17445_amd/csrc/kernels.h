@@ -111,5 +111,11 @@ hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16
                             uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
                             const AppendPiece* pieces, int32_t n_pieces, const int32_t* upd_node,
                             const int32_t* upd_len, int32_t n_upd, int32_t* node_len, hipStream_t s);
+// The same with pieces and updates (x = node, y = length) in device memory,
+// in one launch.
+hipError_t launch_kv_append_dev(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool, uint16_t* v_pool,
+                                int64_t num_blocks, int32_t hkv, int32_t d, const AppendPiece* pieces,
+                                int32_t n_pieces, const int2* upd, int32_t n_upd, int32_t* node_len,
+                                hipStream_t s);
 
 }  // namespace treepo

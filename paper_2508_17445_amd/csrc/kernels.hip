@@ -840,19 +840,14 @@ struct AppendBatch {
   int2 upd[kMaxPieces];
 };
 
+// One block-aligned piece for KV head blockIdx.y: K rows copied with 16-byte
+// moves, V transposed through padded LDS into the pool's [D][32] half blocks.
 template <int D>
-__global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __restrict__ ksrc,
-                                                             const uint16_t* __restrict__ vsrc,
-                                                             uint16_t* __restrict__ kpool,
-                                                             uint16_t* __restrict__ vpool,
-                                                             int64_t num_blocks, int32_t hkv,
-                                                             int32_t* __restrict__ node_len, AppendBatch b) {
+__device__ __forceinline__ void append_piece(const uint16_t* __restrict__ ksrc, const uint16_t* __restrict__ vsrc,
+                                             uint16_t* __restrict__ kpool, uint16_t* __restrict__ vpool,
+                                             int64_t num_blocks, int32_t hkv, const AppendPiece& pc,
+                                             uint16_t* vt) {
   constexpr int kPad = D + 2;
-  __shared__ uint16_t vt[kTile * kPad];
-  if (node_len != nullptr && blockIdx.y == 0 && threadIdx.x == 0 && static_cast<int>(blockIdx.x) < b.n_upd)
-    node_len[b.upd[blockIdx.x].x] = b.upd[blockIdx.x].y;
-  if (static_cast<int>(blockIdx.x) >= b.n) return;
-  const AppendPiece pc = b.p[blockIdx.x];
   const int g = blockIdx.y;
   const int64_t blk = static_cast<int64_t>(g) * num_blocks + pc.block;
   constexpr int kCh = D / 8;
@@ -875,6 +870,38 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
     const int p = pc.off + i;  // token within the 64-token block
     vpool[(blk * kTile + (p / kSub) * kSub) * D + d * kSub + (p % kSub)] = vt[i * kPad + d];
   }
+}
+
+// Pieces and length updates passed by value (up to kMaxPieces per launch).
+template <int D>
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __restrict__ ksrc,
+                                                             const uint16_t* __restrict__ vsrc,
+                                                             uint16_t* __restrict__ kpool,
+                                                             uint16_t* __restrict__ vpool,
+                                                             int64_t num_blocks, int32_t hkv,
+                                                             int32_t* __restrict__ node_len, AppendBatch b) {
+  __shared__ uint16_t vt[kTile * (D + 2)];
+  if (node_len != nullptr && blockIdx.y == 0 && threadIdx.x == 0 && static_cast<int>(blockIdx.x) < b.n_upd)
+    node_len[b.upd[blockIdx.x].x] = b.upd[blockIdx.x].y;
+  if (static_cast<int>(blockIdx.x) >= b.n) return;
+  append_piece<D>(ksrc, vsrc, kpool, vpool, num_blocks, hkv, b.p[blockIdx.x], vt);
+}
+
+// The same with the pieces and length updates in device memory: one launch
+// for any number of pieces.
+template <int D>
+__global__ __launch_bounds__(kThreads) void kv_append_dev_kernel(
+    const uint16_t* __restrict__ ksrc, const uint16_t* __restrict__ vsrc, uint16_t* __restrict__ kpool,
+    uint16_t* __restrict__ vpool, int64_t num_blocks, int32_t hkv, int32_t* __restrict__ node_len,
+    const AppendPiece* __restrict__ pieces, int32_t n, const int2* __restrict__ upd, int32_t n_upd) {
+  __shared__ uint16_t vt[kTile * (D + 2)];
+  if (node_len != nullptr && blockIdx.y == 0 && threadIdx.x == 0 && static_cast<int>(blockIdx.x) < n_upd) {
+    const int2 u = upd[blockIdx.x];
+    node_len[u.x] = u.y;
+  }
+  if (static_cast<int>(blockIdx.x) >= n) return;
+  const AppendPiece pc = pieces[blockIdx.x];
+  append_piece<D>(ksrc, vsrc, kpool, vpool, num_blocks, hkv, pc, vt);
 }
 
 
@@ -1234,6 +1261,23 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
   else
     launch_timed_block(a, prefill_kernel<64, kPrefillWaves>, grid, block, s, a.k_pool, a.v_pool, a.q, a.items,
                        a.tiles, a.sched, a.out, a.lse, a.n_sched, nb, a.hq, a.hkv, a.scale_log2);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append_dev(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool, uint16_t* v_pool,
+                                int64_t num_blocks, int32_t hkv, int32_t d, const AppendPiece* pieces,
+                                int32_t n_pieces, const int2* upd, int32_t n_upd, int32_t* node_len,
+                                hipStream_t s) {
+  if (node_len == nullptr) n_upd = 0;
+  const int32_t gx = n_pieces > n_upd ? n_pieces : n_upd;
+  if (gx <= 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(hkv));
+  if (d == 128)
+    kv_append_dev_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len,
+                                                       pieces, n_pieces, upd, n_upd);
+  else
+    kv_append_dev_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len,
+                                                      pieces, n_pieces, upd, n_upd);
   return hipGetLastError();
 }
 

@@ -703,7 +703,9 @@ struct PrefillPlan {
   std::vector<treepo::PrefillItem> items;
   std::vector<int32_t> tiles;  // int2 records
   std::vector<int32_t> sched;  // [slot * 8 + xcd] -> unit (item * Hkv + KV head), or -1
-  size_t tiles_off = 0, sched_off = 0, bytes = 0;
+  std::vector<treepo::AppendPiece> pieces;  // the append, uploaded with the tables
+  std::vector<int32_t> upd;                 // int2 (node, new length) per appended node
+  size_t tiles_off = 0, sched_off = 0, pieces_off = 0, upd_off = 0, bytes = 0;
 };
 
 // Units (item, KV head) onto the 8 XCDs, longest first: a unit goes to the
@@ -783,10 +785,18 @@ int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, con
   std::stable_sort(pl->items.begin(), pl->items.end(),
                    [](const treepo::PrefillItem& a, const treepo::PrefillItem& b) { return a.nk > b.nk; });
   schedule_prefill(pl, ctx->cfg.num_kv_heads, n_seq);
-  const size_t ib = pl->items.size() * sizeof(treepo::PrefillItem);
-  pl->tiles_off = (ib + 255) / 256 * 256;
-  pl->sched_off = (pl->tiles_off + pl->tiles.size() * sizeof(int32_t) + 255) / 256 * 256;
-  pl->bytes = std::max<size_t>(256, pl->sched_off + pl->sched.size() * sizeof(int32_t));
+  std::vector<std::pair<int32_t, int32_t>> upd;
+  append_pieces(ctx->tree, n, nodes, ntok, &pl->pieces, &upd);
+  for (const auto& u : upd) {
+    pl->upd.push_back(u.first);
+    pl->upd.push_back(u.second);
+  }
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  pl->tiles_off = up(pl->items.size() * sizeof(treepo::PrefillItem));
+  pl->sched_off = up(pl->tiles_off + pl->tiles.size() * sizeof(int32_t));
+  pl->pieces_off = up(pl->sched_off + pl->sched.size() * sizeof(int32_t));
+  pl->upd_off = up(pl->pieces_off + pl->pieces.size() * sizeof(treepo::AppendPiece));
+  pl->bytes = std::max<size_t>(256, pl->upd_off + pl->upd.size() * sizeof(int32_t));
   return TREEPO_OK;
 }
 
@@ -842,15 +852,26 @@ int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const i
   if (!workspace || ws_bytes < pl.bytes || reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
     return fail(ctx, TREEPO_EWORKSPACE,
                 "workspace missing, smaller than treepo_prefill_workspace_size or not 256-byte aligned");
-  st = append_validated(ctx, n, nodes, ntok, k, v, stream);
-  if (st != TREEPO_OK) return st;
   char* wsb = static_cast<char*>(workspace);
   std::vector<char> blob(pl.bytes, 0);
   std::memcpy(blob.data(), pl.items.data(), pl.items.size() * sizeof(treepo::PrefillItem));
   std::memcpy(blob.data() + pl.tiles_off, pl.tiles.data(), pl.tiles.size() * sizeof(int32_t));
   std::memcpy(blob.data() + pl.sched_off, pl.sched.data(), pl.sched.size() * sizeof(int32_t));
+  std::memcpy(blob.data() + pl.pieces_off, pl.pieces.data(), pl.pieces.size() * sizeof(treepo::AppendPiece));
+  std::memcpy(blob.data() + pl.upd_off, pl.upd.data(), pl.upd.size() * sizeof(int32_t));
   hipError_t e = upload(ctx, wsb, blob.data(), blob.size(), stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "prefill table upload");
+  // the append: every piece in one launch, from the uploaded tables
+  e = timed_launch(ctx, TREEPO_KERNEL_APPEND, stream, [&] {
+    return treepo::launch_kv_append_dev(
+        static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), static_cast<uint16_t*>(ctx->cfg.k_pool),
+        static_cast<uint16_t*>(ctx->cfg.v_pool), ctx->cfg.num_blocks, ctx->cfg.num_kv_heads, ctx->cfg.head_dim,
+        reinterpret_cast<const treepo::AppendPiece*>(wsb + pl.pieces_off), static_cast<int32_t>(pl.pieces.size()),
+        reinterpret_cast<const int2*>(wsb + pl.upd_off), static_cast<int32_t>(pl.upd.size() / 2),
+        static_cast<int32_t*>(ctx->cfg.node_len), stream);
+  });
+  if (e != hipSuccess) return hip_fail(ctx, e, "prefill append launch");
+  ctx->tree.apply_append(n, nodes, ntok);
   treepo::PrefillArgs a;
   a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
   a.v_pool = static_cast<const uint16_t*>(ctx->cfg.v_pool);

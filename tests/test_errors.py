@@ -138,17 +138,18 @@ def test_advantage_codes():
 def test_prefill_codes_and_workspace_layout():
     """Prefill validation happens before any device work; the workspace holds
     32-byte work items (up to 128 tokens each), then 8-byte tile records of
-    every chain (32 tokens each), then the XCD schedule (8 int32 per slot),
-    each part at a 256-byte boundary."""
+    every chain (32 tokens each), the XCD schedule (8 int32 per slot), the
+    append's 16-byte block pieces and its 8-byte length updates, each part at
+    a 256-byte boundary."""
     ctx = host_ctx(num_blocks=40, max_nodes=8)
     r = ctx.new_root(300)
-    # 3 items (10, 8 and 4 tiles: one XCD each, one slot); 10 tiles
-    assert ctx.prefill_workspace_size([r], [300]) == 256 + 256 + 8 * 4
+    # 3 items (10, 8 and 4 tiles: one XCD each, one slot); 10 tiles; 5 pieces; 1 update
+    assert ctx.prefill_workspace_size([r], [300]) == 256 + 256 + 256 + 256 + 8
     assert ctx.prefill_workspace_size([r], [0]) == 256
     ctx.kv_commit([r], [100])
     a, b = ctx.fork(r, 2, 200)
-    # a: chain 100 + 129 tokens -> 4 + 5 tiles; 2 items.  b: 100 + 1 -> 4 + 1 tiles; 1 item
-    assert ctx.prefill_workspace_size([a, b], [129, 1]) == 256 + 256 + 8 * 4
+    # a: chain 100 + 129 tokens -> 4 + 5 tiles, 2 items, 3 pieces.  b: 100 + 1 -> 4 + 1 tiles, 1 item, 1 piece
+    assert ctx.prefill_workspace_size([a, b], [129, 1]) == 256 + 256 + 256 + 256 + 2 * 8
     snap = ctx.export_nodes().copy()
     F = FAKE_POOL
     assert _code(ctx.prefill, [a, a], [1, 1], F, F, F, 0.1, F, None, F, 1 << 20) == T.EINVAL   # a node twice
