@@ -172,3 +172,23 @@ def test_prefill_then_segment_decode_with_device_lengths():
         err = float(np.abs(o.cpu().numpy() - ref).max())
         print(f"[prefill live decode {step}] max|out-oracle|={err:.3e}", flush=True)
         assert err <= TOL and float(np.abs(l.cpu().numpy() - ref_l).max()) <= TOL
+
+
+def test_prefill_after_a_cut():
+    """A prompt cut inside (fork_at): its tail keeps growing (a prefill into
+    the tail attends to the whole prompt), and the branches forked at the cut
+    attend to the kept prefix only."""
+    hq, hkv, d = 28, 4, 128
+    rig = _Rig(hq, hkv, d, 777, num_blocks=200)
+    r = rig.ctx.new_root(400)
+    assert rig.model.new_root(400) == r
+    qb, out, lse = rig.prefill([r], [300], 0)
+    rig.check([r], [300], qb, out, lse, "cut: prompt")
+    kids, t = rig.ctx.fork_at(r, 128, 2, 100)
+    assert rig.model.fork_at(r, 128, 2, 100) == (kids, t)
+    k, v = rig.kv[r]
+    rig.kv[t] = (k[128:], v[128:])
+    rig.kv[r] = (k[:128], v[:128])
+    nodes, ntok = [t] + kids, [50, 30, 70]
+    qb, out, lse = rig.prefill(nodes, ntok, 1)
+    rig.check(nodes, ntok, qb, out, lse, "cut: tail and branches")
