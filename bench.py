@@ -11,14 +11,16 @@ rotate over them, so that no step finds its KV in the 256 MB Infinity Cache
 (the whole working set of this tree is ~200 MB).  W untimed warm-up steps,
 then exactly K timed steps between two device synchronisations (after half
 a second of untimed steps in both modes, so that the GPU's clocks have
-settled before the first timed mode).  The library
-brackets every kernel launch with HIP events on the launch stream during the
-timed region, which gives the dominant kernel's average duration.  The same
-protocol times the per-leaf paged-decode baseline, and a streaming-read probe
-gives the attainable HBM read bandwidth.  The fp64 oracle is timed on the
-host cores on the same workload.
+settled before the first timed mode).  A second pass of the K steps runs
+with library profiling on: every launch records HIP events at its kernel's
+own start and end, which gives the dominant kernel's average duration.  The
+same protocol times the per-leaf paged-decode baseline, and a streaming-read
+probe gives the attainable HBM read bandwidth.  The fp64 oracle is timed on
+the host cores on the same workload.
 
-Prints one JSON line.
+Other modes: ``--config N`` (another workload), ``--segment-loop``
+(segment-level decoding over several layers), ``--advantage`` (the TreePO
+advantage) and ``--prefill`` (prompt prefill).  Prints one JSON line.
 """
 
 from __future__ import annotations
