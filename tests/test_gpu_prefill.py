@@ -192,3 +192,16 @@ def test_prefill_after_a_cut():
     nodes, ntok = [t] + kids, [50, 30, 70]
     qb, out, lse = rig.prefill(nodes, ntok, 1)
     rig.check(nodes, ntok, qb, out, lse, "cut: tail and branches")
+
+
+def test_prefill_is_deterministic():
+    """The same call on two identical trees gives bitwise identical rows."""
+    lens = [300, 129, 1]
+    res = []
+    for _ in range(2):
+        rig = _Rig(28, 4, 128, 999, num_blocks=40)
+        roots = [rig.ctx.new_root(n) for n in lens]
+        for n in lens:
+            rig.model.new_root(n)
+        res.append(rig.prefill(roots, lens, 0)[1:])
+    assert np.array_equal(res[0][0], res[1][0]) and np.array_equal(res[0][1], res[1][1])

@@ -128,3 +128,23 @@ def test_prefill_mutation_caught(kind, monkeypatch):
         except (AssertionError, ValueError, IndexError):
             failed += 1
     assert failed >= 1
+
+
+def test_chunking_does_not_change_the_result():
+    """Prefilling a prompt in two calls gives the rows of one call: causal
+    attention of a token depends only on the chain up to it."""
+    hq, hkv, d = 4, 2, 16
+    kv_bits = node_kv_bits(SEED + 1, 0, 90, hkv, d)
+    q = query_bits(SEED + 1, 0, 90, hq, d)
+    one = M.TreeModel(8, 100, 10)
+    r = one.new_root(90)
+    one.append([r], [90])
+    o1, l1 = P.prefill(one, lambda n: kv_bits, [r], [90], q, 0.3)
+    two = M.TreeModel(8, 100, 10)
+    r2 = two.new_root(90)
+    two.append([r2], [55])
+    kv55 = (kv_bits[0][:55], kv_bits[1][:55])
+    oa, la = P.prefill(two, lambda n: kv55, [r2], [55], q[:55], 0.3)
+    two.append([r2], [35])
+    ob, lb = P.prefill(two, lambda n: kv_bits, [r2], [35], q[55:], 0.3)
+    assert np.array_equal(np.concatenate([oa, ob]), o1) and np.array_equal(np.concatenate([la, lb]), l1)
