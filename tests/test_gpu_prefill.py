@@ -205,3 +205,23 @@ def test_prefill_is_deterministic():
             rig.model.new_root(n)
         res.append(rig.prefill(roots, lens, 0)[1:])
     assert np.array_equal(res[0][0], res[1][0]) and np.array_equal(res[0][1], res[1][1])
+
+
+def test_prefill_without_lse():
+    """lse may be null: out is the same as with it."""
+    import torch
+    lens = [200, 33]
+    outs = []
+    for with_lse in (True, False):
+        rig = _Rig(8, 2, 64, 4321, num_blocks=20)
+        roots = [rig.ctx.new_root(n) for n in lens]
+        k, v = zip(*(node_kv_bits(rig.seed, x, n, 2, 64) for x, n in zip(roots, lens)))
+        q = query_bits(rig.seed, 0, sum(lens), 8, 64)
+        out = torch.empty((sum(lens), 8, 64), dtype=torch.float32, device="cuda")
+        lse = torch.empty((sum(lens), 8), dtype=torch.float32, device="cuda") if with_lse else None
+        ws = torch.empty(rig.ctx.prefill_workspace_size(roots, lens), dtype=torch.uint8, device="cuda")
+        rig.ctx.prefill(roots, lens, rig.dev(q), rig.dev(np.concatenate(k)), rig.dev(np.concatenate(v)), rig.scale,
+                        out, lse, ws)
+        torch.cuda.synchronize()
+        outs.append(out.cpu().numpy())
+    assert np.array_equal(outs[0], outs[1])
