@@ -19,8 +19,20 @@
  *     A failing call changes no state (arguments are validated before anything
  *     is mutated).  No C++ exception crosses this boundary.
  *   - "host" pointers are ordinary CPU memory read during the call; "device"
- *     pointers are HIP device memory owned by the caller (the library never
- *     allocates device memory; it allocates pinned host staging for uploads).
+ *     pointers are HIP device memory owned by the caller: pools, queries, K/V
+ *     staging, outputs and workspaces.
+ *   - Ownership rule: the library allocates device memory for one thing only,
+ *     the device image of each cached decode plan (its stream blocks and
+ *     combine counts).  treepo_tree_decode / treepo_paged_decode_naive
+ *     allocate it with hipMalloc on the first decode with a plan that finds
+ *     no retired image large enough, reuse it while the plan stays cached,
+ *     and free it in treepo_destroy (or when a later plan replaces it and its
+ *     last reader has finished).  The image must outlive the calls that read
+ *     it, and caller memory cannot promise that: a caching allocator hands a
+ *     freed workspace to other tensors (and to other contexts) between
+ *     calls, and a plan read from overwritten memory would send the kernels
+ *     to arbitrary pool offsets.  Every other call allocates no device
+ *     memory.  The library also allocates pinned host staging for uploads.
  *   - Device work is enqueued on the caller's stream and is asynchronous; the
  *     node table is host state updated synchronously at call time.  A context
  *     is single-threaded, and its device work must be issued on one stream at a
@@ -96,11 +108,21 @@ typedef struct treepo_config {
 /* Node record exported by treepo_export_nodes: 8 int32 per node. */
 #define TREEPO_NODE_FIELDS 8 /* parent, depth, start, len, cap, block_begin, n_blocks, tree_id */
 
-/* Creates a context for one pool.  No device call is made.  *out receives the
- * handle; EINVAL / EUNSUPPORTED on a bad config. */
+/* Creates a context for one pool.  The only device call is a query of the
+ * current device's compute-unit count, which sizes the decode schedule (one
+ * stream per resident workgroup slot, XCDs of 32 compute units); with no
+ * device visible the planner assumes 256 compute units in 8 XCDs (MI355X).
+ * *out receives the handle; EINVAL / EUNSUPPORTED on a bad config. */
 int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out);
-/* Releases host state and pinned staging (waits for this context's pending
- * uploads).  Null is accepted. */
+
+/* Overrides the machine shape the decode planner sizes its streams for:
+ * compute_units (two resident workgroups each) and xcds (dies the workgroups
+ * are dealt to round robin).  Drops every cached plan.  EINVAL unless
+ * 1 <= xcds <= 8 and xcds <= compute_units <= 4096. */
+int32_t treepo_set_device_shape(treepo_ctx* ctx, int32_t compute_units, int32_t xcds);
+/* Releases host state, pinned staging and the plan images (waits for this
+ * context's pending uploads and for the last readers of its plan images).
+ * Null is accepted. */
 int32_t treepo_destroy(treepo_ctx* ctx);
 
 /* New tree: a root node (the query/prompt segment, depth 0, Sec. 2.2 item 1)
@@ -121,7 +143,7 @@ int32_t treepo_fork(treepo_ctx* ctx, int32_t parent, int32_t n_children,
                     int32_t child_cap, int32_t* children_out);
 
 /* Fallback inside a segment (Alg. 1 Fallback; Sec. 2.2 fallback at segment
- * level; Sec. 4.1 "misaligned fallback", a fallback granularity finer than
+ * level; Sec. 4.2 "misaligned fallback", a fallback granularity finer than
  * the segment): forks n_children (>= 0) children after the first `offset`
  * tokens of `node`.  The node keeps tokens [0, offset); a new tail node (the
  * next id, written to *tail_out) takes tokens [offset, len), the rest of the
@@ -209,10 +231,10 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
  * its descendant leaves' query rows (the nested sub-groups G_j of Sec. 2.3);
  * per-node partials are merged with a log-sum-exp combine.  The schedule
  * (plan) is cached per context (the last four leaf lists and modes) and its
- * device copy lives in memory the context allocates on the first decode with
- * it and frees in treepo_destroy; the workspace holds only this call's
- * partial results, so the caller may reuse it freely between calls (calls
- * that overlap on one workspace race).
+ * device image lives in memory the context allocates (see the ownership rule
+ * above); the workspace holds only this call's partial results, so the
+ * caller may reuse it freely between calls (calls that overlap on one
+ * workspace race).
  * EINVAL (bad id, null pointer, n_leaves < 1, q not 16-byte aligned, scale
  * not positive and finite),
  * EEMPTY (a chain holds no tokens), EWORKSPACE (missing, too small or not
@@ -256,7 +278,7 @@ int32_t treepo_branch_budget(int32_t n_paths, const float* scores, int32_t total
 
 /* Aggregations for treepo_tree_advantage. */
 #define TREEPO_ADV_MEAN 0           /* mean over sub-groups (Sec. 2.3, Eq. tree_ae)         */
-#define TREEPO_ADV_SIZE_WEIGHTED 1  /* |G_j|-weighted mean (Sec. 4.1, Eq. tree_ae_sgw)      */
+#define TREEPO_ADV_SIZE_WEIGHTED 1  /* |G_j|-weighted mean (Sec. 4.2, Eq. tree_ae_sgw)      */
 
 /* Workspace bytes that treepo_tree_advantage needs for these leaves. */
 int32_t treepo_advantage_workspace_size(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,

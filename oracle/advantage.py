@@ -2,7 +2,7 @@
 
 Nothing in the product path may import this module; it shares no code with
 the HIP library.  It follows TreePO Sec. 2.3 (Eq. groups, Eq. tree_ae) and
-the size-weighted variant of Sec. 4.1 (Eq. tree_ae_sgw), taking the steps in
+the size-weighted variant of Sec. 4.2 (Eq. tree_ae_sgw), taking the steps in
 the paper's order:
 
 1. A trajectory is a decoded leaf (one call position p, node leaves[p]); its

@@ -100,7 +100,7 @@ class TreeModel:
     def fork_at(self, node: int, offset: int, n: int, cap: int):
         """Fork n children from node `node` after its first `offset` tokens: a
         fallback that branches inside a segment (Sec. 2.2 fallback at segment
-        level; Sec. 4.1 "misaligned fallback" with a fallback granularity finer
+        level; Sec. 4.2 "misaligned fallback" with a fallback granularity finer
         than the segment).  The node keeps tokens [0, offset); a new tail node
         (the next id) takes tokens [offset, len), the rest of the node's
         capacity and blocks, and the node's children, so every existing

@@ -1,6 +1,6 @@
 // TreePO advantage over the rollout tree (TreePO Sec. 2.3, Eq. groups and
 // Eq. tree_ae; the sub-group-size weighted variant Eq. tree_ae_sgw of
-// Sec. 4.1), one workgroup, fp64 arithmetic:
+// Sec. 4.2), one workgroup, fp64 arithmetic:
 //   1. every sub-group's mean reward, and whether its rewards are all equal
 //      (a query whose group is all equal is rejected);
 //   2. every kept position's sub-group advantages R_p - mean(G_a) over its

@@ -62,7 +62,6 @@ struct AdvantageArgs {
   float* adv;              // [n_pos], device
 };
 hipError_t launch_advantage(const AdvantageArgs& a, hipStream_t s);
-constexpr int32_t kComputeUnits = 256;  // MI355X
 
 // Prefill: causal attention of tokens just appended to a node over its chain.
 // A work item is up to kPrefillRows consecutive new tokens of one sequence;

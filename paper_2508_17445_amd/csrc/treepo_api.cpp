@@ -26,6 +26,19 @@ constexpr size_t kAlign = 256;
 constexpr int kPlanCache = 4;
 constexpr int kRing = 4;
 
+// Machine shape when no device is visible (host-only use): MI355X, 256
+// compute units in 8 XCDs of 32.
+constexpr int32_t kDefaultComputeUnits = 256;
+constexpr int32_t kComputeUnitsPerXcd = 32;
+// Planner tunables, fitted to per-workgroup timestamps of back-to-back
+// config-2 decodes (16 leaves of 7680 tokens): the second workgroup on a CU
+// progressed about 0.80 as fast as the first (the dispatcher fills every CU's
+// first slot before any second one), and the odd-numbered XCDs streamed
+// 0.93-0.94 as many tiles per microsecond as the even ones on every box
+// measured.  Streams are sized in proportion to these speeds.
+constexpr double kSecondSlotSpeed = 0.80;
+constexpr double kOddXcdSpeed = 0.935;
+
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct CachedPlan {
@@ -546,6 +559,19 @@ void build_adv_plan(const treepo::Tree& t, int32_t n, const int32_t* leaves, Adv
   ap->ws_bytes = off;
 }
 
+// The machine the decode planner sizes its streams for: one stream per
+// resident workgroup slot (partial_workgroups_per_cu() per compute unit),
+// workgroups dealt to the XCDs round robin.
+void set_machine(treepo_ctx* ctx, int32_t compute_units, int32_t xcds) {
+  PlanParams& p = ctx->params;
+  p.compute_units = compute_units;
+  p.concurrent_wgs = compute_units * treepo::partial_workgroups_per_cu();
+  p.slot_speed[0] = 1.0;
+  p.slot_speed[1] = kSecondSlotSpeed;
+  p.xcds = xcds;
+  for (int x = 0; x < 8; ++x) p.xcd_speed[x] = x % 2 ? kOddXcdSpeed : 1.0;
+}
+
 int32_t check_ids(treepo_ctx* ctx, int32_t n, const int32_t* leaves) {
   if (n < 1 || !leaves) return fail(ctx, TREEPO_EINVAL, "need at least one leaf");
   for (int32_t i = 0; i < n; ++i)
@@ -577,18 +603,12 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
   ctx->params.head_dim = c.head_dim;
   ctx->params.num_blocks = c.num_blocks;
   ctx->params.max_rows = 128;
-  ctx->params.concurrent_wgs = treepo::kComputeUnits * treepo::partial_workgroups_per_cu();
-  // The second workgroup on a CU gets the smaller share of its issue and
-  // memory bandwidth (measured on config-2 decodes: about 0.80 of the first's
-  // progress over the same time).
-  ctx->params.compute_units = treepo::kComputeUnits;
-  ctx->params.slot_speed[0] = 1.0;
-  ctx->params.slot_speed[1] = 0.80;
-  // Workgroups are dealt to the eight XCDs round robin; the odd-numbered
-  // ones streamed about 0.93-0.94 as many tiles per microsecond as the even
-  // ones in per-workgroup timestamps of config-2 decodes.
-  ctx->params.xcds = 8;
-  for (int x = 0; x < 8; ++x) ctx->params.xcd_speed[x] = x % 2 ? 0.935 : 1.0;
+  int32_t cus = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    cus = kDefaultComputeUnits;
+  set_machine(ctx, cus, std::max(1, std::min(8, cus / kComputeUnitsPerXcd)));
   ctx->live = c.node_len != nullptr;
   ctx->params.live_lengths = ctx->live;
   *out = ctx;
@@ -612,6 +632,20 @@ int32_t treepo_destroy(treepo_ctx* ctx) {
   for (RetiredImage& r : ctx->retired) (void)free_retired(r);
   delete ctx;
   return TREEPO_OK;
+}
+
+int32_t treepo_set_device_shape(treepo_ctx* ctx, int32_t compute_units, int32_t xcds) {
+  if (!ctx) return TREEPO_EINVAL;
+  if (compute_units < 1 || compute_units > 4096 || xcds < 1 || xcds > 8 || compute_units < xcds)
+    return fail(ctx, TREEPO_EINVAL, "compute_units must be in [xcds, 4096] and xcds in [1, 8]");
+  hipError_t e = hipSuccess;
+  for (CachedPlan& cp : ctx->plans) {
+    const hipError_t r = retire_image(ctx, cp);
+    if (e == hipSuccess) e = r;
+  }
+  ctx->plans.clear();
+  set_machine(ctx, compute_units, xcds);
+  return e == hipSuccess ? TREEPO_OK : hip_fail(ctx, e, "plan cache");
 }
 
 int32_t treepo_new_root(treepo_ctx* ctx, int32_t cap_tokens, int32_t* node_out) {

@@ -61,6 +61,7 @@ def load_library(path: str = LIB_PATH):
     sig = {
         "treepo_create": (_i32, [ctypes.POINTER(Config), ctypes.POINTER(_p)]),
         "treepo_destroy": (_i32, [_p]),
+        "treepo_set_device_shape": (_i32, [_p, _i32, _i32]),
         "treepo_new_root": (_i32, [_p, _i32, _pi32]),
         "treepo_fork": (_i32, [_p, _i32, _i32, _i32, _pi32]),
         "treepo_fork_at": (_i32, [_p, _i32, _i32, _i32, _i32, _pi32, _pi32]),
@@ -160,6 +161,9 @@ class Context:
         if st != OK:
             msg = self.lib.treepo_last_error(self.h).decode() or self.lib.treepo_strerror(st).decode()
             raise TreePOError(st, f"{what}: {msg}")
+
+    def set_device_shape(self, compute_units: int, xcds: int):
+        self._check(self.lib.treepo_set_device_shape(self.h, compute_units, xcds), "treepo_set_device_shape")
 
     # ---- tree --------------------------------------------------------------
     def new_root(self, cap: int) -> int:

@@ -72,7 +72,23 @@ class _Log:
         self.ops, self.leaves, self.rows, self.step_append = ops, leaves, rows, None
 
 
+def _bf16_mp(bits: int):
+    """The value of one bf16 bit pattern from its IEEE fields (sign, 8-bit
+    biased exponent, 7-bit fraction), as an exact mpmath number: finite
+    patterns only.  Independent of the oracle's widening."""
+    import mpmath as mp
+    b = int(bits) & 0xFFFF
+    sign = -1 if b >> 15 else 1
+    e, f = (b >> 7) & 0xFF, b & 0x7F
+    assert e != 0xFF, "not a finite bf16"
+    if e == 0:
+        return sign * mp.ldexp(f, -133)          # subnormal: f * 2^-7 * 2^-126
+    return sign * mp.ldexp(128 + f, e - 134)     # (1 + f/128) * 2^(e - 127)
+
+
 def pin_bruteforce(seeds=(1, 2, 3, 4, 5, 6), hq=4, hkv=2, d=8, tol=1e-12):
+    """50-digit brute force from the definition; the bf16 inputs are widened
+    from their bit fields here, not by the oracle."""
     import mpmath as mp
     mp.mp.dps = 50
     for seed in seeds:
@@ -94,19 +110,17 @@ def pin_bruteforce(seeds=(1, 2, 3, 4, 5, 6), hq=4, hkv=2, d=8, tol=1e-12):
             kseq, vseq = [], []
             for n in path:
                 kb, vb = data[n]
-                kf = A.bf16_bits_to_f64(kb)
-                vf = A.bf16_bits_to_f64(vb)
                 for t in range(rows[n]):
-                    kseq.append(kf[t]); vseq.append(vf[t])
-            qf = A.bf16_bits_to_f64(q[pos])
+                    kseq.append([[_bf16_mp(kb[t, g, i]) for i in range(d)] for g in range(hkv)])
+                    vseq.append([[_bf16_mp(vb[t, g, i]) for i in range(d)] for g in range(hkv)])
+            qf = [[_bf16_mp(q[pos, h, i]) for i in range(d)] for h in range(hq)]
             for h in range(hq):
                 g = h // group
-                s = [mp.mpf(scale) * mp.fsum(mp.mpf(qf[h, i]) * mp.mpf(k[g, i]) for i in range(d))
-                     for k in kseq]
+                s = [mp.mpf(scale) * mp.fsum(qf[h][i] * k[g][i] for i in range(d)) for k in kseq]
                 e = [mp.exp(si) for si in s]
                 z = mp.fsum(e)
                 for i in range(d):
-                    o = mp.fsum(ei * mp.mpf(v[g, i]) for ei, v in zip(e, vseq)) / z
+                    o = mp.fsum(ei * v[g][i] for ei, v in zip(e, vseq)) / z
                     assert abs(float(o) - out[pos, h, i]) <= tol, (seed, pos, h, i)
                 assert abs(float(mp.log(z)) - lse[pos, h]) <= tol, (seed, pos, h)
 
@@ -274,6 +288,61 @@ def pin_lse_logsumexp(tol=1e-12):
         assert abs(lse[h] - logsumexp(0.5 * (k[:, 0] @ q[h]))) <= tol
 
 
+def pin_bf16_widening():
+    """The oracle's bf16 -> fp64 widening against torch's own conversion on
+    all 65,536 bit patterns (bit-exact on finite values, signed zeros
+    included; the same class on infinities and NaNs), and against values
+    written out from the IEEE bfloat16 format by hand."""
+    import torch
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):
+        mine = A.bf16_bits_to_f64(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    fin = np.isfinite(ref)
+    assert fin.sum() == 65536 - 2 * 2 ** 7   # exponent 0xFF: 2 infinities + 254 NaNs
+    assert np.array_equal(np.isfinite(mine), fin)
+    assert np.array_equal(mine[fin].view(np.uint64), ref[fin].view(np.uint64))
+    assert np.array_equal(np.isnan(mine), np.isnan(ref))
+    inf = np.isinf(ref)
+    assert inf.sum() == 2 and np.array_equal(mine[inf], ref[inf])
+    hand = {0x3F80: 1.0, 0xC000: -2.0, 0x3E80: 0.25, 0x4049: 3.140625, 0x0000: 0.0, 0x8000: -0.0,
+            0x0001: 2.0 ** -133, 0x807F: -127 * 2.0 ** -133, 0x0080: 2.0 ** -126,
+            0x7F7F: (2 - 2 ** -7) * 2.0 ** 127, 0x7F80: np.inf, 0xFF80: -np.inf}
+    got = A.bf16_bits_to_f64(np.array(list(hand), dtype=np.uint16))
+    for b, g in zip(hand, got):
+        want = hand[b]
+        assert g == want and np.signbit(g) == np.signbit(want), (hex(b), g, want)
+    with np.errstate(invalid="ignore"):
+        assert np.isnan(A.bf16_bits_to_f64(np.array([0x7FC0, 0xFFC1, 0x7F81], dtype=np.uint16))).all()
+    # finite patterns against the field decoding used by the brute force
+    import mpmath as mp
+    rng = np.random.default_rng(3)
+    for b in rng.integers(0, 1 << 16, size=400):
+        if (b >> 7) & 0xFF != 0xFF:
+            assert mp.mpf(A.bf16_bits_to_f64(np.array([b], dtype=np.uint16))[0]) == _bf16_mp(b), hex(b)
+
+
+def pin_positions_subset():
+    """A decode restricted to some call positions (used on the large
+    workloads) returns exactly those rows of the full decode, in the order
+    asked, duplicates and repeats included."""
+    hq, hkv, d = 6, 2, 16
+    for seed in (3, 8, 12):
+        ops, leaves, rows, _ = random_tiny_tree(seed, max_leaves=8)
+        if not leaves:
+            continue
+        log = _Log(ops, leaves, rows)
+        model = M.replay(log, B, 10_000, 10_000)
+        data = {n: node_kv_bits(200 + seed, n, max(rows[n], 1), hkv, d) for n in rows}
+        q = query_bits(200 + seed, 0, len(leaves), hq, d)
+        out, lse = A.tree_decode(model, lambda n: data[n], leaves, q, 0.3)
+        rng = np.random.default_rng(seed)
+        pos = [int(p) for p in rng.integers(0, len(leaves), size=len(leaves) + 3)][::-1]
+        o2, l2 = A.tree_decode(model, lambda n: data[n], leaves, q, 0.3, positions=pos)
+        assert o2.shape == (len(pos), hq, d)
+        assert np.array_equal(o2, out[pos]) and np.array_equal(l2, lse[pos])
+
+
 # ---- node-table closed forms ----------------------------------------------
 
 def pin_binary_heap_tiny():
@@ -360,7 +429,7 @@ def pin_structure_invariants(cfgs=(1, 2, 3, 4, 5)):
             assert nd["len"] == log.rows[n]
 
 
-ALL_PINS = [pin_bruteforce, pin_constant_keys, pin_single_key, pin_zero_query, pin_sdpa,
+ALL_PINS = [pin_bf16_widening, pin_positions_subset, pin_bruteforce, pin_constant_keys, pin_single_key, pin_zero_query, pin_sdpa,
             pin_identical_paths, pin_permutation, pin_cascade, pin_lse_logsumexp,
             pin_binary_heap_tiny, pin_single_tree_counts, pin_long_context_counts,
             pin_structure_invariants]

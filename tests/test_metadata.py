@@ -72,9 +72,10 @@ def _tile_cost(rows):
 SLOT1_SPEED, ODD_XCD_SPEED = 0.80, 0.935
 
 
-def _speed(s):
+def _speed(s, cus=256, xcds=8):
     s = np.asarray(s)
-    return np.where(s < 256, 1.0, SLOT1_SPEED) * np.where(s % 2 == 1, ODD_XCD_SPEED, 1.0)
+    odd = (s % xcds) % 2 == 1 if xcds > 1 else np.zeros(s.shape, bool)
+    return np.where(s < cus, 1.0, SLOT1_SPEED) * np.where(odd, ODD_XCD_SPEED, 1.0)
 
 
 def _plan_checks(ctx, model, leaves, mode):
@@ -227,37 +228,47 @@ def test_plan_covers_each_chain_token_once(cfg):
     assert tree_tok <= naive_tok
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
-def test_stream_sizes(cfg):
-    """One round of resident workgroups (at most 512 x 192 cost units): one
+@pytest.mark.parametrize("cfg,cus,xcds,regime", [
+    (2, 256, 8, "one round"), (4, 256, 8, "guided"),
+    # other machine shapes: a 304-CU part (one round, 608 streams) and a
+    # single 32-CU die (config 2 then takes several rounds)
+    (2, 304, 8, "one round"), (2, 32, 1, "guided"), (4, 80, 4, "guided"),
+])
+def test_stream_sizes(cfg, cus, xcds, regime):
+    """One round of resident workgroups (at most 2 CUs x 192 cost units): one
     stream per slot, estimated cost in proportion to the speed of its slot and
     XCD to within about two tiles.  More work: guided sizes, each stream 1/2
-    of an even 512-way share of the work not yet assigned scaled by its XCD's
-    speed (relative to the mean), clamped to [8, 192]."""
+    of an even (2 CUs)-way share of the work not yet assigned scaled by its
+    XCD's speed (relative to the mean), clamped to [8, 192]."""
     log = build_call_log(cfg)
     from workloads import CONFIGS
     c = CONFIGS[cfg]
     ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    if (cus, xcds) != (256, 8):
+        ctx.set_device_shape(cus, xcds)
     replay_host(ctx, log)
     model = oracle_model(log)
+    slots = 2 * cus
     seen = set()
     for mode in (0, 1):
         pieces, tiles, n_streams = _plan_checks(ctx, model, log.leaves, mode)
         cost = _stream_costs(pieces, n_streams)
         total = cost.sum()
-        if total <= 512 * 192:
+        if total <= slots * 192:
             seen.add("one round")
-            assert n_streams == min(len(tiles), 512) or n_streams >= 0.95 * min(len(tiles), 512)
-            rel = cost / _speed(np.arange(n_streams))
+            assert n_streams == min(len(tiles), slots) or n_streams >= 0.95 * min(len(tiles), slots)
+            rel = cost / _speed(np.arange(n_streams), cus, xcds)
             assert rel.max() <= rel.mean() + 2 * 2.6 + 2.0, (mode, rel.mean(), rel.max())
             # (the last stream takes the remainder, which may be short)
-            assert rel[:-1].min() >= rel.mean() - 2 * 2.6 - 2.0 or n_streams < 512
+            assert rel[:-1].min() >= rel.mean() - 2 * 2.6 - 2.0 or n_streams < slots
         else:
             seen.add("guided")
             kv = _stream_costs(pieces, n_streams, q_cost=0.0)
             before = np.concatenate([[0.0], np.cumsum(kv)[:-1]])
-            xs = np.where(np.arange(n_streams) % 2 == 1, ODD_XCD_SPEED, 1.0) / ((1 + ODD_XCD_SPEED) / 2)
-            want = np.clip(xs * (kv.sum() - before) / (2 * 512), 8, 192)
+            die = np.where((np.arange(n_streams) % xcds) % 2 == 1, ODD_XCD_SPEED, 1.0) if xcds > 1 \
+                else np.ones(n_streams)
+            xs = die / (np.mean(die[:xcds]) if xcds > 1 else 1.0)
+            want = np.clip(xs * (kv.sum() - before) / (2 * slots), 8, 192)
             # a stream closes on the first tile that reaches its size (plus the
             # query tiles of a piece it opens) unless its tile table fills first
             assert (cost[:-1] <= want[:-1] + 2.6 + 2.0).all()
@@ -267,7 +278,7 @@ def test_stream_sizes(cfg):
             short = cost[:-1] < want[:-1] - 1e-6
             assert table_full[:-1][short].all()
             assert cost[-1] <= want[-1] + 2.6 + 2.0
-    assert seen == {2: {"one round"}, 4: {"guided"}}[cfg]
+    assert regime in seen
 
 
 def test_duplicate_and_interior_leaves():

@@ -86,7 +86,33 @@ def _combine_factory(kind):
     return combine
 
 
+def _widen_factory(kind):
+    def widen(bits):
+        b = np.asarray(bits, dtype=np.uint16)
+        if kind == "shift_without_widening":
+            # the shift done in 16 bits: every value becomes 0
+            return (b << np.uint16(8) << np.uint16(8)).astype(np.float64)
+        if kind == "sign_dropped":
+            u = (b & np.uint16(0x7FFF)).astype(np.uint32) << np.uint32(16)
+        else:  # "fraction_truncated": the low fraction bits lost
+            u = (b & np.uint16(0xFFF0)).astype(np.uint32) << np.uint32(16)
+        return u.view(np.float32).astype(np.float64)
+    return widen
+
+
+_orig_tree_decode = A.tree_decode
+
+
+def _decode_positions_sorted(model, node_kv, leaves, q_bits, scale, positions=None):
+    return _orig_tree_decode(model, node_kv, leaves, q_bits, scale,
+                             positions=None if positions is None else sorted(positions))
+
+
 MUTATIONS = {
+    "shift_without_widening": (A, "bf16_bits_to_f64", _widen_factory("shift_without_widening")),
+    "sign_dropped": (A, "bf16_bits_to_f64", _widen_factory("sign_dropped")),
+    "fraction_truncated": (A, "bf16_bits_to_f64", _widen_factory("fraction_truncated")),
+    "positions_sorted": (A, "tree_decode", _decode_positions_sorted),
     "interleaved_heads": (A, "attend", _attend_factory("interleaved_heads")),
     "no_scale": (A, "attend", _attend_factory("no_scale")),
     "k_as_v": (A, "attend", _attend_factory("k_as_v")),

@@ -251,7 +251,7 @@ def gen_long_context(seed: int) -> CallLog:
 def gen_misaligned_fallback(seed: int) -> CallLog:
     """32 prompts of 512 tokens, 7 segments of l=1024 (responses up to 7168
     tokens), width w=16, with a 512-token fallback (the misaligned setting of
-    Sec. 4.1).  Level-synchronous steps: every active path forks into 2
+    Sec. 4.2).  Level-synchronous steps: every active path forks into 2
     children while its prompt holds fewer than w live trajectories (1 after).
     Each child is pruned with p=0.2 after U[1, avail] tokens (an early stop:
     it stays in the forest but is no trajectory), ends with an answer with
