@@ -1,34 +1,50 @@
 """Decode-step throughput of segment-tree attention on one MI355X.
 
-A step is one ``treepo_tree_decode`` call: every active leaf's query (all Hq
-heads) attends over its root-to-leaf chain of segments, with inputs already
-resident in HBM.  The default workload is the single 7B-style tree (1 prompt
-of 512 tokens, segment length 512, binary forks at the first 4 boundaries, 16
-leaves of 7680 tokens, Hq=28 Hkv=4 D=128, bf16 N(0,1) data).
+A step is one pass of the decode path over a batch: ``treepo_tree_decode``
+(node partials + log-sum-exp combine) for every active leaf of the workload,
+and, on workloads whose decode step fuses an append (config 5: one new token
+per leaf), the ``treepo_kv_append`` of that token first.  Inputs are resident
+in HBM when timing starts.  The default workload is the single 7B-style tree
+(1 prompt of 512 tokens, segment length 512, binary forks at the first 4
+boundaries, 16 leaves of 7680 tokens, Hq=28 Hkv=4 D=128, bf16 N(0,1) data).
 
 Timing protocol: ``--replicas`` copies of the pools are built and the steps
 rotate over them, so that no step finds its KV in the 256 MB Infinity Cache
-(the whole working set of this tree is ~200 MB).  W untimed warm-up steps,
-then exactly K timed steps between two device synchronisations (after half
-a second of untimed steps in both modes, so that the GPU's clocks have
-settled before the first timed mode).  A second pass of the K steps runs
-with library profiling on: every launch records HIP events at its kernel's
-own start and end, which gives the dominant kernel's average duration.  The
-same protocol times the per-leaf paged-decode baseline, and a streaming-read
-probe gives the attainable HBM read bandwidth.  The fp64 oracle is timed on
-the host cores on the same workload.
+(config 2's working set is ~200 MB).  After half a second of untimed
+decode steps (the GPU's clocks settle), W untimed warm-up steps, then exactly
+K timed steps between two device synchronisations give ``ms_per_step`` and
+``value``.  A second pass of the K steps runs with library profiling on
+(events at every kernel's own start and end) and gives each kernel's average
+duration; a third pass of max(K, 50) steps records an event between
+consecutive steps and gives the median, p10 and p90 step time.  The same
+protocol times the per-leaf paged-decode baseline.  Two probes give the
+attainable HBM read bandwidth (plain 16-byte loads, and the decode kernels'
+own global->LDS staging), and the fp64 oracle is timed on the host cores on
+the same workload (and on one core for configs 1 and 2).
+
+A fused-append workload grows: each step appends one token to every leaf
+(the plan, built once with device-resident lengths, serves every step), so
+the leaves are built with room for every step of the run and the bytes of a
+step are counted at that step's lengths.
 
 Other modes: ``--config N`` (another workload), ``--segment-loop``
 (segment-level decoding over several layers), ``--advantage`` (the TreePO
-advantage) and ``--prefill`` (prompt prefill).  Prints one JSON line.
+advantage), ``--prefill`` (prompt prefill), ``--profile-pass`` (a short run
+for hardware counters) and ``--summarize`` (writes the rocprofv3 summaries
+under profiles/ from a run's output).  Prints one JSON line.
 """
 
 from __future__ import annotations
 
 import argparse
+import csv
+import dataclasses
+import glob
+import hashlib
 import json
 import math
 import os
+import statistics
 import sys
 import time
 
@@ -37,12 +53,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
-# HBM bytes per partial-kernel launch measured with rocprofv3 counters
-# (FETCH_SIZE and WRITE_SIZE passes, calibrated on a plain copy kernel); the
-# summary records the hash of the kernel source it was taken on.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "partial_kernel_config2_traffic.txt")
+PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2508_17445_amd", "csrc", "kernels.hip")
 METRIC = "tree-decode leaf-token-steps/sec + achieved HBM GB/s on unique KV (1 MI355X)"
+DIST_MIN_STEPS = 50
 
 
 def _parse():
@@ -54,6 +68,7 @@ def _parse():
     ap.add_argument("--replicas", type=int, default=0, help="pool copies rotated over (0: auto)")
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-probes", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--segment-loop", action="store_true",
                     help="instead of the default line: segment-level decoding after a fork, every step one "
@@ -66,44 +81,13 @@ def _parse():
                     help="prompt prefill (causal attention of every prompt of the config, written once into the "
                          "pools for all of its rollouts): one JSON line")
     ap.add_argument("--profile-pass", action="store_true",
-                    help="short run for hardware counters: a few decode steps of the workload, then one "
-                         "1 GiB device copy whose byte counters calibrate the kernels'")
+                    help="short run for hardware counters: --steps steps of the workload in each mode (tree, "
+                         "then per-leaf), then one 1 GiB device copy whose byte counters calibrate the kernels'")
+    ap.add_argument("--summarize", choices=("trace", "traffic"),
+                    help="write profiles/partial_kernel_config<N>_{kernel_trace.md,traffic.txt} from the "
+                         "rocprofv3 output under --dir (see the commands in those files)")
+    ap.add_argument("--dir", default="", help="rocprofv3 output directory for --summarize")
     return ap.parse_args()
-
-
-def _warm_gpu(reps, seconds=0.5):
-    """Decode steps in both modes for about `seconds`, untimed, so that the
-    first timed mode does not run while the GPU is still raising its clocks
-    (without this the first mode measured its steps up to 10% slower)."""
-    import torch
-    bufs = {m: [(r.outputs(), r.workspace(m)) for r in reps] for m in (0, 1)}
-    t0 = time.perf_counter()
-    i = 0
-    while time.perf_counter() - t0 < seconds:
-        for m in (0, 1):
-            j = i % len(reps)
-            fn = reps[j].ctx.tree_decode if m == 0 else reps[j].ctx.paged_decode_naive
-            (out, lse), ws = bufs[m][j]
-            fn(reps[j].leaves, reps[j].q, reps[j].cfg.scale, out, lse, ws)
-        i += 1
-        if i % 64 == 0:
-            torch.cuda.synchronize()
-    torch.cuda.synchronize()
-
-
-def _measured_traffic(config_id):
-    """Counter-measured HBM bytes per partial-kernel launch, or None when no
-    summary exists for this workload or the kernel source changed since."""
-    import hashlib
-    try:
-        kv = dict(line.split(":", 1) for line in open(TRAFFIC_FILE).read().splitlines() if ":" in line)
-        kv = {k.strip(): v.strip() for k, v in kv.items()}
-        src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-        if kv.get("kernels.hip sha256") != src or int(kv.get("config", -1)) != config_id:
-            return None
-        return int(kv["traffic bytes per launch"])
-    except (OSError, KeyError, ValueError):
-        return None
 
 
 def _ensure_built():
@@ -113,86 +97,277 @@ def _ensure_built():
         __graft_entry__.build()
 
 
-def _unique_kv(dt):
-    """Tokens per KV head over the nodes of the leaves' chains, each counted once."""
-    model_len = {}
-    nodes = dt.ctx.export_nodes()
-    used = set()
-    for x in dt.leaves:
-        y = x
-        while y != -1 and y not in used:
-            used.add(y)
-            y = int(nodes[y][0])
-    tok = sum(int(nodes[n][3]) for n in used)
-    logical = 0
-    for x in dt.leaves:
-        y = x
-        while y != -1:
-            logical += int(nodes[y][3])
-            y = int(nodes[y][0])
-    return tok, logical
+def _kernel_sha():
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
 
 
-def _time_mode(reps, mode, steps, warmup, kernel_kind):
-    """Times `steps` decode steps rotating over the replicas.
+def _traffic_file(cfg_id):
+    return os.path.join(PROFILES, f"partial_kernel_config{cfg_id}_traffic.txt")
 
-    Two timed passes of the same length: the first without instrumentation
-    gives the step time; the second brackets every kernel launch with HIP
-    events on the launch stream (library profiling) and gives the average
-    duration of each kernel.
+
+def _measured_traffic(cfg_id):
+    """Counter-measured HBM bytes per partial-kernel launch (tree schedule), or
+    None when no summary exists for this workload or the kernel source changed
+    since it was taken."""
+    try:
+        kv = dict(line.split(":", 1) for line in open(_traffic_file(cfg_id)).read().splitlines() if ":" in line)
+        kv = {k.strip(): v.strip() for k, v in kv.items()}
+        if kv.get("kernels.hip sha256") != _kernel_sha() or int(kv.get("config", -1)) != cfg_id:
+            return None
+        return int(kv["traffic bytes per launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+# ---- the workload on the device --------------------------------------------------
+
+def _with_room(log, room):
+    """The call log with every node that is a decoded leaf reserving `room`
+    more tokens, so that every leaf can take one more token per step for
+    `room` steps (segment-level decoding: the step's token joins its path)."""
+    leaves = set(log.leaves)
+    ops, nid = [], 0
+    for op in log.ops:
+        if op[0] == "root":
+            ops.append(("root", op[1] + (room if nid in leaves else 0)))
+            nid += 1
+        elif op[0] == "fork":
+            kids = range(nid, nid + op[2])
+            ops.append(("fork", op[1], op[2], op[3] + (room if any(k in leaves for k in kids) else 0)))
+            nid += op[2]
+        elif op[0] == "fork_at":
+            raise ValueError("room for step appends is not supported on logs with fork_at")
+        else:
+            ops.append(op)
+    return dataclasses.replace(log, ops=ops)
+
+
+class Workload:
+    """The config's forest on the device (and replicas of it), and one decode
+    step per mode.  On a fused-append config every step first appends one
+    token to every leaf (device-resident lengths: one plan serves the run);
+    every timing pass then starts from a fresh copy of the forest as built
+    (leaves at their configured lengths), made by ``reset``."""
+
+    def __init__(self, cfg_id, args, room):
+        from workloads import CONFIGS, build_call_log
+        from workloads.device import DeviceTree
+        self.cfg = CONFIGS[cfg_id]
+        self.cfg_id = cfg_id
+        self.no_naive = args.no_naive
+        log = build_call_log(cfg_id)
+        self.fused = log.step_append is not None
+        if self.fused:
+            base = DeviceTree(cfg=self.cfg, log=_with_room(log, room), apply_step_append=False, live=True)
+        else:
+            base = DeviceTree(cfg_id=cfg_id)
+        self.base = base
+        self.leaves = list(base.leaves)
+        self.n_leaves = len(self.leaves)
+        c = self.cfg
+        self.kv_bytes_per_tok = c.hkv * c.d * 2 * 2
+        self.uniq_tok, self.logical_tok = self._tokens(base)
+        self.chain0 = self._chain_tokens(base, self.leaves[0])
+        if self.fused:  # the first step's append is part of the step: count its token
+            self.uniq_tok += self.n_leaves
+            self.logical_tok += self.n_leaves
+        uniq_bytes = self.uniq_tok * self.kv_bytes_per_tok
+        self.n_rep = args.replicas or max(1, math.ceil(1.2e9 / uniq_bytes))
+        self.reps = {}
+        self.bufs = {}
+        self.appended = {0: 0, 1: 0}
+        if self.fused:
+            self.reset(0)
+            self.reset(1)
+        else:
+            reps = [base] + [base.clone() for _ in range(self.n_rep - 1)]
+            for m in (0, 1):
+                self.reps[m] = reps
+                self.bufs[m] = [(r.outputs(), r.workspace(m)) for r in reps]
+
+    def reset(self, mode):
+        """Fused-append workloads: fresh copies of the forest for `mode`."""
+        if not self.fused:
+            return
+        import torch
+        self.reps.pop(mode, None)
+        self.bufs.pop(mode, None)
+        torch.cuda.empty_cache()
+        if mode == 1 and self.no_naive:
+            return
+        self.reps[mode] = [self.base.clone() for _ in range(self.n_rep)]
+        self.bufs[mode] = [(r.outputs(), r.workspace(mode)) for r in self.reps[mode]]
+        self.appended[mode] = 0
+
+    @staticmethod
+    def _tokens(dt):
+        nodes = dt.ctx.export_nodes()
+        used = set()
+        logical = 0
+        for x in dt.leaves:
+            y = x
+            while y != -1:
+                logical += int(nodes[y][3])
+                if y not in used:
+                    used.add(y)
+                y = int(nodes[y][0])
+        return sum(int(nodes[n][3]) for n in used), logical
+
+    @staticmethod
+    def _chain_tokens(dt, x):
+        nodes = dt.ctx.export_nodes()
+        t = 0
+        while x != -1:
+            t += int(nodes[x][3])
+            x = int(nodes[x][0])
+        return t
+
+    def step(self, mode, i, decode_only=False):
+        """Step i of `mode` (replica i mod replicas)."""
+        reps = self.reps[mode]
+        j = i % len(reps)
+        r = reps[j]
+        if self.fused and not decode_only:
+            nodes, ntok = r.log.step_append
+            r.ctx.kv_append(nodes, ntok, r.step_k, r.step_v)
+            if j == len(reps) - 1:
+                self.appended[mode] += 1
+        (out, lse), ws = self.bufs[mode][j]
+        fn = r.ctx.tree_decode if mode == 0 else r.ctx.paged_decode_naive
+        fn(r.leaves, r.q, r.cfg.scale, out, lse, ws)
+
+    def step_bytes(self, first_append, count):
+        """Unique KV bytes per step, averaged over `count` steps whose first
+        appends the `first_append`-th token (1-based) of the pass."""
+        if not self.fused:
+            return self.uniq_tok * self.kv_bytes_per_tok
+        extra = first_append - 1 + (count - 1) / 2.0
+        return (self.uniq_tok + extra * self.n_leaves) * self.kv_bytes_per_tok
+
+
+def _warm_gpu(w, seconds=0.5):
+    """Decode steps (no appends) in both modes for about `seconds`, untimed,
+    so that the first timed mode does not run while the GPU is still raising
+    its clocks (without this the first mode measured its steps up to 10%
+    slower)."""
+    import torch
+    t0 = time.perf_counter()
+    i = 0
+    while time.perf_counter() - t0 < seconds:
+        for m in (0, 1):
+            w.step(m, i, decode_only=True)
+        i += 1
+        if i % 16 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
+def _pct(v, q):
+    v = sorted(v)
+    if not v:
+        return float("nan")
+    k = (len(v) - 1) * q
+    lo, hi = math.floor(k), math.ceil(k)
+    return v[lo] + (v[hi] - v[lo]) * (k - lo)
+
+
+def _time_mode(w, mode, steps, warmup):
+    """Times `steps` steps of `mode` rotating over the replicas.
+
+    Pass 1 (uninstrumented) gives the step time.  Pass 2 (same length) runs
+    with library profiling: events at every kernel's own start and end give
+    each kernel's average duration.  Pass 3 (max(steps, 50) steps) records a
+    torch event between consecutive steps on the launch stream and gives the
+    distribution of the step time.
     """
     import torch
-    from paper_2508_17445_amd import KERNEL_COMBINE
-    bufs = []
-    for r in reps:
-        out, lse = r.outputs()
-        bufs.append((out, lse, r.workspace(mode)))
-    fn = [(r.ctx.tree_decode if mode == 0 else r.ctx.paged_decode_naive) for r in reps]
-
-    def run(n):
-        for i in range(n):
-            j = i % len(reps)
-            fn[j](reps[j].leaves, reps[j].q, reps[j].cfg.scale, bufs[j][0], bufs[j][1], bufs[j][2])
-
-    run(warmup)
+    from paper_2508_17445_amd import KERNEL_APPEND, KERNEL_COMBINE, KERNEL_PARTIAL
+    w.reset(mode)
+    for i in range(warmup):
+        w.step(mode, i)
     torch.cuda.synchronize()
+    first = w.appended[mode] + 1
     t0 = time.perf_counter()
-    run(steps)
+    for i in range(steps):
+        w.step(mode, i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    for r in reps:
+    nbytes = w.step_bytes(first, steps)
+    w.reset(mode)
+    for r in w.reps[mode]:
         r.ctx.set_profiling(True)
     torch.cuda.synchronize()
-    t2 = time.perf_counter()
-    run(steps)
+    for i in range(steps):
+        w.step(mode, i)
     torch.cuda.synchronize()
-    t3 = time.perf_counter()
-    kms, kn, cms, cn = 0.0, 0, 0.0, 0
-    for r in reps:
-        a, b = r.ctx.profile_read(kernel_kind)
-        c, d = r.ctx.profile_read(KERNEL_COMBINE)
-        kms += a; kn += b; cms += c; cn += d
+    kern = {}
+    for kind, name in ((KERNEL_PARTIAL, "partial"), (KERNEL_COMBINE, "combine"), (KERNEL_APPEND, "append")):
+        tot, n = 0.0, 0
+        for r in w.reps[mode]:
+            a, b = r.ctx.profile_read(kind)
+            tot += a
+            n += b
+        kern[name] = (tot / n if n else None, n // max(steps, 1))
+    for r in w.reps[mode]:
         r.ctx.set_profiling(False)
-    return {"ms": (t1 - t0) * 1e3 / steps, "ms_instrumented": (t3 - t2) * 1e3 / steps,
-            "kernel_ms": kms / max(kn, 1), "combine_ms": cms / max(cn, 1), "launches": kn // max(steps, 1)}
+    nd = max(steps, DIST_MIN_STEPS)
+    w.reset(mode)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(nd + 1)]
+    torch.cuda.synchronize()
+    for i in range(nd):
+        ev[i].record()
+        w.step(mode, i)
+    ev[nd].record()
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(nd)]
+    return {"ms": (t1 - t0) * 1e3 / steps, "bytes": nbytes, "kern": kern, "first": first,
+            "dist": {"steps": nd, "median_ms": round(_pct(per, 0.5), 5), "p10_ms": round(_pct(per, 0.1), 5),
+                     "p90_ms": round(_pct(per, 0.9), 5)}}
 
 
-def _probe_read(nbytes=4 << 30, iters=10):
+# ---- probes and the oracle -------------------------------------------------------
+
+def _timed(fn, iters):
     import torch
-    from paper_2508_17445_amd import bench_read
-    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    sink = torch.empty(4096, dtype=torch.float32, device="cuda")
-    bench_read(src, nbytes, sink)
+    fn()
     torch.cuda.synchronize()
     st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     st.record()
     for _ in range(iters):
-        bench_read(src, nbytes, sink)
+        fn()
     en.record()
     torch.cuda.synchronize()
-    ms = st.elapsed_time(en) / iters
+    return st.elapsed_time(en) / iters
+
+
+def _probes(work_bytes):
+    """Attainable HBM read bandwidth: a plain 16-byte-load read of 4 GiB, and
+    the decode kernels' staging (16-byte non-temporal global->LDS loads into a
+    ring of four 16 KiB buffers, three in flight, a barrier per chunk; 512
+    workgroups, one contiguous share each) on 4 GiB and on rotating buffers
+    the size of the workload."""
+    import torch
+    from paper_2508_17445_amd import bench_read, bench_stream
+    wgs, chunk = 512, 16384
+    big = 4 << 30
+    src = torch.empty(big, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    res = {"plain_read_4GiB_GBps": round(big / (_timed(lambda: bench_read(src, big, sink), 10) * 1e-3) / 1e9, 1),
+           "staging_4GiB_GBps": round(big / (_timed(lambda: bench_stream(src, big, sink, 3, wgs), 10) * 1e-3)
+                                      / 1e9, 1)}
+    step = wgs * chunk
+    size = max(step, int(work_bytes) // step * step)
+    n = max(1, min(big // size, 20))
+    it = [0]
+
+    def rot():
+        bench_stream(src[(it[0] % n) * size:], size, sink, 3, wgs)
+        it[0] += 1
+    res["staging_workload_size_GBps"] = round(size / (_timed(rot, 4 * n) * 1e-3) / 1e9, 1)
+    res["staging_workload_bytes"] = size
     del src
-    return nbytes / (ms * 1e-3) / 1e9
+    torch.cuda.empty_cache()
+    return res
 
 
 def _blas_threads():
@@ -203,54 +378,299 @@ def _blas_threads():
         return 1
 
 
-def _cpu_baseline(cfg_id, seconds):
-    import numpy as np
+def _oracle_rate(cfg_id, seconds, one_core=False):
+    """The fp64 oracle over whole decode steps of the workload: leaf-token-steps/s."""
+    import contextlib
     from oracle import attention as A
     from oracle import metadata as M
     from workloads import CONFIGS, build_call_log, query_bits
     from workloads.device import NodeData
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        blas_threads = 1
     cfg, log = CONFIGS[cfg_id], build_call_log(cfg_id)
     model = M.replay(log, cfg.block_tokens, 1 << 30, 1 << 30)
     data = NodeData(cfg, log)
     data.prefetch(sorted({n for x in log.leaves for n in model.chain(x)}))
     q = query_bits(cfg.seed, 0, len(log.leaves), cfg.hq, cfg.d)
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        A.tree_decode(model, data, log.leaves, q, cfg.scale)
-        reps += 1
-        if time.perf_counter() - t0 >= seconds:
-            break
-    dt = time.perf_counter() - t0
-    cores = min(len(os.sched_getaffinity(0)), blas_threads)
-    return {"value": len(log.leaves) * reps / dt, "unit": "leaf-token-steps/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"{reps} full decode step(s) of the same workload ({len(log.leaves)} leaves, fp64 numpy, "
-                      f"chains materialised per leaf) in {dt:.1f} s; host has "
-                      f"{len(os.sched_getaffinity(0))} cores, BLAS threads {blas_threads}"}
+    ctx = contextlib.nullcontext()
+    if one_core:
+        from threadpoolctl import threadpool_limits
+        ctx = threadpool_limits(limits=1)
+    with ctx:
+        threads = _blas_threads()
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            A.tree_decode(model, data, log.leaves, q, cfg.scale)
+            reps += 1
+            if time.perf_counter() - t0 >= seconds:
+                break
+        dt = time.perf_counter() - t0
+    return len(log.leaves) * reps / dt, reps, dt, threads
 
 
-def _profile_pass(dt, args):
-    """A few decode steps (tree, then naive) and a 1 GiB copy, nothing else on the GPU."""
+def _cpu_baseline(cfg_id, seconds):
+    rate, reps, dt, threads = _oracle_rate(cfg_id, seconds)
+    host = len(os.sched_getaffinity(0))
+    out = {"value": round(rate, 2), "unit": "leaf-token-steps/s", "cores": min(host, threads), "kind": "oracle",
+           "sample": f"{reps} full decode step(s) of the same workload (fp64 numpy, chains materialised per "
+                     f"leaf) in {dt:.1f} s; host has {host} cores, BLAS threads {threads}"}
+    if cfg_id in (1, 2):
+        one = {}
+        for c in (1, 2):
+            r1, n1, d1, _ = _oracle_rate(c, min(seconds, 4.0), one_core=True)
+            one[f"config{c}"] = {"value": round(r1, 2), "steps": n1, "seconds": round(d1, 2)}
+        out["one_core"] = one
+    return out
+
+
+# ---- hardware-counter runs and their summaries -----------------------------------
+
+def _profile_pass(cfg_id, args):
+    """--steps steps of the workload in each mode (tree, then per-leaf), then
+    one 1 GiB device copy, nothing else on the GPU (fused-append workloads
+    append in every step, as in the bench)."""
     import torch
     from paper_2508_17445_amd import bench_copy
+    w = Workload(cfg_id, args, args.steps + 8)
     for mode in (0, 1):
-        out, lse = dt.outputs()
-        ws = dt.workspace(mode)
-        fn = dt.ctx.tree_decode if mode == 0 else dt.ctx.paged_decode_naive
-        for _ in range(args.steps):
-            fn(dt.leaves, dt.q, dt.cfg.scale, out, lse, ws)
+        for i in range(args.steps):
+            w.step(mode, i)
         torch.cuda.synchronize()
     nbytes = 1 << 30
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     bench_copy(dst, src, nbytes)
     torch.cuda.synchronize()
-    print(json.dumps({"profile_pass": True, "steps_per_mode": args.steps, "copy_bytes": nbytes}), flush=True)
+    print(json.dumps({"profile_pass": True, "config": cfg_id, "steps_per_mode": args.steps,
+                      "copy_bytes": nbytes}), flush=True)
+
+
+def _csv_rows(d, suffix):
+    files = sorted(glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True))
+    if not files:
+        raise SystemExit(f"no *{suffix} under {d}")
+    rows = []
+    for f in files:
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def _bench_line(d):
+    for f in sorted(glob.glob(os.path.join(d, "*.json"))):
+        for line in open(f).read().splitlines()[::-1]:
+            if line.startswith("{") and '"metric"' in line:
+                return json.loads(line)
+    raise SystemExit(f"no bench JSON line under {d}")
+
+
+def _workload_name(cfg_id):
+    from workloads import CONFIGS
+    return CONFIGS[cfg_id].name
+
+
+def _summarize_trace(cfg_id, d):
+    """profiles/partial_kernel_config<N>_kernel_trace.md from a kernel trace
+    of one bench run (its JSON line saved as a .json file in the same dir)."""
+    b = _bench_line(d)
+    rows = _csv_rows(d, "kernel_trace.csv")
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+
+    def dur(r):
+        return (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+    steps, warm = b["steps"], b["warmup"]
+    per_mode = warm + 2 * steps + max(steps, DIST_MIN_STEPS)   # the launches of _time_mode per mode
+    modes = 2 if "naive_baseline" in b else 1
+    lines, avg = [], {}
+    for kname in ("partial_kernel", "combine_kernel", "kv_append_kernel"):
+        ks = [r for r in rows if kname in r["Kernel_Name"]]
+        if not ks:
+            continue
+        ks = ks[-modes * per_mode:]
+        for m in range(modes):
+            blk = ks[m * per_mode:(m + 1) * per_mode][warm:]
+            v = [dur(r) for r in blk]
+            label = ("tree schedule", "per-leaf baseline")[m]
+            avg[(kname, m)] = statistics.mean(v)
+            lines.append(f"| {kname}, {label} | {blk[0]['Grid_Size_X'] if 'Grid_Size_X' in blk[0] else blk[0].get('Grid_Size', '')} "
+                         f"| {len(v)} | {statistics.mean(v):.2f} | {statistics.median(v):.2f} | "
+                         f"{_pct(v, 0.1):.2f} | {_pct(v, 0.9):.2f} | {min(v):.2f} | {max(v):.2f} |")
+    alg = b["roofline"]["algorithmic_bytes_per_launch"]
+    t_avg = avg[("partial_kernel", 0)]
+    txt = f"""# Kernel trace: decode step on config {cfg_id} ({_workload_name(cfg_id)})
+
+Command (repository root `$R` on the GPU box):
+
+```
+cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/trace -o run -- python3 -u $R/bench.py --config {cfg_id} --steps {steps} --warmup {warm} --no-cpu --no-probes > $R/gpurun_out/prof/c{cfg_id}/trace/bench.json
+python3 bench.py --summarize trace --config {cfg_id} --dir gpurun_out/prof/c{cfg_id}/trace
+```
+
+Per-dispatch durations from the kernel trace (microseconds), the launches of
+the bench's timing passes after the W = {warm} warm-up steps of each mode
+(uninstrumented pass, events pass, distribution pass: {per_mode - warm} per mode).
+
+| kernel, schedule | grid (threads) | dispatches | avg | median | p10 | p90 | min | max |
+|---|---|---|---|---|---|---|---|---|
+""" + "\n".join(lines) + f"""
+
+Algorithmic bytes per tree launch (unique KV of the decoded chains at the
+timed steps): {alg} -> {alg / t_avg / 1e6:.3f} TB/s = {alg / t_avg / 1e6 / 8:.3f} of 8 TB/s on the
+kernel-trace average ({t_avg:.2f} us).  The same run's bench line: partial kernel
+{b['roofline']['kernel_avg_ms'] * 1e3:.2f} us on events attached to the kernel (frac {b['roofline']['frac']}),
+step {b['ms_per_step'] * 1e3:.2f} us (median {b['step_distribution']['median_ms'] * 1e3:.2f} us over
+{b['step_distribution']['steps']} steps).
+
+kernels.hip sha256: {_kernel_sha()}
+"""
+    path = os.path.join(PROFILES, f"partial_kernel_config{cfg_id}_kernel_trace.md")
+    open(path, "w").write(txt)
+    print(txt)
+
+
+def _summarize_traffic(cfg_id, d):
+    """profiles/partial_kernel_config<N>_traffic.txt from two counter runs of
+    --profile-pass (FETCH_SIZE in <dir>/fetch, WRITE_SIZE in <dir>/write)."""
+    from workloads import CONFIGS, build_call_log
+    cfg = CONFIGS[cfg_id]
+
+    def agg(sub, counter):
+        rows = [r for r in _csv_rows(os.path.join(d, sub), "counter_collection.csv") if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        part = [float(r["Counter_Value"]) for r in rows if "partial_kernel" in r["Kernel_Name"]]
+        copy = [float(r["Counter_Value"]) for r in rows if "copy_kernel" in r["Kernel_Name"]]
+        n = len(part) // 2   # tree decodes first, then the per-leaf ones
+        return statistics.mean(part[:n]), statistics.mean(part[n:]), statistics.mean(copy), n
+
+    ft, fn, fc, n = agg("fetch", "FETCH_SIZE")
+    wt, wn, wc, _ = agg("write", "WRITE_SIZE")
+    fs, ws = 1048576 / fc, 1048576 / wc
+    fb, wb = round(ft * 1024 * fs), round(wt * 1024 * ws)
+    from workloads.device import DeviceTree  # noqa: F401  (same workload definition)
+    log = build_call_log(cfg_id)
+    alg = _algorithmic_bytes(cfg_id, log)
+    txt = f"""HBM traffic of the node-partial kernel, decode workload config {cfg_id} ({cfg.name}, Hq={cfg.hq} Hkv={cfg.hkv} D={cfg.d})
+Commands (repository root $R on the GPU box; each counter in its own run):
+  cd /tmp && export TMPDIR=/tmp
+  rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/pmc/fetch -o run -- python3 $R/bench.py --profile-pass --config {cfg_id} --steps {n}
+  rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/pmc/write -o run -- python3 $R/bench.py --profile-pass --config {cfg_id} --steps {n}
+  python3 bench.py --summarize traffic --config {cfg_id} --dir gpurun_out/prof/c{cfg_id}/pmc
+The profile pass runs {n} tree decode steps, {n} per-leaf decode steps and one 1 GiB device copy.
+Calibration on the 1 GiB copy kernel: FETCH_SIZE reads {fc:.1f} KiB for 1048576 KiB read (scale {fs:.4f}); WRITE_SIZE reads {wc:.1f} KiB for 1048576 KiB written (scale {ws:.4f}).
+partial_kernel<128>, tree schedule, mean of {n} dispatches:
+  FETCH_SIZE {ft:.1f} KiB -> {fb} bytes read
+  WRITE_SIZE {wt:.1f} KiB -> {wb} bytes written (fp32 partial rows)
+partial_kernel<128>, per-leaf baseline: FETCH_SIZE {fn:.1f} KiB ({round(fn * 1024 * fs)} bytes), WRITE_SIZE {wn:.1f} KiB ({round(wn * 1024 * ws)} bytes)
+Algorithmic bytes per launch (unique KV of the decoded chains): {alg}; measured traffic / algorithmic = {(fb + wb) / alg:.4f}
+config: {cfg_id}
+kernels.hip sha256: {_kernel_sha()}
+fetch bytes per launch: {fb}
+write bytes per launch: {wb}
+traffic bytes per launch: {fb + wb}
+"""
+    open(_traffic_file(cfg_id), "w").write(txt)
+    print(txt)
+
+
+def _algorithmic_bytes(cfg_id, log):
+    """Unique KV bytes of a decode step of the workload (with its fused append)."""
+    from workloads import CONFIGS
+    cfg = CONFIGS[cfg_id]
+    parent = {}
+    nid = 0
+    for op in log.ops:
+        if op[0] == "root":
+            parent[nid] = -1
+            nid += 1
+        elif op[0] == "fork":
+            for k in range(op[2]):
+                parent[nid + k] = op[1]
+            nid += op[2]
+        elif op[0] == "fork_at":
+            t = nid
+            for y, p in list(parent.items()):
+                if p == op[1]:
+                    parent[y] = t
+            parent[t] = op[1]
+            for k in range(op[3]):
+                parent[t + 1 + k] = op[1]
+            nid += 1 + op[3]
+    used = set()
+    for x in log.leaves:
+        while x != -1 and x not in used:
+            used.add(x)
+            x = parent[x]
+    return sum(log.rows[n] for n in used) * cfg.hkv * cfg.d * 4
+
+
+# ---- the decode line ---------------------------------------------------------------
+
+def _decode_line(args):
+    import torch
+    cfg_id = args.config
+    w = Workload(cfg_id, args, max(args.warmup + args.steps, DIST_MIN_STEPS) + 8)
+    cfg = w.cfg
+    _warm_gpu(w)
+    tm = _time_mode(w, 0, args.steps, args.warmup)
+    ms, nbytes = tm["ms"], tm["bytes"]
+    kern_ms, launches = tm["kern"]["partial"]
+    comb_ms = tm["kern"]["combine"][0]
+    value = w.n_leaves / (ms * 1e-3)
+    achieved_kern = nbytes / (kern_ms * 1e-3) / 1e9
+    achieved_step = nbytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "leaf-token-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/K/V; call-log-built tree)",
+        "config": {
+            "workload": f"config {cfg_id}: {cfg.name}" + (" (append of one token per leaf + decode per step)"
+                                                          if w.fused else ""),
+            "leaves": w.n_leaves, "hq": cfg.hq, "hkv": cfg.hkv, "head_dim": cfg.d,
+            "unique_kv_tokens": w.uniq_tok, "logical_kv_tokens": w.logical_tok,
+            "unique_kv_bytes_per_step": round(nbytes), "share_ratio": round(w.logical_tok / w.uniq_tok, 4),
+            "pool_replicas": len(w.reps[0]),
+        },
+        "achieved_unique_kv_GBps_step": round(achieved_step, 1),
+        "call_level_frac": round(achieved_step / PEAK_HBM_GBPS, 4),
+        "step_distribution": tm["dist"],
+        "roofline": {"bound": "hbm", "achieved": round(achieved_kern, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved_kern / PEAK_HBM_GBPS, 4), "traffic": _measured_traffic(cfg_id),
+                     "kernel": "partial_kernel<128>", "kernel_avg_ms": round(kern_ms, 5),
+                     "launches_per_step": launches, "algorithmic_bytes_per_launch": round(nbytes)},
+        "combine_avg_ms": round(comb_ms, 5),
+    }
+    if w.fused:
+        line["config"]["leaf_chain_tokens_timed"] = [w.chain0 + tm["first"], w.chain0 + tm["first"] + args.steps - 1]
+        ap_ms = tm["kern"]["append"][0]
+        line["append_avg_ms"] = round(ap_ms, 5) if ap_ms is not None else None
+    if not args.no_naive:
+        tn = _time_mode(w, 1, args.steps, args.warmup)
+        nms = tn["ms"]
+        line["naive_baseline"] = {"ms_per_step": round(nms, 5), "value": round(w.n_leaves / (nms * 1e-3), 1),
+                                  "kernel_avg_ms": round(tn["kern"]["partial"][0], 5),
+                                  "combine_avg_ms": round(tn["kern"]["combine"][0], 5),
+                                  "step_distribution": tn["dist"],
+                                  "speedup_tree_vs_naive": round(nms / ms, 4),
+                                  "speedup_median": round(tn["dist"]["median_ms"] / tm["dist"]["median_ms"], 4)}
+    uniq = w.uniq_tok * w.kv_bytes_per_tok
+    w.reps.clear()
+    w.bufs.clear()
+    del w
+    torch.cuda.empty_cache()
+    if not args.no_probes:
+        pr = _probes(uniq)
+        line["probes"] = pr
+        line["roofline"]["frac_of_staging_probe"] = round(achieved_kern / pr["staging_workload_size_GBps"], 4)
+    if not args.no_cpu:
+        line["cpu_baseline"] = _cpu_baseline(cfg_id, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
 
 
 def _advantage(args):
@@ -521,80 +941,22 @@ def main():
         print(json.dumps({"error": "the decode path runs on one GPU only; it has no multi-GPU mode",
                           "n_gpus": args.gpus}))
         sys.exit(2)
-    import torch
+    if args.summarize:
+        if not args.dir:
+            raise SystemExit("--summarize needs --dir")
+        (_summarize_trace if args.summarize == "trace" else _summarize_traffic)(args.config, args.dir)
+        return
     _ensure_built()
-    from paper_2508_17445_amd import KERNEL_PARTIAL
-    from workloads import CONFIGS
-    from workloads.device import DeviceTree
-
     if args.advantage:
         _advantage(args)
-        return
-    if args.prefill:
+    elif args.prefill:
         _prefill(args)
-        return
-    if args.segment_loop:
+    elif args.segment_loop:
         _segment_loop(args)
-        return
-    cfg = CONFIGS[args.config]
-    base = DeviceTree(cfg_id=args.config)
-    if args.profile_pass:
-        _profile_pass(base, args)
-        return
-    uniq_tok, logical_tok = _unique_kv(base)
-    kv_bytes_per_tok = cfg.hkv * cfg.d * 2 * 2
-    uniq_bytes = uniq_tok * kv_bytes_per_tok
-    n_rep = args.replicas or max(1, math.ceil(1.2e9 / uniq_bytes))
-    reps = [base] + [base.clone() for _ in range(n_rep - 1)]
-
-    _warm_gpu(reps)
-    tm = _time_mode(reps, 0, args.steps, args.warmup, KERNEL_PARTIAL)
-    ms, kern_ms, comb_ms, launches = tm["ms"], tm["kernel_ms"], tm["combine_ms"], tm["launches"]
-    n_leaves = len(base.leaves)
-    value = n_leaves / (ms * 1e-3)
-    achieved_step = uniq_bytes / (ms * 1e-3) / 1e9
-    achieved_kern = uniq_bytes / (kern_ms * 1e-3) / 1e9
-    line = {
-        "metric": METRIC,
-        "value": round(value, 1),
-        "unit": "leaf-token-steps/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 5),
-        "ms_per_step_with_kernel_events": round(tm["ms_instrumented"], 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) bf16 q/K/V; call-log-built tree)",
-        "config": {
-            "workload": f"config {args.config}: {cfg.name}", "leaves": n_leaves, "hq": cfg.hq, "hkv": cfg.hkv,
-            "head_dim": cfg.d, "unique_kv_tokens": uniq_tok, "logical_kv_tokens": logical_tok,
-            "unique_kv_bytes": uniq_bytes, "share_ratio": round(logical_tok / uniq_tok, 4),
-            "pool_replicas": n_rep,
-        },
-        "achieved_unique_kv_GBps_step": round(achieved_step, 1),
-        "roofline": {"bound": "hbm", "achieved": round(achieved_kern, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(achieved_kern / PEAK_HBM_GBPS, 4), "traffic": _measured_traffic(args.config),
-                     "kernel": "partial_kernel<128>", "kernel_avg_ms": round(kern_ms, 5),
-                     "launches_per_step": launches,
-                     "algorithmic_bytes_per_launch": uniq_bytes},
-        "combine_avg_ms": round(comb_ms, 5),
-    }
-    if not args.no_naive:
-        tn = _time_mode(reps, 1, args.steps, args.warmup, KERNEL_PARTIAL)
-        nms = tn["ms"]
-        line["naive_baseline"] = {"ms_per_step": round(nms, 5), "value": round(n_leaves / (nms * 1e-3), 1),
-                                  "kernel_avg_ms": round(tn["kernel_ms"], 5),
-                                  "combine_avg_ms": round(tn["combine_ms"], 5),
-                                  "speedup_tree_vs_naive": round(nms / ms, 4)}
-    line["probe_read_GBps"] = round(_probe_read(), 1)
-    del reps, base
-    torch.cuda.empty_cache()
-    if not args.no_cpu:
-        line["cpu_baseline"] = _cpu_baseline(args.config, args.cpu_seconds)
-    print(json.dumps(line), flush=True)
+    elif args.profile_pass:
+        _profile_pass(args.config, args)
+    else:
+        _decode_line(args)
 
 
 if __name__ == "__main__":

@@ -35,7 +35,9 @@ int32_t treepo_bench_read(const void* src, size_t bytes, float* sink, hipStream_
  *           barrier per chunk (the decode pipeline);
  *   mode 1: the same staging with chunks assigned grid-stride;
  *   mode 2: each workgroup reads one contiguous share with 16-byte register
- *           loads.
+ *           loads;
+ *   mode 3: mode 0 with the non-temporal hint on every load (exactly the
+ *           decode kernels' tile loads).
  * bytes must be a multiple of 16 KiB * workgroups, 1 <= workgroups <= 4096,
  * src 16-byte aligned.  Returns 0, TREEPO_EINVAL or TREEPO_EHIP. */
 int32_t treepo_bench_stream(const void* src, size_t bytes, float* sink, int32_t mode,

@@ -41,9 +41,14 @@ __global__ __launch_bounds__(kThreads) void read_kernel(const uint4* __restrict_
 // does) or takes chunks grid-stride.
 constexpr int kChunk = 16384;
 
+template <bool NT>
 __device__ __forceinline__ void lds_load16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(g), "s"(lds) : "memory", "m0");
+  if (NT)
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
+                 :: "v"(g), "s"(lds) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "s"(lds) : "memory", "m0");
 }
 
 template <int N>
@@ -51,6 +56,7 @@ __device__ __forceinline__ void landed_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(N) : "memory");
 }
 
+template <bool NT>
 __global__ __launch_bounds__(kThreads) void stream_lds_kernel(const char* __restrict__ src, int64_t nchunks,
                                                               int32_t blocked, float* __restrict__ sink) {
   __shared__ __attribute__((aligned(1024))) char buf[4][kChunk];
@@ -69,7 +75,7 @@ __global__ __launch_bounds__(kThreads) void stream_lds_kernel(const char* __rest
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int slot = wave * 4 + j;
-      lds_load16(g + slot * 1024 + lane * 16, __builtin_amdgcn_readfirstlane(b + slot * 1024));
+      lds_load16<NT>(g + slot * 1024 + lane * 16, __builtin_amdgcn_readfirstlane(b + slot * 1024));
     }
   };
   for (int64_t p = 0; p < 3 && p < count; ++p) issue(p);
@@ -106,16 +112,18 @@ __global__ __launch_bounds__(kThreads) void stream_reg_kernel(const uint4* __res
 extern "C" int32_t treepo_bench_stream(const void* src, size_t bytes, float* sink, int32_t mode,
                                        int32_t workgroups, hipStream_t stream) {
   if (!src || !sink || workgroups < 1 || workgroups > 4096 || reinterpret_cast<uintptr_t>(src) % 16 ||
-      mode < 0 || mode > 2)
+      mode < 0 || mode > 3)
     return TREEPO_EINVAL;
   if (bytes % (static_cast<size_t>(kChunk) * workgroups) != 0) return TREEPO_EINVAL;
   const int64_t nchunks = static_cast<int64_t>(bytes / kChunk);
   if (mode == 2)
     stream_reg_kernel<<<workgroups, kThreads, 0, stream>>>(static_cast<const uint4*>(src),
                                                            static_cast<int64_t>(bytes / 16 / workgroups), sink);
+  else if (mode == 3)
+    stream_lds_kernel<true><<<workgroups, kThreads, 0, stream>>>(static_cast<const char*>(src), nchunks, 1, sink);
   else
-    stream_lds_kernel<<<workgroups, kThreads, 0, stream>>>(static_cast<const char*>(src), nchunks, mode == 0 ? 1 : 0,
-                                                           sink);
+    stream_lds_kernel<false><<<workgroups, kThreads, 0, stream>>>(static_cast<const char*>(src), nchunks,
+                                                                  mode == 0 ? 1 : 0, sink);
   return hipGetLastError() == hipSuccess ? TREEPO_OK : TREEPO_EHIP;
 }
 

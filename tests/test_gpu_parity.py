@@ -1,9 +1,9 @@
 """GPU parity: the HIP path (through the C-ABI) vs the fp64 oracle.
 
 Bar: max |out - oracle| <= 2e-3 and max |lse - oracle| <= 2e-3 over every
-compared element (bf16 inputs, fp32 accumulation).  Small workloads are
-compared in full; the large ones at full size on sampled leaves that the
-oracle computes one by one.  Both the cascade (tree) path and the per-leaf
+compared element (bf16 inputs, fp32 accumulation).  Every workload is
+compared in full, at full size: every leaf of every tree (the oracle works
+one tree at a time).  Both the cascade (tree) path and the per-leaf
 baseline are checked, plus determinism and edge cases (ragged tails,
 zero-length nodes, one-token chains, duplicate and interior leaves, GQA
 group sizes from 1 to 48, D = 64 and 128).
@@ -117,15 +117,67 @@ def test_ragged_and_degenerate_shapes():
             _check(dt, mode, tag=f"ragged-d{d}")
 
 
+def _oracle_by_tree(dt):
+    """The oracle over every call position, one tree at a time (the oracle's
+    per-node cache then holds one tree's fp64 K/V at a time)."""
+    log, cfg = dt.log, dt.cfg
+    model = M.replay(log, cfg.block_tokens, dt.num_blocks, max(log.n_nodes, 1))
+    q = query_bits(cfg.seed, 0, len(log.leaves), cfg.hq, cfg.d)
+    by_tree = {}
+    for p, x in enumerate(log.leaves):
+        by_tree.setdefault(model.nodes[x]["tree_id"], []).append(p)
+    ref = np.empty((len(log.leaves), cfg.hq, cfg.d))
+    ref_lse = np.empty((len(log.leaves), cfg.hq))
+    for t, pos in sorted(by_tree.items()):
+        o, l = A.tree_decode(model, dt.data, log.leaves, q, cfg.scale, positions=pos)
+        ref[pos], ref_lse[pos] = o, l
+    return ref, ref_lse
+
+
 @pytest.mark.parametrize("cfg_id", [3, 4, 5, 6])
-def test_large_configs_sampled(cfg_id):
+def test_large_configs_every_leaf(cfg_id):
+    """The full-size workloads, every leaf of every tree against the oracle,
+    in both modes; the two modes (different plans: stream cuts, partial slots)
+    also agree with each other."""
     import torch
     dt = _dt(cfg_id)
-    n = len(dt.leaves)
-    rng = np.random.default_rng(cfg_id)
-    pos = sorted(set([0, n - 1] + [int(x) for x in rng.choice(n, size=min(n, 14), replace=False)]))
+    outs = {}
     for mode in (0, 1):
-        _check(dt, mode, positions=pos, tag=f"cfg{cfg_id}")
+        out, lse = dt.decode(mode)
+        torch.cuda.synchronize()
+        outs[mode] = (out.cpu().numpy(), lse.cpu().numpy())
+        assert np.isfinite(outs[mode][0]).all() and np.isfinite(outs[mode][1]).all()
+    print(f"[cfg{cfg_id}] {len(dt.leaves)} leaves decoded; oracle ...", flush=True)
+    ref, ref_lse = _oracle_by_tree(dt)
+    for mode in (0, 1):
+        o, l = outs[mode]
+        err, err_l = float(np.abs(o - ref).max()), float(np.abs(l - ref_lse).max())
+        print(f"[parity cfg{cfg_id} all {len(dt.leaves)} leaves mode={mode}] max|out-oracle|={err:.3e} "
+              f"mean={float(np.abs(o - ref).mean()):.3e} max|lse-oracle|={err_l:.3e}", flush=True)
+        assert err <= TOL and err_l <= TOL
+    assert float(np.abs(outs[0][0] - outs[1][0]).max()) <= TOL
+    del dt
+    torch.cuda.empty_cache()
+
+
+def test_many_entries_per_key():
+    """Leaves whose (leaf, KV head) keys collect hundreds of partial entries
+    (a 40,000-token root cut over every stream, then a short fork): the
+    combine's rounds past the first 64 entries."""
+    import torch
+    ops = [("root", 40_000), ("append", [0], [40_000]), ("fork", 0, 2, 64), ("append", [1, 2], [17, 64])]
+    log = _Log(ops, [1, 2, 0], {0: 40_000, 1: 17, 2: 64})
+    log.n_nodes = 3
+    dt = _dt(cfg=_random_cfg(91, 8, 2, 128), log=log)
+    pieces, rowsets, _, _ = dt.ctx.export_plan(dt.leaves, 0)
+    count = {}
+    for pc in pieces:
+        for x in rowsets[pc[0]:pc[0] + pc[1]]:
+            count[(int(x), int(pc[3]))] = count.get((int(x), int(pc[3])), 0) + 1
+    print(f"[entries per key] {sorted(count.values())}", flush=True)
+    assert min(count.values()) > 128
+    for mode in (0, 1):
+        _check(dt, mode, tag="many-entries")
     del dt
     torch.cuda.empty_cache()
 
