@@ -356,12 +356,18 @@ def _probes(work_bytes):
            "staging_4GiB_GBps": round(big / (_timed(lambda: bench_stream(src, big, sink, 3, wgs), 10) * 1e-3)
                                       / 1e9, 1)}
     step = wgs * chunk
-    size = max(step, int(work_bytes) // step * step)
+    # rotating buffers of the workload's size (at most the 4 GiB source; at
+    # most 20 of them), every one inside the source
+    size = min(big // step, max(1, int(work_bytes) // step)) * step
     n = max(1, min(big // size, 20))
+    assert size % step == 0 and 0 < n * size <= big
+
     it = [0]
 
     def rot():
-        bench_stream(src[(it[0] % n) * size:], size, sink, 3, wgs)
+        off = (it[0] % n) * size
+        assert off + size <= big
+        bench_stream(src[off:off + size], size, sink, 3, wgs)
         it[0] += 1
     res["staging_workload_size_GBps"] = round(size / (_timed(rot, 4 * n) * 1e-3) / 1e9, 1)
     res["staging_workload_bytes"] = size
