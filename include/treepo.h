@@ -252,6 +252,25 @@ int32_t treepo_paged_decode_naive(treepo_ctx* ctx, int32_t n_leaves, const int32
                                   const void* q, float scale, float* out, float* lse,
                                   void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code that may not call
+ * hipMalloc, tight serving loops, harnesses that forbid it): the cascade
+ * decode of treepo_tree_decode with the same arguments and results, minus
+ * the workspace.  The plan image and the partial slots live in a static
+ * device array of the library, 64 MiB per device (each device the library
+ * runs on holds its own until the process ends), not in memory the call
+ * allocates: it calls no hipMalloc, hipFree or pinned-memory allocation
+ * (plan and length uploads are copied from pageable host memory, and a plan
+ * evicted from the cache keeps its image buffer for a later allocating
+ * call to free).  Every call on a device shares that array and leaves its
+ * contents there; the plan image is uploaded only when another plan used
+ * the array since, and partial slots are always rewritten before they are
+ * read.  Calls that overlap on one device race: issue them on one stream or
+ * synchronise between them.  EWORKSPACE when the plan image plus the
+ * partial slots exceed 64 MiB (treepo_last_error gives the bytes needed);
+ * otherwise the errors of treepo_tree_decode. */
+int32_t treepo_tree_decode_noalloc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, const void* q,
+                                   float scale, float* out, float* lse, hipStream_t stream);
+
 /* ---- branching budget ---------------------------------------------------- */
 
 #define TREEPO_BUDGET_EVEN 0       /* budget transfer: spread evenly (Sec. 2.2)                */

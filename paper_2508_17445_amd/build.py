@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtreepo.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["tree_core.cpp", "treepo_api.cpp", "kernels.hip", "advantage.hip", "bench_kernels.hip"]
+SOURCES = ["tree_core.cpp", "treepo_api.cpp", "kernels.hip", "advantage.hip", "bench_kernels.hip", "noalloc.hip"]
 ARCH = "gfx950"
 # Packed fp32 ops are kept out of the generated code.  The first 16 dwords of
 # every kernel's arguments are preloaded into SGPRs at dispatch, so a kernel's

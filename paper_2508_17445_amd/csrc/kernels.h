@@ -33,6 +33,14 @@ struct DecodeArgs {
   float* lse;              // fp32 [n_leaves][Hq] or null
 };
 
+// The decode entry point that allocates nothing keeps a plan image and the
+// partial slots in one static device array of this many bytes per device
+// (noalloc.hip).  noalloc_scratch gives its address on the current device
+// (looked up once per device) and the slot recording which plan image it
+// holds (0: none).
+constexpr size_t kNoAllocScratchBytes = size_t{64} << 20;
+hipError_t noalloc_scratch(void** ptr, uint64_t** holder);
+
 // One workgroup per stream: every piece's node partials.
 hipError_t launch_partial(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);

@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -41,7 +42,10 @@ constexpr double kOddXcdSpeed = 0.935;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+std::atomic<uint64_t> g_plan_uid{0};
+
 struct CachedPlan {
+  uint64_t uid = 0;  // process-unique id of this plan build
   uint64_t version = 0;
   int32_t mode = 0;
   std::vector<int32_t> leaves;
@@ -118,6 +122,7 @@ struct treepo_ctx {
   // the next decode uploads the host table on its stream.
   bool live = false;
   bool dev_len_stale = true;
+  std::vector<int32_t> len_stage;  // host lengths of the last pageable upload (no-alloc decode)
   double prof_ms[TREEPO_KERNEL_KINDS] = {};
   int64_t prof_n[TREEPO_KERNEL_KINDS] = {};
 
@@ -262,7 +267,7 @@ hipError_t free_retired(RetiredImage& r) {
 // stream of its last decode marks when no kernel reads it any more (a device
 // synchronisation if it was read on several streams).  Keeps the list short
 // by freeing the oldest buffers.
-hipError_t retire_image(treepo_ctx* ctx, CachedPlan& cp) {
+hipError_t retire_image(treepo_ctx* ctx, CachedPlan& cp, bool trim = true) {
   hipError_t e = hipSuccess;
   if (cp.up_ev) {
     (void)hipEventDestroy(cp.up_ev);
@@ -290,7 +295,7 @@ hipError_t retire_image(treepo_ctx* ctx, CachedPlan& cp) {
   cp.dev_cap = 0;
   cp.dev_valid = false;
   cp.multi_stream = false;
-  while (ctx->retired.size() > kMaxRetired) {
+  while (trim && ctx->retired.size() > kMaxRetired) {
     const hipError_t f = free_retired(ctx->retired.front());
     ctx->retired.erase(ctx->retired.begin());
     if (e == hipSuccess) e = f;
@@ -348,7 +353,11 @@ hipError_t stage_image(treepo_ctx* ctx, CachedPlan& cp, hipStream_t s) {
   return hipSuccess;
 }
 
-int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode, CachedPlan** out) {
+// The cached plan for these leaves and mode, built if needed.  With
+// may_free false an evicted plan's image is retired without freeing any
+// device memory (the no-alloc entry point).
+int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode, CachedPlan** out,
+                 bool may_free = true) {
   ++ctx->clock;
   for (CachedPlan& cp : ctx->plans) {
     // with device lengths a plan outlives appends (it covers unfrozen nodes up
@@ -384,6 +393,7 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   cp.off_part_ml = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * 2 * sizeof(float));
   cp.ws_bytes = off;
+  cp.uid = ++g_plan_uid;
   cp.version = ctx->live ? ctx->tree.shape_version() : ctx->tree.version();
   cp.mode = mode;
   cp.leaves.assign(leaves, leaves + n);
@@ -391,7 +401,7 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   if (static_cast<int>(ctx->plans.size()) >= kPlanCache) {
     auto lru = std::min_element(ctx->plans.begin(), ctx->plans.end(),
                                 [](const CachedPlan& a, const CachedPlan& b) { return a.last_use < b.last_use; });
-    hipError_t e = retire_image(ctx, *lru);
+    hipError_t e = retire_image(ctx, *lru, may_free);
     if (e != hipSuccess) return hip_fail(ctx, e, "plan cache");
     *lru = std::move(cp);
     *out = &*lru;
@@ -402,38 +412,40 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   return TREEPO_OK;
 }
 
-int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q, float scale,
-               float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream, int32_t mode) {
-  if (!ctx) return TREEPO_EINVAL;
+int32_t check_decode_args(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q, float scale,
+                          float* out) {
   if (!q || !out) return fail(ctx, TREEPO_EINVAL, "null q or out");
   if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return fail(ctx, TREEPO_EINVAL, "q must be 16-byte aligned");
   if (!(scale > 0.f) || !std::isfinite(scale)) return fail(ctx, TREEPO_EINVAL, "scale must be positive and finite");
   std::string err;
-  int32_t st = ctx->tree.check_leaves(n, leaves, &err);
-  if (st != treepo::kOk) return fail(ctx, st, err);
-  CachedPlan* cp = nullptr;
-  st = get_plan(ctx, n, leaves, mode, &cp);
-  if (st != TREEPO_OK) return st;
-  if (!ws || ws_bytes < cp->ws_bytes || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
-    return fail(ctx, TREEPO_EWORKSPACE,
-                "workspace missing, smaller than treepo_decode_workspace_size or not 256-byte aligned");
-  char* wsb = static_cast<char*>(ws);
-  {
-    const hipError_t e = stage_image(ctx, *cp, stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "plan upload");
+  const int32_t st = ctx->tree.check_leaves(n, leaves, &err);
+  return st == treepo::kOk ? TREEPO_OK : fail(ctx, st, err);
+}
+
+// Uploads the host length table to node_len on `s` when it is stale: through
+// the pinned ring, or (pinned false) straight from pageable host memory kept
+// in the context.
+hipError_t stage_lengths(treepo_ctx* ctx, hipStream_t s, bool pinned) {
+  if (!ctx->live || !ctx->dev_len_stale) return hipSuccess;
+  const auto& nd = ctx->tree.nodes();
+  std::vector<int32_t>& lens = ctx->len_stage;
+  lens.resize(nd.size());
+  for (size_t i = 0; i < nd.size(); ++i) lens[i] = nd[i].len;
+  if (!lens.empty()) {
+    const hipError_t e = pinned ? upload(ctx, ctx->cfg.node_len, lens.data(), lens.size() * sizeof(int32_t), s)
+                                : hipMemcpyAsync(ctx->cfg.node_len, lens.data(), lens.size() * sizeof(int32_t),
+                                                 hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
   }
-  const char* img = static_cast<const char*>(cp->dev);
-  if (ctx->live && ctx->dev_len_stale) {
-    const auto& nd = ctx->tree.nodes();
-    std::vector<int32_t> lens(nd.size());
-    for (size_t i = 0; i < nd.size(); ++i) lens[i] = nd[i].len;
-    if (!lens.empty()) {
-      hipError_t e = upload(ctx, ctx->cfg.node_len, lens.data(), lens.size() * sizeof(int32_t), stream);
-      if (e != hipSuccess) return hip_fail(ctx, e, "length table upload");
-    }
-    ctx->dev_len_stale = false;
-  }
-  const Plan& p = cp->plan;
+  ctx->dev_len_stale = false;
+  return hipSuccess;
+}
+
+// Launches the node-partial and combine kernels of a plan whose image is at
+// `img` (device) with its partial slots in `wsb` (device).
+int32_t launch_decode(treepo_ctx* ctx, const CachedPlan& cp, const char* img, char* wsb, int32_t n, const void* q,
+                      float scale, float* out, float* lse, hipStream_t stream) {
+  const Plan& p = cp.plan;
   treepo::DecodeArgs a;
   a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
   a.v_pool = static_cast<const uint16_t*>(ctx->cfg.v_pool);
@@ -445,12 +457,12 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   a.q = static_cast<const uint16_t*>(q);
   a.scale_log2 = scale * 1.4426950408889634f;
   a.node_len = static_cast<const int32_t*>(ctx->cfg.node_len);
-  a.blocks = reinterpret_cast<const int32_t*>(img + cp->off_blocks);
+  a.blocks = reinterpret_cast<const int32_t*>(img + cp.off_blocks);
   a.block_ints = p.block_ints;
   a.n_streams = static_cast<int32_t>(p.streams.size());
-  a.part_o = reinterpret_cast<float*>(wsb + cp->off_part_o);
-  a.part_ml = reinterpret_cast<float*>(wsb + cp->off_part_ml);
-  a.comb_count = reinterpret_cast<const int32_t*>(img + cp->off_comb);
+  a.part_o = reinterpret_cast<float*>(wsb + cp.off_part_o);
+  a.part_ml = reinterpret_cast<float*>(wsb + cp.off_part_ml);
+  a.comb_count = reinterpret_cast<const int32_t*>(img + cp.off_comb);
   a.emax = p.emax;
   a.n_leaves = n;
   a.out = out;
@@ -468,6 +480,60 @@ int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q,
   });
   if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
   return TREEPO_OK;
+}
+
+int32_t decode(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q, float scale,
+               float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream, int32_t mode) {
+  if (!ctx) return TREEPO_EINVAL;
+  int32_t st = check_decode_args(ctx, n, leaves, q, scale, out);
+  if (st != TREEPO_OK) return st;
+  CachedPlan* cp = nullptr;
+  st = get_plan(ctx, n, leaves, mode, &cp);
+  if (st != TREEPO_OK) return st;
+  if (!ws || ws_bytes < cp->ws_bytes || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return fail(ctx, TREEPO_EWORKSPACE,
+                "workspace missing, smaller than treepo_decode_workspace_size or not 256-byte aligned");
+  hipError_t e = stage_image(ctx, *cp, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "plan upload");
+  e = stage_lengths(ctx, stream, true);
+  if (e != hipSuccess) return hip_fail(ctx, e, "length table upload");
+  return launch_decode(ctx, *cp, static_cast<const char*>(cp->dev), static_cast<char*>(ws), n, q, scale, out, lse,
+                       stream);
+}
+
+// The cascade decode with the plan image and partial slots in the library's
+// static device scratch (treepo_tree_decode_noalloc).  The scratch records
+// which plan image it holds, so a plan is uploaded only when another plan
+// (of any context) used the scratch since; uploads go straight from the
+// plan's pageable host image, so no pinned staging is allocated.
+int32_t decode_noalloc(treepo_ctx* ctx, int32_t n, const int32_t* leaves, const void* q, float scale, float* out,
+                       float* lse, hipStream_t stream) {
+  if (!ctx) return TREEPO_EINVAL;
+  int32_t st = check_decode_args(ctx, n, leaves, q, scale, out);
+  if (st != TREEPO_OK) return st;
+  CachedPlan* cp = nullptr;
+  st = get_plan(ctx, n, leaves, TREEPO_MODE_TREE, &cp, false);
+  if (st != TREEPO_OK) return st;
+  const size_t img_bytes = align_up(std::max<size_t>(cp->blob.size(), 1));
+  if (img_bytes + cp->ws_bytes > treepo::kNoAllocScratchBytes)
+    return fail(ctx, TREEPO_EWORKSPACE,
+                "decode needs " + std::to_string(img_bytes + cp->ws_bytes) + " bytes of scratch (plan image " +
+                    std::to_string(img_bytes) + ", partial slots " + std::to_string(cp->ws_bytes) +
+                    "); the no-alloc scratch holds " + std::to_string(treepo::kNoAllocScratchBytes));
+  void* base = nullptr;
+  uint64_t* holder = nullptr;
+  hipError_t e = treepo::noalloc_scratch(&base, &holder);
+  if (e != hipSuccess) return hip_fail(ctx, e, "no-alloc scratch");
+  char* sb = static_cast<char*>(base);
+  if (*holder != cp->uid) {
+    *holder = 0;
+    e = hipMemcpyAsync(sb, cp->blob.data(), cp->blob.size(), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "plan upload (scratch)");
+    *holder = cp->uid;
+  }
+  e = stage_lengths(ctx, stream, false);
+  if (e != hipSuccess) return hip_fail(ctx, e, "length table upload");
+  return launch_decode(ctx, *cp, sb, sb + img_bytes, n, q, scale, out, lse, stream);
 }
 
 // Splits a validated append into block-aligned pieces (source rows in call order).
@@ -1011,6 +1077,11 @@ int32_t treepo_tree_decode(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
                            float scale, float* out, float* lse, void* workspace, size_t ws_bytes,
                            hipStream_t stream) {
   return decode(ctx, n_leaves, leaves, q, scale, out, lse, workspace, ws_bytes, stream, TREEPO_MODE_TREE);
+}
+
+int32_t treepo_tree_decode_noalloc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, const void* q,
+                                   float scale, float* out, float* lse, hipStream_t stream) {
+  return decode_noalloc(ctx, n_leaves, leaves, q, scale, out, lse, stream);
 }
 
 int32_t treepo_paged_decode_naive(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,

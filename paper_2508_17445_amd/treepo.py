@@ -71,6 +71,7 @@ def load_library(path: str = LIB_PATH):
         "treepo_decode_workspace_size": (_i32, [_p, _i32, _pi32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
         "treepo_tree_decode": (_i32, [_p, _i32, _pi32, _p, ctypes.c_float, _p, _p, _p, ctypes.c_size_t, _p]),
         "treepo_paged_decode_naive": (_i32, [_p, _i32, _pi32, _p, ctypes.c_float, _p, _p, _p, ctypes.c_size_t, _p]),
+        "treepo_tree_decode_noalloc": (_i32, [_p, _i32, _pi32, _p, ctypes.c_float, _p, _p, _p]),
         "treepo_num_nodes": (_i32, [_p, _pi32]),
         "treepo_export_nodes": (_i32, [_p, _pi32, _i32, _pi32]),
         "treepo_export_chains": (_i32, [_p, _i32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32, _pi32]),
@@ -222,6 +223,12 @@ class Context:
     def paged_decode_naive(self, leaves, q, scale, out, lse, workspace, ws_bytes=None, stream=None):
         self._decode(self.lib.treepo_paged_decode_naive, "treepo_paged_decode_naive", leaves, q, scale,
                      out, lse, workspace, ws_bytes, stream)
+
+    def tree_decode_noalloc(self, leaves, q, scale, out, lse, stream=None):
+        lv = _arr32(leaves)
+        self._check(self.lib.treepo_tree_decode_noalloc(self.h, len(lv), _ptr32(lv), _dev(q), ctypes.c_float(scale),
+                                                        _dev(out), _dev(lse), _stream(stream)),
+                    "treepo_tree_decode_noalloc")
 
     # ---- export ------------------------------------------------------------
     def num_nodes(self) -> int:

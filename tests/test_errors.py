@@ -168,3 +168,24 @@ def test_prefill_codes_and_workspace_layout():
     # nothing to prefill: no device work, no state change
     ctx.prefill([a, b], [0, 0], None, None, None, 0.1, None, None, None, 0)
     assert np.array_equal(ctx.export_nodes(), snap)
+
+
+def test_noalloc_decode_rejects_plans_beyond_its_scratch():
+    """The decode that allocates nothing keeps a plan image and the partial
+    slots in 64 MiB of static device scratch; a decode needing more is
+    EWORKSPACE (checked on the host, before any device call), with the bytes
+    needed in the message."""
+    from tests.lib_helpers import replay_host
+    from workloads import CONFIGS, build_call_log
+    c = CONFIGS[3]
+    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    log = build_call_log(3)
+    replay_host(ctx, log)
+    assert ctx.workspace_size(log.leaves, 0) > 64 << 20
+    with pytest.raises(TreePOError) as e:
+        ctx.tree_decode_noalloc(log.leaves, FAKE_POOL, c.scale, FAKE_POOL, None)
+    assert e.value.code == T.EWORKSPACE and "no-alloc scratch holds 67108864" in str(e.value)
+    # the usual argument checks come first
+    assert _code(ctx.tree_decode_noalloc, log.leaves, 0, c.scale, FAKE_POOL, None) == T.EINVAL
+    assert _code(ctx.tree_decode_noalloc, log.leaves, FAKE_POOL, -1.0, FAKE_POOL, None) == T.EINVAL
+    assert _code(ctx.tree_decode_noalloc, [10 ** 6], FAKE_POOL, c.scale, FAKE_POOL, None) == T.EINVAL
