@@ -253,8 +253,9 @@ def _warm_gpu(w, seconds=0.5):
     import torch
     t0 = time.perf_counter()
     i = 0
+    modes = (0,) if w.no_naive else (0, 1)
     while time.perf_counter() - t0 < seconds:
-        for m in (0, 1):
+        for m in modes:
             w.step(m, i, decode_only=True)
         i += 1
         if i % 16 == 0:
@@ -499,6 +500,14 @@ def _summarize_trace(cfg_id, d):
             lines.append(f"| {kname}, {label} | {blk[0]['Grid_Size_X'] if 'Grid_Size_X' in blk[0] else blk[0].get('Grid_Size', '')} "
                          f"| {len(v)} | {statistics.mean(v):.2f} | {statistics.median(v):.2f} | "
                          f"{_pct(v, 0.1):.2f} | {_pct(v, 0.9):.2f} | {min(v):.2f} | {max(v):.2f} |")
+    stats = []
+    try:
+        for r in _csv_rows(d, "kernel_stats.csv"):
+            if any(k in r["Name"] for k in ("partial_kernel", "combine_kernel", "kv_append_kernel")):
+                stats.append(f"| {r['Name'][:60]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                             f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    except SystemExit:
+        pass
     alg = b["roofline"]["algorithmic_bytes_per_launch"]
     t_avg = avg[("partial_kernel", 0)]
     txt = f"""# Kernel trace: decode step on config {cfg_id} ({_workload_name(cfg_id)})
@@ -506,7 +515,7 @@ def _summarize_trace(cfg_id, d):
 Command (repository root `$R` on the GPU machine):
 
 ```
-cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/trace -o run -- python3 -u $R/bench.py --config {cfg_id} --steps {steps} --warmup {warm} --no-cpu --no-probes > $R/gpurun_out/prof/c{cfg_id}/trace/bench.json
+cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/trace -o run -- python3 -u $R/bench.py --config {cfg_id} --steps {steps} --warmup {warm} --no-cpu --no-probes --no-naive > $R/gpurun_out/prof/c{cfg_id}/trace/bench.json
 python3 bench.py --summarize trace --config {cfg_id} --dir gpurun_out/prof/c{cfg_id}/trace
 ```
 
@@ -517,6 +526,13 @@ the bench's timing passes after the W = {warm} warm-up steps of each mode
 | kernel, schedule | grid (threads) | dispatches | avg | median | p10 | p90 | min | max |
 |---|---|---|---|---|---|---|---|---|
 """ + "\n".join(lines) + f"""
+
+rocprofv3 `--stats` summary of the same run (every dispatch of the kernel,
+the untimed warm-up steps included; microseconds):
+
+| kernel | calls | avg | min | max |
+|---|---|---|---|---|
+""" + "\n".join(stats) + f"""
 
 Algorithmic bytes per tree launch (unique KV of the decoded chains at the
 timed steps): {alg} -> {alg / t_avg / 1e6:.3f} TB/s = {alg / t_avg / 1e6 / 8:.3f} of 8 TB/s on the
