@@ -487,7 +487,8 @@ def _summarize_trace(cfg_id, d):
     per_mode = warm + 2 * steps + max(steps, DIST_MIN_STEPS)   # the launches of _time_mode per mode
     modes = 2 if "naive_baseline" in b else 1
     lines, avg = [], {}
-    for kname in ("partial_kernel", "combine_kernel", "kv_append_kernel"):
+    names = ("partial_kernel", "combine_kernel") + (("kv_append_kernel",) if "append_avg_ms" in b else ())
+    for kname in names:
         ks = [r for r in rows if kname in r["Kernel_Name"]]
         if not ks:
             continue
@@ -503,7 +504,7 @@ def _summarize_trace(cfg_id, d):
     stats = []
     try:
         for r in _csv_rows(d, "kernel_stats.csv"):
-            if any(k in r["Name"] for k in ("partial_kernel", "combine_kernel", "kv_append_kernel")):
+            if any(k in r["Name"] for k in names):
                 stats.append(f"| {r['Name'][:60]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                              f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
     except SystemExit:
