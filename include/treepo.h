@@ -392,10 +392,13 @@ int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  *     valid = first_row | (n_rows << 16);
  *   per query segment, the element offset (x * Hq + kv_head * G) * D of the
  *     G query rows of the piece's leaf x, padded to a multiple of 4;
- *   per query segment, the partial row (key * E + e) * G of the piece's entry
- *     for its leaf x, key = x * Hkv + kv_head, where e counts the pieces
- *     before it (plan order) that cover the same key and E is the largest
- *     count over the keys; padded to a multiple of 4.
+ *   per query segment, the partial row (base(key) + e) * G of the piece's
+ *     entry for its leaf x, key = x * Hkv + kv_head, where e counts the
+ *     pieces before it (plan order) that cover the same key; base(key) =
+ *     key * E (E the largest count over the keys) when the combine's
+ *     speculative first round, the O rows of min(E, 32) entries of every key
+ *     (N keys * G * min(E, 32) * (4 D + 8) bytes), is at most 8 MiB, else
+ *     the sum of the counts of the keys before it; padded to a multiple of 4.
  * Pass a null array to query the sizes only. */
 int32_t treepo_export_blocks(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves, int32_t mode,
                              int32_t* blocks, int32_t* block_ints, int32_t* n_streams);

@@ -23,8 +23,9 @@ struct DecodeArgs {
   int32_t n_streams;
   float* part_o;           // fp32 [partial_rows][D], unnormalised
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
-  const int32_t* comb_count;  // per key (leaf, KV head): partial entries to merge
-  int32_t emax;               // entries per key at most (partial slot stride)
+  const int2* comb;           // per key (leaf, KV head): {first entry, entries to merge}
+  int32_t emax;               // entries per key at most (partial slot stride of strided plans)
+  bool compact;               // entries packed by prefix sums (else key k starts at entry k * emax)
   // Profiling: when set, the launch records these events at the kernel's
   // start and end (hipExtLaunchKernelGGL), so they time the kernel alone.
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;

@@ -697,17 +697,25 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
 
 // ---- combine ------------------------------------------------------------------
 //
-// One wave per (leaf, query head h = g G + h'): over the n = comb_count[key]
-// partial entries of key = (leaf, g), m* = max m_e, L = sum l_e 2^(m_e - m*),
-// out = sum 2^(m_e - m*) O_e / L, lse = (m* + log2 L) ln 2.  Partials without
-// tokens (m = -inf) contribute nothing.  Entry e sits at the fixed row
-// (key emax + e) G + h', so the (m, l) pairs (one entry per lane) and the
-// first 16 O rows (every lane its d-slice) are loaded in the same round as the
-// count, for all emax entries the slots can hold; entries past the count
-// (stale values of earlier calls) are masked out by selection.  A key with up
-// to 16 entries costs one memory round trip; later rows follow in batches of
-// 16 independent loads.  The sum runs in the plan's fixed entry order, so
-// results are deterministic.
+// One wave per (leaf, query head h = g G + h'): over the n partial entries of
+// key = (leaf, g), m* = max m_e, L = sum l_e 2^(m_e - m*), out = sum
+// 2^(m_e - m*) O_e / L, lse = (m* + log2 L) ln 2.  Partials without tokens
+// (m = -inf) contribute nothing.  Entry e of the key sits at partial row
+// (base + e) G + h'; comb[key] = {base, n}.  Two layouts:
+//   strided (base = key E, E the largest count): the (m, l) pairs of entries
+//     0..min(E, 64)-1 (one per lane) and the O rows of entries
+//     0..min(E, R0)-1 (every lane its d-slice) are loaded in the same round
+//     as the count, so a key with up to R0 entries costs one memory round
+//     trip; entries past the count (stale values of earlier calls) are
+//     masked out by selection.  For plans whose speculative reads are small
+//     (the decode is then latency bound).
+//   compact (base = the prefix sum of the counts): {base, n} first, then
+//     exactly the n entries' rows -- a second round trip, but no row is read
+//     that the key does not hold (plans with many keys, where the combine is
+//     bound by the bytes it reads).
+// Later entries follow in batches of 16 independent row loads.  The sum runs
+// in the plan's fixed entry order, so results are deterministic.
+
 // Adds sum over entries k in [k0, cnt) of the round starting at entry `base`
 // of w_k O_k to o (w_k in lane k of w), 16 independent row loads at a time.
 template <int D>
@@ -735,14 +743,13 @@ __device__ __forceinline__ void combine_rows(float (&o)[D / 64], const float* __
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __restrict__ comb_count, int32_t emax,
+template <int D, int R0, bool kCompact>
+__global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restrict__ comb, int32_t emax,
                                                            const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml,
                                                            float* __restrict__ out, float* __restrict__ lse,
                                                            int32_t n_leaves, int32_t hq, int32_t hkv, int32_t group) {
   constexpr int kPL = D / 64;
-  constexpr int kGroup = 16;
   const int lane = threadIdx.x & 63;
   const int gw = static_cast<int>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (gw >= n_leaves * hq) return;
@@ -751,27 +758,42 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
   const int g = h / group;
   const int hp = h % group;
   const int key = x * hkv + g;
-  const int64_t row0 = static_cast<int64_t>(key) * emax * group + hp;  // entry e: row0 + e * group
-  const int n = comb_count[key];
+  int n, base, lim;
+  if (kCompact) {
+    const int2 c = comb[key];
+    base = __builtin_amdgcn_readfirstlane(c.x);
+    n = __builtin_amdgcn_readfirstlane(c.y);
+    lim = n;          // rows the key holds
+  } else {
+    base = key * emax;
+    n = comb[key].y;  // lands with the speculative loads below
+    lim = emax;       // rows its slots can hold
+  }
+  const int64_t row0 = static_cast<int64_t>(base) * group + hp;  // entry e: row0 + e * group
 
-  // round 0, issued before the count is known: (m, l) of entries 0..63 and O
-  // rows of entries 0..15, each clamped to the slots
-  const int avail = emax < 64 ? emax : 64;
+  // round 0: (m, l) of entries 0..min(lim, 64)-1 and O rows of entries
+  // 0..min(lim, R0)-1
+  const int avail = lim < 64 ? lim : 64;
+  const int avail_o = lim < R0 ? lim : R0;
   const int64_t my_row = row0 + static_cast<int64_t>(lane < avail ? lane : avail - 1) * group;
-  float v[kGroup][kPL];
+  float v[R0][kPL];
 #pragma unroll
-  for (int i = 0; i < kGroup; ++i) {
-    const int k = i < avail ? i : avail - 1;
-    const float* po = part_o + (row0 + static_cast<int64_t>(k) * group) * D + lane * kPL;
+  for (int i = 0; i < R0; ++i) {
+    if (i < avail_o) {
+      const float* po = part_o + (row0 + static_cast<int64_t>(i) * group) * D + lane * kPL;
 #pragma unroll
-    for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+      for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < kPL; ++j) v[i][j] = 0.f;
+    }
   }
   const float m_ld = part_ml[2 * my_row];
   const float l_ld = part_ml[2 * my_row + 1];
   // keeps every round-0 load ahead of the count-dependent code (otherwise the
   // compiler may sink a load under the weight test, a second round trip)
 #pragma unroll
-  for (int i = 0; i < kGroup; ++i)
+  for (int i = 0; i < R0; ++i)
 #pragma unroll
     for (int j = 0; j < kPL; ++j) asm volatile("" ::"v"(v[i][j]));
   asm volatile("" ::"v"(m_ld), "v"(l_ld));
@@ -790,17 +812,17 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
 #pragma unroll
   for (int j = 0; j < kPL; ++j) o[j] = 0.f;
 #pragma unroll
-  for (int i = 0; i < kGroup; ++i) {
+  for (int i = 0; i < R0; ++i) {
     // entries past the count have w = 0 and may hold anything: select, not multiply
     const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), i));
 #pragma unroll
     for (int j = 0; j < kPL; ++j) o[j] = wk == 0.f ? o[j] : fmaf(wk, v[i][j], o[j]);
   }
-  if (n > kGroup) {
-    combine_rows<D>(o, part_o, row0, group, 0, kGroup, cnt, w, lane);
-    for (int base = 64; base < n; base += 64) {
-      cnt = n - base < 64 ? n - base : 64;
-      const int64_t r = row0 + static_cast<int64_t>(base + (lane < cnt ? lane : 0)) * group;
+  if (n > R0) {
+    combine_rows<D>(o, part_o, row0, group, 0, R0, cnt, w, lane);
+    for (int b = 64; b < n; b += 64) {
+      cnt = n - b < 64 ? n - b : 64;
+      const int64_t r = row0 + static_cast<int64_t>(b + (lane < cnt ? lane : 0)) * group;
       mi = lane < cnt ? part_ml[2 * r] : -INFINITY;
       li = lane < cnt ? part_ml[2 * r + 1] : 0.f;
       float cm = mi;
@@ -816,7 +838,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int32_t* __rest
 #pragma unroll
       for (int j = 0; j < kPL; ++j) o[j] *= keep;
       run_m = nm;
-      combine_rows<D>(o, part_o, row0, group, base, 0, cnt, w, lane);
+      combine_rows<D>(o, part_o, row0, group, b, 0, cnt, w, lane);
     }
   }
   const float inv = 1.f / run_l;
@@ -1233,15 +1255,26 @@ hipError_t launch_partial(const DecodeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int D>
+void launch_combine_d(const DecodeArgs& a, dim3 grid, hipStream_t s) {
+  if (a.compact)
+    launch_timed(a, combine_kernel<D, 16, true>, grid, s, a.comb, a.emax, a.part_o, a.part_ml, a.out, a.lse,
+                 a.n_leaves, a.hq, a.hkv, a.group);
+  else if (a.emax > 16)
+    launch_timed(a, combine_kernel<D, 32, false>, grid, s, a.comb, a.emax, a.part_o, a.part_ml, a.out, a.lse,
+                 a.n_leaves, a.hq, a.hkv, a.group);
+  else
+    launch_timed(a, combine_kernel<D, 16, false>, grid, s, a.comb, a.emax, a.part_o, a.part_ml, a.out, a.lse,
+                 a.n_leaves, a.hq, a.hkv, a.group);
+}
+
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   const int64_t waves = static_cast<int64_t>(a.n_leaves) * a.hq;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
   if (a.d == 128)
-    launch_timed(a, combine_kernel<128>, grid, s, a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
-                 a.n_leaves, a.hq, a.hkv, a.group);
+    launch_combine_d<128>(a, grid, s);
   else
-    launch_timed(a, combine_kernel<64>, grid, s, a.comb_count, a.emax, a.part_o, a.part_ml, a.out, a.lse,
-                 a.n_leaves, a.hq, a.hkv, a.group);
+    launch_combine_d<64>(a, grid, s);
   return hipGetLastError();
 }
 

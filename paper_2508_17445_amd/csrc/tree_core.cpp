@@ -587,15 +587,30 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
 
   // ---- partial slots: entry e of key (leaf x, KV head g) -------------------------------
   // Every piece adds one entry to each of its leaves' keys, in piece order (the
-  // fixed merge order); entry e of key k holds rows (k * emax + e) * G + h'.
+  // fixed merge order); entry e of key k holds rows (base[k] + e) * G + h'.
+  // Strided layout (base[k] = k * emax) when the combine's speculative first
+  // round (the O rows of min(emax, 32) entries of every key) reads little;
+  // else compact (base = the prefix sum of the counts).
   const int64_t nkeys = static_cast<int64_t>(n_leaves) * Hkv;
   out->comb_count.assign(nkeys, 0);
   for (const Piece& pc : out->pieces)
     for (int32_t j = 0; j < pc.n_leaves; ++j)
       ++out->comb_count[static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g];
   out->emax = 1;
-  for (int32_t c : out->comb_count) out->emax = std::max(out->emax, c);
-  out->partial_rows = nkeys * out->emax * G;
+  int64_t entries = 0;
+  for (int32_t c : out->comb_count) {
+    out->emax = std::max(out->emax, c);
+    entries += c;
+  }
+  const int64_t spec_bytes = nkeys * G * std::min(out->emax, 32) * (static_cast<int64_t>(p.head_dim) * 4 + 8);
+  out->compact = spec_bytes > kStridedCombineBytes;
+  out->comb_base.assign(nkeys, 0);
+  int64_t acc_e = 0;
+  for (int64_t k = 0; k < nkeys; ++k) {
+    out->comb_base[k] = static_cast<int32_t>(out->compact ? acc_e : k * out->emax);
+    acc_e += out->comb_count[k];
+  }
+  out->partial_rows = (out->compact ? entries : nkeys * out->emax) * G;
   if (out->partial_rows > INT32_MAX) {
     if (err) *err = "too many partial rows";
     return kEUnsupported;
@@ -607,7 +622,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
       const Stream& st = out->streams[pc.stream];
       for (int32_t j = 0; j < pc.n_leaves; ++j) {
         const int64_t key = static_cast<int64_t>(out->rowsets[pc.rowset_begin + j]) * Hkv + pc.g;
-        out->dests[st.seg_off + pc.seg_begin + j] = static_cast<int32_t>((key * out->emax + next[key]++) * G);
+        out->dests[st.seg_off + pc.seg_begin + j] = static_cast<int32_t>((out->comb_base[key] + next[key]++) * G);
       }
     }
   }

@@ -99,6 +99,12 @@ class Tree {
 
 enum PlanMode : int32_t { kModeTree = 0, kModeNaive = 1 };
 
+// The combine reads the O rows of the first min(emax, 32) entries of every
+// key before it knows the key's count when that costs at most this many
+// bytes (one memory round trip); larger plans pack the entries and read
+// exactly the rows each key holds.
+constexpr int64_t kStridedCombineBytes = int64_t{8} << 20;
+
 // Tokens per decode tile (half of a 64-token pool block).
 constexpr int32_t kPlanTileTokens = 32;
 // Upper bounds on the tiles, query segments and pieces of one stream (sized
@@ -230,11 +236,15 @@ struct Plan {
   int32_t block_ints = 0;
   // Partial slots.  Key (leaf x, KV head g) = x * Hkv + g has comb_count[key]
   // entries (one per piece over its chain, in plan order, at most emax); entry
-  // e holds the partial rows (key * emax + e) * G + h' for query heads
-  // g * G + h'.  dests (parallel to segs) gives, per (piece, leaf), the row of
-  // its entry's h' = 0.
+  // e holds the partial rows (comb_base[key] + e) * G + h' for query heads
+  // g * G + h', with comb_base[key] = key * emax (strided) or the prefix sum
+  // of the counts (compact: plans whose strided combine would read more than
+  // kStridedCombineBytes in its speculative first round).  dests (parallel to
+  // segs) gives, per (piece, leaf), the row of its entry's h' = 0.
   std::vector<int32_t> comb_count;
+  std::vector<int32_t> comb_base;
   int32_t emax = 0;
+  bool compact = false;
   std::vector<int32_t> dests;
   int64_t partial_rows = 0;
   int64_t unique_kv_tokens = 0;   // tokens streamed per KV head (tree: unique)

@@ -383,10 +383,15 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
     off = align_up(off + bytes);
   };
   place(&cp.off_blocks, p.blocks.size() * sizeof(int32_t));
-  place(&cp.off_comb, p.comb_count.size() * sizeof(int32_t));
+  std::vector<int32_t> comb(2 * p.comb_count.size());
+  for (size_t k = 0; k < p.comb_count.size(); ++k) {
+    comb[2 * k] = p.comb_base[k];
+    comb[2 * k + 1] = p.comb_count[k];
+  }
+  place(&cp.off_comb, comb.size() * sizeof(int32_t));
   cp.blob.assign(off, 0);
   put(cp.blob, cp.off_blocks, p.blocks);
-  put(cp.blob, cp.off_comb, p.comb_count);
+  put(cp.blob, cp.off_comb, comb);
   off = 0;
   cp.off_part_o = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
@@ -462,8 +467,9 @@ int32_t launch_decode(treepo_ctx* ctx, const CachedPlan& cp, const char* img, ch
   a.n_streams = static_cast<int32_t>(p.streams.size());
   a.part_o = reinterpret_cast<float*>(wsb + cp.off_part_o);
   a.part_ml = reinterpret_cast<float*>(wsb + cp.off_part_ml);
-  a.comb_count = reinterpret_cast<const int32_t*>(img + cp.off_comb);
+  a.comb = reinterpret_cast<const int2*>(img + cp.off_comb);
   a.emax = p.emax;
+  a.compact = p.compact;
   a.n_leaves = n;
   a.out = out;
   a.lse = lse;
