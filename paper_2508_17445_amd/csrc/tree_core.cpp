@@ -313,10 +313,12 @@ struct Run {
 
 // A piece's query tile takes a step of the tile pipeline like a KV tile (the
 // loads of 64 rows, repeats of the last row for a small piece) but no
-// matrix work.  Swept on the five workloads (0.25-1.0): 0.5 is within 0.3% of the
-// best on each; 1.0 makes 192-cost streams of long one-leaf sequences hold
-// 191 KV tiles, 5% slower on config 5's per-leaf plan.
-constexpr double kQTileCost = 0.5;
+// matrix work; with the piece's start and end (partial-row stores, softmax
+// state reset) it costs about 1.2 KV tiles: a least-squares fit of
+// per-workgroup end times of config-2 decodes (16 leaves x 7680 tokens,
+// 35 launches) to the streams' tile and piece counts gave 1.22 per piece
+// with tile costs within 0.1 of tile_cost below.
+constexpr double kQTileCost = 1.2;
 // Guided stream sizes when the work takes several rounds of workgroups.
 constexpr double kGuide = 2.0;
 constexpr double kGuideMinCost = 8.0;
