@@ -280,14 +280,17 @@ def test_stream_sizes(cfg, cus, xcds, regime):
             xs = die / (np.mean(die[:xcds]) if xcds > 1 else 1.0)
             want = np.clip(xs * (kv.sum() - before) / (2 * slots), 8, 192)
             # a stream closes on the first tile that reaches its size (plus the
-            # query tiles of a piece it opens) unless its tile table fills first
-            assert (cost[:-1] <= want[:-1] + 2.6 + 2.5).all()
-            # ... or one of its tables (tiles, query segments, pieces) fills first
+            # query tiles of a piece it opens), or finishes the sequence it is
+            # in when at most its size (kSnapFinish = 1) is left of it
+            assert (cost[:-1] <= 2.0 * want[:-1] + 2 * 2.6 + 2.5).all()
+            # it closes early only at a sequence boundary within half its size
+            # (kSnapEarly = 0.5), or when one of its tables (tiles, query
+            # segments, pieces) fills
             hdr = ctx.export_blocks(log.leaves, mode)[:, :3]
             table_full = (hdr[:, 1] >= 256 - 3) | (hdr[:, 2] > 256 - 128 // (c.hq // c.hkv)) | (hdr[:, 0] >= 127)
-            short = cost[:-1] < want[:-1] - 1e-6
+            short = cost[:-1] < 0.5 * want[:-1] - 2 * 2.6 - 2.5
             assert table_full[:-1][short].all()
-            assert cost[-1] <= want[-1] + 2.6 + 2.5
+            assert cost[-1] <= 2.0 * want[-1] + 2 * 2.6 + 2.5
     assert regime in seen
 
 
