@@ -172,7 +172,7 @@ class Workload:
             self.uniq_tok += self.n_leaves
             self.logical_tok += self.n_leaves
         uniq_bytes = self.uniq_tok * self.kv_bytes_per_tok
-        self.n_rep = args.replicas or max(1, math.ceil(1.2e9 / uniq_bytes))
+        self.n_rep = args.replicas or min(16, max(1, math.ceil(1.2e9 / uniq_bytes)))
         self.reps = {}
         self.bufs = {}
         self.appended = {0: 0, 1: 0}
@@ -394,8 +394,13 @@ def _oracle_rate(cfg_id, seconds, one_core=False):
     from workloads.device import NodeData
     cfg, log = CONFIGS[cfg_id], build_call_log(cfg_id)
     model = M.replay(log, cfg.block_tokens, 1 << 30, 1 << 30)
+    # workloads of many trees: the leaves of the first tree (a bounded sample)
+    pos = list(range(len(log.leaves)))
+    if len(pos) > 64:
+        first = model.nodes[log.leaves[0]]["tree_id"]
+        pos = [p for p, x in enumerate(log.leaves) if model.nodes[x]["tree_id"] == first]
     data = NodeData(cfg, log)
-    data.prefetch(sorted({n for x in log.leaves for n in model.chain(x)}))
+    data.prefetch(sorted({n for p in pos for n in model.chain(log.leaves[p])}))
     q = query_bits(cfg.seed, 0, len(log.leaves), cfg.hq, cfg.d)
     ctx = contextlib.nullcontext()
     if one_core:
@@ -405,24 +410,27 @@ def _oracle_rate(cfg_id, seconds, one_core=False):
         threads = _blas_threads()
         reps, t0 = 0, time.perf_counter()
         while True:
-            A.tree_decode(model, data, log.leaves, q, cfg.scale)
+            A.tree_decode(model, data, log.leaves, q, cfg.scale,
+                          positions=None if len(pos) == len(log.leaves) else pos)
             reps += 1
             if time.perf_counter() - t0 >= seconds:
                 break
         dt = time.perf_counter() - t0
-    return len(log.leaves) * reps / dt, reps, dt, threads
+    return len(pos) * reps / dt, reps, dt, threads, len(pos), len(log.leaves)
 
 
 def _cpu_baseline(cfg_id, seconds):
-    rate, reps, dt, threads = _oracle_rate(cfg_id, seconds)
+    rate, reps, dt, threads, n_pos, n_all = _oracle_rate(cfg_id, seconds)
     host = len(os.sched_getaffinity(0))
+    what = "full decode step(s) of the same workload" if n_pos == n_all else \
+        f"decode(s) of the {n_pos} leaves of its first tree (of {n_all} leaves)"
     out = {"value": round(rate, 2), "unit": "leaf-token-steps/s", "cores": min(host, threads), "kind": "oracle",
-           "sample": f"{reps} full decode step(s) of the same workload (fp64 numpy, chains materialised per "
-                     f"leaf) in {dt:.1f} s; host has {host} cores, BLAS threads {threads}"}
+           "sample": f"{reps} {what} (fp64 numpy, chains materialised per leaf) in {dt:.1f} s; host has "
+                     f"{host} cores, BLAS threads {threads}"}
     if cfg_id in (1, 2):
         one = {}
         for c in (1, 2):
-            r1, n1, d1, _ = _oracle_rate(c, min(seconds, 4.0), one_core=True)
+            r1, n1, d1, _, _, _ = _oracle_rate(c, min(seconds, 4.0), one_core=True)
             one[f"config{c}"] = {"value": round(r1, 2), "steps": n1, "seconds": round(d1, 2)}
         out["one_core"] = one
     return out
