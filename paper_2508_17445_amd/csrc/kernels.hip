@@ -200,6 +200,7 @@ __device__ __forceinline__ void wait_tile(int k, int ntot) {
 struct Scalars {
   int32_t hq, hkv, group;
   float scale_log2;
+  int32_t write_through;  // partial rows stored write-through (large plans)
 };
 
 #define TREEPO_PARTIAL_PARAMS                                                         \
@@ -273,6 +274,24 @@ __device__ __forceinline__ int64_t partial_row(const BlockTables& bt, int seg, i
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Stores 16 bytes of a partial row.  Write-through (sc1: device scope) for
+// plans with compact slots, whose partial rows far exceed the L2 (45-83 MB
+// for the 64-prompt batch rollout, the irregular 32-prompt tree and the
+// 16k-token long-context tree): their write-back from L2 while the KV stream
+// is read cost up to a fifth of the kernel (a timing build without the
+// stores ran the irregular tree 21% faster), and writing them through took
+// the batch rollout's kernel from 1.258 to 1.179 ms, the irregular tree's
+// from 0.408 to 0.399 and the long-context tree's from 1.916 to 1.846.
+// Small plans, whose few MB of partials stay in the L2, keep write-back
+// stores (16 leaves of 7680 tokens, write-through: 35.6 -> 37.2 us).  The
+// s_nop covers the store-data hazard the compiler cannot see through the asm.
+__device__ __forceinline__ void store_partial(float* p, const f32x4& v, bool write_through) {
+  if (write_through)
+    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" :: "v"(p), "v"(v) : "memory");
+  else
+    *reinterpret_cast<f32x4*>(p) = v;
+}
 
 __device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
@@ -481,7 +500,7 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
     const int64_t slot = partial_row(bt, pc.seg, m, sc.group);
 #pragma unroll
     for (int db = 0; db < kDBw; ++db)
-      *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * (db0 + db) + 4 * a) = acc[db];
+      store_partial(part_o + slot * D + 16 * (db0 + db) + 4 * a, acc[db], sc.write_through != 0);
     if (a == 0 && db0 == 0) {
       part_ml[slot * 2 + 0] = m_ref;
       part_ml[slot * 2 + 1] = l_sum;
@@ -620,7 +639,7 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
       const int64_t slot = partial_row(bt, pc.seg, m, sc.group);
 #pragma unroll
       for (int db = 0; db < kDB; ++db)
-        *reinterpret_cast<f32x4*>(part_o + slot * D + 16 * db + 4 * a) = acc[i][db];
+        store_partial(part_o + slot * D + 16 * db + 4 * a, acc[i][db], sc.write_through != 0);
       if (a == 0) {
         part_ml[slot * 2 + 0] = m_ref[i];
         part_ml[slot * 2 + 1] = l;
@@ -1244,7 +1263,7 @@ void launch_timed(const A& a, F kernel, dim3 grid, hipStream_t s, Args... args) 
 hipError_t launch_partial(const DecodeArgs& a, hipStream_t s) {
   if (a.n_streams <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(a.n_streams));
-  const Scalars sc{a.hq, a.hkv, a.group, a.scale_log2};
+  const Scalars sc{a.hq, a.hkv, a.group, a.scale_log2, a.compact ? 1 : 0};
   if (a.block_ints <= 0 || a.block_ints > kMaxBlockInts || a.block_ints % 4 != 0) return hipErrorInvalidValue;
   if (a.d == 128)
     launch_timed(a, partial_kernel<128>, grid, s, a.blocks, a.block_ints, a.node_len, a.k_pool, a.v_pool, a.q,

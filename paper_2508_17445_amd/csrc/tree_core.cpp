@@ -315,7 +315,7 @@ struct Run {
 // loads of 64 rows, repeats of the last row for a small piece) but no
 // matrix work; with the piece's start and end (partial-row stores, softmax
 // state reset) it costs about 1.2 KV tiles: a least-squares fit of
-// per-workgroup end times of config-2 decodes (16 leaves x 7680 tokens,
+// per-workgroup end times of decodes of a 16-leaf tree (leaves of 7680 tokens,
 // 35 launches) to the streams' tile and piece counts gave 1.22 per piece
 // with tile costs within 0.1 of tile_cost below.
 constexpr double kQTileCost = 1.2;
@@ -326,10 +326,11 @@ constexpr double kGuide = 2.0;
 // kSnapFinish, close before a new sequence within kSnapEarly of the size.
 // Partial rows written by the decode kernel cost far more than their bytes
 // (they reach memory while the KV stream is read: removing them entirely
-// made config 3's kernel 16% faster), so fewer cuts pay for less even
-// stream sizes.  Measured against no snapping, kernel time: configs 3, 4
-// and 5 -2.5%, -1.4%, -2.7% at (1.0, 0.5); (0.5, 0.25) gave -2.4%,
-// -2.4%, +4%.
+// made the 64-prompt batch rollout's kernel 16% faster), so fewer cuts pay
+// for less even stream sizes.  Measured against no snapping, kernel time of
+// the batch rollout, the irregular 32-prompt tree and the 16k-token
+// long-context tree: -2.5%, -1.4%, -2.7% at (1.0, 0.5); (0.5, 0.25) gave
+// -2.4%, -2.4%, +4%.
 constexpr double kSnapFinish = 1.0;
 constexpr double kSnapEarly = 0.5;
 constexpr double kGuideMinCost = 8.0;

@@ -32,7 +32,7 @@ constexpr int kRing = 4;
 constexpr int32_t kDefaultComputeUnits = 256;
 constexpr int32_t kComputeUnitsPerXcd = 32;
 // Planner tunables, fitted to per-workgroup timestamps of back-to-back
-// config-2 decodes (16 leaves of 7680 tokens): the second workgroup on a CU
+// decodes of a 16-leaf tree (leaves of 7680 tokens): the second workgroup on a CU
 // progressed about 0.80 as fast as the first (the dispatcher fills every CU's
 // first slot before any second one), and the odd-numbered XCDs streamed
 // 0.93-0.94 as many tiles per microsecond as the even ones on every box
