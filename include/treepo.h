@@ -68,15 +68,18 @@ extern "C" {
 typedef struct treepo_ctx treepo_ctx;
 
 /*
- * Pool shape.  K pool, device bf16, layout [Hkv][num_blocks][B][D]: token row
- * r = block * B + offset of KV head g starts at element ((g*num_blocks*B)+r)*D.
- * V pool, device bf16, layout [Hkv][num_blocks][2][D][B/2]: every half block
- * of 32 tokens is stored transposed, so element (g, r, d) is at
- * (g*num_blocks*B + (r/32)*32)*D + d*32 + r%32.
- * head_dim D must be 64 or 128, block_tokens B must be 64 (the decode kernels
- * stream 32-token half blocks), Hq % Hkv == 0 and Hq / Hkv <= 128.  Pools are caller-owned,
- * 16-byte aligned, and must stay valid until treepo_destroy; their contents
- * need no initialisation.
+ * Pool shape (R = num_blocks * B rows per KV head).  K pool, device bf16,
+ * layout [Hkv][R][D]: token row r = block * B + offset of KV head g starts at
+ * element (g*R + r)*D.  V pool, device bf16, layout [Hkv][R/16][D][16]: every
+ * group of 16 rows is stored transposed, so element (g, r, d) is at
+ * (g*R + (r/16)*16)*D + d*16 + r%16.
+ * head_dim D must be 64 or 128, block_tokens B 16, 32 or 64 (blocks are the
+ * unit in which nodes reserve pool rows; the kernels stream 32-token tiles
+ * from any 16-row boundary), Hq % Hkv == 0 and Hq / Hkv <= 128.  With B = 16
+ * the pool's last block is never reserved: a node's last tile may read up to
+ * 16 rows past its blocks, and this keeps every read inside the pool.  Pools
+ * are caller-owned, 16-byte aligned, and must stay valid until
+ * treepo_destroy; their contents need no initialisation.
  *
  * node_len (optional, device int32[max_nodes], caller-owned, contents kept by
  * the library, valid until treepo_destroy): the nodes' token counts on the
@@ -373,8 +376,8 @@ int32_t treepo_export_desc(treepo_ctx* ctx, int32_t n_leaves, const int32_t* lea
  * TREEPO_TILE_FIELDS int32 each {block, node, tile_in_node, valid_tokens}
  * (valid_tokens as of planning; with node_len a plan is reused while nodes
  * grow and the kernels read the current counts of tiles not yet full):
- * tile k of a node holds its tokens [32k, 32k+32) and lives in pool block
- * block_begin + k/2.  *n_streams receives the stream count.  Pass null arrays
+ * tile k of a node holds its tokens [32k, 32k+32) and starts in pool block
+ * block_begin + 32k/B.  *n_streams receives the stream count.  Pass null arrays
  * to query the counts only. */
 int32_t treepo_export_plan(treepo_ctx* ctx, int32_t n_leaves, const int32_t* leaves,
                            int32_t mode, int32_t* pieces, int32_t* rowsets, int32_t* tiles,

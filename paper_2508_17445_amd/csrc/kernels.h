@@ -7,13 +7,13 @@
 
 namespace treepo {
 
-constexpr int kTile = 64;  // tokens per pool block
+constexpr int kTile = 64;  // rows of an append piece at most (a 64-row chunk of the pool)
 
 // Device views of the decode plan and buffers (record layouts in tree_core.h).
 struct DecodeArgs {
-  const uint16_t* k_pool;  // bf16 [Hkv][num_blocks][64][D]
-  const uint16_t* v_pool;  // bf16 [Hkv][num_blocks][2][D][32] (V^T per 32-token half block)
-  int64_t num_blocks;
+  const uint16_t* k_pool;  // bf16 [Hkv][R][D], R = pool rows per KV head
+  const uint16_t* v_pool;  // bf16 [Hkv][R / 16][D][16] (V^T per 16-row group)
+  int64_t pool_rows;       // R
   int32_t hq, hkv, group, d;
   const uint16_t* q;       // bf16 [n_leaves][Hq][D]
   float scale_log2;        // softmax scale * log2(e)
@@ -74,9 +74,10 @@ hipError_t launch_advantage(const AdvantageArgs& a, hipStream_t s);
 
 // Prefill: causal attention of tokens just appended to a node over its chain.
 // A work item is up to kPrefillRows consecutive new tokens of one sequence;
-// the kernel runs it for every query head.  Tile records (int2): x = half
-// block 2 * block + half (32-token tile of the pools, KV head added by the
-// kernel), y = (chain position of the tile's first token) << 6 | tokens.
+// the kernel runs it for every query head.  Tile records (int2): x = (first
+// row of the 32-token tile in KV head 0's pool rows) / 16 (the kernel adds
+// KV head g's R / 16), y = (chain position of the tile's first token) << 6 |
+// tokens.
 constexpr int32_t kPrefillRows = 128;
 struct PrefillItem {
   int32_t row0;      // packed row (of q, out, lse) of the item's first token
@@ -89,7 +90,7 @@ struct PrefillItem {
 struct PrefillArgs {
   const uint16_t* k_pool;
   const uint16_t* v_pool;
-  int64_t num_blocks;
+  int64_t pool_rows;         // pool rows per KV head (a multiple of 16)
   int32_t hq, hkv, d;
   const uint16_t* q;         // bf16 [rows][Hq][D]
   const PrefillItem* items;  // n_items, longest first
@@ -104,8 +105,8 @@ struct PrefillArgs {
 };
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s);
 
-// One block-aligned run of appended tokens: source rows [src_row, +count) go
-// to token offsets [off, off + count) of pool block `block` (off + count <= 64).
+// One run of appended tokens: source rows [src_row, +count) go to pool rows
+// [64 block + off, +count) of every KV head (off + count <= 64).
 struct AppendPiece {
   int32_t src_row;
   int32_t block;
@@ -116,13 +117,13 @@ struct AppendPiece {
 // node_len (device lengths table or null) receives len[i] at node[i] for the
 // n_upd appended nodes (n_upd <= n_pieces).
 hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool,
-                            uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
+                            uint16_t* v_pool, int64_t pool_rows, int32_t hkv, int32_t d,
                             const AppendPiece* pieces, int32_t n_pieces, const int32_t* upd_node,
                             const int32_t* upd_len, int32_t n_upd, int32_t* node_len, hipStream_t s);
 // The same with pieces and updates (x = node, y = length) in device memory,
 // in one launch.
 hipError_t launch_kv_append_dev(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool, uint16_t* v_pool,
-                                int64_t num_blocks, int32_t hkv, int32_t d, const AppendPiece* pieces,
+                                int64_t pool_rows, int32_t hkv, int32_t d, const AppendPiece* pieces,
                                 int32_t n_pieces, const int2* upd, int32_t n_upd, int32_t* node_len,
                                 hipStream_t s);
 

@@ -12,10 +12,11 @@
 // running max, sum) in fp32.  The combine merges, per leaf and query head, the
 // partials of its chain (exact log-sum-exp algebra).
 //
-// Layouts: K pool [Hkv][blocks][64][D] (token rows), V pool
-// [Hkv][blocks][2][D][32] (each 32-token half block transposed, so a d-row
-// holds 32 consecutive tokens).  The decode kernels stream half blocks
-// (32-token tiles), each one contiguous 8 KiB (D = 128) range per pool.
+// Layouts (R = pool rows per KV head = blocks * B): K pool [Hkv][R][D]
+// (token rows), V pool [Hkv][R / 16][D][16] (each 16-row group transposed,
+// so a d-row of a group holds 16 consecutive tokens).  The kernels stream
+// 32-token tiles -- 32 consecutive rows of a node from a 16-row boundary --,
+// each one contiguous 8 KiB (D = 128) range per pool.
 #include "kernels.h"
 
 #include <hip/hip_ext.h>
@@ -44,8 +45,9 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 
 // ---- KV tile staging ----------------------------------------------------------
 //
-// A tile is 32 tokens: one half of a 64-token pool block.  LDS tile = K rows
-// [32][D] then V^T rows [D][32], in 16-byte chunks with XOR swizzles that make
+// A tile is 32 tokens: two consecutive 16-row groups of the pool.  LDS tile =
+// K rows [32][D] then V^T rows [D][32] (chunks 0-1 of a d-row from the first
+// group, 2-3 from the second), in 16-byte chunks with XOR swizzles that make
 // the compute reads conflict free (per 8-lane LDS phase):
 //   K: chunk c of token row r sits at position c ^ ((r & 3) | ((r >> 1) & 4));
 //      the MFMA reader takes one chunk of rows {R+0..3, R+8..11} -- 8 distinct
@@ -123,6 +125,17 @@ __device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_
 template <int D>
 constexpr int dma_per_tile() { return D / 32; }
 
+// Rows of a transposed V group of the pool.
+constexpr int kVGroup = 16;
+
+// Global byte offset, within a tile's V^T data, of 16-byte chunk q (tokens
+// 8q .. 8q + 7) of d-row d: chunks 0-1 lie in the tile's first 16-row group
+// ([D][16], d-rows of 32 bytes), chunks 2-3 in the second.
+template <int D>
+__device__ __forceinline__ uint32_t v_chunk_off(int d, int q) {
+  return (q >> 1) * (D * kVGroup * 2) + d * (kVGroup * 2) + (q & 1) * 16;
+}
+
 // The tile pipeline of a workgroup: LDS buffers, this lane's byte offsets in
 // a tile's K and V^T ranges for each of its loads (the swizzles of the LDS
 // layout applied on the global side), and the record of the next tile to
@@ -149,18 +162,19 @@ __device__ __forceinline__ void pipe_init(Pipe<D>& p, uint32_t buf0, int ntot, i
     const int row = c / kKChunks;
     p.koff[j] = row * (D * 2) + (((c % kKChunks) ^ k_swz(row)) << 4);
     const int vrow = c >> 2;
-    p.voff[j] = vrow * (kSub * 2) + (((c & 3) ^ v_swz(vrow)) << 4);
+    p.voff[j] = v_chunk_off<D>(vrow, (c & 3) ^ v_swz(vrow));
   }
 }
 
-// Stages half block `hb` (= 2 * (g * num_blocks + block) + half) into the LDS
-// buffer at byte address `dst`.
+// Stages the tile whose first row is pool row 16 t16 (KV head included: t16 =
+// (g * R + first row of head g's pool) / 16) into the LDS buffer at byte
+// address `dst`.
 // An empty live tile keeps its place in the load count, but every lane reads
 // the tile's first 16 bytes (one request per load instruction).
 template <int D>
 __device__ __forceinline__ void dma_tile(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                         int hb, bool empty, uint32_t dst, const Pipe<D>& p, int wave) {
-  const int64_t off = static_cast<int64_t>(hb) * kSub * D;
+                                         int t16, bool empty, uint32_t dst, const Pipe<D>& p, int wave) {
+  const int64_t off = static_cast<int64_t>(t16) * kVGroup * D;
   const uint16_t* kg = kpool + off;
   const uint16_t* vg = vpool + off;
   const uint32_t vd = dst + kSub * D * 2;
@@ -881,22 +895,21 @@ struct AppendBatch {
   int2 upd[kMaxPieces];
 };
 
-// One block-aligned piece for KV head blockIdx.y: K rows copied with 16-byte
-// moves, V transposed through padded LDS into the pool's [D][32] half blocks.
+// One piece for KV head blockIdx.y: K rows copied with 16-byte moves, V
+// transposed through padded LDS into the pool's [D][16] groups.
 template <int D>
 __device__ __forceinline__ void append_piece(const uint16_t* __restrict__ ksrc, const uint16_t* __restrict__ vsrc,
                                              uint16_t* __restrict__ kpool, uint16_t* __restrict__ vpool,
-                                             int64_t num_blocks, int32_t hkv, const AppendPiece& pc,
-                                             uint16_t* vt) {
+                                             int64_t rows, int32_t hkv, const AppendPiece& pc, uint16_t* vt) {
   constexpr int kPad = D + 2;
   const int g = blockIdx.y;
-  const int64_t blk = static_cast<int64_t>(g) * num_blocks + pc.block;
+  const int64_t row0 = static_cast<int64_t>(g) * rows + static_cast<int64_t>(pc.block) * kTile + pc.off;
   constexpr int kCh = D / 8;
   for (int idx = threadIdx.x; idx < pc.count * kCh; idx += kThreads) {
     const int i = idx / kCh, c = idx % kCh;
     const int64_t src = (static_cast<int64_t>(pc.src_row + i) * hkv + g) * D + c * 8;
     const uint4 kvv = *reinterpret_cast<const uint4*>(ksrc + src);
-    *reinterpret_cast<uint4*>(kpool + (blk * kTile + pc.off + i) * D + c * 8) = kvv;
+    *reinterpret_cast<uint4*>(kpool + (row0 + i) * D + c * 8) = kvv;
     const uint4 vv = *reinterpret_cast<const uint4*>(vsrc + src);
     const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
@@ -908,8 +921,8 @@ __device__ __forceinline__ void append_piece(const uint16_t* __restrict__ ksrc, 
   __syncthreads();
   for (int idx = threadIdx.x; idx < D * pc.count; idx += kThreads) {
     const int d = idx / pc.count, i = idx % pc.count;
-    const int p = pc.off + i;  // token within the 64-token block
-    vpool[(blk * kTile + (p / kSub) * kSub) * D + d * kSub + (p % kSub)] = vt[i * kPad + d];
+    const int64_t p = row0 + i;  // pool row (KV head included; g * rows is a multiple of 16)
+    vpool[(p / kVGroup) * kVGroup * D + d * kVGroup + p % kVGroup] = vt[i * kPad + d];
   }
 }
 
@@ -919,13 +932,13 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
                                                              const uint16_t* __restrict__ vsrc,
                                                              uint16_t* __restrict__ kpool,
                                                              uint16_t* __restrict__ vpool,
-                                                             int64_t num_blocks, int32_t hkv,
+                                                             int64_t rows, int32_t hkv,
                                                              int32_t* __restrict__ node_len, AppendBatch b) {
   __shared__ uint16_t vt[kTile * (D + 2)];
   if (node_len != nullptr && blockIdx.y == 0 && threadIdx.x == 0 && static_cast<int>(blockIdx.x) < b.n_upd)
     node_len[b.upd[blockIdx.x].x] = b.upd[blockIdx.x].y;
   if (static_cast<int>(blockIdx.x) >= b.n) return;
-  append_piece<D>(ksrc, vsrc, kpool, vpool, num_blocks, hkv, b.p[blockIdx.x], vt);
+  append_piece<D>(ksrc, vsrc, kpool, vpool, rows, hkv, b.p[blockIdx.x], vt);
 }
 
 // The same with the pieces and length updates in device memory: one launch
@@ -933,7 +946,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint16_t* __r
 template <int D>
 __global__ __launch_bounds__(kThreads) void kv_append_dev_kernel(
     const uint16_t* __restrict__ ksrc, const uint16_t* __restrict__ vsrc, uint16_t* __restrict__ kpool,
-    uint16_t* __restrict__ vpool, int64_t num_blocks, int32_t hkv, int32_t* __restrict__ node_len,
+    uint16_t* __restrict__ vpool, int64_t rows, int32_t hkv, int32_t* __restrict__ node_len,
     const AppendPiece* __restrict__ pieces, int32_t n, const int2* __restrict__ upd, int32_t n_upd) {
   __shared__ uint16_t vt[kTile * (D + 2)];
   if (node_len != nullptr && blockIdx.y == 0 && threadIdx.x == 0 && static_cast<int>(blockIdx.x) < n_upd) {
@@ -942,7 +955,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_dev_kernel(
   }
   if (static_cast<int>(blockIdx.x) >= n) return;
   const AppendPiece pc = pieces[blockIdx.x];
-  append_piece<D>(ksrc, vsrc, kpool, vpool, num_blocks, hkv, pc, vt);
+  append_piece<D>(ksrc, vsrc, kpool, vpool, rows, hkv, pc, vt);
 }
 
 
@@ -990,14 +1003,15 @@ struct PfPipe {
       } else {
         const int c = (sl - kKSlots) * 64 + lane;
         const int vrow = c >> 2;
-        off[j] = vrow * (kSub * 2) + (((c & 3) ^ v_swz(vrow)) << 4);
+        off[j] = v_chunk_off<D>(vrow, (c & 3) ^ v_swz(vrow));
       }
     }
   }
-  // Stages half block hb into the buffer at LDS byte address dst.
+  // Stages the tile whose first row is pool row 16 t16 into the buffer at
+  // LDS byte address dst.
   __device__ __forceinline__ void issue(const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool,
-                                        int hb, uint32_t dst, int wave) const {
-    const int64_t o = static_cast<int64_t>(hb) * kSub * D;
+                                        int t16, uint32_t dst, int wave) const {
+    const int64_t o = static_cast<int64_t>(t16) * kVGroup * D;
 #pragma unroll
     for (int j = 0; j < kSlots; ++j) {
       const int sl = wave * kSlots + j;
@@ -1024,7 +1038,7 @@ template <int D, int W>
 __global__ __launch_bounds__(64 * W, W / 2) void prefill_kernel(
     const uint16_t* __restrict__ kpool, const uint16_t* __restrict__ vpool, const uint16_t* __restrict__ q,
     const PrefillItem* __restrict__ items, const int2* __restrict__ tiles, const int32_t* __restrict__ sched,
-    float* __restrict__ out, float* __restrict__ lse, int32_t n_sched, int32_t num_blocks, int32_t hq, int32_t hkv,
+    float* __restrict__ out, float* __restrict__ lse, int32_t n_sched, int32_t rows16, int32_t hq, int32_t hkv,
     float scale_log2) {
   constexpr int kKS = D / 32;  // QK k-steps
   constexpr int kDB = D / 16;  // PV output d-blocks
@@ -1051,7 +1065,7 @@ __global__ __launch_bounds__(64 * W, W / 2) void prefill_kernel(
   const PrefillItem it = items[item_i];
   const int nk = it.nk;
   const int2* __restrict__ tl = tiles + it.tile_off;
-  const int hb_base = 2 * g * num_blocks;
+  const int hb_base = g * rows16;  // KV head g's pool rows start at row 16 hb_base
 
   // Q^T operands: lane holds row kRows wave + 16 rb + r16, d chunk 4 ks + a
   uint4 qb[kRB][kKS];
@@ -1303,9 +1317,10 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
   if (a.n_sched <= 0 || a.n_sched % 8 != 0) return hipErrorInvalidValue;
   const int64_t group = a.hq / a.hkv;
   const int64_t wgs = static_cast<int64_t>(a.n_sched) * group;
-  if (wgs > 0x7FFFFFFF || 2 * a.hkv * a.num_blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  if (wgs > 0x7FFFFFFF || a.pool_rows % kVGroup != 0 || a.hkv * (a.pool_rows / kVGroup) > 0x7FFFFFFF)
+    return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(wgs));
-  const int32_t nb = static_cast<int32_t>(a.num_blocks);
+  const int32_t nb = static_cast<int32_t>(a.pool_rows / kVGroup);
   const dim3 block(64 * kPrefillWaves);
   if (a.d == 128)
     launch_timed_block(a, prefill_kernel<128, kPrefillWaves>, grid, block, s, a.k_pool, a.v_pool, a.q, a.items,
@@ -1317,7 +1332,7 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_kv_append_dev(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool, uint16_t* v_pool,
-                                int64_t num_blocks, int32_t hkv, int32_t d, const AppendPiece* pieces,
+                                int64_t rows, int32_t hkv, int32_t d, const AppendPiece* pieces,
                                 int32_t n_pieces, const int2* upd, int32_t n_upd, int32_t* node_len,
                                 hipStream_t s) {
   if (node_len == nullptr) n_upd = 0;
@@ -1325,16 +1340,16 @@ hipError_t launch_kv_append_dev(const uint16_t* k_src, const uint16_t* v_src, ui
   if (gx <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(hkv));
   if (d == 128)
-    kv_append_dev_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len,
+    kv_append_dev_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, rows, hkv, node_len,
                                                        pieces, n_pieces, upd, n_upd);
   else
-    kv_append_dev_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len,
+    kv_append_dev_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, rows, hkv, node_len,
                                                       pieces, n_pieces, upd, n_upd);
   return hipGetLastError();
 }
 
 hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_pool,
-                            uint16_t* v_pool, int64_t num_blocks, int32_t hkv, int32_t d,
+                            uint16_t* v_pool, int64_t rows, int32_t hkv, int32_t d,
                             const AppendPiece* pieces, int32_t n_pieces, const int32_t* upd_node,
                             const int32_t* upd_len, int32_t n_upd, int32_t* node_len, hipStream_t s) {
   if (node_len == nullptr) n_upd = 0;
@@ -1347,9 +1362,9 @@ hipError_t launch_kv_append(const uint16_t* k_src, const uint16_t* v_src, uint16
     const int32_t gx = b.n > b.n_upd ? b.n : b.n_upd;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(hkv));
     if (d == 128)
-      kv_append_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len, b);
+      kv_append_kernel<128><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, rows, hkv, node_len, b);
     else
-      kv_append_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, num_blocks, hkv, node_len, b);
+      kv_append_kernel<64><<<grid, kThreads, 0, s>>>(k_src, v_src, k_pool, v_pool, rows, hkv, node_len, b);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

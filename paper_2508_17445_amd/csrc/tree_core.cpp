@@ -358,7 +358,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     if (err) *err = "GQA group larger than the kernels' row limit";
     return kEUnsupported;
   }
-  if (2 * static_cast<int64_t>(Hkv) * p.num_blocks > INT32_MAX ||
+  if (static_cast<int64_t>(Hkv) * p.num_blocks * B / 16 > INT32_MAX ||
       static_cast<int64_t>(n_leaves) * p.num_q_heads * p.head_dim > INT32_MAX) {
     if (err) *err = "pool or query tensor too large for 32-bit tile and row offsets";
     return kEUnsupported;
@@ -405,13 +405,12 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
     for (int32_t n : r.nodes) {
       const int32_t ln = nd[n].len;
       constexpr int32_t T = kPlanTileTokens;
-      const int32_t per_block = B / T;
       // with device lengths an unfrozen node is planned up to its capacity
       const bool grows = p.live_lengths && nd[n].n_children == 0 && ln < nd[n].cap;
       const int32_t span = grows ? nd[n].cap : ln;
       for (int32_t k = 0; k * T < span; ++k) {
         Tile tl;
-        tl.block = nd[n].block_begin + k / per_block;
+        tl.block = nd[n].block_begin + k * T / B;  // the block of the tile's first token
         tl.node = n;
         tl.tile_in_node = k;
         tl.valid = std::max(0, std::min(T, ln - k * T));
@@ -596,7 +595,9 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         st->piece_end = static_cast<int32_t>(out->pieces.size());
         new_piece = false;
       }
-      const int32_t half = tl.tile_in_node & 1;
+      // first pool row of the tile over 16, KV head g's rows included
+      const int64_t row = (static_cast<int64_t>(sq.g) * p.num_blocks + nd[tl.node].block_begin) * B +
+                          static_cast<int64_t>(tl.tile_in_node) * kPlanTileTokens;
       int32_t valid = tl.valid;
       if (live) {
         valid = -1 - st->n_live++;
@@ -604,7 +605,7 @@ int32_t build_plan(const Tree& t, int32_t n_leaves, const int32_t* leaves, PlanM
         out->live.push_back(tl.tile_in_node * kPlanTileTokens);
       }
       out->stream_tiles.push_back(
-          StreamTile{static_cast<int32_t>(2 * (static_cast<int64_t>(sq.g) * p.num_blocks + tl.block) + half), valid});
+          StreamTile{static_cast<int32_t>(row / 16), valid});
       out->tiles.push_back(tl);
       ++st->n_tiles;
       ++out->pieces.back().n_tiles;

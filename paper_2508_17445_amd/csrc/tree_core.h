@@ -40,8 +40,13 @@ struct Node {
 
 class Tree {
  public:
+  // With 16-token blocks the pool's last block is never reserved: a node's
+  // last 32-token tile may reach 16 rows past its blocks, and this keeps
+  // such a tile inside the pool.
   Tree(int32_t block_tokens, int64_t num_blocks, int32_t max_nodes)
-      : B_(block_tokens), num_blocks_(num_blocks), max_nodes_(max_nodes) {}
+      : B_(block_tokens),
+        num_blocks_(block_tokens < 32 && num_blocks > 0 ? num_blocks - 1 : num_blocks),
+        max_nodes_(max_nodes) {}
 
   int32_t new_root(int32_t cap, int32_t* node_out, std::string* err);
   int32_t fork(int32_t parent, int32_t n, int32_t cap, int32_t* out, std::string* err);
@@ -160,8 +165,9 @@ struct Stream {
 constexpr int32_t kStreamInts = 8;
 static_assert(sizeof(Stream) == kStreamInts * sizeof(int32_t), "stream record size");
 
-// Device record of a tile.  KV tile: hb = 2 * (g * num_blocks + block) + half
-// >= 0 locates its K and V data, valid = tokens holding data (1..32), or, for
+// Device record of a tile.  KV tile: hb = (first pool row of the tile, KV
+// head g's g * num_blocks * B rows included) / 16 >= 0 locates its K and V
+// data, valid = tokens holding data (1..32), or, for
 // a live tile, valid = -1 - i: entry i = {node, base} of the stream's live
 // table, and the tile holds min(32, max(0, len(node) - base)) tokens at decode
 // time.  Query tile: hb = -1 - (the piece's first segment, stream-local),

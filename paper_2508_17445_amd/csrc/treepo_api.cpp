@@ -132,6 +132,11 @@ struct treepo_ctx {
 
 namespace {
 
+// Pool rows per KV head.
+int64_t pool_rows(const treepo_ctx* ctx) {
+  return static_cast<int64_t>(ctx->cfg.num_blocks) * ctx->cfg.block_tokens;
+}
+
 int32_t fail(treepo_ctx* ctx, int32_t code, const std::string& msg) {
   if (ctx) ctx->last_error = msg;
   return code;
@@ -454,7 +459,7 @@ int32_t launch_decode(treepo_ctx* ctx, const CachedPlan& cp, const char* img, ch
   treepo::DecodeArgs a;
   a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
   a.v_pool = static_cast<const uint16_t*>(ctx->cfg.v_pool);
-  a.num_blocks = ctx->cfg.num_blocks;
+  a.pool_rows = pool_rows(ctx);
   a.hq = ctx->cfg.num_q_heads;
   a.hkv = ctx->cfg.num_kv_heads;
   a.group = a.hq / a.hkv;
@@ -557,9 +562,11 @@ void append_pieces(const treepo::Tree& t, int32_t n, const int32_t* nodes, const
     int32_t cur = it == pending.end() ? nd.len : it->second;
     int32_t left = ntok[i];
     while (left > 0) {
-      const int32_t off = cur % B;
-      const int32_t cnt = std::min(left, B - off);
-      out->push_back(treepo::AppendPiece{src, nd.block_begin + cur / B, off, cnt});
+      // pieces end at 64-row boundaries of the pool (whatever the block size)
+      const int64_t row = static_cast<int64_t>(nd.block_begin) * B + cur;
+      const int32_t off = static_cast<int32_t>(row % treepo::kTile);
+      const int32_t cnt = std::min(left, treepo::kTile - off);
+      out->push_back(treepo::AppendPiece{src, static_cast<int32_t>(row / treepo::kTile), off, cnt});
       src += cnt;
       cur += cnt;
       left -= cnt;
@@ -664,7 +671,8 @@ int32_t treepo_create(const treepo_config* cfg, treepo_ctx** out) {
       !c.k_pool || !c.v_pool || reinterpret_cast<uintptr_t>(c.k_pool) % 16 != 0 ||
       reinterpret_cast<uintptr_t>(c.v_pool) % 16 != 0 || reinterpret_cast<uintptr_t>(c.node_len) % 4 != 0)
     return TREEPO_EINVAL;
-  if ((c.head_dim != 64 && c.head_dim != 128) || c.block_tokens != treepo::kTile ||
+  if ((c.head_dim != 64 && c.head_dim != 128) ||
+      (c.block_tokens != 16 && c.block_tokens != 32 && c.block_tokens != 64) ||
       c.num_q_heads / c.num_kv_heads > 128)
     return TREEPO_EUNSUPPORTED;
   treepo_ctx* ctx = new (std::nothrow) treepo_ctx(c);
@@ -791,7 +799,7 @@ int32_t append_validated(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const
     const hipError_t e = timed_launch(ctx, TREEPO_KERNEL_APPEND, stream, [&] {
       return treepo::launch_kv_append(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                                       static_cast<uint16_t*>(ctx->cfg.k_pool),
-                                      static_cast<uint16_t*>(ctx->cfg.v_pool), ctx->cfg.num_blocks,
+                                      static_cast<uint16_t*>(ctx->cfg.v_pool), pool_rows(ctx),
                                       ctx->cfg.num_kv_heads, ctx->cfg.head_dim, pieces.data(),
                                       static_cast<int32_t>(pieces.size()), upd_node.data(), upd_len.data(),
                                       static_cast<int32_t>(upd.size()), static_cast<int32_t*>(ctx->cfg.node_len),
@@ -850,6 +858,7 @@ int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, con
                            PrefillPlan* pl) {
   const auto& nd = ctx->tree.nodes();
   constexpr int32_t kT = 32;
+  const int32_t B = ctx->tree.block_tokens();
   std::vector<int32_t> chain;
   std::vector<int32_t> firsts;
   int64_t row = 0;
@@ -869,7 +878,7 @@ int32_t build_prefill_plan(treepo_ctx* ctx, int32_t n, const int32_t* nodes, con
       for (int32_t j = 0; j * kT < len; ++j) {
         const int32_t first = b.start + j * kT;
         const int32_t cnt = std::min(kT, len - j * kT);
-        pl->tiles.push_back(2 * (b.block_begin + j / 2) + (j & 1));
+        pl->tiles.push_back(static_cast<int32_t>((static_cast<int64_t>(b.block_begin) * B + j * kT) / 16));
         pl->tiles.push_back((first << 6) | cnt);
         firsts.push_back(first);
       }
@@ -971,7 +980,7 @@ int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const i
   e = timed_launch(ctx, TREEPO_KERNEL_APPEND, stream, [&] {
     return treepo::launch_kv_append_dev(
         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), static_cast<uint16_t*>(ctx->cfg.k_pool),
-        static_cast<uint16_t*>(ctx->cfg.v_pool), ctx->cfg.num_blocks, ctx->cfg.num_kv_heads, ctx->cfg.head_dim,
+        static_cast<uint16_t*>(ctx->cfg.v_pool), pool_rows(ctx), ctx->cfg.num_kv_heads, ctx->cfg.head_dim,
         reinterpret_cast<const treepo::AppendPiece*>(wsb + pl.pieces_off), static_cast<int32_t>(pl.pieces.size()),
         reinterpret_cast<const int2*>(wsb + pl.upd_off), static_cast<int32_t>(pl.upd.size() / 2),
         static_cast<int32_t*>(ctx->cfg.node_len), stream);
@@ -981,7 +990,7 @@ int32_t treepo_prefill(treepo_ctx* ctx, int32_t n, const int32_t* nodes, const i
   treepo::PrefillArgs a;
   a.k_pool = static_cast<const uint16_t*>(ctx->cfg.k_pool);
   a.v_pool = static_cast<const uint16_t*>(ctx->cfg.v_pool);
-  a.num_blocks = ctx->cfg.num_blocks;
+  a.pool_rows = pool_rows(ctx);
   a.hq = ctx->cfg.num_q_heads;
   a.hkv = ctx->cfg.num_kv_heads;
   a.d = ctx->cfg.head_dim;

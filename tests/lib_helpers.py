@@ -42,5 +42,5 @@ def replay_host(ctx, log, step_append=True):
     return ids
 
 
-def oracle_model(log, num_blocks=1 << 20, max_nodes=1 << 20):
-    return M.replay(log, 64, num_blocks, max_nodes)
+def oracle_model(log, num_blocks=1 << 20, max_nodes=1 << 20, block_tokens=64):
+    return M.replay(log, block_tokens, num_blocks, max_nodes)

@@ -25,7 +25,9 @@ def test_create_rejects_bad_configs():
         (dict(hq=6, hkv=4, d=64), T.EINVAL),
         (dict(hq=4, hkv=1, d=96), T.EUNSUPPORTED),
         (dict(hq=258, hkv=2, d=128), T.EUNSUPPORTED),
-        (dict(hq=4, hkv=1, d=64, block_tokens=16), T.EUNSUPPORTED),
+        (dict(hq=4, hkv=1, d=64, block_tokens=8), T.EUNSUPPORTED),
+        (dict(hq=4, hkv=1, d=64, block_tokens=48), T.EUNSUPPORTED),
+        (dict(hq=4, hkv=1, d=64, block_tokens=128), T.EUNSUPPORTED),
     ]
     for kw, code in bad:
         bt = kw.pop("block_tokens", 64)
@@ -35,6 +37,24 @@ def test_create_rejects_bad_configs():
     with pytest.raises(TreePOError) as e:
         Context(4, 1, 64, 10, 10, 0, FAKE_POOL)
     assert e.value.code == T.EINVAL
+    for bt in (16, 32, 64):  # the block sizes the pools take
+        Context(4, 1, 64, 10, 10, FAKE_POOL, FAKE_POOL, bt).close()
+
+
+def test_sixteen_token_blocks_keep_the_last_block_free():
+    """With B = 16 a node's last 32-token tile may reach 16 rows past its
+    blocks; the pool's last block is never reserved, so such a read stays in
+    the pool.  B = 32 and 64 reserve every block."""
+    ensure_lib()
+    from paper_2508_17445_amd import Context
+    for bt, usable in ((16, 9), (32, 10), (64, 10)):
+        ctx = Context(4, 1, 64, 10, 10, FAKE_POOL, FAKE_POOL, bt)
+        ctx.new_root(bt * (usable - 1))
+        ctx.new_root(bt)
+        with pytest.raises(TreePOError) as e:
+            ctx.new_root(1)
+        assert e.value.code == T.ENOMEM
+        ctx.close()
 
 
 def test_each_code_and_no_state_change():

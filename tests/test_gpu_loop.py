@@ -37,13 +37,14 @@ def _segment_log(cfg_id):
     return CallLog(ops=ops, step_append=None, leaves=leaves, rows=rows, n_nodes=nid), base
 
 
-@pytest.mark.parametrize("live", [True, False])
-def test_segment_decode_loop(live):
+@pytest.mark.parametrize("live,bt", [(True, 64), (False, 64), (True, 16)])
+def test_segment_decode_loop(live, bt):
+    import dataclasses
     import torch
     from workloads.device import DeviceTree
-    cfg = CONFIGS[1]
+    cfg = dataclasses.replace(CONFIGS[1], block_tokens=bt)
     log, base = _segment_log(1)
-    print(f"[loop cfg=1 live={live}]", flush=True)
+    print(f"[loop cfg=1 live={live} B={bt}]", flush=True)
     dt = DeviceTree(cfg=cfg, log=log, keep_host_data=True, live=live)
     model = M.replay(log, cfg.block_tokens, dt.num_blocks, log.n_nodes)
     leaves = log.leaves

@@ -98,10 +98,12 @@ def test_random_trees(seed, hq, hkv, d):
         _check(dt, mode, tag=f"rand{seed}")
 
 
-def test_ragged_and_degenerate_shapes():
+@pytest.mark.parametrize("bt", [64, 16])
+def test_ragged_and_degenerate_shapes(bt):
     """One-token chains, a leaf whose own node is empty, tails of 1 and 63
     tokens, a chain crossing many partial tiles, an interior node decoded as a
-    leaf, and a 64-token-aligned chain."""
+    leaf, and a 64-token-aligned chain; pools in 64- and 16-token blocks."""
+    import dataclasses
     ops = [("root", 1), ("append", [0], [1]),                   # 0: one token
            ("root", 200), ("append", [1], [129]),               # 1: 2 full tiles + 1
            ("fork", 1, 3, 64), ("append", [2, 3, 4], [63, 0, 64]),
@@ -112,9 +114,31 @@ def test_ragged_and_degenerate_shapes():
     log = _Log(ops, leaves, rows)
     log.n_nodes = 8
     for (hq, hkv, d) in ((28, 4, 128), (4, 1, 64)):
-        dt = _dt(cfg=_random_cfg(77, hq, hkv, d), log=log)
+        dt = _dt(cfg=dataclasses.replace(_random_cfg(77, hq, hkv, d), block_tokens=bt), log=log)
         for mode in (0, 1):
-            _check(dt, mode, tag=f"ragged-d{d}")
+            _check(dt, mode, tag=f"ragged-d{d}-B{bt}")
+
+
+@pytest.mark.parametrize("bt", [16, 32])
+def test_block_sizes(bt):
+    """Pools reserved in 16- and 32-token blocks.  With B = 16 a node starts
+    on any 16-row boundary, so its 32-token tiles straddle the pool's 32-row
+    lines and a node's last tile reaches into the next node's rows.  The tiny
+    workload (16-token segments, one block each at B = 16), the single
+    7,680-token tree and random trees, in both modes."""
+    import dataclasses
+    for cfg_id in (1, 2):
+        cfg = dataclasses.replace(CONFIGS[cfg_id], block_tokens=bt)
+        dt = _dt(cfg=cfg, log=build_call_log(cfg_id))
+        for mode in (0, 1):
+            _check(dt, mode, tag=f"cfg{cfg_id}-B{bt}")
+    for seed, hq, hkv, d in ((3, 8, 8, 128), (4, 6, 3, 64), (5, 28, 4, 128)):
+        ops, leaves, rows, _ = random_tiny_tree(seed, max_leaves=10, max_tokens=400)
+        log = _Log(ops, leaves or [0], rows)
+        log.n_nodes = len(rows)
+        dt = _dt(cfg=dataclasses.replace(_random_cfg(seed, hq, hkv, d), block_tokens=bt), log=log)
+        for mode in (0, 1):
+            _check(dt, mode, tag=f"rand{seed}-B{bt}")
 
 
 def _oracle_by_tree(dt):

@@ -2,8 +2,9 @@
 fp64 oracle: causal attention of appended tokens over their chain.
 
 Bar: max |out - oracle| <= 2e-3 and max |lse - oracle| <= 2e-3 over every
-compared element.  Ragged prompt lengths around the 32-token tile and the
-128-token work item (1, 31, 32, 33, 127, 128, 129, ...), child segments that
+compared element.  Ragged prompt lengths around the 32-token tile and
+the 128-token work item (1, 31, 32, 33, 127, 128, 129, 255, 256, 257, 513,
+...), child segments that
 attend to their whole chain, GQA groups 1 to 7, D = 64 and 128, the decode
 after a prefill (the pool holds the prefilled rows), and the prompts of the
 batch-rollout and long-context workloads at full size on sampled rows.
@@ -28,18 +29,18 @@ pytestmark = pytest.mark.gpu
 class _Rig:
     """Pools, a context and the oracle model side by side."""
 
-    def __init__(self, hq, hkv, d, seed, num_blocks, max_nodes=4096, live=False):
+    def __init__(self, hq, hkv, d, seed, num_blocks, max_nodes=4096, live=False, bt=B):
         import torch
         from paper_2508_17445_amd import Context
         self.hq, self.hkv, self.d, self.seed = hq, hkv, d, seed
         self.scale = 1.0 / np.sqrt(d)
-        elems = hkv * num_blocks * B * d
+        elems = hkv * num_blocks * bt * d
         # pools filled with NaN bit patterns: rows past a node's length must never be read
         self.kp = torch.full((elems,), -1, dtype=torch.int16, device="cuda").view(torch.bfloat16)
         self.vp = torch.full((elems,), -1, dtype=torch.int16, device="cuda").view(torch.bfloat16)
         self.node_len = torch.zeros(max_nodes, dtype=torch.int32, device="cuda") if live else None
-        self.ctx = Context(hq, hkv, d, num_blocks, max_nodes, self.kp, self.vp, B, node_len=self.node_len)
-        self.model = M.TreeModel(B, num_blocks, max_nodes)
+        self.ctx = Context(hq, hkv, d, num_blocks, max_nodes, self.kp, self.vp, bt, node_len=self.node_len)
+        self.model = M.TreeModel(bt, num_blocks - (1 if bt < 32 else 0), max_nodes)
         self.kv = {}
 
     def dev(self, bits):
@@ -78,12 +79,13 @@ class _Rig:
         assert err <= TOL and err_l <= TOL
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(28, 4, 128), (4, 1, 64), (8, 8, 128), (12, 2, 64)])
-def test_ragged_prompts_then_segments(hq, hkv, d):
+@pytest.mark.parametrize("hq,hkv,d,bt", [(28, 4, 128, 64), (4, 1, 64, 64), (8, 8, 128, 64), (12, 2, 64, 64),
+                                         (28, 4, 128, 16), (4, 1, 64, 32)])
+def test_ragged_prompts_then_segments(hq, hkv, d, bt):
     import torch
-    lens = [1, 31, 32, 33, 64, 127, 128, 129, 300, 257]
-    print(f"[prefill ragged hq={hq} hkv={hkv} d={d}]", flush=True)
-    rig = _Rig(hq, hkv, d, 31 + d, num_blocks=400)
+    lens = [1, 31, 32, 33, 64, 127, 128, 129, 300, 257, 255, 256, 513]
+    print(f"[prefill ragged hq={hq} hkv={hkv} d={d} B={bt}]", flush=True)
+    rig = _Rig(hq, hkv, d, 31 + d, num_blocks=400 * 64 // bt, bt=bt)
     roots = []
     for ln in lens:
         roots.append(rig.ctx.new_root(ln))
@@ -133,7 +135,7 @@ def test_workload_prompts_sampled(cfg_id):
     rows = set()
     for i in rng.choice(len(plens), size=min(6, len(plens)), replace=False):
         b, e = int(starts[i]), int(starts[i + 1])
-        rows |= {b, b + 1, e - 1, b + 127, b + 128} | {int(x) for x in rng.integers(b, e, size=4)}
+        rows |= {b, b + 1, e - 1, b + 127, b + 128, b + 255, b + 256} | {int(x) for x in rng.integers(b, e, size=4)}
     rows = sorted(r for r in rows if r < starts[-1])
     rig.check(roots, plens, qb, out, lse, f"cfg{cfg_id}", rows=rows)
     del rig

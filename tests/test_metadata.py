@@ -29,21 +29,23 @@ def _compare(ctx, model, leaves):
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
-def test_workload_metadata_bit_exact(cfg):
+@pytest.mark.parametrize("bt", [16, 32, 64])
+def test_workload_metadata_bit_exact(cfg, bt):
     log = build_call_log(cfg)
-    ctx = host_ctx()
+    ctx = host_ctx(block_tokens=bt)
     ids = replay_host(ctx, log)
     assert ids == list(range(log.n_nodes))
-    _compare(ctx, oracle_model(log), log.leaves)
+    _compare(ctx, oracle_model(log, block_tokens=bt), log.leaves)
 
 
 @pytest.mark.parametrize("seed", range(40))
 def test_random_tree_metadata_bit_exact(seed):
     ops, leaves, rows, _ = random_tiny_tree(seed, max_leaves=12, max_tokens=700)
     log = _Log(ops, leaves, rows)
-    ctx = host_ctx()
+    bt = (16, 32, 64)[seed % 3]
+    ctx = host_ctx(block_tokens=bt)
     replay_host(ctx, log)
-    model = oracle_model(log)
+    model = oracle_model(log, block_tokens=bt)
     _compare(ctx, model, leaves or [0])
 
 
@@ -109,8 +111,8 @@ def _plan_checks(ctx, model, leaves, mode):
             ln, cap = model.nodes[n]["len"], model.nodes[n]["cap"]
             # with device lengths an unfrozen node is covered up to its capacity
             span = cap if live_mode and model.n_children[n] == 0 and ln < cap else ln
-            for k in range((span + 31) // 32):     # 32-token tiles, two per 64-token block
-                want.append((model.nodes[n]["block_begin"] + k // 2, n, k, max(0, min(32, ln - 32 * k))))
+            for k in range((span + 31) // 32):     # 32-token tiles; a tile starts in block 32 k / B
+                want.append((model.nodes[n]["block_begin"] + 32 * k // model.B, n, k, max(0, min(32, ln - 32 * k))))
         for g in range(hkv):
             got = sorted(covered[(pos, g)])
             # a reused live plan reports the counts of its planning time (the
@@ -127,6 +129,7 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
     give each (leaf, KV head) key entries 0..count-1 in piece order."""
     blocks = ctx.export_blocks(leaves, mode)
     hq, hkv, d, nb = ctx.cfg.num_q_heads, ctx.cfg.num_kv_heads, ctx.cfg.head_dim, ctx.cfg.num_blocks
+    B = ctx.cfg.block_tokens
     G = hq // hkv
     bi = blocks.shape[1]
     assert blocks.shape[0] == n_streams and bi % 4 == 0 and bi <= MAX_BLOCK_INTS
@@ -179,8 +182,10 @@ def _block_checks(ctx, leaves, mode, pieces, rowsets, tiles, n_streams, stream_n
             for t in range(nt):
                 blk, node, tin, valid = (int(v) for v in tiles[ptile + t])
                 hb, v = (int(x) for x in st[stile + nq + t])
-                assert hb == 2 * (g * nb + blk) + tin % 2
-                assert 0 <= hb < 2 * hkv * nb
+                # first pool row of the tile over 16, KV head g's rows included
+                assert hb * 16 == (g * nb + int(nodes[node][5])) * B + 32 * tin
+                assert blk == int(nodes[node][5]) + 32 * tin // B
+                assert 0 <= hb and hb * 16 + 32 <= hkv * nb * B
                 # a tile of an unfrozen node that was not full when planned is
                 # live: its count is read on the device (such nodes are planned
                 # up to their capacity); `valid` is the count at planning time
@@ -220,14 +225,14 @@ def _stream_costs(pieces, n_streams, q_cost=1.2, cut_q=False):
     return cost
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 4, 6])
-def test_plan_covers_each_chain_token_once(cfg):
+@pytest.mark.parametrize("cfg,bt", [(1, 64), (2, 64), (4, 64), (6, 64), (1, 16), (4, 16), (2, 32)])
+def test_plan_covers_each_chain_token_once(cfg, bt):
     log = build_call_log(cfg)
     from workloads import CONFIGS
     c = CONFIGS[cfg]
-    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d, block_tokens=bt)
     replay_host(ctx, log)
-    model = oracle_model(log)
+    model = oracle_model(log, block_tokens=bt)
     p_t, tiles_t, _ = _plan_checks(ctx, model, log.leaves, 0)
     p_n, tiles_n, _ = _plan_checks(ctx, model, log.leaves, 1)
     # the tree plan streams every node once per leaf group; the naive plan once per leaf

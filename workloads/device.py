@@ -73,7 +73,8 @@ class DeviceTree:
         self.log = log if log is not None else build_call_log(cfg_id)
         self.device = device
         c = self.cfg
-        self.num_blocks = pool_blocks(self.log, c.block_tokens) + extra_blocks
+        # with 16-token blocks the library keeps the pool's last block free
+        self.num_blocks = pool_blocks(self.log, c.block_tokens) + extra_blocks + (1 if c.block_tokens < 32 else 0)
         elems = c.hkv * self.num_blocks * c.block_tokens * c.d
         self.k_pool = torch.empty(elems, dtype=torch.bfloat16, device=device)
         self.v_pool = torch.empty(elems, dtype=torch.bfloat16, device=device)
