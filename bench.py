@@ -80,6 +80,8 @@ def _parse():
     ap.add_argument("--prefill", action="store_true",
                     help="prompt prefill (causal attention of every prompt of the config, written once into the "
                          "pools for all of its rollouts): one JSON line")
+    ap.add_argument("--overlap", action="store_true",
+                    help="how matrix-core and vector-ALU work share a SIMD (treepo_bench_overlap): one JSON line")
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for hardware counters: --steps steps of the workload in each mode (tree, "
                          "then per-leaf), then one 1 GiB device copy whose byte counters calibrate the kernels'")
@@ -892,6 +894,39 @@ def _prefill(args):
     print(json.dumps(line), flush=True)
 
 
+def _overlap():
+    """Clock units (s_memtime) per round of 8 independent MFMAs, of 24
+    independent FMAs, and of both interleaved, per wave, at 1, 2 and 4 waves
+    per SIMD (one workgroup on one CU).  The FMA-alone time at 4 waves per
+    SIMD gives the vector ALU's cost per FMA when saturated.  For 1 and 2
+    waves per SIMD the line sets the time of both against full overlap (the
+    slower of the two alone) and against serial issue (one wave: the sum of
+    the two alone; two waves: the MFMA time plus the saturated cost of both
+    waves' FMAs)."""
+    import numpy as np
+    import torch
+    from paper_2508_17445_amd import bench_overlap
+    sink = torch.empty(1024, dtype=torch.float32, device="cuda")
+    cyc = torch.zeros(16, dtype=torch.int64, device="cuda")
+    iters = 4000
+    res = {}
+    for w in (1, 2, 4):
+        for mode, name in ((0, "mfma"), (1, "fma"), (2, "both")):
+            bench_overlap(mode, w, iters, sink, cyc)            # warm-up (clocks ramp)
+            bench_overlap(mode, w, iters, sink, cyc)
+            torch.cuda.synchronize()
+            c = cyc[:4 * w].cpu().numpy().astype(np.float64)
+            res[f"{name}_w{w}"] = round(float(c.mean()) / iters, 2)
+    fma_unit = res["fma_w4"] / (4 * 24)
+    line = {"metric": "matrix/vector overlap on one SIMD (clock units per round per wave)", "rounds": iters,
+            "per_round": res, "fma_saturated_units": round(fma_unit, 3)}
+    for w in (1, 2):
+        serial = res["mfma_w1"] + res["fma_w1"] if w == 1 else res["mfma_w2"] + 2 * 24 * fma_unit
+        line[f"w{w}"] = {"both": res[f"both_w{w}"], "full_overlap": max(res[f"mfma_w{w}"], res[f"fma_w{w}"]),
+                         "serial": round(serial, 2)}
+    print(json.dumps(line), flush=True)
+
+
 def _chain(parents, x):
     c = []
     while x >= 0:
@@ -982,6 +1017,8 @@ def main():
         _advantage(args)
     elif args.prefill:
         _prefill(args)
+    elif args.overlap:
+        _overlap()
     elif args.segment_loop:
         _segment_loop(args)
     elif args.profile_pass:

@@ -43,6 +43,18 @@ int32_t treepo_bench_read(const void* src, size_t bytes, float* sink, hipStream_
 int32_t treepo_bench_stream(const void* src, size_t bytes, float* sink, int32_t mode,
                             int32_t workgroups, hipStream_t stream);
 
+/* How matrix-core and vector-ALU work share a SIMD.  One workgroup of
+ * 256 * waves_per_simd threads (1 <= waves_per_simd <= 4: waves per SIMD);
+ * each wave runs `iters` rounds of eight independent
+ * v_mfma_f32_16x16x32_bf16 (mode 0), 24 independent fp32 FMAs (mode 1), or
+ * both interleaved one MFMA then three FMAs (mode 2), and writes its
+ * s_memtime clock delta to cycles[wave] (device, >= 16 uint64) and one float
+ * per thread to sink (device, >= 1024 floats).  If the two units overlapped,
+ * mode 2 would take about as long as the slower of modes 0 and 1.  Returns
+ * 0, TREEPO_EINVAL or TREEPO_EHIP. */
+int32_t treepo_bench_overlap(int32_t mode, int32_t waves_per_simd, int32_t iters, float* sink, uint64_t* cycles,
+                             hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

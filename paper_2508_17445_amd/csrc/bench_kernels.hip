@@ -1,4 +1,5 @@
-// Bandwidth probes: a plain copy (byte-counter calibration) and a streaming read.
+// Bandwidth probes: a plain copy (byte-counter calibration) and a streaming
+// read; and a probe of how matrix-core and vector-ALU work share a SIMD.
 #include <hip/hip_runtime.h>
 
 #include "treepo.h"
@@ -107,7 +108,61 @@ __global__ __launch_bounds__(kThreads) void stream_reg_kernel(const uint4* __res
   if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(acc & 0xFFFF);
 }
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One workgroup; every wave runs `iters` rounds of eight independent
+// v_mfma_f32_16x16x32_bf16 (MF) and/or 24 independent FMAs (VA), issued as
+// one MFMA then three FMAs, and stores its own clock delta (s_memtime).
+template <bool MF, bool VA>
+__global__ __launch_bounds__(1024) void overlap_kernel(float* __restrict__ sink, uint64_t* __restrict__ cycles,
+                                                       int iters) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 a, b;
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<__bf16>(0.001f * (lane + i));
+    b[i] = static_cast<__bf16>(0.002f * (lane - i));
+  }
+  f32x4 acc[8];
+  for (int j = 0; j < 8; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float x[16];
+  for (int j = 0; j < 16; ++j) x[j] = 0.01f * (lane + j);
+  const uint64_t t0 = __builtin_amdgcn_s_memtime();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (MF) acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
+      if (VA) {
+#pragma unroll
+        for (int v = 0; v < 3; ++v) x[(3 * j + v) & 15] = fmaf(x[(3 * j + v) & 15], 0.999f, 0.001f);
+      }
+      if (MF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (VA) __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+    }
+  }
+  const uint64_t t1 = __builtin_amdgcn_s_memtime();
+  float sum = 0.f;
+  for (int j = 0; j < 8; ++j) sum += acc[j][0] + acc[j][1] + acc[j][2] + acc[j][3];
+  for (int j = 0; j < 16; ++j) sum += x[j];
+  sink[threadIdx.x] = sum;
+  if (lane == 0) cycles[threadIdx.x >> 6] = t1 - t0;
+}
+
 }  // namespace
+
+extern "C" int32_t treepo_bench_overlap(int32_t mode, int32_t waves_per_simd, int32_t iters, float* sink,
+                                        uint64_t* cycles, hipStream_t stream) {
+  if (!sink || !cycles || mode < 0 || mode > 2 || waves_per_simd < 1 || waves_per_simd > 4 || iters < 1)
+    return TREEPO_EINVAL;
+  const dim3 block(256 * waves_per_simd);
+  if (mode == 0)
+    overlap_kernel<true, false><<<1, block, 0, stream>>>(sink, cycles, iters);
+  else if (mode == 1)
+    overlap_kernel<false, true><<<1, block, 0, stream>>>(sink, cycles, iters);
+  else
+    overlap_kernel<true, true><<<1, block, 0, stream>>>(sink, cycles, iters);
+  return hipGetLastError() == hipSuccess ? TREEPO_OK : TREEPO_EHIP;
+}
 
 extern "C" int32_t treepo_bench_stream(const void* src, size_t bytes, float* sink, int32_t mode,
                                        int32_t workgroups, hipStream_t stream) {

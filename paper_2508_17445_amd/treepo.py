@@ -91,6 +91,7 @@ def load_library(path: str = LIB_PATH):
         "treepo_bench_copy": (_i32, [_p, _p, ctypes.c_size_t, _p]),
         "treepo_bench_read": (_i32, [_p, ctypes.c_size_t, _p, _p]),
         "treepo_bench_stream": (_i32, [_p, ctypes.c_size_t, _p, _i32, _i32, _p]),
+        "treepo_bench_overlap": (_i32, [_i32, _i32, _i32, _p, _p, _p]),
     }
     for name, (res, args) in sig.items():
         if name.startswith("treepo_bench_") and not hasattr(lib, name):
@@ -367,6 +368,13 @@ def bench_read(src, nbytes: int, sink, stream=None):
     st = lib.treepo_bench_read(_dev(src), nbytes, _dev(sink), _stream(stream))
     if st != OK:
         raise TreePOError(st, "treepo_bench_read")
+
+
+def bench_overlap(mode: int, waves_per_simd: int, iters: int, sink, cycles, stream=None):
+    lib = load_library()
+    st = lib.treepo_bench_overlap(mode, waves_per_simd, iters, _dev(sink), _dev(cycles), _stream(stream))
+    if st != OK:
+        raise TreePOError(st, "treepo_bench_overlap")
 
 
 def bench_stream(src, nbytes: int, sink, mode: int, workgroups: int, stream=None):
