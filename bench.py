@@ -85,9 +85,11 @@ def _parse():
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for hardware counters: --steps steps of the workload in each mode (tree, "
                          "then per-leaf), then one 1 GiB device copy whose byte counters calibrate the kernels'")
-    ap.add_argument("--summarize", choices=("trace", "traffic"),
-                    help="write profiles/partial_kernel_config<N>_{kernel_trace.md,traffic.txt} from the "
-                         "rocprofv3 output under --dir (see the commands in those files)")
+    ap.add_argument("--summarize", choices=("trace", "traffic", "mfma", "prefill", "advantage"),
+                    help="write a profiles/ summary from the rocprofv3 output under --dir (the commands are in "
+                         "each file): trace, traffic, mfma -> partial_kernel_config<N>_*; prefill -> "
+                         "prefill_kernel_config<N>_{kernel_trace.md,counters.txt}; advantage -> "
+                         "advantage_kernel_config<N>_kernel_trace.md")
     ap.add_argument("--dir", default="", help="rocprofv3 output directory for --summarize")
     return ap.parse_args()
 
@@ -603,6 +605,228 @@ traffic bytes per launch: {fb + wb}
     print(txt)
 
 
+def _host_plan_ctx(cfg_id):
+    """A host-only context holding the workload's tree (metadata appends; the
+    pools are never touched), for exporting the plans the GPU ran."""
+    from paper_2508_17445_amd import Context
+    from workloads import CONFIGS, build_call_log
+    cfg, log = CONFIGS[cfg_id], build_call_log(cfg_id)
+    from workloads.device import pool_blocks
+    fake = 0x10000
+    ctx = Context(cfg.hq, cfg.hkv, cfg.d, pool_blocks(log, cfg.block_tokens) + 1, max(log.n_nodes, 1), fake,
+                  fake + 64, cfg.block_tokens)
+    for op in log.ops:
+        if op[0] == "root":
+            ctx.new_root(op[1])
+        elif op[0] == "fork":
+            ctx.fork(op[1], op[2], op[3])
+        elif op[0] == "fork_at":
+            ctx.fork_at(op[1], op[2], op[3], op[4])
+        else:
+            ctx.kv_commit(op[1], op[2])
+    if log.step_append is not None:
+        ctx.kv_commit(*log.step_append)
+    return ctx, cfg, log
+
+
+def _summarize_mfma(cfg_id, d):
+    """profiles/partial_kernel_config<N>_mfma.txt from one SQ counter pass of
+    --profile-pass (MFMA instructions, MFMA busy cycles) and the plans the
+    library makes for the workload (predicted MFMA count, MFMA row fill)."""
+    ctx, cfg, log = _host_plan_ctx(cfg_id)
+    rows = [r for r in _csv_rows(d, "counter_collection.csv") if "partial_kernel" in r["Kernel_Name"]]
+    disp = sorted({int(r["Dispatch_Id"]) for r in rows})
+    first = set(disp[:len(disp) // 2])   # the profile pass runs the tree decodes first, then the per-leaf ones
+    by = {0: {}, 1: {}}
+    for r in rows:
+        by[0 if int(r["Dispatch_Id"]) in first else 1].setdefault(r["Counter_Name"], []).append(
+            float(r["Counter_Value"]))
+    D = cfg.d
+
+    def per_tile(n_rows):
+        # MFMAs per KV tile of a piece: column-split pieces (<= 32 rows) run
+        # 8 QK MFMAs on each of the 4 waves and split the PV d-blocks over
+        # them; larger pieces run 8 QK + 2 (hi, lo) x D/16 PV MFMAs per 16-row block
+        if n_rows <= 16:
+            return 4 * (8 + 2 * (D // 16 // 4))
+        if n_rows <= 32:
+            return 4 * (8 + 2 * (D // 16 // 2))
+        return math.ceil(n_rows / 16) * (8 + 2 * (D // 16))
+
+    out = []
+    for mode, name in ((0, "tree schedule"), (1, "per-leaf baseline")):
+        pieces, _, _, ns = ctx.export_plan(log.leaves, mode)
+        m = {k: statistics.mean(v) for k, v in by[mode].items()}
+        exp = sum(int(p[5]) * per_tile(int(p[2])) for p in pieces)
+
+        def cls(ps):
+            t = sum(int(p[5]) for p in ps)
+            mf = sum(int(p[5]) * per_tile(int(p[2])) for p in ps)
+            rb = sum(int(p[5]) * 16 * math.ceil(int(p[2]) / 16) for p in ps)
+            useful = sum(int(p[5]) * int(p[2]) for p in ps)
+            return t, mf, (useful / rb if rb else 0.0)
+
+        ts, ms_, fs = cls([p for p in pieces if p[1] > 1])
+        t1, m1, f1 = cls([p for p in pieces if p[1] == 1])
+        gui = m["GRBM_GUI_ACTIVE"] / 8   # summed over the 8 XCDs
+        util = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * 1024)
+        out.append(
+            f"partial_kernel<{D}>, {name} (grid {ns} x 256), mean of {len(by[mode]['GRBM_GUI_ACTIVE'])} dispatches:\n"
+            f"  SQ_INSTS_VALU_MFMA_BF16      {m['SQ_INSTS_VALU_MFMA_BF16']:.0f} MFMA instructions "
+            f"(v_mfma_f32_16x16x32_bf16); the plan predicts {exp}\n"
+            f"  SQ_INSTS_VALU_MFMA_MOPS_BF16 {m['SQ_INSTS_VALU_MFMA_MOPS_BF16']:.0f} -> "
+            f"{m['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512 / 1e9:.3f} GFLOP issued per launch\n"
+            f"  SQ_VALU_MFMA_BUSY_CYCLES     {m['SQ_VALU_MFMA_BUSY_CYCLES']:.0f}; GRBM_GUI_ACTIVE "
+            f"{m['GRBM_GUI_ACTIVE']:.0f} (8 XCDs) -> MFMA busy {100 * util:.1f}% of 1024 SIMDs x {gui:.0f} cycles\n"
+            f"  SQ_INSTS_VALU {m['SQ_INSTS_VALU']:.0f}, SQ_WAVES {m['SQ_WAVES']:.0f}, "
+            f"SQ_BUSY_CU_CYCLES {m['SQ_BUSY_CU_CYCLES']:.0f}\n"
+            f"  KV tiles of shared-node pieces (more than one leaf): {ts} tiles, {ms_} MFMAs "
+            f"({100 * ms_ / max(exp, 1):.1f}% of the launch), MFMA row fill {100 * fs:.1f}%\n"
+            f"  KV tiles of one-leaf pieces: {t1} tiles, {m1} MFMAs, MFMA row fill {100 * f1:.1f}%")
+    ctx.close()
+    counters = ("SQ_INSTS_VALU_MFMA_BF16 SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES "
+                "SQ_WAVES SQ_INSTS_VALU GRBM_GUI_ACTIVE")
+    txt = f"""MFMA use of the node-partial kernel, decode workload config {cfg_id} ({cfg.name}, Hq={cfg.hq} Hkv={cfg.hkv} D={cfg.d})
+Commands (repository root $R on the GPU box; one counter pass):
+  cd /tmp && export TMPDIR=/tmp
+  rocprofv3 --pmc {counters} --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/mfma -o run -- python3 $R/bench.py --profile-pass --config {cfg_id} --steps 10
+  python3 bench.py --summarize mfma --config {cfg_id} --dir gpurun_out/prof/c{cfg_id}/mfma
+The profile pass runs 10 tree decodes, 10 per-leaf decodes and one 1 GiB device copy.
+Prediction from the plan (treepo_export_plan): per KV tile, a piece of <= 16 query rows issues 4 waves x (8 QK + {2 * (D // 64)} PV) MFMAs,
+17-32 rows 4 x (8 + {2 * (D // 32)}), more rows {8 + 2 * (D // 16)} per 16-row block (8 QK + {2 * (D // 16)} PV; PV runs twice, on the hi and lo bf16 parts of P).
+Row fill = query rows / (16 x row blocks) of the MFMA tiles, weighted by KV tiles.
+
+""" + "\n".join(out) + f"""
+
+kernels.hip sha256: {_kernel_sha()}
+"""
+    path = os.path.join(PROFILES, f"partial_kernel_config{cfg_id}_mfma.txt")
+    open(path, "w").write(txt)
+    print(txt)
+
+
+def _summarize_prefill(cfg_id, d):
+    """profiles/prefill_kernel_config<N>_{kernel_trace.md,counters.txt} from a
+    kernel trace of `bench.py --prefill` (<dir>/trace, its JSON line saved
+    there) and two SQ counter passes (<dir>/sq, <dir>/mfma)."""
+    from workloads import CONFIGS, build_call_log
+    cfg, log = CONFIGS[cfg_id], build_call_log(cfg_id)
+    plens = [op[1] for op in log.ops if op[0] == "root"]
+    b = _bench_line(os.path.join(d, "trace"))
+    rows = _csv_rows(os.path.join(d, "trace"), "kernel_trace.csv")
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+
+    def dur(r):
+        return (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+    def stats(v):
+        return f"{len(v)} | {statistics.mean(v):.2f} | {statistics.median(v):.2f} | {min(v):.2f} | {max(v):.2f}"
+
+    pf = [r for r in rows if "prefill_kernel" in r["Kernel_Name"]]
+    ap = [dur(r) for r in rows if "kv_append_dev_kernel" in r["Kernel_Name"]]
+    warm, steps = b["warmup"], b["steps"]
+    timed = pf[warm:warm + steps]
+    flops = b["roofline"]["algorithmic_flops_per_launch"]
+    avg = statistics.mean(dur(r) for r in timed)
+    grid = timed[0].get("Grid_Size_X", timed[0].get("Grid_Size", ""))
+    head = f"prefill of the config-{cfg_id} prompts ({len(plens)} prompts, {sum(plens):,} tokens, " \
+           f"Hq={cfg.hq} Hkv={cfg.hkv} D={cfg.d})"
+    naive = b.get("per_rollout_baseline")
+    txt = f"""# Kernel trace: {head}
+
+Commands (repository root `$R` on the GPU box):
+
+```
+cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/pfprof/c{cfg_id}/trace -o run -- python3 -u $R/bench.py --prefill --config {cfg_id} --steps {steps} --warmup {warm} --no-cpu > $R/gpurun_out/pfprof/c{cfg_id}/trace/bench.json
+python3 bench.py --summarize prefill --config {cfg_id} --dir gpurun_out/pfprof/c{cfg_id}
+```
+
+Each step is one `treepo_prefill` call over all {len(plens)} prompts (fresh root nodes
+every step): one KV-append launch (pieces read from the uploaded tables), then one prefill launch.
+Prefill dispatches in order: {warm} warm-up, {steps} timed, 1 with events attached (then the
+per-rollout baseline's).
+
+| kernel | grid (threads) | dispatches | avg us | median us | min us | max us |
+|---|---|---|---|---|---|---|
+| prefill_kernel<{cfg.d}>, timed steps | {grid} | {stats([dur(r) for r in timed])} |
+| kv_append_dev_kernel<{cfg.d}> (all calls) | - | {stats(ap)} |
+
+Algorithmic FLOPs per launch (causal QK and PV, 4 D flops per query-key pair
+and query head): {flops} -> {flops / (avg * 1e-6) / 1e12:.1f} TFLOP/s on the
+trace average = {flops / (avg * 1e-6) / 1e12 / 2500:.3f} of the 2.5 PFLOP/s
+bf16 dense peak.  The same run's bench line: the kernel at
+{b["kernel_avg_ms"] * 1e3:.1f} us with events attached to it
+({b["roofline"]["achieved"]} TFLOP/s), the whole call (append + host tables
++ upload + prefill) at {b["ms_per_step"] * 1e3:.1f} us""" + (f""", and prefilling every
+prompt once per rollout ({naive["prompt_copies"]} copies) at {naive["ms_per_step"] * 1e3:.0f} us
+({naive["speedup_shared_vs_per_rollout"]}x).""" if naive else ".") + f"""
+
+kernels.hip sha256: {_kernel_sha()}
+"""
+    open(os.path.join(PROFILES, f"prefill_kernel_config{cfg_id}_kernel_trace.md"), "w").write(txt)
+    print(txt)
+    agg = {}
+    for sub in ("sq", "mfma"):
+        for r in _csv_rows(os.path.join(d, sub), "counter_collection.csv"):
+            if "prefill_kernel" in r["Kernel_Name"]:
+                agg.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    m = {k: statistics.mean(v) for k, v in agg.items()}
+    busy = m["SQ_BUSY_CU_CYCLES"]
+    sq = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_INSTS_VALU SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT "
+          "SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_LDS SQ_WAVE_CYCLES")
+    mf = "SQ_INSTS_VALU_MFMA_BF16 SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_WAVES GRBM_GUI_ACTIVE"
+    txt2 = f"""SQ counters of the {head}
+Commands (repository root $R on the GPU box; each pass its own run):
+  cd /tmp && export TMPDIR=/tmp
+  rocprofv3 --pmc {sq} --output-format csv -d $R/gpurun_out/pfprof/c{cfg_id}/sq -o run -- python3 $R/bench.py --prefill --config {cfg_id} --steps 3 --warmup 1 --no-cpu --no-naive
+  rocprofv3 --pmc {mf} --output-format csv -d $R/gpurun_out/pfprof/c{cfg_id}/mfma -o run -- python3 $R/bench.py --prefill --config {cfg_id} --steps 3 --warmup 1 --no-cpu --no-naive
+  python3 bench.py --summarize prefill --config {cfg_id} --dir gpurun_out/pfprof/c{cfg_id}
+Means over the prefill dispatches of each run ({len(agg.get("SQ_BUSY_CU_CYCLES", []))} and {len(agg.get("SQ_WAVES", []))}):
+""" + "".join(f"  {k}: {v:.0f}\n" for k, v in sorted(m.items())) + f"""Derived (per CU, 256 CUs; MFMA busy counted per SIMD, 4 per CU):
+  MFMA pipe busy: {m["SQ_VALU_MFMA_BUSY_CYCLES"] / 4 / busy:.3f} of the CU busy cycles
+  VALU active: {m["SQ_ACTIVE_INST_VALU"] / busy:.3f}; LDS active: {m["SQ_ACTIVE_INST_LDS"] / busy:.3f}; LDS bank-conflict cycles: {m["SQ_LDS_BANK_CONFLICT"] / busy:.3f}
+  MFMA instructions per launch {m["SQ_INSTS_VALU_MFMA_BF16"]:.0f} -> {m["SQ_INSTS_VALU_MFMA_BF16"] * 16384 / flops:.2f} x the algorithmic FLOPs executed
+kernels.hip sha256: {_kernel_sha()}
+"""
+    open(os.path.join(PROFILES, f"prefill_kernel_config{cfg_id}_counters.txt"), "w").write(txt2)
+    print(txt2)
+
+
+def _summarize_advantage(cfg_id, d):
+    """profiles/advantage_kernel_config<N>_kernel_trace.md from the kernel
+    statistics of one `bench.py --advantage` run (its JSON line saved in
+    <dir>)."""
+    b = _bench_line(d)
+    stats = [r for r in _csv_rows(d, "kernel_stats.csv") if "advantage_kernel" in r["Name"]]
+    s0 = stats[0]
+    txt = f"""# Kernel trace: TreePO advantage over config {cfg_id}'s decoded leaves ({_workload_name(cfg_id)})
+
+Commands (repository root `$R` on the GPU box):
+
+```
+cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/advprof/c{cfg_id} -o run -- python3 -u $R/bench.py --advantage --config {cfg_id} --steps {b["steps"]} --warmup {b["warmup"]} --no-cpu > $R/gpurun_out/advprof/c{cfg_id}/bench.json
+python3 bench.py --summarize advantage --config {cfg_id} --dir gpurun_out/advprof/c{cfg_id}
+```
+
+rocprofv3 `--stats` ({b["warmup"]} warm-up + {b["steps"]} timed calls + the calls with the
+library's events attached to the kernel):
+
+| kernel | calls | avg us | min us | max us |
+|---|---|---|---|---|
+| advantage_kernel | {s0["Calls"]} | {float(s0["AverageNs"]) / 1e3:.2f} | {float(s0["MinNs"]) / 1e3:.2f} | {float(s0["MaxNs"]) / 1e3:.2f} |
+
+The bench line of the same run: {b["ms_per_step"] * 1e3:.1f} us per call back to back (host index
+arrays cached for the tree shape and leaf list, their upload through pinned
+staging, the kernel), {b.get("kernel_avg_ms", float("nan")) * 1e3:.1f} us on the kernel's attached events,
+{b["value"] / 1e6:.1f} M trajectories/s.  One workgroup; the time is dependent global
+loads (sub-group members, each pair's sub-group mean), not bandwidth.
+
+advantage.hip sha256: {hashlib.sha256(open(os.path.join(ROOT, "paper_2508_17445_amd", "csrc", "advantage.hip"), "rb").read()).hexdigest()}
+"""
+    open(os.path.join(PROFILES, f"advantage_kernel_config{cfg_id}_kernel_trace.md"), "w").write(txt)
+    print(txt)
+
+
 def _algorithmic_bytes(cfg_id, log):
     """Unique KV bytes of a decode step of the workload (with its fused append)."""
     from workloads import CONFIGS
@@ -1010,7 +1234,8 @@ def main():
     if args.summarize:
         if not args.dir:
             raise SystemExit("--summarize needs --dir")
-        (_summarize_trace if args.summarize == "trace" else _summarize_traffic)(args.config, args.dir)
+        {"trace": _summarize_trace, "traffic": _summarize_traffic, "mfma": _summarize_mfma,
+         "prefill": _summarize_prefill, "advantage": _summarize_advantage}[args.summarize](args.config, args.dir)
         return
     _ensure_built()
     if args.advantage:
