@@ -815,7 +815,7 @@ library's events attached to the kernel):
 |---|---|---|---|---|
 | advantage_kernel | {s0["Calls"]} | {float(s0["AverageNs"]) / 1e3:.2f} | {float(s0["MinNs"]) / 1e3:.2f} | {float(s0["MaxNs"]) / 1e3:.2f} |
 
-The bench line of the same run: {b["ms_per_step"] * 1e3:.1f} us per call back to back (host index
+The bench line of the same run: {b["call_ms"] * 1e3:.1f} us per call back to back (host index
 arrays cached for the tree shape and leaf list, their upload through pinned
 staging, the kernel), {b.get("kernel_avg_ms", float("nan")) * 1e3:.1f} us on the kernel's attached events,
 {b["value"] / 1e6:.1f} M trajectories/s.  One workgroup; the time is dependent global
