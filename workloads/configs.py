@@ -338,7 +338,7 @@ class Config:
 
 
 CONFIGS = {
-    1: Config("tiny-binary-8leaf", 1, 4, 1, 64, gen_tiny),
+    1: Config("tiny-binary-8leaf", 1, 4, 1, 64, gen_tiny, block_tokens=16),  # one block per 16-token segment
     2: Config("single-tree-16leaf-7680", 2, 28, 4, 128, gen_single_tree),
     3: Config("batch-64x16-rollout", 3, 28, 4, 128, gen_batch_rollout),
     4: Config("irregular-32-prompt", 4, 28, 4, 128, gen_irregular),
