@@ -110,7 +110,7 @@ enum PlanMode : int32_t { kModeTree = 0, kModeNaive = 1 };
 // exactly the rows each key holds.
 constexpr int64_t kStridedCombineBytes = int64_t{8} << 20;
 
-// Tokens per decode tile (half of a 64-token pool block).
+// Tokens per decode tile (32 consecutive rows of a node from a 16-row line of the pool).
 constexpr int32_t kPlanTileTokens = 32;
 // Upper bounds on the tiles, query segments and pieces of one stream (sized
 // for the kernel's LDS copy of its stream block).  A piece holds at least one

@@ -1,7 +1,7 @@
 """GPU parity of segment-level decoding (Sec. 2.2): after a fork, every step
 appends one token to each leaf and decodes.  With device lengths
 (treepo_config.node_len) one plan serves the whole segment -- tiles fill,
-cross 32-token tile and 64-token block lines, and start empty -- and each step
+cross 32-token tile and block lines (blocks of 64 and of 16 tokens), and start empty -- and each step
 is checked against the fp64 oracle of the tree at that step; without them
 every step re-plans.  Same bar as the other parity tests (2e-3).
 """
