@@ -376,6 +376,23 @@ def pin_binary_heap_tiny():
         assert ds[n] == [n - 7]
 
 
+def pin_binary_heap_tiny_16_token_blocks():
+    """Config 1 with 16-token blocks: the 64-token root reserves blocks 0-3,
+    node n >= 1 (one 16-token segment) block n + 3; a leaf's blocks are its
+    chain's runs, 4 + 3 = 7 of them for 112 tokens."""
+    log = build_call_log(1)
+    m = M.replay(log, 16, 10_000, 10_000)
+    for n in range(15):
+        rec = dict(zip(M.TreeModel.FIELDS, m.record(n)))
+        assert (rec["block_begin"], rec["n_blocks"]) == ((0, 4) if n == 0 else (n + 3, 1))
+    for x in range(7, 15):
+        anc = [x]
+        while anc[-1]:
+            anc.append((anc[-1] - 1) // 2)
+        want = [0, 1, 2, 3] + [a + 3 for a in anc[::-1][1:]]
+        assert m.leaf_blocks(x) == want and len(want) == 7
+
+
 def pin_single_tree_counts():
     """Config 2: 191 nodes, each 512 tokens = 8 blocks at 8n; 16 leaves with
     15-node chains of 7680 tokens; 97,792 unique tokens."""
@@ -431,5 +448,5 @@ def pin_structure_invariants(cfgs=(1, 2, 3, 4, 5)):
 
 ALL_PINS = [pin_bf16_widening, pin_positions_subset, pin_bruteforce, pin_constant_keys, pin_single_key, pin_zero_query, pin_sdpa,
             pin_identical_paths, pin_permutation, pin_cascade, pin_lse_logsumexp,
-            pin_binary_heap_tiny, pin_single_tree_counts, pin_long_context_counts,
+            pin_binary_heap_tiny, pin_binary_heap_tiny_16_token_blocks, pin_single_tree_counts, pin_long_context_counts,
             pin_structure_invariants]
