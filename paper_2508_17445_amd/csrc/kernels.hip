@@ -246,8 +246,9 @@ __device__ __forceinline__ void dma_qtile(const uint16_t* __restrict__ q, int se
 
 // Issues tile k of the stream (KV or query; `rec` its record) into buffer
 // k mod 4.  `lengths` says whether the live tiles' lengths have landed in LDS;
-// before that a live tile is loaded in full (it lies inside its node's
-// reserved blocks) and only the compute looks at its length.
+// before that a live tile is loaded in full (it lies inside the pool: its
+// node's reserved rows, or with 16-token blocks up to 16 rows past them) and
+// only the compute looks at its length.
 template <int D>
 __device__ __forceinline__ void dma_stream_tile(TREEPO_PARTIAL_PARAMS, int k, int2 rec, const BlockTables& bt,
                                                 const Pipe<D>& p, int wave, int lane, bool lengths) {
@@ -885,8 +886,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
 //
 // One workgroup per (piece, KV head).  K rows are copied with 16-byte moves;
 // V rows are transposed through LDS (padded rows, no bank conflicts) and
-// written as runs of consecutive tokens of each d-row of the transposed half
-// blocks.
+// written as runs of consecutive tokens of each d-row of the transposed
+// 16-row groups.
 constexpr int kMaxPieces = 128;
 struct AppendBatch {
   int32_t n;      // pieces
