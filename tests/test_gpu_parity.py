@@ -184,6 +184,33 @@ def test_large_configs_every_leaf(cfg_id):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("cfg_id,hq,hkv", [(2, 16, 2), (4, 32, 4)])
+def test_head_dim_64_full_size(cfg_id, hq, hkv):
+    """D = 64 at full size: the 16-leaf 7,680-token tree (one round of streams)
+    and the irregular 32-prompt trees (several rounds; 32-leaf roots give 256
+    rows at G = 8, cut into two leaf groups), every leaf against the oracle
+    in both modes."""
+    import dataclasses
+    import torch
+    cfg = dataclasses.replace(CONFIGS[cfg_id], hq=hq, hkv=hkv, d=64)
+    dt = _dt(cfg=cfg, log=build_call_log(cfg_id))
+    outs = {}
+    for mode in (0, 1):
+        out, lse = dt.decode(mode)
+        torch.cuda.synchronize()
+        outs[mode] = (out.cpu().numpy(), lse.cpu().numpy())
+        assert np.isfinite(outs[mode][0]).all() and np.isfinite(outs[mode][1]).all()
+    ref, ref_lse = _oracle_by_tree(dt)
+    for mode in (0, 1):
+        o, l = outs[mode]
+        err, err_l = float(np.abs(o - ref).max()), float(np.abs(l - ref_lse).max())
+        print(f"[parity cfg{cfg_id} D=64 all {len(dt.leaves)} leaves mode={mode}] max|out-oracle|={err:.3e} "
+              f"max|lse-oracle|={err_l:.3e}", flush=True)
+        assert err <= TOL and err_l <= TOL
+    del dt
+    torch.cuda.empty_cache()
+
+
 def test_many_entries_per_key():
     """Leaves whose (leaf, KV head) keys collect hundreds of partial entries
     (a 40,000-token root cut over every stream, then a short fork): the
