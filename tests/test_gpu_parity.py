@@ -211,6 +211,30 @@ def test_head_dim_64_full_size(cfg_id, hq, hkv):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("n_leaves,hq,hkv", [(1024, 28, 4), (4096, 8, 8)])
+def test_wide_root(n_leaves, hq, hkv):
+    """One 1,000-token root under 1,024 or 4,096 one- to three-token leaves:
+    the root's rows (leaves x G) are cut into dozens of leaf groups of at most
+    128 rows, streams hold many pieces and up to a full table of query
+    segments, and every leaf's key merges the root's partial with its own."""
+    import torch
+    rng = np.random.default_rng(n_leaves)
+    own = [int(x) for x in rng.integers(1, 4, n_leaves)]
+    ops = [("root", 1000), ("append", [0], [1000]), ("fork", 0, n_leaves, 64),
+           ("append", list(range(1, n_leaves + 1)), own)]
+    rows = {0: 1000, **{1 + i: own[i] for i in range(n_leaves)}}
+    log = _Log(ops, list(range(1, n_leaves + 1)), rows)
+    log.n_nodes = n_leaves + 1
+    dt = _dt(cfg=_random_cfg(200 + hq, hq, hkv, 128), log=log)
+    pieces, _, _, ns = dt.ctx.export_plan(dt.leaves, 0)
+    print(f"[wide root] {n_leaves} leaves: {ns} streams, {len(pieces)} pieces, "
+          f"{len({int(p[0]) for p in pieces if p[1] > 1})} root leaf groups", flush=True)
+    for mode in (0, 1):
+        _check(dt, mode, tag=f"wide-root-{n_leaves}")
+    del dt
+    torch.cuda.empty_cache()
+
+
 def test_many_entries_per_key():
     """Leaves whose (leaf, KV head) keys collect hundreds of partial entries
     (a 40,000-token root cut over every stream, then a short fork): the
