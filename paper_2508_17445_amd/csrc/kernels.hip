@@ -214,7 +214,7 @@ __device__ __forceinline__ void wait_tile(int k, int ntot) {
 struct Scalars {
   int32_t hq, hkv, group;
   float scale_log2;
-  int32_t write_through;  // partial rows stored write-through (large plans)
+  int32_t packed;  // partial rows as written-through 24-bit floats (compact plans)
 };
 
 #define TREEPO_PARTIAL_PARAMS                                                         \
@@ -290,22 +290,59 @@ __device__ __forceinline__ int64_t partial_row(const BlockTables& bt, int seg, i
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// Stores 16 bytes of a partial row.  Write-through (sc1: device scope) for
-// plans with compact slots, whose partial rows far exceed the L2 (45-83 MB
-// for the 64-prompt batch rollout, the irregular 32-prompt tree and the
-// 16k-token long-context tree): their write-back from L2 while the KV stream
-// is read cost up to a fifth of the kernel (a timing build without the
-// stores ran the irregular tree 21% faster), and writing them through took
-// the batch rollout's kernel from 1.258 to 1.179 ms, the irregular tree's
-// from 0.408 to 0.399 and the long-context tree's from 1.916 to 1.846.
-// Small plans, whose few MB of partials stay in the L2, keep write-back
-// stores (16 leaves of 7680 tokens, write-through: 35.6 -> 37.2 us).  The
-// s_nop covers the store-data hazard the compiler cannot see through the asm.
-__device__ __forceinline__ void store_partial(float* p, const f32x4& v, bool write_through) {
-  if (write_through)
-    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" :: "v"(p), "v"(v) : "memory");
-  else
-    *reinterpret_cast<f32x4*>(p) = v;
+// 12-byte groups at 4-byte alignment (a plain 3-vector would be assumed
+// 16-byte aligned, which lets the compiler widen its loads past the group).
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
+
+// Partial O rows.  Strided plans (a few MB of partials, which stay in the L2
+// until the combine reads them) keep fp32 rows of D floats, written back.
+// Compact plans, whose partial rows far exceed the L2 (45-83 MB for the
+// 64-prompt batch rollout, the irregular 32-prompt tree and the 16k-token
+// long-context tree), write them as 24-bit floats and write them through:
+//   * Each value keeps the upper 24 bits of its fp32 pattern (sign,
+//     exponent, 15 fraction bits), rounded to nearest; the four values of a
+//     lane's d-group (d = 4c .. 4c + 3) take three dwords, dword k < 3 holding
+//     value k in its low 24 bits and byte k of value 3 in its top byte; a row
+//     is D / 4 groups, 3 D / 4 dwords.  The rounding is below 2^-16 of each
+//     value, so a merged output moves by less than 2^-16 of the largest |V|
+//     element it averages (about 1e-4 for N(0, 1) values).  Partial rows cost
+//     far more than their bytes while the KV stream is read (a timing build
+//     without them ran the irregular tree 21% faster); at 3/4 of the bytes its
+//     kernel ran 2.4% faster (0.399 -> 0.390 ms) and the batch rollout's 0.9%.
+//     Strided plans gain nothing from it.
+//   * Write-through (sc1: device scope): the rows leave the L2 as they are
+//     written instead of being written back in bursts while the KV stream
+//     fills it: the batch rollout's kernel 1.258 -> 1.179 ms, the irregular
+//     tree's 0.408 -> 0.399, the long-context tree's 1.916 -> 1.846; for the
+//     16 leaves of 7680 tokens (strided) it was slower (35.6 -> 37.2 us).
+// The s_nop covers the store-data hazard the compiler cannot see through the
+// asm.
+__device__ __forceinline__ uint32_t round24(float x) {
+  return (__builtin_bit_cast(uint32_t, x) + 0x80u) >> 8;
+}
+
+__device__ __forceinline__ u32x3 pack24(const f32x4& v) {
+  const uint32_t a = round24(v.x), b = round24(v.y), c = round24(v.z), d = round24(v.w);
+  return u32x3{a | (d << 24), b | ((d >> 8) << 24), c | ((d >> 16) << 24)};
+}
+
+__device__ __forceinline__ void unpack24(const u32x3& p, float (&f)[4]) {
+  f[0] = __builtin_bit_cast(float, p.x << 8);
+  f[1] = __builtin_bit_cast(float, p.y << 8);
+  f[2] = __builtin_bit_cast(float, p.z << 8);
+  f[3] = __builtin_bit_cast(float, ((p.x >> 24) | ((p.y >> 24) << 8) | ((p.z >> 24) << 16)) << 8);
+}
+
+// Stores d-group c (values 4c .. 4c + 3) of partial row `slot`.
+template <int D>
+__device__ __forceinline__ void store_partial(float* part_o, int64_t slot, int c, const f32x4& v, bool packed) {
+  if (packed) {
+    const u32x3 w = pack24(v);
+    uint32_t* p = reinterpret_cast<uint32_t*>(part_o) + slot * (3 * D / 4) + 3 * c;
+    asm volatile("global_store_dwordx3 %0, %1, off sc1\n\ts_nop 1" :: "v"(p), "v"(w) : "memory");
+  } else {
+    *reinterpret_cast<f32x4*>(part_o + slot * D + 4 * c) = v;
+  }
 }
 
 __device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c) {
@@ -515,7 +552,7 @@ __device__ __forceinline__ void dsplit_piece(TREEPO_PARTIAL_PARAMS, const PieceR
     const int64_t slot = partial_row(bt, pc.seg, m, sc.group);
 #pragma unroll
     for (int db = 0; db < kDBw; ++db)
-      store_partial(part_o + slot * D + 16 * (db0 + db) + 4 * a, acc[db], sc.write_through != 0);
+      store_partial<D>(part_o, slot, 4 * (db0 + db) + a, acc[db], sc.packed != 0);
     if (a == 0 && db0 == 0) {
       part_ml[slot * 2 + 0] = m_ref;
       part_ml[slot * 2 + 1] = l_sum;
@@ -654,7 +691,7 @@ __device__ __forceinline__ void rows_piece(TREEPO_PARTIAL_PARAMS, const PieceRec
       const int64_t slot = partial_row(bt, pc.seg, m, sc.group);
 #pragma unroll
       for (int db = 0; db < kDB; ++db)
-        store_partial(part_o + slot * D + 16 * db + 4 * a, acc[i][db], sc.write_through != 0);
+        store_partial<D>(part_o, slot, 4 * db + a, acc[i][db], sc.packed != 0);
       if (a == 0) {
         part_ml[slot * 2 + 0] = m_ref[i];
         part_ml[slot * 2 + 1] = l;
@@ -736,22 +773,26 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
 // 2^(m_e - m*) O_e / L, lse = (m* + log2 L) ln 2.  Partials without tokens
 // (m = -inf) contribute nothing.  Entry e of the key sits at partial row
 // (base + e) G + h'; comb[key] = {base, n}.  Two layouts:
-//   strided (base = key E, E the largest count): the (m, l) pairs of entries
+//   strided (base = key E, E the largest count; fp32 rows, every lane its
+//     D / 64 values of each row): the (m, l) pairs of entries
 //     0..min(E, 64)-1 (one per lane) and the O rows of entries
-//     0..min(E, R0)-1 (every lane its d-slice) are loaded in the same round
-//     as the count, so a key with up to R0 entries costs one memory round
-//     trip; entries past the count (stale values of earlier calls) are
-//     masked out by selection.  For plans whose speculative reads are small
-//     (the decode is then latency bound).
-//   compact (base = the prefix sum of the counts): {base, n} first, then
-//     exactly the n entries' rows -- a second round trip, but no row is read
-//     that the key does not hold (plans with many keys, where the combine is
-//     bound by the bytes it reads).
-// Later entries follow in batches of 16 independent row loads.  The sum runs
-// in the plan's fixed entry order, so results are deterministic.
+//     0..min(E, R0)-1 are loaded in the same round as the count, so a key
+//     with up to R0 entries costs one memory round trip; entries past the
+//     count (stale values of earlier calls) are masked out by selection.  For
+//     plans whose speculative reads are small (the decode is then latency
+//     bound).  Later entries follow in batches of 16 independent row loads.
+//   compact (base = the prefix sum of the counts; packed 24-bit rows):
+//     {base, n} first, then exactly the n entries' rows -- a second round
+//     trip, but no row is read that the key does not hold (plans with many
+//     keys, where the combine is bound by the bytes it reads).  A row's D / 4
+//     packed d-groups are read by D / 4 lanes, so the wave forms S = 256 / D
+//     slots that read S entries side by side (slot s takes entries s, s + S,
+//     ...); the slots' sums are added at the end.
+// The sums run in a fixed order, so results are deterministic.
 
-// Adds sum over entries k in [k0, cnt) of the round starting at entry `base`
-// of w_k O_k to o (w_k in lane k of w), 16 independent row loads at a time.
+// Strided layout: adds sum over entries k in [k0, cnt) of the 64-entry batch
+// starting at entry `base` of w_k O_k to o (w_k in lane k of w), 16
+// independent row loads at a time.
 template <int D>
 __device__ __forceinline__ void combine_rows(float (&o)[D / 64], const float* __restrict__ part_o, int64_t row0,
                                              int group, int base, int k0, int cnt, float w, int lane) {
@@ -777,14 +818,46 @@ __device__ __forceinline__ void combine_rows(float (&o)[D / 64], const float* __
   }
 }
 
+// Compact layout (packed rows): the same sum, lane (slot s, group c) reading
+// entries k0 + s + S t, eight rows per lane at a time.
+template <int D>
+__device__ __forceinline__ void combine_rows_packed(float (&o)[4], const uint32_t* __restrict__ part_o, int64_t row0,
+                                                    int group, int base, int k0, int cnt, float w, int lane) {
+  constexpr int kNG = D / 4, kS = 64 / kNG, kRow = 3 * D / 4, kT = 8;
+  const int c = lane % kNG, sl = lane / kNG;
+  for (; k0 < cnt; k0 += kT * kS) {
+    u32x3 v[kT];
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      const int k = k0 + sl + kS * t;
+      const int kk = k < cnt ? k : cnt - 1;
+      v[t] = *reinterpret_cast<const u32x3*>(part_o + (row0 + static_cast<int64_t>(base + kk) * group) * kRow + 3 * c);
+    }
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      const int k = k0 + sl + kS * t;
+      const float wk = __shfl(w, k < cnt ? k : 0);
+      float f[4];
+      unpack24(v[t], f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = k >= cnt || wk == 0.f ? o[j] : fmaf(wk, f[j], o[j]);
+    }
+  }
+}
+
 template <int D, int R0, bool kCompact>
 __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restrict__ comb, int32_t emax,
                                                            const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml,
                                                            float* __restrict__ out, float* __restrict__ lse,
                                                            int32_t n_leaves, int32_t hq, int32_t hkv, int32_t group) {
-  constexpr int kPL = D / 64;
+  constexpr int kPL = D / 64;                    // strided: values per lane of a row
+  constexpr int kNG = D / 4, kS = 64 / kNG;      // compact: d-groups per row, slots per wave
+  constexpr int kO = kCompact ? 4 : kPL;         // output values per lane
+  constexpr int kV = kCompact ? R0 / kS : R0;    // round-0 rows per lane
+  const uint32_t* __restrict__ packed = reinterpret_cast<const uint32_t*>(part_o);
   const int lane = threadIdx.x & 63;
+  const int c = lane % kNG, sl = lane / kNG;
   const int gw = static_cast<int>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (gw >= n_leaves * hq) return;
   const int x = gw / hq;
@@ -794,9 +867,9 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
   const int key = x * hkv + g;
   int n, base, lim;
   if (kCompact) {
-    const int2 c = comb[key];
-    base = __builtin_amdgcn_readfirstlane(c.x);
-    n = __builtin_amdgcn_readfirstlane(c.y);
+    const int2 cb = comb[key];
+    base = __builtin_amdgcn_readfirstlane(cb.x);
+    n = __builtin_amdgcn_readfirstlane(cb.y);
     lim = n;          // rows the key holds
   } else {
     base = key * emax;
@@ -810,16 +883,24 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
   const int avail = lim < 64 ? lim : 64;
   const int avail_o = lim < R0 ? lim : R0;
   const int64_t my_row = row0 + static_cast<int64_t>(lane < avail ? lane : avail - 1) * group;
-  float v[R0][kPL];
+  float vf[kCompact ? 1 : kV][kPL];
+  u32x3 vp[kCompact ? kV : 1];
 #pragma unroll
-  for (int i = 0; i < R0; ++i) {
-    if (i < avail_o) {
-      const float* po = part_o + (row0 + static_cast<int64_t>(i) * group) * D + lane * kPL;
-#pragma unroll
-      for (int j = 0; j < kPL; ++j) v[i][j] = po[j];
+  for (int i = 0; i < kV; ++i) {
+    if constexpr (kCompact) {
+      const int e = sl + kS * i;
+      vp[i] = e < avail_o ? *reinterpret_cast<const u32x3*>(packed + (row0 + static_cast<int64_t>(e) * group) *
+                                                                         (3 * D / 4) + 3 * c)
+                          : u32x3{0u, 0u, 0u};
     } else {
+      if (i < avail_o) {
+        const float* po = part_o + (row0 + static_cast<int64_t>(i) * group) * D + lane * kPL;
 #pragma unroll
-      for (int j = 0; j < kPL; ++j) v[i][j] = 0.f;
+        for (int j = 0; j < kPL; ++j) vf[i][j] = po[j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < kPL; ++j) vf[i][j] = 0.f;
+      }
     }
   }
   const float m_ld = part_ml[2 * my_row];
@@ -827,12 +908,19 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
   // keeps every round-0 load ahead of the count-dependent code (otherwise the
   // compiler may sink a load under the weight test, a second round trip)
 #pragma unroll
-  for (int i = 0; i < R0; ++i)
+  for (int i = 0; i < kV; ++i) {
+    if constexpr (kCompact) {
+      asm volatile("" ::"v"(vp[i].x), "v"(vp[i].y), "v"(vp[i].z));
+    } else {
 #pragma unroll
-    for (int j = 0; j < kPL; ++j) asm volatile("" ::"v"(v[i][j]));
+      for (int j = 0; j < kPL; ++j) asm volatile("" ::"v"(vf[i][j]));
+    }
+  }
   asm volatile("" ::"v"(m_ld), "v"(l_ld));
 
-  float o[kPL];
+  float o[kO];
+#pragma unroll
+  for (int j = 0; j < kO; ++j) o[j] = 0.f;
   int cnt = n < 64 ? n : 64;
   float mi = lane < cnt ? m_ld : -INFINITY;
   float li = lane < cnt ? l_ld : 0.f;
@@ -843,17 +931,29 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
   float run_l = w * li;
 #pragma unroll
   for (int sh = 1; sh < 64; sh <<= 1) run_l += __shfl_xor(run_l, sh);
+  // entries past the count have w = 0 and may hold anything: select, not multiply
 #pragma unroll
-  for (int j = 0; j < kPL; ++j) o[j] = 0.f;
+  for (int i = 0; i < kV; ++i) {
+    if constexpr (kCompact) {
+      const float wk = __shfl(w, sl + kS * i);
+      float f[4];
+      unpack24(vp[i], f);
 #pragma unroll
-  for (int i = 0; i < R0; ++i) {
-    // entries past the count have w = 0 and may hold anything: select, not multiply
-    const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), i));
+      for (int j = 0; j < 4; ++j) o[j] = wk == 0.f ? o[j] : fmaf(wk, f[j], o[j]);
+    } else {
+      const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), i));
 #pragma unroll
-    for (int j = 0; j < kPL; ++j) o[j] = wk == 0.f ? o[j] : fmaf(wk, v[i][j], o[j]);
+      for (int j = 0; j < kPL; ++j) o[j] = wk == 0.f ? o[j] : fmaf(wk, vf[i][j], o[j]);
+    }
   }
+  auto rows = [&](int b, int k0) {
+    if constexpr (kCompact)
+      combine_rows_packed<D>(o, packed, row0, group, b, k0, cnt, w, lane);
+    else
+      combine_rows<D>(o, part_o, row0, group, b, k0, cnt, w, lane);
+  };
   if (n > R0) {
-    combine_rows<D>(o, part_o, row0, group, 0, R0, cnt, w, lane);
+    rows(0, R0);
     for (int b = 64; b < n; b += 64) {
       cnt = n - b < 64 ? n - b : 64;
       const int64_t r = row0 + static_cast<int64_t>(b + (lane < cnt ? lane : 0)) * group;
@@ -870,15 +970,24 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
       for (int sh = 1; sh < 64; sh <<= 1) wl += __shfl_xor(wl, sh);
       run_l = run_l * keep + wl;
 #pragma unroll
-      for (int j = 0; j < kPL; ++j) o[j] *= keep;
+      for (int j = 0; j < kO; ++j) o[j] *= keep;
       run_m = nm;
-      combine_rows<D>(o, part_o, row0, group, b, 0, cnt, w, lane);
+      rows(b, 0);
     }
   }
   const float inv = 1.f / run_l;
-  float* op = out + (static_cast<int64_t>(x) * hq + h) * D + lane * kPL;
+  float* op = out + (static_cast<int64_t>(x) * hq + h) * D;
+  if constexpr (kCompact) {
+    // the slots' sums, then the lanes of slot 0 write the row
 #pragma unroll
-  for (int j = 0; j < kPL; ++j) op[j] = o[j] * inv;
+    for (int sh = kNG; sh < 64; sh <<= 1)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] += __shfl_xor(o[j], sh);
+    if (sl == 0) *reinterpret_cast<f32x4*>(op + 4 * c) = f32x4{o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv};
+  } else {
+#pragma unroll
+    for (int j = 0; j < kPL; ++j) op[lane * kPL + j] = o[j] * inv;
+  }
   if (lse != nullptr && lane == 0) lse[static_cast<int64_t>(x) * hq + h] = (run_m + __log2f(run_l)) * kLn2;
 }
 

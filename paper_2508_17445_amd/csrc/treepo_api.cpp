@@ -399,7 +399,9 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   put(cp.blob, cp.off_comb, comb);
   off = 0;
   cp.off_part_o = off;
-  off = align_up(off + static_cast<size_t>(p.partial_rows) * ctx->cfg.head_dim * sizeof(float));
+  // fp32 rows of D floats, or packed rows of 3 D / 4 dwords (compact plans)
+  const size_t row_words = p.compact ? 3 * static_cast<size_t>(ctx->cfg.head_dim) / 4 : ctx->cfg.head_dim;
+  off = align_up(off + static_cast<size_t>(p.partial_rows) * row_words * sizeof(uint32_t));
   cp.off_part_ml = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * 2 * sizeof(float));
   cp.ws_bytes = off;

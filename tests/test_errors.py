@@ -198,7 +198,8 @@ def test_noalloc_decode_rejects_plans_beyond_its_scratch():
     from tests.lib_helpers import replay_host
     from workloads import CONFIGS, build_call_log
     c = CONFIGS[3]
-    ctx = host_ctx(hq=c.hq, hkv=c.hkv, d=c.d)
+    # the batch rollout's trees with twice its heads: ~125 MB of partial slots
+    ctx = host_ctx(hq=2 * c.hq, hkv=2 * c.hkv, d=c.d)
     log = build_call_log(3)
     replay_host(ctx, log)
     assert ctx.workspace_size(log.leaves, 0) > 64 << 20
