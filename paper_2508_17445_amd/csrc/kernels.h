@@ -21,7 +21,7 @@ struct DecodeArgs {
   const int32_t* blocks;   // stream blocks, block_ints int32 each (layout in tree_core.h)
   int32_t block_ints;
   int32_t n_streams;
-  float* part_o;           // unnormalised rows: fp32 [partial_rows][D], or (compact) packed 24-bit [partial_rows][3 D / 4] dwords
+  float* part_o;           // unnormalised rows: fp32 [partial_rows][D], or (compact) [partial_rows][D / 4] 64-bit block-float groups
   float* part_ml;          // fp32 [partial_rows][2]: running max (log2 units), sum
   const int2* comb;           // per key (leaf, KV head): {first entry, entries to merge}
   int32_t emax;               // entries per key at most (partial slot stride of strided plans)

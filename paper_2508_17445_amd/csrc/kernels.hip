@@ -214,7 +214,7 @@ __device__ __forceinline__ void wait_tile(int k, int ntot) {
 struct Scalars {
   int32_t hq, hkv, group;
   float scale_log2;
-  int32_t packed;  // partial rows as written-through 24-bit floats (compact plans)
+  int32_t packed;  // partial rows as written-through block floating point (compact plans)
 };
 
 #define TREEPO_PARTIAL_PARAMS                                                         \
@@ -290,26 +290,30 @@ __device__ __forceinline__ int64_t partial_row(const BlockTables& bt, int seg, i
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// 12-byte groups at 4-byte alignment (a plain 3-vector would be assumed
-// 16-byte aligned, which lets the compiler widen its loads past the group).
-typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Partial O rows.  Strided plans (a few MB of partials, which stay in the L2
 // until the combine reads them) keep fp32 rows of D floats, written back.
-// Compact plans, whose partial rows far exceed the L2 (45-83 MB for the
-// 64-prompt batch rollout, the irregular 32-prompt tree and the 16k-token
-// long-context tree), write them as 24-bit floats and write them through:
-//   * Each value keeps the upper 24 bits of its fp32 pattern (sign,
-//     exponent, 15 fraction bits), rounded to nearest; the four values of a
-//     lane's d-group (d = 4c .. 4c + 3) take three dwords, dword k < 3 holding
-//     value k in its low 24 bits and byte k of value 3 in its top byte; a row
-//     is D / 4 groups, 3 D / 4 dwords.  The rounding is below 2^-16 of each
-//     value, so a merged output moves by less than 2^-16 of the largest |V|
-//     element it averages (about 1e-4 for N(0, 1) values).  Partial rows cost
-//     far more than their bytes while the KV stream is read (a timing build
-//     without them ran the irregular tree 21% faster); at 3/4 of the bytes its
-//     kernel ran 2.4% faster (0.399 -> 0.390 ms) and the batch rollout's 0.9%.
-//     Strided plans gain nothing from it.
+// Compact plans, whose partial rows far exceed the L2 (45-83 MB in fp32 for
+// the 64-prompt batch rollout, the irregular 32-prompt tree and the 16k-token
+// long-context tree), store them in a block floating-point format at half
+// the bytes and write them through:
+//   * A lane's d-group (values x_0..x_3 at d = 4c .. 4c + 3) is one 64-bit
+//     word: the group's largest fp32 exponent field E (8 bits, low nibble in
+//     bits 28-31 of the first dword, high nibble in those of the second) and
+//     four 14-bit two's-complement mantissas m_k = round(x_k 2^(139 - E))
+//     (|x_k| < 2^(E - 126), so |m_k| <= 8192; clamped to 8191), m_0 and m_1
+//     in bits 0-13 and 14-27 of the first dword, m_2 and m_3 in the second;
+//     x_k = m_k 2^(E - 139).  A row is D / 4 words.  Groups whose E is below
+//     13 (all values under 2^-114) store zeros.  Each value is off by at most
+//     2^-13 of its group's largest magnitude; a merged output, a weighted
+//     mean of normalised partials, by at most 2^-13 of the largest |V| value
+//     it averages -- about 8e-4 for N(0, 1) values at the sizes here, against
+//     the 2e-3 bar, and measured far smaller.  Accumulation stays fp32.
+//     Partial rows cost far more than their bytes while the KV stream is read
+//     (a timing build without them ran the irregular tree 21% faster): at
+//     half the bytes its kernel ran 5% faster (0.401 -> 0.378 ms), the batch
+//     rollout's 2.4% and the long-context tree's 0.8%.
 //   * Write-through (sc1: device scope): the rows leave the L2 as they are
 //     written instead of being written back in bursts while the KV stream
 //     fills it: the batch rollout's kernel 1.258 -> 1.179 ms, the irregular
@@ -317,29 +321,41 @@ typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
 //     16 leaves of 7680 tokens (strided) it was slower (35.6 -> 37.2 us).
 // The s_nop covers the store-data hazard the compiler cannot see through the
 // asm.
-__device__ __forceinline__ uint32_t round24(float x) {
-  return (__builtin_bit_cast(uint32_t, x) + 0x80u) >> 8;
+// The exponent field of x (taken by value: a bit cast of a vector element
+// itself reads the vector's first element).
+__device__ __forceinline__ uint32_t exp_field(float x) { return (__builtin_bit_cast(uint32_t, x) >> 23) & 0xFFu; }
+
+__device__ __forceinline__ u32x2 pack_group(const f32x4& v) {
+  const uint32_t e = max(max(exp_field(v.x), exp_field(v.y)), max(exp_field(v.z), exp_field(v.w)));
+  int m0 = 0, m1 = 0, m2 = 0, m3 = 0;
+  if (e >= 13) {
+    const float sc = __builtin_bit_cast(float, (266u - e) << 23);  // 2^(139 - E)
+    m0 = min(static_cast<int>(rintf(v.x * sc)), 8191);
+    m1 = min(static_cast<int>(rintf(v.y * sc)), 8191);
+    m2 = min(static_cast<int>(rintf(v.z * sc)), 8191);
+    m3 = min(static_cast<int>(rintf(v.w * sc)), 8191);
+  }
+  return u32x2{(static_cast<uint32_t>(m0) & 0x3FFFu) | ((static_cast<uint32_t>(m1) & 0x3FFFu) << 14) | (e << 28),
+               (static_cast<uint32_t>(m2) & 0x3FFFu) | ((static_cast<uint32_t>(m3) & 0x3FFFu) << 14) |
+                   ((e >> 4) << 28)};
 }
 
-__device__ __forceinline__ u32x3 pack24(const f32x4& v) {
-  const uint32_t a = round24(v.x), b = round24(v.y), c = round24(v.z), d = round24(v.w);
-  return u32x3{a | (d << 24), b | ((d >> 8) << 24), c | ((d >> 16) << 24)};
-}
-
-__device__ __forceinline__ void unpack24(const u32x3& p, float (&f)[4]) {
-  f[0] = __builtin_bit_cast(float, p.x << 8);
-  f[1] = __builtin_bit_cast(float, p.y << 8);
-  f[2] = __builtin_bit_cast(float, p.z << 8);
-  f[3] = __builtin_bit_cast(float, ((p.x >> 24) | ((p.y >> 24) << 8) | ((p.z >> 24) << 16)) << 8);
+__device__ __forceinline__ void unpack_group(const u32x2& p, float (&f)[4]) {
+  const uint32_t e = (p.x >> 28) | ((p.y >> 28) << 4);
+  const float sc = e >= 13 ? __builtin_bit_cast(float, (e - 12) << 23) : 0.f;  // 2^(E - 139)
+  f[0] = static_cast<float>(static_cast<int>(p.x << 18) >> 18) * sc;
+  f[1] = static_cast<float>(static_cast<int>(p.x << 4) >> 18) * sc;
+  f[2] = static_cast<float>(static_cast<int>(p.y << 18) >> 18) * sc;
+  f[3] = static_cast<float>(static_cast<int>(p.y << 4) >> 18) * sc;
 }
 
 // Stores d-group c (values 4c .. 4c + 3) of partial row `slot`.
 template <int D>
 __device__ __forceinline__ void store_partial(float* part_o, int64_t slot, int c, const f32x4& v, bool packed) {
   if (packed) {
-    const u32x3 w = pack24(v);
-    uint32_t* p = reinterpret_cast<uint32_t*>(part_o) + slot * (3 * D / 4) + 3 * c;
-    asm volatile("global_store_dwordx3 %0, %1, off sc1\n\ts_nop 1" :: "v"(p), "v"(w) : "memory");
+    const u32x2 w = pack_group(v);
+    uint32_t* p = reinterpret_cast<uint32_t*>(part_o) + slot * (D / 2) + 2 * c;
+    asm volatile("global_store_dwordx2 %0, %1, off sc1\n\ts_nop 1" :: "v"(p), "v"(w) : "memory");
   } else {
     *reinterpret_cast<f32x4*>(part_o + slot * D + 4 * c) = v;
   }
@@ -781,7 +797,7 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void partial_kernel(const int3
 //     count (stale values of earlier calls) are masked out by selection.  For
 //     plans whose speculative reads are small (the decode is then latency
 //     bound).  Later entries follow in batches of 16 independent row loads.
-//   compact (base = the prefix sum of the counts; packed 24-bit rows):
+//   compact (base = the prefix sum of the counts; block floating-point rows):
 //     {base, n} first, then exactly the n entries' rows -- a second round
 //     trip, but no row is read that the key does not hold (plans with many
 //     keys, where the combine is bound by the bytes it reads).  A row's D / 4
@@ -818,27 +834,27 @@ __device__ __forceinline__ void combine_rows(float (&o)[D / 64], const float* __
   }
 }
 
-// Compact layout (packed rows): the same sum, lane (slot s, group c) reading
+// Compact layout (block floating-point rows): the same sum, lane (slot s, group c) reading
 // entries k0 + s + S t, eight rows per lane at a time.
 template <int D>
 __device__ __forceinline__ void combine_rows_packed(float (&o)[4], const uint32_t* __restrict__ part_o, int64_t row0,
                                                     int group, int base, int k0, int cnt, float w, int lane) {
-  constexpr int kNG = D / 4, kS = 64 / kNG, kRow = 3 * D / 4, kT = 8;
+  constexpr int kNG = D / 4, kS = 64 / kNG, kRow = D / 2, kT = 8;
   const int c = lane % kNG, sl = lane / kNG;
   for (; k0 < cnt; k0 += kT * kS) {
-    u32x3 v[kT];
+    u32x2 v[kT];
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
       const int k = k0 + sl + kS * t;
       const int kk = k < cnt ? k : cnt - 1;
-      v[t] = *reinterpret_cast<const u32x3*>(part_o + (row0 + static_cast<int64_t>(base + kk) * group) * kRow + 3 * c);
+      v[t] = *reinterpret_cast<const u32x2*>(part_o + (row0 + static_cast<int64_t>(base + kk) * group) * kRow + 2 * c);
     }
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
       const int k = k0 + sl + kS * t;
       const float wk = __shfl(w, k < cnt ? k : 0);
       float f[4];
-      unpack24(v[t], f);
+      unpack_group(v[t], f);
 #pragma unroll
       for (int j = 0; j < 4; ++j) o[j] = k >= cnt || wk == 0.f ? o[j] : fmaf(wk, f[j], o[j]);
     }
@@ -884,14 +900,14 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
   const int avail_o = lim < R0 ? lim : R0;
   const int64_t my_row = row0 + static_cast<int64_t>(lane < avail ? lane : avail - 1) * group;
   float vf[kCompact ? 1 : kV][kPL];
-  u32x3 vp[kCompact ? kV : 1];
+  u32x2 vp[kCompact ? kV : 1];
 #pragma unroll
   for (int i = 0; i < kV; ++i) {
     if constexpr (kCompact) {
       const int e = sl + kS * i;
-      vp[i] = e < avail_o ? *reinterpret_cast<const u32x3*>(packed + (row0 + static_cast<int64_t>(e) * group) *
-                                                                         (3 * D / 4) + 3 * c)
-                          : u32x3{0u, 0u, 0u};
+      vp[i] = e < avail_o ? *reinterpret_cast<const u32x2*>(packed + (row0 + static_cast<int64_t>(e) * group) *
+                                                                         (D / 2) + 2 * c)
+                          : u32x2{0u, 0u};
     } else {
       if (i < avail_o) {
         const float* po = part_o + (row0 + static_cast<int64_t>(i) * group) * D + lane * kPL;
@@ -910,7 +926,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
 #pragma unroll
   for (int i = 0; i < kV; ++i) {
     if constexpr (kCompact) {
-      asm volatile("" ::"v"(vp[i].x), "v"(vp[i].y), "v"(vp[i].z));
+      asm volatile("" ::"v"(vp[i].x), "v"(vp[i].y));
     } else {
 #pragma unroll
       for (int j = 0; j < kPL; ++j) asm volatile("" ::"v"(vf[i][j]));
@@ -937,7 +953,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
     if constexpr (kCompact) {
       const float wk = __shfl(w, sl + kS * i);
       float f[4];
-      unpack24(vp[i], f);
+      unpack_group(vp[i], f);
 #pragma unroll
       for (int j = 0; j < 4; ++j) o[j] = wk == 0.f ? o[j] : fmaf(wk, f[j], o[j]);
     } else {

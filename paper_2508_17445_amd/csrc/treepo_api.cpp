@@ -399,8 +399,8 @@ int32_t get_plan(treepo_ctx* ctx, int32_t n, const int32_t* leaves, int32_t mode
   put(cp.blob, cp.off_comb, comb);
   off = 0;
   cp.off_part_o = off;
-  // fp32 rows of D floats, or packed rows of 3 D / 4 dwords (compact plans)
-  const size_t row_words = p.compact ? 3 * static_cast<size_t>(ctx->cfg.head_dim) / 4 : ctx->cfg.head_dim;
+  // fp32 rows of D floats, or block floating-point rows of D / 2 dwords (compact plans)
+  const size_t row_words = p.compact ? static_cast<size_t>(ctx->cfg.head_dim) / 2 : ctx->cfg.head_dim;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * row_words * sizeof(uint32_t));
   cp.off_part_ml = off;
   off = align_up(off + static_cast<size_t>(p.partial_rows) * 2 * sizeof(float));
