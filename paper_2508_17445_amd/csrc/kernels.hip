@@ -845,12 +845,14 @@ __device__ __forceinline__ void combine_rows_packed(float (&o)[4], const uint32_
     u32x2 v[kT];
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
+      if (k0 + kS * t >= cnt) break;  // wave-uniform
       const int k = k0 + sl + kS * t;
       const int kk = k < cnt ? k : cnt - 1;
       v[t] = *reinterpret_cast<const u32x2*>(part_o + (row0 + static_cast<int64_t>(base + kk) * group) * kRow + 2 * c);
     }
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
+      if (k0 + kS * t >= cnt) break;
       const int k = k0 + sl + kS * t;
       const float wk = __shfl(w, k < cnt ? k : 0);
       float f[4];
@@ -951,6 +953,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const int2* __restric
 #pragma unroll
   for (int i = 0; i < kV; ++i) {
     if constexpr (kCompact) {
+      if (kS * i >= avail_o) break;  // no slot holds an entry from here on (wave-uniform)
       const float wk = __shfl(w, sl + kS * i);
       float f[4];
       unpack_group(vp[i], f);

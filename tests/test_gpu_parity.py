@@ -257,6 +257,35 @@ def test_many_entries_per_key():
     torch.cuda.empty_cache()
 
 
+def test_compact_plan_many_entries_per_key():
+    """A plan with compact partial slots (block floating-point rows) whose keys
+    hold 59-74 entries each: a 60,000-token root under 8 leaves, G = 8, 8 KV
+    heads, cut over every stream -- the compact combine's later rows and its
+    second batch of 64 entries."""
+    import torch
+    n = 8
+    ops = [("root", 60_000), ("append", [0], [60_000]), ("fork", 0, n, 64),
+           ("append", list(range(1, n + 1)), [5] * n)]
+    log = _Log(ops, list(range(1, n + 1)), {0: 60_000, **{1 + i: 5 for i in range(n)}})
+    log.n_nodes = n + 1
+    dt = _dt(cfg=_random_cfg(93, 64, 8, 128), log=log)
+    pieces, rowsets, _, _ = dt.ctx.export_plan(dt.leaves, 0)
+    count = {}
+    for pc in pieces:
+        for x in rowsets[pc[0]:pc[0] + pc[1]]:
+            count[(int(x), int(pc[3]))] = count.get((int(x), int(pc[3])), 0) + 1
+    rows = sum(count.values()) * 8
+    print(f"[entries per key] {min(count.values())}-{max(count.values())}; workspace "
+          f"{dt.ctx.workspace_size(dt.leaves, 0)} B for {rows} partial rows", flush=True)
+    assert max(count.values()) > 64
+    # compact slots: rows of D / 2 dwords plus (m, l), not fp32 rows at a stride of the largest count
+    assert dt.ctx.workspace_size(dt.leaves, 0) < rows * (128 * 4 + 8)
+    for mode in (0, 1):
+        _check(dt, mode, tag="compact-many-entries")
+    del dt
+    torch.cuda.empty_cache()
+
+
 def test_shared_workspace_between_contexts():
     """One workspace buffer used in turn by two contexts (different shapes and
     plans) and filled with 0xFF before every call: the plans live in memory
