@@ -233,9 +233,10 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
  * Cascade schedule: every node's K/V is read once and scored against all of
  * its descendant leaves' query rows (the nested sub-groups G_j of Sec. 2.3);
  * per-node partials are merged with a log-sum-exp combine (partial rows in
- * fp32, or, for schedules whose partials far exceed the L2, in 24-bit floats:
- * an output then moves by less than 2^-16 of the largest |V| value it
- * averages; accumulation is fp32 throughout).  The schedule
+ * fp32, or, for schedules whose partials far exceed the L2, in block floating
+ * point -- 14-bit mantissas under a shared exponent per 4 values: an output
+ * then moves by less than 2^-13 of the largest |V| value it averages;
+ * accumulation is fp32 throughout).  The schedule
  * (plan) is cached per context (the last four leaf lists and modes) and its
  * device image lives in memory the context allocates (see the ownership rule
  * above); the workspace holds only this call's partial results, so the

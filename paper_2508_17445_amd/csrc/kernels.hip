@@ -312,8 +312,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 //     the 2e-3 bar, and measured far smaller.  Accumulation stays fp32.
 //     Partial rows cost far more than their bytes while the KV stream is read
 //     (a timing build without them ran the irregular tree 21% faster): at
-//     half the bytes its kernel ran 5% faster (0.401 -> 0.378 ms), the batch
-//     rollout's 2.4% and the long-context tree's 0.8%.
+//     half the bytes its kernel ran 6% faster (0.401 -> 0.377 ms), the batch
+//     rollout's 2% (1.178 -> 1.153 ms) and the long-context tree's 0.5%.
 //   * Write-through (sc1: device scope): the rows leave the L2 as they are
 //     written instead of being written back in bursts while the KV stream
 //     fills it: the batch rollout's kernel 1.258 -> 1.179 ms, the irregular
