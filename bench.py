@@ -592,7 +592,7 @@ The profile pass runs {n} tree decode steps, {n} per-leaf decode steps and one 1
 Calibration on the 1 GiB copy kernel: FETCH_SIZE reads {fc:.1f} KiB for 1048576 KiB read (scale {fs:.4f}); WRITE_SIZE reads {wc:.1f} KiB for 1048576 KiB written (scale {ws:.4f}).
 partial_kernel<128>, tree schedule, mean of {n} dispatches:
   FETCH_SIZE {ft:.1f} KiB -> {fb} bytes read
-  WRITE_SIZE {wt:.1f} KiB -> {wb} bytes written (fp32 partial rows)
+  WRITE_SIZE {wt:.1f} KiB -> {wb} bytes written (partial rows)
 partial_kernel<128>, per-leaf baseline: FETCH_SIZE {fn:.1f} KiB ({round(fn * 1024 * fs)} bytes), WRITE_SIZE {wn:.1f} KiB ({round(wn * 1024 * ws)} bytes)
 Algorithmic bytes per launch (unique KV of the decoded chains): {alg}; measured traffic / algorithmic = {(fb + wb) / alg:.4f}
 config: {cfg_id}
