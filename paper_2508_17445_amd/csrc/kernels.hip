@@ -23,6 +23,7 @@
 
 #include <math.h>
 
+#include "partial_format.h"
 #include "tree_core.h"
 
 namespace treepo {
@@ -298,18 +299,13 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // the 64-prompt batch rollout, the irregular 32-prompt tree and the 16k-token
 // long-context tree), store them in a block floating-point format at half
 // the bytes and write them through:
-//   * A lane's d-group (values x_0..x_3 at d = 4c .. 4c + 3) is one 64-bit
-//     word: the group's largest fp32 exponent field E (8 bits, low nibble in
-//     bits 28-31 of the first dword, high nibble in those of the second) and
-//     four 14-bit two's-complement mantissas m_k = round(x_k 2^(139 - E))
-//     (|x_k| < 2^(E - 126), so |m_k| <= 8192; clamped to 8191), m_0 and m_1
-//     in bits 0-13 and 14-27 of the first dword, m_2 and m_3 in the second;
-//     x_k = m_k 2^(E - 139).  A row is D / 4 words.  Groups whose E is below
-//     13 (all values under 2^-114) store zeros.  Each value is off by at most
-//     2^-13 of its group's largest magnitude; a merged output, a weighted
-//     mean of normalised partials, by at most 2^-13 of the largest |V| value
-//     it averages -- about 8e-4 for N(0, 1) values at the sizes here, against
-//     the 2e-3 bar, and measured far smaller.  Accumulation stays fp32.
+//   * A lane's d-group (values at d = 4c .. 4c + 3) is one 64-bit word, 14-bit
+//     mantissas under the group's exponent (format in partial_format.h); a
+//     row is D / 4 words.  Each value is off by at most 2^-13 of its group's
+//     largest magnitude; a merged output, a weighted mean of normalised
+//     partials, by at most 2^-13 of the largest |V| value it averages --
+//     about 8e-4 for N(0, 1) values at the sizes here, against the 2e-3 bar,
+//     and measured far smaller.  Accumulation stays fp32.
 //     Partial rows cost far more than their bytes while the KV stream is read
 //     (a timing build without them ran the irregular tree 21% faster): at
 //     half the bytes its kernel ran 6% faster (0.401 -> 0.377 ms), the batch
@@ -319,35 +315,18 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 //     fills it: the batch rollout's kernel 1.258 -> 1.179 ms, the irregular
 //     tree's 0.408 -> 0.399, the long-context tree's 1.916 -> 1.846; for the
 //     16 leaves of 7680 tokens (strided) it was slower (35.6 -> 37.2 us).
-// The s_nop covers the store-data hazard the compiler cannot see through the
-// asm.
-// The exponent field of x (taken by value: a bit cast of a vector element
-// itself reads the vector's first element).
-__device__ __forceinline__ uint32_t exp_field(float x) { return (__builtin_bit_cast(uint32_t, x) >> 23) & 0xFFu; }
+// The s_nop in the store covers the store-data hazard the compiler cannot see
+// through the asm.
 
+// The d-group's four values are passed by value (a bit cast of a vector
+// element itself reads the vector's first element).
 __device__ __forceinline__ u32x2 pack_group(const f32x4& v) {
-  const uint32_t e = max(max(exp_field(v.x), exp_field(v.y)), max(exp_field(v.z), exp_field(v.w)));
-  int m0 = 0, m1 = 0, m2 = 0, m3 = 0;
-  if (e >= 13) {
-    const float sc = __builtin_bit_cast(float, (266u - e) << 23);  // 2^(139 - E)
-    m0 = min(static_cast<int>(rintf(v.x * sc)), 8191);
-    m1 = min(static_cast<int>(rintf(v.y * sc)), 8191);
-    m2 = min(static_cast<int>(rintf(v.z * sc)), 8191);
-    m3 = min(static_cast<int>(rintf(v.w * sc)), 8191);
-  }
-  return u32x2{(static_cast<uint32_t>(m0) & 0x3FFFu) | ((static_cast<uint32_t>(m1) & 0x3FFFu) << 14) | (e << 28),
-               (static_cast<uint32_t>(m2) & 0x3FFFu) | ((static_cast<uint32_t>(m3) & 0x3FFFu) << 14) |
-                   ((e >> 4) << 28)};
+  uint32_t w0, w1;
+  pack_group4(v.x, v.y, v.z, v.w, &w0, &w1);
+  return u32x2{w0, w1};
 }
 
-__device__ __forceinline__ void unpack_group(const u32x2& p, float (&f)[4]) {
-  const uint32_t e = (p.x >> 28) | ((p.y >> 28) << 4);
-  const float sc = e >= 13 ? __builtin_bit_cast(float, (e - 12) << 23) : 0.f;  // 2^(E - 139)
-  f[0] = static_cast<float>(static_cast<int>(p.x << 18) >> 18) * sc;
-  f[1] = static_cast<float>(static_cast<int>(p.x << 4) >> 18) * sc;
-  f[2] = static_cast<float>(static_cast<int>(p.y << 18) >> 18) * sc;
-  f[3] = static_cast<float>(static_cast<int>(p.y << 4) >> 18) * sc;
-}
+__device__ __forceinline__ void unpack_group(const u32x2& p, float (&f)[4]) { unpack_group4(p.x, p.y, f); }
 
 // Stores d-group c (values 4c .. 4c + 3) of partial row `slot`.
 template <int D>
