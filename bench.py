@@ -525,7 +525,7 @@ def _summarize_trace(cfg_id, d):
     t_avg = avg[("partial_kernel", 0)]
     txt = f"""# Kernel trace: decode step on config {cfg_id} ({_workload_name(cfg_id)})
 
-Command (repository root `$R` on the GPU box):
+Command (repository root `$R` on the MI355X host):
 
 ```
 cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/trace -o run -- python3 -u $R/bench.py --config {cfg_id} --steps {steps} --warmup {warm} --no-cpu --no-probes --no-naive > $R/gpurun_out/prof/c{cfg_id}/trace/bench.json
@@ -583,7 +583,7 @@ def _summarize_traffic(cfg_id, d):
     log = build_call_log(cfg_id)
     alg = _algorithmic_bytes(cfg_id, log)
     txt = f"""HBM traffic of the node-partial kernel, decode workload config {cfg_id} ({cfg.name}, Hq={cfg.hq} Hkv={cfg.hkv} D={cfg.d})
-Commands (repository root $R on the GPU box; each counter in its own run):
+Commands (repository root $R on the MI355X host; each counter in its own run):
   cd /tmp && export TMPDIR=/tmp
   rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/pmc/fetch -o run -- python3 $R/bench.py --profile-pass --config {cfg_id} --steps {n}
   rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/pmc/write -o run -- python3 $R/bench.py --profile-pass --config {cfg_id} --steps {n}
@@ -687,7 +687,7 @@ def _summarize_mfma(cfg_id, d):
     counters = ("SQ_INSTS_VALU_MFMA_BF16 SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES "
                 "SQ_WAVES SQ_INSTS_VALU GRBM_GUI_ACTIVE")
     txt = f"""MFMA use of the node-partial kernel, decode workload config {cfg_id} ({cfg.name}, Hq={cfg.hq} Hkv={cfg.hkv} D={cfg.d})
-Commands (repository root $R on the GPU box; one counter pass):
+Commands (repository root $R on the MI355X host; one counter pass):
   cd /tmp && export TMPDIR=/tmp
   rocprofv3 --pmc {counters} --output-format csv -d $R/gpurun_out/prof/c{cfg_id}/mfma -o run -- python3 $R/bench.py --profile-pass --config {cfg_id} --steps 10
   python3 bench.py --summarize mfma --config {cfg_id} --dir gpurun_out/prof/c{cfg_id}/mfma
@@ -734,7 +734,7 @@ def _summarize_prefill(cfg_id, d):
     naive = b.get("per_rollout_baseline")
     txt = f"""# Kernel trace: {head}
 
-Commands (repository root `$R` on the GPU box):
+Commands (repository root `$R` on the MI355X host):
 
 ```
 cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/pfprof/c{cfg_id}/trace -o run -- python3 -u $R/bench.py --prefill --config {cfg_id} --steps {steps} --warmup {warm} --no-cpu > $R/gpurun_out/pfprof/c{cfg_id}/trace/bench.json
@@ -776,7 +776,7 @@ kernels.hip sha256: {_kernel_sha()}
           "SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_LDS SQ_WAVE_CYCLES")
     mf = "SQ_INSTS_VALU_MFMA_BF16 SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_WAVES GRBM_GUI_ACTIVE"
     txt2 = f"""SQ counters of the {head}
-Commands (repository root $R on the GPU box; each pass its own run):
+Commands (repository root $R on the MI355X host; each pass its own run):
   cd /tmp && export TMPDIR=/tmp
   rocprofv3 --pmc {sq} --output-format csv -d $R/gpurun_out/pfprof/c{cfg_id}/sq -o run -- python3 $R/bench.py --prefill --config {cfg_id} --steps 3 --warmup 1 --no-cpu --no-naive
   rocprofv3 --pmc {mf} --output-format csv -d $R/gpurun_out/pfprof/c{cfg_id}/mfma -o run -- python3 $R/bench.py --prefill --config {cfg_id} --steps 3 --warmup 1 --no-cpu --no-naive
@@ -801,7 +801,7 @@ def _summarize_advantage(cfg_id, d):
     s0 = stats[0]
     txt = f"""# Kernel trace: TreePO advantage over config {cfg_id}'s decoded leaves ({_workload_name(cfg_id)})
 
-Commands (repository root `$R` on the GPU box):
+Commands (repository root `$R` on the MI355X host):
 
 ```
 cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv -d $R/gpurun_out/advprof/c{cfg_id} -o run -- python3 -u $R/bench.py --advantage --config {cfg_id} --steps {b["steps"]} --warmup {b["warmup"]} --no-cpu > $R/gpurun_out/advprof/c{cfg_id}/bench.json
