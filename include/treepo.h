@@ -236,7 +236,9 @@ int32_t treepo_decode_workspace_size(treepo_ctx* ctx, int32_t n_leaves,
  * fp32, or, for schedules whose partials far exceed the L2, in block floating
  * point -- 14-bit mantissas under a shared exponent per 4 values: an output
  * then moves by less than 2^-13 of the largest |V| value it averages;
- * accumulation is fp32 throughout).  The schedule
+ * accumulation is fp32 throughout).  Non-finite inputs give non-finite
+ * outputs where the definition does (a NaN or infinity in V spoils its
+ * column; in block floating point the column's group of 4).  The schedule
  * (plan) is cached per context (the last four leaf lists and modes) and its
  * device image lives in memory the context allocates (see the ownership rule
  * above); the workspace holds only this call's partial results, so the

@@ -7,7 +7,10 @@
 //        in bits 0-13 and 14-27 of word 0, m_2 and m_3 in word 1;
 //   x_k = m_k 2^(E - 139).
 // Groups whose E is below 13 (every value under 2^-114) store zeros.  Each
-// value is off by at most 2^-13 of its group's largest magnitude.
+// value is off by at most 2^-13 of its group's largest magnitude.  A group
+// holding an infinity or a NaN (E = 255) is stored as E = 255 with zero
+// mantissas and decodes to four NaNs, so non-finite partials stay
+// non-finite.
 #ifndef TREEPO_PARTIAL_FORMAT_H
 #define TREEPO_PARTIAL_FORMAT_H
 
@@ -30,7 +33,7 @@ __host__ __device__ inline void pack_group4(float x0, float x1, float x2, float 
   const uint32_t ea = e0 > e1 ? e0 : e1, eb = e2 > e3 ? e2 : e3;
   const uint32_t e = ea > eb ? ea : eb;
   int32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
-  if (e >= 13) {
+  if (e >= 13 && e < 255) {
     const float sc = __builtin_bit_cast(float, (266u - e) << 23);  // 2^(139 - E)
     m0 = group_mantissa(x0, sc);
     m1 = group_mantissa(x1, sc);
@@ -43,7 +46,9 @@ __host__ __device__ inline void pack_group4(float x0, float x1, float x2, float 
 
 __host__ __device__ inline void unpack_group4(uint32_t w0, uint32_t w1, float* f) {
   const uint32_t e = (w0 >> 28) | ((w1 >> 28) << 4);
-  const float sc = e >= 13 ? __builtin_bit_cast(float, (e - 12) << 23) : 0.f;  // 2^(E - 139)
+  // 2^(E - 139); NaN for a non-finite group
+  const float sc = e == 255 ? __builtin_bit_cast(float, 0x7FC00000u)
+                            : (e >= 13 ? __builtin_bit_cast(float, (e - 12) << 23) : 0.f);
   f[0] = static_cast<float>(static_cast<int32_t>(w0 << 18) >> 18) * sc;
   f[1] = static_cast<float>(static_cast<int32_t>(w0 << 4) >> 18) * sc;
   f[2] = static_cast<float>(static_cast<int32_t>(w1 << 18) >> 18) * sc;

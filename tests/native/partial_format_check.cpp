@@ -2,7 +2,8 @@
 // (paper_2508_17445_amd/csrc/partial_format.h): the documented bit layout on
 // hand-worked groups, and the error bound -- every decoded value within 2^-13
 // of its group's largest magnitude -- on random groups spanning the fp32
-// exponent range, with sign mixes, zeros and values 2^-20 below the maximum.
+// exponent range, with sign mixes, zeros and values 2^-20 below the maximum;
+// groups holding an infinity or a NaN decode to NaNs.
 // Prints "ok <worst relative error>" or the first failure.
 #include <math.h>
 #include <stdio.h>
@@ -43,6 +44,28 @@ int main() {
     return 1;
   // all zeros, and a group below 2^-114, store zeros (E < 13 keeps its nibbles)
   if (check_exact(0.0f, 0.0f, 0.0f, 0.0f, 0u, 0u)) return 1;
+  // a group holding an infinity or a NaN: E = 255, zero mantissas, four NaNs
+  {
+    const float bad[3] = {INFINITY, -INFINITY, NAN};
+    for (int i = 0; i < 3; ++i)
+      for (int k = 0; k < 4; ++k) {
+        float x[4] = {1.0f, -2.0f, 0.25f, 0.0f};
+        x[k] = bad[i];
+        uint32_t a, b;
+        pack_group4(x[0], x[1], x[2], x[3], &a, &b);
+        if (a != (0xFu << 28) || b != (0xFu << 28)) {
+          printf("non-finite group %d/%d: %08x %08x\n", i, k, a, b);
+          return 1;
+        }
+        float f[4];
+        unpack_group4(a, b, f);
+        for (int j = 0; j < 4; ++j)
+          if (!isnan(f[j])) {
+            printf("non-finite group %d/%d decodes to %g at %d\n", i, k, f[j], j);
+            return 1;
+          }
+      }
+  }
   std::mt19937 g(7);
   std::normal_distribution<float> n(0.f, 1.f);
   std::uniform_real_distribution<float> u(-100.f, 100.f), v(-20.f, 0.f);

@@ -309,3 +309,95 @@ def test_shared_workspace_between_contexts():
                 torch.cuda.synchronize()
                 print(f"[shared workspace it={it} cfg={t.cfg.name} mode={mode}]", flush=True)
                 assert torch.equal(out, refs[(id(t), mode)])
+
+
+def _poisoned_kv(monkeypatch, node, tok, g, d, bits):
+    """Makes the workload generators give V[node][tok, g, d] the bf16 pattern
+    `bits` (a NaN or an infinity)."""
+    import workloads.device as wd
+    gen1, genm = wd.node_kv_bits, wd.many_node_kv_bits
+
+    def poison(o, kv):
+        if o != node:
+            return kv
+        k, v = kv
+        v = v.copy()
+        v[tok, g, d] = bits
+        return k, v
+
+    monkeypatch.setattr(wd, "node_kv_bits", lambda seed, o, rows, hkv, dd: poison(o, gen1(seed, o, rows, hkv, dd)))
+    monkeypatch.setattr(wd, "many_node_kv_bits",
+                        lambda seed, nr, hkv, dd, threads=None: [poison(o, kv) for (o, _), kv in
+                                                                 zip(nr, genm(seed, nr, hkv, dd, threads))])
+
+
+def _four_level_tree(fan, tokens):
+    """A root and three levels of `fan`-way forks; node ids in fork order."""
+    ops = [("root", tokens[0]), ("append", [0], [tokens[0]])]
+    rows = {0: tokens[0]}
+    level, nxt = [0], 1
+    for depth in range(1, 4):
+        new = []
+        for p in level:
+            ops.append(("fork", p, fan, tokens[depth]))
+            kids = list(range(nxt, nxt + fan))
+            nxt += fan
+            ops.append(("append", kids, [tokens[depth]] * fan))
+            rows.update({c: tokens[depth] for c in kids})
+            new += kids
+        level = new
+    log = _Log(ops, level, rows)
+    log.n_nodes = nxt
+    return log
+
+
+@pytest.mark.parametrize("kind", ["nan", "inf"])
+@pytest.mark.parametrize("shape", ["strided", "compact"])
+def test_non_finite_values_stay_non_finite(kind, shape, monkeypatch):
+    """One V entry of the shared root set to NaN or +inf: the outputs of that
+    column (every leaf, the KV head's query heads) are non-finite, as in the
+    oracle, and every other output matches it.  In a plan with compact
+    partial slots the non-finite value spoils its whole 4-value d-group of
+    the partial rows (the block format keeps no finite values beside a
+    non-finite one), so there the outputs of that d-group's columns are
+    non-finite too -- never a finite stand-in."""
+    import torch
+    g, d = 1, 37
+    _poisoned_kv(monkeypatch, 0, 123, g, d, 0x7FC0 if kind == "nan" else 0x7F80)
+    if shape == "strided":
+        log = _four_level_tree(2, [300, 70, 50, 30])
+        cfg = _random_cfg(95, 8, 2, 128)
+    else:
+        log = _four_level_tree(4, [2048, 512, 256, 64])
+        cfg = _random_cfg(96, 64, 8, 128)
+    dt = _dt(cfg=cfg, log=log)
+    G = cfg.hq // cfg.hkv
+    pieces, rowsets, _, _ = dt.ctx.export_plan(dt.leaves, 0)
+    count = {}
+    for pc in pieces:
+        for x in rowsets[pc[0]:pc[0] + pc[1]]:
+            count[(int(x), int(pc[3]))] = count.get((int(x), int(pc[3])), 0) + 1
+    ws = dt.ctx.workspace_size(dt.leaves, 0)
+    # strided slots hold fp32 rows for the largest entry count of every key
+    compact = ws < len(count) * max(count.values()) * G * (cfg.d * 4 + 8)
+    print(f"[non-finite {kind} {shape}] leaves {len(dt.leaves)} workspace {ws} B compact={compact}", flush=True)
+    assert compact == (shape == "compact")
+    ref, ref_lse = _oracle(dt)
+    bad_ref = ~np.isfinite(ref)
+    assert bad_ref[:, g * G:(g + 1) * G, d].all() and bad_ref.sum() == len(dt.leaves) * G
+    group = np.zeros_like(bad_ref)
+    group[:, g * G:(g + 1) * G, 4 * (d // 4):4 * (d // 4) + 4] = True
+    for mode in (0, 1):
+        out, lse = dt.decode(mode)
+        torch.cuda.synchronize()
+        o, l = out.cpu().numpy(), lse.cpu().numpy()
+        bad = ~np.isfinite(o)
+        print(f"[non-finite {kind} {shape} mode={mode}] non-finite outputs {int(bad.sum())} "
+              f"(oracle {int(bad_ref.sum())})", flush=True)
+        assert (bad | ~bad_ref).all(), "a non-finite oracle output came out finite"
+        assert not (bad & ~group).any(), "non-finite outputs outside the poisoned d-group"
+        ok = ~bad & ~bad_ref
+        assert float(np.abs(o[ok] - ref[ok]).max()) <= TOL
+        assert np.isfinite(l).all() and float(np.abs(l - ref_lse).max()) <= TOL
+    del dt
+    torch.cuda.empty_cache()
