@@ -54,7 +54,9 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBPS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2508_17445_amd", "csrc", "kernels.hip")
+# the decode kernels' sources: their hash gates the stored counter summaries
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2508_17445_amd", "csrc", f) for f in ("kernels.hip", "partial_format.h")]
+KERNEL_SHA_LABEL = "kernels.hip + partial_format.h sha256"
 METRIC = "tree-decode leaf-token-steps/sec + achieved HBM GB/s on unique KV (1 MI355X)"
 DIST_MIN_STEPS = 50
 
@@ -102,7 +104,10 @@ def _ensure_built():
 
 
 def _kernel_sha():
-    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
 
 
 def _traffic_file(cfg_id):
@@ -116,7 +121,7 @@ def _measured_traffic(cfg_id):
     try:
         kv = dict(line.split(":", 1) for line in open(_traffic_file(cfg_id)).read().splitlines() if ":" in line)
         kv = {k.strip(): v.strip() for k, v in kv.items()}
-        if kv.get("kernels.hip sha256") != _kernel_sha() or int(kv.get("config", -1)) != cfg_id:
+        if kv.get(KERNEL_SHA_LABEL) != _kernel_sha() or int(kv.get("config", -1)) != cfg_id:
             return None
         return int(kv["traffic bytes per launch"])
     except (OSError, KeyError, ValueError):
@@ -554,7 +559,7 @@ kernel-trace average ({t_avg:.2f} us).  The same run's bench line: partial kerne
 step {b['ms_per_step'] * 1e3:.2f} us (median {b['step_distribution']['median_ms'] * 1e3:.2f} us over
 {b['step_distribution']['steps']} steps).
 
-kernels.hip sha256: {_kernel_sha()}
+{KERNEL_SHA_LABEL}: {_kernel_sha()}
 """
     path = os.path.join(PROFILES, f"partial_kernel_config{cfg_id}_kernel_trace.md")
     open(path, "w").write(txt)
@@ -596,7 +601,7 @@ partial_kernel<128>, tree schedule, mean of {n} dispatches:
 partial_kernel<128>, per-leaf baseline: FETCH_SIZE {fn:.1f} KiB ({round(fn * 1024 * fs)} bytes), WRITE_SIZE {wn:.1f} KiB ({round(wn * 1024 * ws)} bytes)
 Algorithmic bytes per launch (unique KV of the decoded chains): {alg}; measured traffic / algorithmic = {(fb + wb) / alg:.4f}
 config: {cfg_id}
-kernels.hip sha256: {_kernel_sha()}
+{KERNEL_SHA_LABEL}: {_kernel_sha()}
 fetch bytes per launch: {fb}
 write bytes per launch: {wb}
 traffic bytes per launch: {fb + wb}
@@ -698,7 +703,7 @@ Row fill = query rows / (16 x row blocks) of the MFMA tiles, weighted by KV tile
 
 """ + "\n".join(out) + f"""
 
-kernels.hip sha256: {_kernel_sha()}
+{KERNEL_SHA_LABEL}: {_kernel_sha()}
 """
     path = os.path.join(PROFILES, f"partial_kernel_config{cfg_id}_mfma.txt")
     open(path, "w").write(txt)
@@ -761,7 +766,7 @@ bf16 dense peak.  The same run's bench line: the kernel at
 prompt once per rollout ({naive["prompt_copies"]} copies) at {naive["ms_per_step"] * 1e3:.0f} us
 ({naive["speedup_shared_vs_per_rollout"]}x).""" if naive else ".") + f"""
 
-kernels.hip sha256: {_kernel_sha()}
+{KERNEL_SHA_LABEL}: {_kernel_sha()}
 """
     open(os.path.join(PROFILES, f"prefill_kernel_config{cfg_id}_kernel_trace.md"), "w").write(txt)
     print(txt)
@@ -786,7 +791,7 @@ Means over the prefill dispatches of each run ({len(agg.get("SQ_BUSY_CU_CYCLES",
   MFMA pipe busy: {m["SQ_VALU_MFMA_BUSY_CYCLES"] / 4 / busy:.3f} of the CU busy cycles
   VALU active: {m["SQ_ACTIVE_INST_VALU"] / busy:.3f}; LDS active: {m["SQ_ACTIVE_INST_LDS"] / busy:.3f}; LDS bank-conflict cycles: {m["SQ_LDS_BANK_CONFLICT"] / busy:.3f}
   MFMA instructions per launch {m["SQ_INSTS_VALU_MFMA_BF16"]:.0f} -> {m["SQ_INSTS_VALU_MFMA_BF16"] * 16384 / flops:.2f} x the algorithmic FLOPs executed
-kernels.hip sha256: {_kernel_sha()}
+{KERNEL_SHA_LABEL}: {_kernel_sha()}
 """
     open(os.path.join(PROFILES, f"prefill_kernel_config{cfg_id}_counters.txt"), "w").write(txt2)
     print(txt2)
